@@ -1,0 +1,93 @@
+"""Pins for the scoring oracle (CPU).
+
+Checked against: brute-force sorting on tiny inputs, k = 1 as argmax, exact
+rational dot products on dyadic data (where the dequantized store equals the
+input), the Hoelder bound eps*||q||_1 of Appendix "Rank invariance, in full" on
+every (query, record) pair, and Theorem "Score deficit" combined with the
+quantization bound.
+"""
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+import synth
+from oracle import dedup, qeps, score
+
+
+def _store(seed=0, n=300, d=64, eps=1e-3):
+    rng = np.random.default_rng(seed)
+    x = synth.unit_rows(rng, n, d).astype(np.float32)
+    q = synth.unit_rows(rng, 20, d).astype(np.float32)
+    c = qeps.codes(x, eps).reshape(n, d)
+    return x, q, c, eps
+
+
+def test_topk_matches_sorted_brute_force():
+    x, q, c, eps = _store()
+    ids = np.arange(c.shape[0], dtype=np.int64) * 3 + 5
+    s = score.scores(q, c, eps)
+    # plant exact ties: copy a record under a larger id
+    c2 = np.concatenate([c, c[:10]])
+    ids2 = np.concatenate([ids, 10_000 + np.arange(10)])
+    s2 = score.scores(q, c2, eps)
+    for k in (1, 3, 10, 310, 400):
+        ts, ti = score.topk(s2, ids2, k)
+        for j in range(q.shape[0]):
+            ref = sorted(zip((-s2[j]).tolist(), ids2.tolist()))[:k]
+            want_i = [i for _, i in ref] + [-1] * (k - len(ref))
+            assert ti[j].tolist() == want_i
+            assert np.all(np.isneginf(ts[j, len(ref):]))
+    assert s.shape == (q.shape[0], c.shape[0])
+
+
+def test_k1_is_argmax():
+    x, q, c, eps = _store(1)
+    ids = np.arange(c.shape[0], dtype=np.int64)
+    s = score.scores(q, c, eps)
+    _, ti = score.topk(s, ids, 1)
+    assert np.array_equal(ti[:, 0], np.argmax(s, axis=1))
+
+
+def test_dyadic_scores_are_exact_dot_products():
+    # eps = 2^-12 and inputs on the grid 2^-11: x_hat == x, so the score is the
+    # exact inner product of the raw vectors.
+    rng = np.random.default_rng(2)
+    eps = 2.0 ** -12
+    x = (np.round(synth.unit_rows(rng, 40, 32) * 2048) / 2048).astype(np.float32)
+    q = synth.unit_rows(rng, 5, 32).astype(np.float32)
+    c = qeps.codes(x, eps).reshape(x.shape)
+    assert np.array_equal(qeps.decode(c, eps).reshape(x.shape), x)
+    s = score.scores(q, c, eps)
+    for j in range(q.shape[0]):
+        for y in range(0, x.shape[0], 7):
+            exact = sum(Fraction(float(a)) * Fraction(float(b)) for a, b in zip(q[j], x[y]))
+            assert s[j, y] == pytest.approx(float(exact), abs=1e-15)
+
+
+@pytest.mark.parametrize("eps", [1e-4, 1e-3, 1e-2])
+def test_hoelder_bound_every_pair(eps):
+    x, q, c, _ = _store(3, eps=eps)
+    s_hat = score.scores(q, c, eps)
+    s_true = q.astype(np.float64) @ x.astype(np.float64).T
+    beta = score.bound(q, eps)
+    assert np.all(np.abs(s_true - s_hat) <= beta[:, None] * (1 + 1e-12) + 1e-15)
+    # the bound is eps*||q||_1 (and not, e.g., eps*||q||_2)
+    assert np.allclose(beta, eps * np.abs(q.astype(np.float64)).sum(1), rtol=0, atol=1e-17)
+
+
+def test_dedup_plus_quantization_bound():
+    # Theorem "Score deficit" with delta_hat, plus beta for the quantized store:
+    # -beta <= max_S q.x - max_R q.x_hat <= ||q|| delta_hat + beta.
+    t = synth.tiny_ingest(n=1200, dup_frac=0.2)
+    x, tau, eps = t["x"], t["tau"], t["eps"]
+    r = dedup.greedy(x, tau)
+    kept = r["kept"]
+    c = qeps.codes(x[kept], eps).reshape(kept.size, x.shape[1])
+    q = t["q"]
+    ts, ti, beta = score.score_topk(q, c, kept, eps, 1)
+    top_s = (q.astype(np.float64) @ x.astype(np.float64).T).max(1)
+    gap = top_s - ts[:, 0]
+    qn = np.linalg.norm(q.astype(np.float64), axis=1)
+    assert np.all(gap >= -beta - 1e-12)
+    assert np.all(gap <= qn * r["delta_hat"] + beta + 1e-12)
