@@ -1,0 +1,207 @@
+/*
+ * lam.h -- C ABI of liblam, the MI355X (gfx950) hot path of LAM, the lossy
+ * agent memory of "LAM: A Lossy Agent Memory Framework With a Retrieval-Score
+ * Error Bound".
+ *
+ * Three operations, each as the paper states it:
+ *   1. Q_eps, the error-bounded quantizer of Section 2.2 ("Three layers", L1):
+ *      q = round(x / 2 eps) per coordinate, so |x - q*2eps| <= eps.
+ *   2. The epsilon error-bounded near-duplicate test of Section 2.3,
+ *      Algorithm "admit": arrivals, in order, are dropped iff a retained record
+ *      lies within l2 distance delta = sqrt(2 - 2 tau) (Eq. identity,
+ *      Section 2.1); the representative is the lowest-indexed such record
+ *      (Appendix "Representative selection"); the measured bound delta_hat is
+ *      reported (Appendix "The measured bound").
+ *   3. Retrieval scoring of queries against the quantized retained store,
+ *      dequantized on the fly, with top-k and the per-query bound
+ *      eps * ||q||_1 on |q.x - q.x_hat| (Appendix "Rank invariance, in full").
+ *
+ * Conventions for every call:
+ *   - Pointers named *_dev are device pointers on the context's device; the
+ *     caller owns them.  Pointers without the suffix are host memory.  The
+ *     library keeps no caller pointer after a call returns.
+ *   - Device work is enqueued on the context's stream, in call order.  Calls
+ *     that fill a host struct (marked "synchronous") wait for that stream
+ *     before returning; the others return once the work is enqueued.
+ *   - Every call returns a lam_status.  On LAM_EINVAL / LAM_ERANGE /
+ *     LAM_ECAPACITY / LAM_ESTATE detected on the host nothing is enqueued and
+ *     no output is written.  When the device detects the error (non-finite
+ *     input, |x| above a declared absmax) the call returns that status, the
+ *     store is left as it was, and the contents of caller output buffers are
+ *     unspecified.  LAM_EDEVICE reports a HIP runtime error; the context
+ *     should then be destroyed.
+ *   - lam_last_error() returns a thread-local message for the last non-OK
+ *     status of the calling thread.
+ *   - One context per host thread; a store must not be used by two calls at
+ *     once.  Calls that overlap on one device through different contexts are
+ *     independent (each context owns its scratch memory).
+ */
+#ifndef LAM_H
+#define LAM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define LAM_ABI_VERSION 1
+
+typedef enum lam_status {
+  LAM_OK = 0,
+  LAM_EINVAL = 1,     /* bad argument, or non-finite / out-of-range input data  */
+  LAM_ERANGE = 2,     /* |x| above the declared absmax, or code range >= 2^31   */
+  LAM_ENOMEM = 3,     /* device or host allocation failed                       */
+  LAM_ECAPACITY = 4,  /* the store cannot take the batch                        */
+  LAM_EDEVICE = 5,    /* HIP runtime error                                      */
+  LAM_ESTATE = 6      /* call not valid in the object's state                   */
+} lam_status;
+
+int lam_abi_version(void);
+const char* lam_status_name(lam_status s);
+const char* lam_last_error(void);
+
+/* ------------------------------------------------------------------ context */
+typedef struct lam_ctx lam_ctx;
+
+/* device: HIP device ordinal.  hip_stream: a hipStream_t on that device, or
+ * NULL for the null stream.  The stream is borrowed, not owned. */
+lam_status lam_ctx_create(int device, void* hip_stream, lam_ctx** out);
+void lam_ctx_destroy(lam_ctx* ctx);
+lam_status lam_ctx_synchronize(lam_ctx* ctx);
+
+/* Per-kernel timing with HIP events recorded on the context's stream around
+ * each launch of the named kernels while enabled.  read() is synchronous and
+ * returns the summed elapsed milliseconds and launch count of one kernel name
+ * (0 / 0 if never launched).  For benchmarks; off by default. */
+lam_status lam_ctx_profile(lam_ctx* ctx, int enable);
+lam_status lam_ctx_profile_reset(lam_ctx* ctx);
+lam_status lam_ctx_profile_read(lam_ctx* ctx, const char* kernel, double* total_ms, int64_t* launches);
+
+/* ------------------------------------------------------------------ Q_eps   */
+/* Section 2.2 (L1): Q_eps(x) = round(x / 2eps), with round half to even of the
+ * exact real quotient of the float32 x by the binary64 step s = 2*eps.  Codes
+ * are two's-complement integers of width b, element i occupying bits
+ * [i*b, (i+1)*b) of a little-endian stream of uint32 words, least significant
+ * bit first; unused bits of the last word are zero. */
+enum { LAM_PACK_BITS = 0,   /* b = max(1, ceil(log2(2M + 1)))            */
+       LAM_PACK_BYTES = 1   /* b = smallest of 8, 16, 32 that holds +-M  */ };
+
+typedef struct lam_qparams {
+  double eps;           /* error budget; |x - code*step| <= eps on exact reals */
+  double step;          /* s = 2 * eps                                          */
+  float absmax;         /* A, declared or measured                              */
+  int32_t bits;         /* b                                                    */
+  int32_t mode;         /* LAM_PACK_BITS or LAM_PACK_BYTES                      */
+  int32_t max_code;     /* M = Q_eps(A) < 2^31                                  */
+  int64_t n;            /* number of codes                                      */
+  uint64_t code_bytes;  /* 4 * ceil(n * b / 32)                                 */
+} lam_qparams;
+
+/* Host only: the width plan for n values bounded by absmax.
+ * EINVAL: eps not finite or outside [2^-60, 2^20], absmax not finite or < 0,
+ * n < 0, bad mode.  ERANGE: M >= 2^31. */
+lam_status lam_qeps_plan(double eps, float absmax, int mode, int64_t n, lam_qparams* out);
+
+/* Encode n float32 values.  absmax > 0 declares A (every |x| must be <= A,
+ * else ERANGE); absmax <= 0 measures A = max|x| on the device first (one extra
+ * read of x).  codes_dev receives code_bytes bytes and needs at least that
+ * capacity (EINVAL otherwise).  x_dev must be 4-byte aligned; codes_dev
+ * 4-byte aligned.  Synchronous (fills *out).  EINVAL also for NaN/Inf in x. */
+lam_status lam_quantize(lam_ctx* ctx, const float* x_dev, int64_t n, double eps, float absmax,
+                        int mode, uint32_t* codes_dev, uint64_t codes_cap_bytes, lam_qparams* out);
+
+/* Decode p->n codes: x_hat = float32(float64(code * step)) (round to binary64,
+ * then to binary32; the bound holds on the exact code*step).  Asynchronous. */
+lam_status lam_dequantize(lam_ctx* ctx, const uint32_t* codes_dev, const lam_qparams* p, float* xhat_dev);
+
+/* ------------------------------------------------------------------ store   */
+/* The retained set R of Algorithm "admit": float32 rows of the kept
+ * arrivals in arrival order, with their global ids (0-based arrival ordinals
+ * counted over every ingest call on the store).  Library-owned device memory,
+ * sized for `capacity` rows at creation.  dim must be a positive multiple of
+ * 32 (at most 4096); tau in (-1, 1]; the merge radius is delta^2 = 2 - 2 tau. */
+typedef struct lam_store lam_store;
+
+lam_status lam_store_create(lam_ctx* ctx, int32_t dim, double tau, int64_t capacity, lam_store** out);
+void lam_store_destroy(lam_store* store);
+
+typedef struct lam_store_info {
+  int64_t size;          /* retained rows                                       */
+  int64_t capacity;
+  int64_t n_seen;        /* arrivals ingested so far (next global id)           */
+  int32_t dim;
+  int32_t quantized;     /* 1 once lam_store_quantize has run on every row      */
+  double tau;
+  double delta_hat_run;  /* max substitution distance over all calls            */
+  lam_qparams q;         /* valid when quantized                                */
+} lam_store_info;
+
+lam_status lam_store_get_info(const lam_store* store, lam_store_info* out);
+
+/* Empty the store (size, n_seen, delta_hat and codes reset; memory kept), as
+ * if newly created.  Asynchronous. */
+lam_status lam_store_clear(lam_ctx* ctx, lam_store* store);
+
+typedef struct lam_ingest_stats {
+  int64_t n_in;                 /* arrivals in this call                        */
+  int64_t n_kept;
+  int64_t n_dropped;
+  int64_t store_size;           /* retained rows after the call                 */
+  int64_t n_ambiguous_pairs;    /* pairs whose screened distance lay within the
+                                   screen's error bound of delta^2 and were
+                                   decided by the exact binary64 test           */
+  int64_t n_exact_escalations;  /* pairs within 1e-12 of delta^2 in binary64,
+                                   decided on exact integers on the host        */
+  double delta_hat_call;        /* max ||x_i - x_rep|| over this call's merges  */
+  double delta_hat_run;         /* same over the store's lifetime               */
+} lam_ingest_stats;
+
+/* Algorithm "admit" over x_dev (n rows of dim float32, row-major, expected
+ * unit-normalised; used exactly as given).  For each arrival i, in order:
+ * rep_dev[i] = global id of the lowest-indexed retained row y with
+ * sum_d (x_i,d - y_d)^2 <= 2 - 2 tau (exact reals, inclusive), which drops i;
+ * or -1, and i is appended to the store with global id n_seen + i.
+ * max_cos_dev (optional, NULL to skip): max over rows retained at i's arrival
+ * of the dot product x_i . y in the screen's precision (|error| <= 1.1e-3 for
+ * unit rows), -inf if none.  stats (optional) is filled synchronously; rep and
+ * max_cos are written asynchronously unless stats is requested.
+ * EINVAL: n < 0, NaN/Inf or |x| >= 256 in a coordinate (store unchanged).
+ * ECAPACITY: size + n > capacity (checked before any work). */
+lam_status lam_dedup_ingest(lam_ctx* ctx, lam_store* store, const float* x_dev, int64_t n,
+                            int64_t* rep_dev, float* max_cos_dev, lam_ingest_stats* stats);
+
+/* Q_eps over every retained row (the store's codec, Algorithm "admit",
+ * "store the compressed embedding"); rows start on word boundaries (dim is a
+ * multiple of 32).  Same absmax semantics as lam_quantize.  Synchronous.
+ * Rows retained later are not coded until this is called again. */
+lam_status lam_store_quantize(lam_ctx* ctx, lam_store* store, double eps, float absmax, int mode,
+                              lam_qparams* out);
+
+/* Decode the store's codes into xhat_dev (size x dim float32, row-major):
+ * x_hat = float32(float64(code * step)), the reconstruction the scores use.
+ * ESTATE if the store is not quantized.  Asynchronous. */
+lam_status lam_store_dequantize(lam_ctx* ctx, const lam_store* store, float* xhat_dev);
+
+/* Copy the retained ids (size int64) and, if codes_dev is not NULL and the
+ * store is quantized, the packed codes (q.code_bytes bytes) out.  Async. */
+lam_status lam_store_export(lam_ctx* ctx, const lam_store* store, int64_t* ids_dev,
+                            uint32_t* codes_dev, uint64_t codes_cap_bytes);
+
+/* Score nq float32 queries (row-major, dim each) against the quantized store:
+ * score(j, y) = step * sum_d q_j,d * code_y,d, i.e. q_j . x_hat_y with the
+ * exact dequantized row, accumulated in float32 (|error| <= 1e-5 for unit
+ * rows).  Per query the k best by (score desc, id asc) go to scores_dev and
+ * ids_dev (nq x k, row-major), padded with (-inf, -1) past the store size.
+ * bound_dev (optional): eps * ||q_j||_1 rounded up to float32.
+ * 1 <= k <= 64.  ESTATE if the store is not quantized (or has rows added
+ * since).  A query row holding NaN/Inf gets (NaN, -1) in all k slots and a
+ * NaN bound instead of an error status.  Asynchronous. */
+lam_status lam_score_topk(lam_ctx* ctx, const lam_store* store, const float* q_dev, int64_t nq,
+                          int32_t k, float* scores_dev, int64_t* ids_dev, float* bound_dev);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* LAM_H */

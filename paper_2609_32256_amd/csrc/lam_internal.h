@@ -1,0 +1,157 @@
+// Internal declarations of liblam: context, store, scratch arena, error state
+// and the kernel launchers.  Not part of the ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <string>
+#include <vector>
+
+#include "lam.h"
+
+namespace lam {
+
+// ------------------------------------------------------------------ errors
+void set_error(const char* fmt, ...);
+
+struct Status {
+  lam_status s;
+};
+
+#define LAM_HIP(call)                                                            \
+  do {                                                                           \
+    hipError_t e_ = (call);                                                      \
+    if (e_ != hipSuccess) {                                                      \
+      ::lam::set_error("%s failed: %s (%s:%d)", #call, hipGetErrorString(e_),    \
+                       __FILE__, __LINE__);                                      \
+      return LAM_EDEVICE;                                                        \
+    }                                                                            \
+  } while (0)
+
+#define LAM_CHECK(cond, status, ...)                                             \
+  do {                                                                           \
+    if (!(cond)) {                                                               \
+      ::lam::set_error(__VA_ARGS__);                                             \
+      return (status);                                                           \
+    }                                                                            \
+  } while (0)
+
+#define LAM_TRY(expr)                                                            \
+  do {                                                                           \
+    lam_status s_ = (expr);                                                      \
+    if (s_ != LAM_OK) return s_;                                                 \
+  } while (0)
+
+// ------------------------------------------------------------------ device buffer
+struct DevBuf {
+  void* p = nullptr;
+  size_t bytes = 0;
+  lam_status ensure(size_t need);   // grows (never shrinks); contents not kept
+  void release();
+  template <class T> T* as() const { return static_cast<T*>(p); }
+};
+
+// Device-side status words written by kernels and read back at the end of a
+// synchronous call.  Pinned host mirror for the readback.
+struct DevFlags {
+  uint32_t nonfinite;      // NaN/Inf seen in an input
+  uint32_t out_of_range;   // |x| > declared absmax, or |x| >= 256 for the screen
+  uint32_t absmax_bits;    // max |x| as float bits (measured absmax)
+  uint32_t pair_overflow;  // bit 0: ambiguous-pair list overflowed; bit 1: a pair needs the exact host test
+  uint32_t n_pairs;        // ambiguous pairs found
+  uint32_t n_escalate;     // pairs decided by the exact host test
+  uint32_t n_kept;         // arrivals retained by this ingest
+  uint32_t pairs_needed;   // pair-list capacity that would have sufficed
+  unsigned long long dhat2_bits;  // max merged d^2 (binary64 bits, non-negative)
+  uint32_t ebmax_call_bits;       // max per-row screen error term over the call's rows
+  uint32_t pad;
+};
+
+// ------------------------------------------------------------------ profiling
+struct ProfRec {
+  const char* name;
+  hipEvent_t a, b;
+};
+
+}  // namespace lam
+
+struct lam_ctx {
+  int device = 0;
+  hipStream_t stream = nullptr;
+  lam::DevFlags* flags_dev = nullptr;   // device status words
+  lam::DevFlags* flags_host = nullptr;  // pinned mirror
+  // scratch arena, grown on demand
+  lam::DevBuf scratch[12];
+  // profiling
+  uint32_t pair_cap = 1u << 20;         // ambiguous-pair list capacity (grows on overflow)
+  bool profiling = false;
+  std::vector<lam::ProfRec> prof;
+  std::vector<hipEvent_t> event_pool;
+};
+
+struct lam_store {
+  lam_ctx* ctx = nullptr;
+  int32_t dim = 0;
+  double tau = 0.0;
+  double d2 = 0.0;          // delta^2 = 2 - 2 tau (binary64)
+  int64_t capacity = 0;
+  int64_t size = 0;
+  int64_t n_seen = 0;
+  double delta_hat_run = 0.0;
+  // retained rows (capacity rows each)
+  float* x32 = nullptr;       // float32 rows
+  _Float16* x16 = nullptr;    // float16 rows scaled by 2^8 (screen operand)
+  float* hn = nullptr;        // ||x||^2 / 2 (float32, rounded to nearest)
+  float* l1 = nullptr;        // ||x||_1 (float32, rounded up)
+  float* nrm = nullptr;       // ||x||_2 (float32, rounded up)
+  int64_t* ids = nullptr;     // global ids
+  float* stat_dev = nullptr;  // [0] max ||x||_2, [1] max ||x||_1 over rows (as float bits, atomic max)
+  // codes
+  uint32_t* codes = nullptr;
+  uint64_t codes_cap = 0;
+  int64_t coded_rows = 0;     // rows covered by the current codes
+  lam_qparams q{};
+};
+
+namespace lam {
+
+// profiling helpers (no-ops unless ctx->profiling)
+lam_status prof_begin(lam_ctx* ctx, const char* name, size_t* slot);
+lam_status prof_end(lam_ctx* ctx, size_t slot);
+
+struct ProfScope {
+  lam_ctx* ctx;
+  size_t slot = (size_t)-1;
+  lam_status st = LAM_OK;
+  ProfScope(lam_ctx* c, const char* name) : ctx(c) { st = prof_begin(ctx, name, &slot); }
+  ~ProfScope() { if (slot != (size_t)-1) prof_end(ctx, slot); }
+};
+
+// status words: cleared by a kernel, read back with a stream synchronisation
+lam_status clear_flags(lam_ctx* ctx);
+lam_status read_flags(lam_ctx* ctx);
+
+// ------------------------------------------------------------------ Q_eps (qeps.hip)
+lam_status qeps_plan_host(double eps, float absmax, int mode, int64_t n, lam_qparams* out);
+lam_status launch_absmax(lam_ctx* ctx, const float* x, int64_t n, uint32_t* absmax_bits_dev);
+lam_status launch_encode(lam_ctx* ctx, const float* x, int64_t n, const lam_qparams& p,
+                         uint32_t* codes, uint32_t* viol_dev);
+lam_status launch_decode(lam_ctx* ctx, const uint32_t* codes, const lam_qparams& p, float* xhat);
+
+// ------------------------------------------------------------------ dedup (dedup.hip)
+lam_status dedup_ingest(lam_ctx* ctx, lam_store* st, const float* x, int64_t n, int64_t* rep,
+                        float* max_cos, lam_ingest_stats* stats);
+lam_status store_alloc(lam_store* st);
+size_t store_meta_bytes();   // device bookkeeping block of a store (cleared by lam_store_clear)
+void store_free(lam_store* st);
+
+// ------------------------------------------------------------------ scoring (score.hip)
+lam_status score_topk(lam_ctx* ctx, const lam_store* st, const float* q, int64_t nq, int32_t k,
+                      float* scores, int64_t* ids, float* bound);
+
+// ------------------------------------------------------------------ exact host predicate (exact.cpp)
+// sum_d (a_d - b_d)^2 <= 2 - 2 tau on exact reals, float32 rows a, b of length d.
+bool exact_within(const float* a, const float* b, int d, double tau);
+
+}  // namespace lam

@@ -1,0 +1,391 @@
+// Retrieval scoring against the quantized store, dequantized on the fly, with
+// top-k per query and the per-query bound eps * ||q||_1 (Hoelder applied to
+// the per-coordinate bound of Q_eps, Appendix "Rank invariance, in full").
+//
+// score(j, y) = s * sum_d q_j,d * code_y,d  (s = 2 eps), i.e. q_j . x_hat_y with
+// the exact dequantized row.  Codes of at most 12 bits are exact in fp16.
+// Each query is scaled by a power of two 2^e_j (max |q| into [2^14, 2^15)) and
+// split into fp16 hi + lo parts, q 2^e = hi + lo + r with |r| <= 2^-22 |q 2^e|;
+// hi*code and lo*code are exact in fp32 and the MFMA accumulates in fp32.  The
+// score is acc * float32(s 2^-e_j).
+//
+// Kernel layout: a workgroup owns 128 queries and a contiguous range ("split")
+// of the store, walked in 128-row tiles.  Per tile the codes are unpacked from
+// their b-bit words straight into an fp16 LDS slab (no dequantized copy exists
+// in HBM) and multiplied with the query slabs on v_mfma_f32_32x32x16_f16.  Wave
+// w holds queries [32w, 32w + 32) against all 128 rows of the tile, so every
+// query lives in two lanes of one wave; each lane keeps a sorted private list
+// of its best KL (score, row) pairs in registers, touched only when a score
+// reaches the list's current threshold.  A merge kernel then picks the k best
+// per query from all lists by (score desc, id asc).
+#include <cmath>
+#include <cstring>
+
+#include "lam_internal.h"
+#include "mfma_tile.h"
+
+namespace lam {
+namespace {
+
+constexpr int kNoRow = 0x7fffffff;
+
+enum ScoreScratch { S_QHI = 7, S_QLO, S_QMETA, S_PART };
+
+struct QMeta {
+  float osc;     // float32(s * 2^-e): multiplies the raw accumulator
+  float bound;   // eps * ||q||_1 rounded up, or NaN for an invalid query
+  int bad;       // query holds NaN/Inf
+  int pad;
+};
+
+__device__ __forceinline__ float ru32(double d) {
+  float f = (float)d;
+  if ((double)f < d) f = __uint_as_float(__float_as_uint(f) + 1u);   // d >= 0 here
+  return f;
+}
+
+__global__ __launch_bounds__(256) void k_score_prep(const float* __restrict__ q, int64_t nq, int D, double s,
+                                                    double eps, _Float16* __restrict__ qhi,
+                                                    _Float16* __restrict__ qlo, QMeta* __restrict__ meta) {
+  const int lane = threadIdx.x & 63;
+  const int64_t j = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (j >= nq) return;
+  const float* p = q + j * D;
+  float mx = 0.0f;
+  double l1 = 0.0;
+  bool bad = false;
+  for (int d = lane; d < D; d += 64) {
+    const float v = p[d];
+    const float a = fabsf(v);
+    bad |= !(a <= 3.402823466e38f);
+    mx = fmaxf(mx, a);
+    l1 += (double)a;
+  }
+  for (int o = 32; o > 0; o >>= 1) {
+    mx = fmaxf(mx, __shfl_xor(mx, o));
+    l1 += __shfl_xor(l1, o);
+  }
+  bad = __ballot(bad) != 0ull;
+  int e = 0;
+  if (!bad && mx > 0.0f) e = 14 - ilogbf(mx);   // max |q| 2^e in [2^14, 2^15)
+  const float sc = ldexpf(1.0f, e);
+  for (int d = lane; d < D; d += 64) {
+    const float v = bad ? 0.0f : p[d] * sc;     // exact power-of-two scaling
+    const _Float16 h = (_Float16)v;
+    const _Float16 l = (_Float16)(v - (float)h);
+    qhi[j * D + d] = h;
+    qlo[j * D + d] = l;
+  }
+  if (lane == 0) {
+    QMeta m;
+    m.osc = (float)ldexp(s, -e);
+    m.bound = bad ? __builtin_nanf("") : ru32(eps * l1 * (1.0 + 0x1p-50));
+    m.bad = bad ? 1 : 0;
+    m.pad = 0;
+    meta[j] = m;
+  }
+}
+
+struct ScoreArgs {
+  const uint32_t* codes;
+  int64_t n;            // store rows
+  int D;
+  int64_t row_words;    // D * b / 32
+  const _Float16* qhi;
+  const _Float16* qlo;
+  const QMeta* meta;
+  int64_t nq;
+  int nqt;              // query tiles
+  int splits;
+  int64_t tiles_per_split;
+  float* part_s;        // [nq][splits][2][KL]
+  int32_t* part_r;
+};
+
+__device__ __forceinline__ bool better(float a, int ra, float b, int rb) {
+  return a > b || (a == b && ra < rb);
+}
+
+// Unpacks 32 b-bit codes starting at word w (element 0 at bit 0) to fp16.
+template <int B>
+__device__ __forceinline__ void unpack32(const uint32_t* __restrict__ w, _Float16* __restrict__ out) {
+  uint32_t v[B + 1];
+#pragma unroll
+  for (int i = 0; i < B; ++i) v[i] = w[i];
+  v[B] = 0u;
+#pragma unroll
+  for (int e = 0; e < 32; ++e) {
+    const int bit = e * B, wi = bit >> 5, off = bit & 31;
+    uint32_t u = v[wi] >> off;
+    if (off + B > 32) u |= v[wi + 1] << (32 - off);
+    const int32_t c = (int32_t)(u << (32 - B)) >> (32 - B);
+    out[e] = (_Float16)(float)c;
+  }
+}
+
+template <int B, int KL>
+__global__ __launch_bounds__(kWG) void k_score(ScoreArgs a) {
+  __shared__ _Float16 lds[6 * kTB * kLdk];
+  // slab buffers: codes (A) at 0 / 1, query hi at 2 / 3, query lo at 4 / 5
+  auto buf = [&](int i) -> _Float16* { return lds + i * (kTB * kLdk); };
+  const int qt = blockIdx.x % a.nqt;
+  const int split = blockIdx.x / a.nqt;
+  const int64_t ntiles = (a.n + kTB - 1) / kTB;
+  const int64_t t0 = (int64_t)split * a.tiles_per_split;
+  const int64_t t1 = min(ntiles, t0 + a.tiles_per_split);
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int64_t qbase = (int64_t)qt * kTB;
+  const int qrows = (int)min<int64_t>(kTB, a.nq - qbase);
+  const int64_t j = qbase + wave * 32 + (lane & 31);
+  const float osc = (j < a.nq) ? a.meta[j].osc : 0.0f;
+  const _Float16* QH = a.qhi + qbase * a.D;
+  const _Float16* QL = a.qlo + qbase * a.D;
+
+  float ls[KL];
+  int lr[KL];
+#pragma unroll
+  for (int p = 0; p < KL; ++p) {
+    ls[p] = -INFINITY;
+    lr[p] = kNoRow;
+  }
+
+  const int urow = threadIdx.x >> 1, uhalf = threadIdx.x & 1;   // unpack: 2 threads per row
+  for (int64_t tile = t0; tile < t1; ++tile) {
+    const int64_t rbase = tile * kTB;
+    const int rows = (int)min<int64_t>(kTB, a.n - rbase);
+    floatx16 acc[4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[t][r] = 0.0f;
+
+    // stage 0
+    auto load_codes = [&](int k0, uint32_t (&cw)[B]) {
+      if (urow < rows && k0 + 32 * uhalf < a.D) {
+        const uint32_t* src = a.codes + (rbase + urow) * a.row_words + (int64_t)(k0 / 32 + uhalf) * B;
+#pragma unroll
+        for (int i = 0; i < B; ++i) cw[i] = src[i];
+      } else {
+#pragma unroll
+        for (int i = 0; i < B; ++i) cw[i] = 0u;
+      }
+    };
+    auto store_codes = [&](_Float16* s, const uint32_t (&cw)[B]) {
+      _Float16 h[32];
+      unpack32<B>(cw, h);
+      _Float16* dst = s + urow * kLdk + uhalf * 32;
+#pragma unroll
+      for (int i = 0; i < 32; i += 8) *reinterpret_cast<uint4*>(dst + i) = *reinterpret_cast<const uint4*>(h + i);
+    };
+    uint32_t cw[B];
+    SlabRegs rh, rl;
+    load_codes(0, cw);
+    slab_load(QH, qrows, a.D, 0, a.D, rh);
+    slab_load(QL, qrows, a.D, 0, a.D, rl);
+    store_codes(buf(0), cw);
+    slab_store(buf(2), rh);
+    slab_store(buf(4), rl);
+    __syncthreads();
+    int cur = 0;
+    for (int k0 = 0; k0 < a.D; k0 += kBK) {
+      const bool more = k0 + kBK < a.D;
+      if (more) {
+        load_codes(k0 + kBK, cw);
+        slab_load(QH, qrows, a.D, k0 + kBK, a.D, rh);
+        slab_load(QL, qrows, a.D, k0 + kBK, a.D, rl);
+      }
+#pragma unroll
+      for (int kk = 0; kk < kBK / 16; ++kk) {
+        const half8 bh = frag_load(buf(2 + cur), wave * 32, kk);
+        const half8 bl = frag_load(buf(4 + cur), wave * 32, kk);
+        half8 fa[4];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) fa[t] = frag_load(buf(cur), t * 32, kk);
+#pragma unroll
+        for (int t = 0; t < 4; ++t) acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fa[t], bh, acc[t], 0, 0, 0);
+#pragma unroll
+        for (int t = 0; t < 4; ++t) acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fa[t], bl, acc[t], 0, 0, 0);
+      }
+      if (more) {
+        store_codes(buf(cur ^ 1), cw);
+        slab_store(buf(2 + (cur ^ 1)), rh);
+        slab_store(buf(4 + (cur ^ 1)), rl);
+      }
+      __syncthreads();
+      cur ^= 1;
+    }
+
+    // epilogue: candidates against this lane's list threshold
+    float mx = -INFINITY;
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int rl_ = t * 32 + acc_row(r, lane);
+        const float sc = acc[t][r] * osc;
+        mx = (rl_ < rows) ? fmaxf(mx, sc) : mx;
+      }
+    const bool hot = mx >= ls[KL - 1];
+    if (__ballot(hot) != 0ull) {
+      // Park this wave's 64 scores per lane in LDS (free after the K loop) and
+      // let the hot lanes walk them in a plain loop.
+      float* wl = reinterpret_cast<float*>(lds) + wave * 64 * 64;
+#pragma unroll
+      for (int t = 0; t < 4; ++t)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) wl[(t * 16 + r) * 64 + lane] = acc[t][r] * osc;
+      if (hot) {
+        for (int e = 0; e < 64; ++e) {
+          const int rl_ = (e >> 4) * 32 + acc_row(e & 15, lane);
+          if (rl_ >= rows) continue;
+          const float sc = wl[e * 64 + lane];
+          const int row = (int)(rbase + rl_);
+          if (!better(sc, row, ls[KL - 1], lr[KL - 1])) continue;
+          int qpos = 0;
+#pragma unroll
+          for (int p = 0; p < KL; ++p) qpos += better(ls[p], lr[p], sc, row) ? 1 : 0;
+#pragma unroll
+          for (int p = KL - 1; p >= 0; --p) {
+            const float ps = (p > 0) ? ls[p - 1] : 0.0f;
+            const int pr = (p > 0) ? lr[p - 1] : 0;
+            ls[p] = (p > qpos) ? ps : (p == qpos ? sc : ls[p]);
+            lr[p] = (p > qpos) ? pr : (p == qpos ? row : lr[p]);
+          }
+        }
+      }
+    }
+    __syncthreads();   // LDS is reused by the next tile's first slab
+  }
+  if (j < a.nq) {
+    const int slot = lane >> 5;
+    const int64_t o = ((j * a.splits + split) * 2 + slot) * (int64_t)KL;
+#pragma unroll
+    for (int p = 0; p < KL; ++p) {
+      a.part_s[o + p] = ls[p];
+      a.part_r[o + p] = lr[p];
+    }
+  }
+}
+
+// One wave per query: k rounds, each taking the best candidate that is worse
+// than the previous pick under (score desc, row asc).
+__global__ __launch_bounds__(256) void k_topk_merge(int64_t nq, int cands, int k, const float* __restrict__ ps,
+                                                    const int32_t* __restrict__ pr, const QMeta* __restrict__ meta,
+                                                    const int64_t* __restrict__ ids, float* __restrict__ out_s,
+                                                    int64_t* __restrict__ out_i, float* __restrict__ bound) {
+  const int lane = threadIdx.x & 63;
+  const int64_t j = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (j >= nq) return;
+  const QMeta m = meta[j];
+  if (lane == 0 && bound) bound[j] = m.bound;
+  if (m.bad) {
+    for (int t = lane; t < k; t += 64) {
+      out_s[j * k + t] = __builtin_nanf("");
+      out_i[j * k + t] = -1;
+    }
+    return;
+  }
+  const float* s = ps + j * (int64_t)cands;
+  const int32_t* r = pr + j * (int64_t)cands;
+  float prev_s = INFINITY;
+  int prev_r = -1;
+  for (int t = 0; t < k; ++t) {
+    float bs = -INFINITY;
+    int br = kNoRow;
+    for (int c = lane; c < cands; c += 64) {
+      const float cs = s[c];
+      const int cr = r[c];
+      if (cr == kNoRow) continue;
+      if (!better(prev_s, prev_r, cs, cr)) continue;   // already taken
+      if (better(cs, cr, bs, br)) { bs = cs; br = cr; }
+    }
+    for (int o = 32; o > 0; o >>= 1) {
+      const float os = __shfl_xor(bs, o);
+      const int orr = __shfl_xor(br, o);
+      if (better(os, orr, bs, br)) { bs = os; br = orr; }
+    }
+    if (lane == 0) {
+      out_s[j * k + t] = (br == kNoRow) ? -INFINITY : bs;
+      out_i[j * k + t] = (br == kNoRow) ? -1 : ids[br];
+    }
+    prev_s = bs;
+    prev_r = br;
+  }
+}
+
+template <int B, int KL>
+void launch_score_b(dim3 grid, hipStream_t st, const ScoreArgs& a) {
+  hipLaunchKernelGGL((k_score<B, KL>), grid, dim3(kWG), 0, st, a);
+}
+
+template <int B>
+lam_status launch_score(int kl, dim3 grid, hipStream_t st, const ScoreArgs& a) {
+  if (kl == 16) launch_score_b<B, 16>(grid, st, a);
+  else launch_score_b<B, 64>(grid, st, a);
+  return LAM_OK;
+}
+
+template <int B>
+lam_status dispatch_bits(int b, int kl, dim3 grid, hipStream_t st, const ScoreArgs& a) {
+  if (b == B) return launch_score<B>(kl, grid, st, a);
+  if constexpr (B < 12) return dispatch_bits<B + 1>(b, kl, grid, st, a);
+  set_error("scoring supports codes of at most 12 bits (got %d)", b);
+  return LAM_ESTATE;
+}
+
+}  // namespace
+
+lam_status score_topk(lam_ctx* ctx, const lam_store* st, const float* q, int64_t nq, int32_t k, float* scores,
+                      int64_t* ids, float* bound) {
+  if (nq == 0) return LAM_OK;
+  const int D = st->dim;
+  const int b = st->q.bits;
+  LAM_CHECK(b >= 1 && b <= 12, LAM_ESTATE,
+            "scoring supports codes of at most 12 bits (store codes have %d); quantize with a larger eps", b);
+  const int KL = (k <= 16) ? 16 : 64;
+  const int64_t n = st->size;
+  LAM_TRY(ctx->scratch[S_QHI].ensure((size_t)nq * D * 2));
+  LAM_TRY(ctx->scratch[S_QLO].ensure((size_t)nq * D * 2));
+  LAM_TRY(ctx->scratch[S_QMETA].ensure((size_t)nq * sizeof(QMeta)));
+  {
+    ProfScope ps(ctx, "score_prep");
+    hipLaunchKernelGGL(k_score_prep, dim3((unsigned)((nq + 3) / 4)), dim3(256), 0, ctx->stream, q, nq, D, st->q.step,
+                       st->q.eps, ctx->scratch[S_QHI].as<_Float16>(), ctx->scratch[S_QLO].as<_Float16>(),
+                       ctx->scratch[S_QMETA].as<QMeta>());
+    LAM_HIP(hipGetLastError());
+  }
+  const int nqt = (int)((nq + kTB - 1) / kTB);
+  const int64_t ntiles = (n + kTB - 1) / kTB;
+  int splits = 1;
+  if (ntiles > 0) {
+    const int64_t want = std::max<int64_t>(1, (1024 + nqt - 1) / nqt);
+    splits = (int)std::min<int64_t>(want, ntiles);
+  }
+  const int64_t tps = ntiles > 0 ? (ntiles + splits - 1) / splits : 0;
+  if (ntiles > 0) splits = (int)((ntiles + tps - 1) / tps);
+  const int cands = splits * 2 * KL;
+  LAM_TRY(ctx->scratch[S_PART].ensure((size_t)nq * cands * 8));
+  float* part_s = ctx->scratch[S_PART].as<float>();
+  int32_t* part_r = reinterpret_cast<int32_t*>(part_s + (size_t)nq * cands);
+  if (ntiles > 0) {
+    ScoreArgs a{st->codes, n, D, (int64_t)D * b / 32, ctx->scratch[S_QHI].as<_Float16>(),
+                ctx->scratch[S_QLO].as<_Float16>(), ctx->scratch[S_QMETA].as<QMeta>(), nq, nqt, splits, tps,
+                part_s, part_r};
+    const int64_t grid = (int64_t)nqt * splits;
+    LAM_CHECK(grid < (1LL << 31), LAM_EINVAL, "scoring grid too large");
+    ProfScope ps(ctx, "score_mfma");
+    LAM_TRY(dispatch_bits<1>(b, KL, dim3((unsigned)grid), ctx->stream, a));
+    LAM_HIP(hipGetLastError());
+  }
+  {
+    ProfScope ps(ctx, "score_merge");
+    hipLaunchKernelGGL(k_topk_merge, dim3((unsigned)((nq + 3) / 4)), dim3(256), 0, ctx->stream, nq,
+                       ntiles > 0 ? cands : 0, k, part_s, part_r, ctx->scratch[S_QMETA].as<QMeta>(), st->ids, scores,
+                       ids, bound);
+    LAM_HIP(hipGetLastError());
+  }
+  return LAM_OK;
+}
+
+}  // namespace lam

@@ -1,0 +1,144 @@
+"""GPU parity of the greedy near-duplicate test (Algorithm "admit") against the
+oracle: identical representatives (bit-exact decisions), deletion digest,
+delta_hat within 1e-12, max-cos within the screen bound; invariance to how the
+stream is split into calls; exact ties; error paths."""
+import numpy as np
+import pytest
+
+import synth
+from oracle import dedup, invariants
+
+pytestmark = pytest.mark.gpu
+
+
+def _dev(a):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def _ingest(lam, x, tau, batch, capacity=None, max_cos=False):
+    s = lam.Store(x.shape[1], tau, capacity or x.shape[0])
+    reps, stats, cos = [], [], []
+    xd = _dev(x)
+    for b0 in range(0, x.shape[0], batch):
+        r = s.ingest(xd[b0:b0 + batch], max_cos=max_cos)
+        reps.append(r[0].cpu().numpy())
+        stats.append(r[1])
+        if max_cos:
+            cos.append(r[2].cpu().numpy())
+    rep = np.concatenate(reps) if reps else np.zeros(0, np.int64)
+    return s, rep, stats, (np.concatenate(cos) if max_cos else None)
+
+
+@pytest.fixture(scope="module")
+def tiny():
+    t = synth.tiny_ingest()
+    t["ref"] = dedup.greedy(t["x"], t["tau"])
+    return t
+
+
+def test_tiny_parity(lam, tiny):
+    s, rep, stats, cos = _ingest(lam, tiny["x"], tiny["tau"], tiny["batch"], max_cos=True)
+    ref = tiny["ref"]
+    assert np.array_equal(rep, ref["rep"])
+    assert dedup.deletion_digest(rep) == dedup.deletion_digest(ref["rep"])
+    assert np.array_equal(s.ids().cpu().numpy(), ref["kept"])
+    assert abs(stats[-1]["delta_hat_run"] - ref["delta_hat"]) <= 1e-12
+    assert sum(st["n_kept"] for st in stats) == ref["kept"].size
+    # max cos: screened in fp16 with fp32 accumulation, within the screen bound
+    fin = np.isfinite(ref["max_cos"])
+    assert np.array_equal(np.isfinite(cos), fin)
+    assert np.max(np.abs(cos[fin] - ref["max_cos"][fin])) <= 1.1e-3
+
+
+@pytest.mark.parametrize("batch", [1, 7, 64, 1000, 4096])
+def test_tiny_partition_invariance(lam, tiny, batch):
+    x = tiny["x"] if batch >= 64 else tiny["x"][:600]
+    ref = tiny["ref"]["rep"][: x.shape[0]]
+    _, rep, stats, _ = _ingest(lam, x, tiny["tau"], batch)
+    assert np.array_equal(rep, ref)
+
+
+def test_repeat_runs_identical(lam, tiny):
+    d = set()
+    for _ in range(3):
+        _, rep, _, _ = _ingest(lam, tiny["x"], tiny["tau"], 1024)
+        d.add(dedup.deletion_digest(rep))
+    assert len(d) == 1
+
+
+def test_exact_ties_and_escalation(lam):
+    rng = np.random.default_rng(5)
+    a, b, b_in, b_out, tau = synth.dyadic_ties(rng, 200, 128)
+    x = np.concatenate([a, b, b_in, b_out, synth.unit_rows(rng, 300, 128).astype(np.float32)])
+    x = x[rng.permutation(x.shape[0])]
+    ref = dedup.greedy(x, tau)
+    assert ref["n_exact"] > 0
+    _, rep, stats, _ = _ingest(lam, x, tau, 256)
+    assert np.array_equal(rep, ref["rep"])
+    assert sum(st["n_exact_escalations"] for st in stats) > 0
+    assert abs(stats[-1]["delta_hat_run"] - ref["delta_hat"]) <= 1e-12
+
+
+def test_inclusive_threshold_pair(lam):
+    a = np.zeros((1, 64), np.float32)
+    a[0, 0] = 0.5
+    x = np.concatenate([np.zeros((1, 64), np.float32), a])
+    _, rep, stats, _ = _ingest(lam, x, 0.875, 2)
+    assert rep.tolist() == [-1, 0]
+    assert stats[-1]["delta_hat_call"] == 0.5
+
+
+@pytest.mark.parametrize("tau", [0.95, 0.99])
+def test_subset_parity(lam, tau):
+    """27,986 clustered rows in batches of 1,024 (the benchmark's launch
+    configuration), exhaustive parity with the oracle."""
+    cfg = synth.subset_ingest()
+    x = cfg["x"]
+    ref = dedup.greedy(x, tau, block=512)
+    _, rep, stats, _ = _ingest(lam, x, tau, 1024)
+    assert np.array_equal(rep, ref["rep"])
+    assert abs(stats[-1]["delta_hat_run"] - ref["delta_hat"]) <= 1e-12
+    amb = sum(st["n_ambiguous_pairs"] for st in stats)
+    print(f"tau={tau}: kept {np.count_nonzero(rep < 0)} of {rep.size}, ambiguous pairs {amb}")
+
+
+def test_gpu_output_invariants(lam):
+    cfg = synth.subset_ingest()
+    x, tau = cfg["x"][:6000], 0.95
+    _, rep, stats, _ = _ingest(lam, x, tau, 1024)
+    assert invariants.cover(x, rep, tau) == []
+    assert invariants.packing(x, rep, tau) == []
+    assert stats[-1]["delta_hat_run"] <= dedup.delta(tau)
+
+
+def test_errors_leave_store_unchanged(lam):
+    rng = np.random.default_rng(1)
+    x = synth.unit_rows(rng, 300, 64).astype(np.float32)
+    s = lam.Store(64, 0.95, 400)
+    s.ingest(_dev(x[:100]))
+    size = s.size
+    bad = x[100:200].copy()
+    bad[50, 3] = np.nan
+    with pytest.raises(lam.LamError) as e:
+        s.ingest(_dev(bad))
+    assert e.value.name == "LAM_EINVAL" and s.size == size and s.info().n_seen == 100
+    big = x[100:200].copy()
+    big[7, 0] = 300.0
+    with pytest.raises(lam.LamError) as e:
+        s.ingest(_dev(big))
+    assert e.value.name == "LAM_EINVAL" and s.size == size
+    with pytest.raises(lam.LamError) as e:
+        s.ingest(_dev(synth.unit_rows(rng, 301, 64).astype(np.float32)))
+    assert e.value.name == "LAM_ECAPACITY" and s.size == size
+    # the store still works and matches the oracle on the clean stream
+    rep2, _ = s.ingest(_dev(x[100:]))
+    ref = dedup.greedy(x, 0.95)
+    assert np.array_equal(rep2.cpu().numpy(), ref["rep"][100:])
+
+
+def test_empty_batch(lam):
+    import torch
+    s = lam.Store(64, 0.95, 10)
+    rep, st = s.ingest(torch.empty((0, 64), dtype=torch.float32, device="cuda"))
+    assert rep.numel() == 0 and st["n_in"] == 0 and s.size == 0

@@ -1,0 +1,148 @@
+"""GPU parity of dequant-fused top-k scoring against the oracle: scores within
+1e-5 of the oracle's binary64 scores, ids equal except where the oracle's own
+scores are within twice the tolerance of each other, bound eps*||q||_1."""
+import numpy as np
+import pytest
+
+import synth
+from oracle import dedup, qeps, score
+
+pytestmark = pytest.mark.gpu
+TOL = 1e-5
+
+
+def _dev(a):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def _compare(gs, gi, codes_rows, ids, q, eps, k, tol=TOL):
+    """gs/gi: GPU top-k.  Every returned id must be a stored id whose oracle
+    score is within tol of the GPU score; the returned set must be a valid
+    top-k: each GPU score >= the oracle's k-th score - 2 tol."""
+    S = score.scores(q, codes_rows, eps)
+    ts, ti = score.topk(S, ids, k)
+    pos = {int(v): i for i, v in enumerate(ids.tolist())}
+    worst = 0.0
+    for j in range(q.shape[0]):
+        nvalid = min(k, len(ids))
+        assert np.all(gi[j, nvalid:] == -1)
+        row = [pos[int(v)] for v in gi[j, :nvalid]]
+        assert len(set(row)) == nvalid
+        err = np.abs(gs[j, :nvalid].astype(np.float64) - S[j, row])
+        worst = max(worst, float(err.max()) if nvalid else 0.0)
+        assert np.all(err <= tol), (j, err.max())
+        assert np.all(S[j, row] >= ts[j, nvalid - 1] - 2 * tol)
+        # positions where the oracle order is separated by more than 2 tol agree
+        gap_ok = np.ones(nvalid, bool)
+        sj = np.concatenate([[np.inf], ts[j, :nvalid], [ts[j, nvalid] if nvalid < k else -np.inf]])
+        for p in range(nvalid):
+            gap_ok[p] = (sj[p] - sj[p + 1] > 2 * tol) and (sj[p + 1] - sj[p + 2] > 2 * tol)
+        assert np.array_equal(gi[j, :nvalid][gap_ok], ti[j, :nvalid][gap_ok])
+    return worst
+
+
+def _store_from_rows(lam, x, tau=1.0, spare=0):
+    s = lam.Store(x.shape[1], tau, x.shape[0] + spare)
+    xd = _dev(x)
+    for b0 in range(0, x.shape[0], 4096):
+        s.ingest(xd[b0:b0 + 4096])
+    return s
+
+
+def test_tiny_end_to_end(lam):
+    t = synth.tiny_ingest()
+    x, tau, eps, k, q = t["x"], t["tau"], t["eps"], t["k"], t["q"]
+    ref = dedup.greedy(x, tau)
+    kept = ref["kept"]
+    s = lam.Store(x.shape[1], tau, x.shape[0])
+    xd = _dev(x)
+    for b0 in range(0, x.shape[0], 1024):
+        s.ingest(xd[b0:b0 + 1024])
+    p = s.quantize(eps)
+    codes_ref = qeps.codes(x[kept], eps)
+    plan = qeps.plan(eps, float(np.abs(x[kept]).max()))
+    assert p.bits == plan["bits"]
+    assert np.array_equal(s.codes().cpu().numpy().view(np.uint32), qeps.pack(codes_ref, p.bits))
+    gs, gi, gb = s.score_topk(_dev(q), k)
+    worst = _compare(gs.cpu().numpy(), gi.cpu().numpy(), codes_ref.reshape(kept.size, -1), kept, q, eps, k)
+    beta = score.bound(q, eps)
+    gbn = gb.cpu().numpy().astype(np.float64)
+    assert np.all(gbn >= beta) and np.all(gbn - beta <= np.spacing(gbn.astype(np.float32)))
+    print(f"max |score - oracle| = {worst:.3g}")
+
+
+@pytest.mark.parametrize("k", [1, 10, 16, 17, 50, 64])
+@pytest.mark.parametrize("n", [5, 300, 1000])
+def test_ragged_sizes_and_k(lam, k, n):
+    rng = np.random.default_rng(n * 100 + k)
+    x = synth.unit_rows(rng, n, 96).astype(np.float32)
+    q = synth.unit_rows(rng, 37, 96).astype(np.float32)
+    s = _store_from_rows(lam, x)
+    s.quantize(1e-3, absmax=1.0)
+    gs, gi, _ = s.score_topk(_dev(q), k)
+    c = qeps.codes(x, 1e-3).reshape(n, -1)
+    _compare(gs.cpu().numpy(), gi.cpu().numpy(), c, np.arange(n), q, 1e-3, k)
+
+
+def test_duplicate_rows_tie_break_by_id(lam):
+    rng = np.random.default_rng(2)
+    base = synth.unit_rows(rng, 40, 64).astype(np.float32)
+    x = np.concatenate([base, base + np.float32(0.0)])   # exact copies, later ids
+    s = lam.Store(64, 1.0, 80)
+    # tau = 1 merges exact copies; keep them by ingesting a slightly moved copy
+    x[40:, 0] += np.float32(1e-2)
+    s.ingest(_dev(x))
+    s.quantize(0.02, absmax=1.0)     # coarse step: moved copies share codes
+    c = qeps.codes(x, 0.02).reshape(80, -1)
+    q = synth.unit_rows(rng, 8, 64).astype(np.float32)
+    gs, gi, _ = s.score_topk(_dev(q), 20)
+    _compare(gs.cpu().numpy(), gi.cpu().numpy(), c, np.arange(80), q, 0.02, 20)
+
+
+def test_invalid_query_rows(lam):
+    rng = np.random.default_rng(3)
+    x = synth.unit_rows(rng, 200, 64).astype(np.float32)
+    s = _store_from_rows(lam, x)
+    s.quantize(1e-3)
+    q = synth.unit_rows(rng, 4, 64).astype(np.float32)
+    q[2, 5] = np.inf
+    gs, gi, gb = s.score_topk(_dev(q), 5)
+    gs, gi, gb = gs.cpu().numpy(), gi.cpu().numpy(), gb.cpu().numpy()
+    assert np.all(np.isnan(gs[2])) and np.all(gi[2] == -1) and np.isnan(gb[2])
+    assert np.all(gi[[0, 1, 3]] >= 0)
+
+
+def test_state_errors(lam):
+    rng = np.random.default_rng(4)
+    x = synth.unit_rows(rng, 50, 64).astype(np.float32)
+    s = _store_from_rows(lam, x, spare=10)
+    with pytest.raises(lam.LamError) as e:
+        s.score_topk(_dev(x[:2]), 3)
+    assert e.value.name == "LAM_ESTATE"
+    s.quantize(1e-3)
+    s.ingest(_dev(synth.unit_rows(rng, 5, 64).astype(np.float32)))
+    with pytest.raises(lam.LamError) as e:
+        s.score_topk(_dev(x[:2]), 3)
+    assert e.value.name == "LAM_ESTATE"
+    s.quantize(1e-3)
+    with pytest.raises(lam.LamError) as e:
+        s.score_topk(_dev(x[:2]), 65)
+    assert e.value.name == "LAM_EINVAL"
+
+
+def test_corpus_sampled(lam):
+    """361,802 clustered rows quantized at eps = 1e-3, 4,096 queries, top-10:
+    the benchmark's launch configuration; oracle scores on a sample of 64
+    queries against the whole store."""
+    cfg = synth.corpus_retrieval()
+    x, q, eps, k = cfg["x"], cfg["q"], cfg["eps"], cfg["k"]
+    s = _store_from_rows(lam, x)
+    p = s.quantize(eps)
+    gs, gi, _ = s.score_topk(_dev(q), k)
+    gs, gi = gs.cpu().numpy(), gi.cpu().numpy()
+    c = qeps.codes(x, eps).reshape(x.shape[0], -1)
+    assert p.bits == qeps.plan(eps, float(np.abs(x).max()))["bits"]
+    sample = np.random.default_rng(0).choice(q.shape[0], 64, replace=False)
+    worst = _compare(gs[sample], gi[sample], c, np.arange(x.shape[0]), q[sample], eps, k)
+    print(f"corpus: max |score - oracle| = {worst:.3g}")
