@@ -1,0 +1,228 @@
+#!/usr/bin/env python3
+"""Benchmark of the LAM hot path on one MI355X.
+
+One step is one pass of the whole hot path over synthetic inputs shaped like
+the paper's workloads:
+  1. Q_eps encode + decode of 2^26 float32 values (half N(0, 0.04^2), half
+     U(-1, 1)) at eps = 1e-3 with a declared absmax of 1 (10-bit codes); four
+     input sets rotate so that no pass reads from the 256 MB last-level cache;
+  2. the greedy near-duplicate test over the 27,986-row subset stream (600
+     trajectories of ~47 chunks, D = 768) in batches of 1,024, tau = 0.95,
+     into a cleared store;
+  3. Q_eps of the retained store at eps = 1e-3 (absmax measured on the GPU),
+     and its decode;
+  4. top-10 scoring of 1,024 queries against the quantized store.
+value = near-duplicate pairs per second of the whole step, counting the
+algorithmic pairs of exhaustive greedy (each arrival against every row
+retained at its arrival).
+
+Usage: python bench.py [--steps K] [--warmup W] [--no-cpu-baseline]
+Prints one JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, published
+MFMA_F16_PEAK_TFLOPS = 2500.0  # MI355X dense fp16 matrix, published
+D = 768
+EPS = 1e-3
+TAU = 0.95
+BATCH = 1024
+TOPK = 10
+RAW_LOG2N = 26
+RAW_SETS = 4
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--no-cpu-baseline", action="store_true", help="skip timing the CPU oracle")
+    return ap.parse_args()
+
+
+def cpu_baseline(x, pairs):
+    """The oracle, as it stands, on the same subset stream (dedup only)."""
+    import numpy as np  # noqa: F401
+    from oracle import dedup
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
+    except Exception:
+        threads = os.cpu_count() or 1
+    t0 = time.perf_counter()
+    r = dedup.greedy(x, TAU, block=512)
+    dt = time.perf_counter() - t0
+    return r, {"value": pairs / dt / 1e6, "unit": "M pairs/s", "cores": int(threads), "kind": "oracle",
+               "seconds": dt,
+               "sample": f"exhaustive greedy over the whole {x.shape[0]}-row subset stream (ingest only; "
+                         f"binary64 BLAS screen + exact rational ties)"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU: this build has no multi-GPU path (asked for --gpus {args.gpus})",
+              file=sys.stderr)
+        sys.exit(2)
+    sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
+    import numpy as np
+    import torch
+    import synth
+    import paper_2609_32256_amd as lam
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    # ------------------------------------------------------------ inputs (resident in HBM)
+    raw = synth.raw_qeps(log2n=RAW_LOG2N)["x"]
+    n_raw = raw.size
+    raw_sets = [torch.from_numpy(raw).to(dev)]
+    for s in range(1, RAW_SETS):   # same values, distinct buffers (cache rotation)
+        raw_sets.append(raw_sets[0].clone())
+    p_raw = lam.qeps_plan(EPS, 1.0, "bits", n_raw)
+    raw_codes = [torch.empty(p_raw.code_bytes // 4, dtype=torch.int32, device=dev) for _ in range(RAW_SETS)]
+    raw_out = [torch.empty(n_raw, dtype=torch.float32, device=dev) for _ in range(RAW_SETS)]
+
+    cfg = synth.subset_ingest()
+    x = cfg["x"]
+    xd = torch.from_numpy(x).to(dev)
+    qd = torch.from_numpy(cfg["q"]).to(dev)
+    n = x.shape[0]
+    ctx = lam.default_context()
+    store = lam.Store(D, TAU, n, ctx=ctx)
+    xhat = torch.empty((n, D), dtype=torch.float32, device=dev)
+    topk_out = (torch.empty((qd.shape[0], TOPK), dtype=torch.float32, device=dev),
+                torch.empty((qd.shape[0], TOPK), dtype=torch.int64, device=dev),
+                torch.empty(qd.shape[0], dtype=torch.float32, device=dev))
+    reps = [torch.empty(min(BATCH, n - b0), dtype=torch.int64, device=dev) for b0 in range(0, n, BATCH)]
+
+    def step(i):
+        k = i % RAW_SETS
+        _, p = lam.quantize(raw_sets[k], EPS, absmax=1.0, out=raw_codes[k], ctx=ctx)
+        lam.dequantize(raw_codes[k], p, out=raw_out[k], ctx=ctx)
+        store.clear()
+        for bi, b0 in enumerate(range(0, n, BATCH)):
+            store.ingest(xd[b0:b0 + BATCH], rep=reps[bi])
+        store.quantize(EPS)
+        store.dequantize(out=xhat)
+        store.score_topk(qd, TOPK, out=topk_out)
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+
+    # algorithmic pair counts from the decisions (identical every step)
+    rep = torch.cat(reps).cpu().numpy()
+    kept = rep < 0
+    kept_before = np.concatenate([[0], np.cumsum(kept)[:-1]])
+    pairs = int(kept_before.sum())                       # sum over arrivals of |R| at arrival
+    screen_store_pairs = 0
+    screen_chunk_pairs = 0
+    for b0 in range(0, n, BATCH):
+        nb = min(BATCH, n - b0)
+        screen_store_pairs += nb * int(kept_before[b0])
+        screen_chunk_pairs += nb * (nb - 1) // 2
+    n_store = int(kept.sum())
+    info = store.info()
+
+    ctx.profile_reset()
+    ctx.profile(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(args.warmup + i)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ctx.profile(False)
+    ms = (t1 - t0) * 1e3 / args.steps
+
+    kinfo = {}
+    for name in ("qeps_encode", "qeps_decode", "dedup_prep", "dedup_screen_store", "dedup_screen_chunk",
+                 "dedup_verify", "dedup_resolve", "dedup_append", "store_absmax", "store_encode", "store_decode",
+                 "score_prep", "score_mfma", "score_merge"):
+        tot, cnt = ctx.profile_read(name)
+        if cnt:
+            kinfo[name] = {"ms_per_step": tot / args.steps, "launches_per_step": cnt / args.steps,
+                           "avg_launch_ms": tot / cnt}
+    bq = p_raw.bits / 8.0
+    store_elems = n_store * D
+    bs = info.q.bits / 8.0
+    work = {  # algorithmic units per step: (amount, unit, peak, bound)
+        "qeps_encode": ((4 + bq) * n_raw / 1e9, "GB", HBM_PEAK_GBS, "hbm"),
+        "qeps_decode": ((4 + bq) * n_raw / 1e9, "GB", HBM_PEAK_GBS, "hbm"),
+        "store_encode": ((4 + bs) * store_elems / 1e9, "GB", HBM_PEAK_GBS, "hbm"),
+        "store_decode": ((4 + bs) * store_elems / 1e9, "GB", HBM_PEAK_GBS, "hbm"),
+        "dedup_screen_store": (2.0 * D * screen_store_pairs / 1e12, "TFLOP", MFMA_F16_PEAK_TFLOPS, "mfma"),
+        "dedup_screen_chunk": (2.0 * D * screen_chunk_pairs / 1e12, "TFLOP", MFMA_F16_PEAK_TFLOPS, "mfma"),
+        "score_mfma": (2.0 * D * qd.shape[0] * n_store / 1e12, "TFLOP", MFMA_F16_PEAK_TFLOPS, "mfma"),
+    }
+    for name, (amt, unit, peak, bound) in work.items():
+        if name in kinfo:
+            rate = amt / (kinfo[name]["ms_per_step"] / 1e3)
+            kinfo[name].update({"achieved": rate, "unit": unit + "/s", "peak": peak, "frac": rate / peak})
+    dominant = max(kinfo, key=lambda k: kinfo[k]["ms_per_step"])
+    dom_work = work.get(dominant)
+    if dom_work:
+        d = kinfo[dominant]
+        per_launch = dom_work[0] / d["launches_per_step"]
+        achieved = per_launch / (d["avg_launch_ms"] / 1e3)
+        roofline = {"kernel": dominant, "bound": dom_work[3], "achieved": achieved,
+                    "peak": dom_work[2], "unit": "GB/s" if dom_work[1] == "GB" else "TFLOP/s",
+                    "frac": achieved / dom_work[2], "traffic": None}
+    else:
+        roofline = {"kernel": dominant, "bound": "latency", "achieved": None, "peak": None, "unit": None,
+                    "frac": None, "traffic": None}
+
+    value = pairs / (ms / 1e3) / 1e6
+    enc = kinfo.get("qeps_encode", {})
+    out = {
+        "metric": "Q_eps encode GB/s; near-dup M pairs/s at D=768; queries/s; % of roofline",
+        "value": value,
+        "unit": "M pairs/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16",
+        "data": "synthetic",
+        "config": {
+            "workload": (f"subset ingest: {n} x {D} float32 unit rows in 600 trajectories, batches of {BATCH}, "
+                         f"tau={TAU}; store Q_eps eps={EPS} + decode; {qd.shape[0]} queries top-{TOPK}; "
+                         f"plus raw Q_eps encode+decode of 2^{RAW_LOG2N} float32 at eps={EPS}"),
+            "pairs_per_step": pairs,
+            "retained": n_store,
+            "store_code_bits": int(info.q.bits),
+            "raw_code_bits": int(p_raw.bits),
+        },
+        "qeps_encode_GBps": enc.get("achieved", 0.0) * 1.0 if enc else None,
+        "queries_per_s": (qd.shape[0] / (sum(kinfo[k]["ms_per_step"] for k in ("score_prep", "score_mfma",
+                                                                                "score_merge") if k in kinfo)
+                                          / 1e3)),
+        "roofline": roofline,
+        "kernels": kinfo,
+    }
+    if not args.no_cpu_baseline:
+        ref, cb = cpu_baseline(x, pairs)
+        if not np.array_equal(ref["rep"], rep):
+            raise SystemExit("GPU decisions differ from the oracle on the benchmark stream")
+        out["cpu_baseline"] = cb
+    else:
+        out["cpu_baseline"] = None
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -24,7 +24,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "liblam.so")
 
 if not os.path.exists(LIB_PATH):
-    raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2609_32256_amd.build`")
+    raise ImportError(f"{LIB_PATH} is missing: build it with `python paper_2609_32256_amd/build.py`")
 
 _lib = ctypes.CDLL(LIB_PATH)
 

@@ -1,6 +1,8 @@
 """Builds liblam.so (HIP, gfx950) in place, next to this file.
 
-    python -m paper_2609_32256_amd.build        # or build() from Python
+    python paper_2609_32256_amd/build.py        # or __graft_entry__.build()
+
+(Run it as a script: importing the package itself needs the built library.)
 
 Every source is compiled for gfx950 only, with packed-fp32 instruction
 selection disabled, then linked into one shared library exporting the C ABI

@@ -104,7 +104,8 @@ lam_status read_flags(lam_ctx* ctx) {
 
 // Shared body of lam_quantize and lam_store_quantize.
 lam_status quantize_impl(lam_ctx* ctx, const float* x, int64_t n, double eps, float absmax, int mode,
-                         uint32_t* codes, uint64_t cap, lam_qparams* out, DevBuf* grow_into) {
+                         uint32_t* codes, uint64_t cap, lam_qparams* out, DevBuf* grow_into,
+                         bool store_path = false) {
   lam_qparams p{};
   // argument checks that do not depend on the data
   LAM_TRY(qeps_plan_host(eps, 0.0f, mode, n, &p));
@@ -112,7 +113,7 @@ lam_status quantize_impl(lam_ctx* ctx, const float* x, int64_t n, double eps, fl
   LAM_TRY(clear_flags(ctx));
   float a = absmax;
   if (!(absmax > 0.0f)) {
-    LAM_TRY(launch_absmax(ctx, x, n, &ctx->flags_dev->absmax_bits));
+    LAM_TRY(launch_absmax(ctx, x, n, &ctx->flags_dev->absmax_bits, store_path ? "store_absmax" : "qeps_absmax"));
     LAM_TRY(read_flags(ctx));
     const uint32_t bits = ctx->flags_host->absmax_bits;
     LAM_CHECK(bits < 0x7f800000u, LAM_EINVAL, "input holds NaN or Inf");
@@ -127,7 +128,7 @@ lam_status quantize_impl(lam_ctx* ctx, const float* x, int64_t n, double eps, fl
   LAM_CHECK(codes != nullptr || n == 0, LAM_EINVAL, "codes buffer is NULL");
   LAM_CHECK(cap >= p.code_bytes, LAM_EINVAL, "codes capacity %llu < %llu bytes needed",
             (unsigned long long)cap, (unsigned long long)p.code_bytes);
-  LAM_TRY(launch_encode(ctx, x, n, p, codes, &ctx->flags_dev->nonfinite));
+  LAM_TRY(launch_encode(ctx, x, n, p, codes, &ctx->flags_dev->nonfinite, store_path ? "store_encode" : "qeps_encode"));
   LAM_TRY(read_flags(ctx));
   LAM_CHECK(ctx->flags_host->nonfinite == 0, LAM_EINVAL, "input holds NaN or Inf (%u elements)",
             ctx->flags_host->nonfinite);
@@ -339,7 +340,7 @@ lam_status lam_store_quantize(lam_ctx* ctx, lam_store* st, double eps, float abs
   const int64_t n = st->size * (int64_t)st->dim;
   DevBuf holder{st->codes, st->codes_cap};
   lam_qparams p{};
-  lam_status s = quantize_impl(ctx, st->x32, n, eps, absmax, mode, nullptr, 0, &p, &holder);
+  lam_status s = quantize_impl(ctx, st->x32, n, eps, absmax, mode, nullptr, 0, &p, &holder, true);
   st->codes = holder.as<uint32_t>();
   st->codes_cap = holder.bytes;
   if (s != LAM_OK) {
@@ -372,7 +373,7 @@ lam_status lam_store_dequantize(lam_ctx* ctx, const lam_store* st, float* xhat_d
   LAM_CHECK(xhat_dev != nullptr || st->size == 0, LAM_EINVAL, "xhat is NULL");
   LAM_CHECK(((uintptr_t)xhat_dev & 3u) == 0, LAM_EINVAL, "xhat must be 4-byte aligned");
   DeviceGuard g(ctx->device);
-  return launch_decode(ctx, st->codes, st->q, xhat_dev);
+  return launch_decode(ctx, st->codes, st->q, xhat_dev, "store_decode");
 }
 
 lam_status lam_store_export(lam_ctx* ctx, const lam_store* st, int64_t* ids_dev, uint32_t* codes_dev,

@@ -134,10 +134,12 @@ lam_status read_flags(lam_ctx* ctx);
 
 // ------------------------------------------------------------------ Q_eps (qeps.hip)
 lam_status qeps_plan_host(double eps, float absmax, int mode, int64_t n, lam_qparams* out);
-lam_status launch_absmax(lam_ctx* ctx, const float* x, int64_t n, uint32_t* absmax_bits_dev);
+lam_status launch_absmax(lam_ctx* ctx, const float* x, int64_t n, uint32_t* absmax_bits_dev,
+                         const char* prof_name = "qeps_absmax");
 lam_status launch_encode(lam_ctx* ctx, const float* x, int64_t n, const lam_qparams& p,
-                         uint32_t* codes, uint32_t* viol_dev);
-lam_status launch_decode(lam_ctx* ctx, const uint32_t* codes, const lam_qparams& p, float* xhat);
+                         uint32_t* codes, uint32_t* viol_dev, const char* prof_name = "qeps_encode");
+lam_status launch_decode(lam_ctx* ctx, const uint32_t* codes, const lam_qparams& p, float* xhat,
+                         const char* prof_name = "qeps_decode");
 
 // ------------------------------------------------------------------ dedup (dedup.hip)
 lam_status dedup_ingest(lam_ctx* ctx, lam_store* st, const float* x, int64_t n, int64_t* rep,

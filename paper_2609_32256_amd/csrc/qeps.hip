@@ -248,12 +248,12 @@ lam_status qeps_plan_host(double eps, float absmax, int mode, int64_t n, lam_qpa
   return LAM_OK;
 }
 
-lam_status launch_absmax(lam_ctx* ctx, const float* x, int64_t n, uint32_t* absmax_bits_dev) {
+lam_status launch_absmax(lam_ctx* ctx, const float* x, int64_t n, uint32_t* absmax_bits_dev, const char* prof_name) {
   if (n == 0) return LAM_OK;
   const bool vec = ((uintptr_t)x & 15u) == 0;
   const int64_t work = vec ? (n + 3) / 4 : n;
   const int blocks = (int)std::min<int64_t>(4096, (work + kThreads - 1) / kThreads);
-  ProfScope ps(ctx, "qeps_absmax");
+  ProfScope ps(ctx, prof_name);
   if (vec)
     hipLaunchKernelGGL(k_absmax<true>, dim3(blocks), dim3(kThreads), 0, ctx->stream, x, n, absmax_bits_dev);
   else
@@ -263,27 +263,27 @@ lam_status launch_absmax(lam_ctx* ctx, const float* x, int64_t n, uint32_t* absm
 }
 
 lam_status launch_encode(lam_ctx* ctx, const float* x, int64_t n, const lam_qparams& p, uint32_t* codes,
-                         uint32_t* flags2) {
+                         uint32_t* flags2, const char* prof_name) {
   if (n == 0) return LAM_OK;
   LAM_CHECK(p.bits >= 1 && p.bits <= 32, LAM_EINVAL, "bad code width %d", p.bits);
   const bool vec = ((uintptr_t)x & 15u) == 0;
   const int64_t tiles = (n + kTile - 1) / kTile;
   LAM_CHECK(tiles < (1LL << 31), LAM_EINVAL, "too many elements");
   const uint64_t nwords = p.code_bytes / 4u;
-  ProfScope ps(ctx, "qeps_encode");
+  ProfScope ps(ctx, prof_name);
   encode_dispatch<1>(p.bits, vec, dim3((unsigned)tiles), ctx->stream, x, n, p.step, p.eps, p.absmax, codes,
                      nwords, flags2);
   LAM_HIP(hipGetLastError());
   return LAM_OK;
 }
 
-lam_status launch_decode(lam_ctx* ctx, const uint32_t* codes, const lam_qparams& p, float* xhat) {
+lam_status launch_decode(lam_ctx* ctx, const uint32_t* codes, const lam_qparams& p, float* xhat, const char* prof_name) {
   if (p.n == 0) return LAM_OK;
   LAM_CHECK(p.bits >= 1 && p.bits <= 32, LAM_EINVAL, "bad code width %d", p.bits);
   const bool vec = ((uintptr_t)xhat & 15u) == 0;
   const int64_t tiles = (p.n + kTile - 1) / kTile;
   LAM_CHECK(tiles < (1LL << 31), LAM_EINVAL, "too many elements");
-  ProfScope ps(ctx, "qeps_decode");
+  ProfScope ps(ctx, prof_name);
   decode_dispatch<1>(p.bits, vec, dim3((unsigned)tiles), ctx->stream, codes, p.n, (uint64_t)(p.code_bytes / 4u),
                      p.step, xhat);
   LAM_HIP(hipGetLastError());
