@@ -147,7 +147,7 @@ def main():
     ms = (t1 - t0) * 1e3 / args.steps
 
     kinfo = {}
-    for name in ("qeps_encode", "qeps_decode", "dedup_prep", "dedup_screen_store", "dedup_screen_chunk",
+    for name in ("qeps_encode", "qeps_decode", "dedup_prep", "dedup_screen",
                  "dedup_verify", "dedup_resolve", "dedup_append", "store_absmax", "store_encode", "store_decode",
                  "score_prep", "score_mfma", "score_merge"):
         tot, cnt = ctx.profile_read(name)
@@ -162,8 +162,8 @@ def main():
         "qeps_decode": ((4 + bq) * n_raw / 1e9, "GB", HBM_PEAK_GBS, "hbm"),
         "store_encode": ((4 + bs) * store_elems / 1e9, "GB", HBM_PEAK_GBS, "hbm"),
         "store_decode": ((4 + bs) * store_elems / 1e9, "GB", HBM_PEAK_GBS, "hbm"),
-        "dedup_screen_store": (2.0 * D * screen_store_pairs / 1e12, "TFLOP", MFMA_F16_PEAK_TFLOPS, "mfma"),
-        "dedup_screen_chunk": (2.0 * D * screen_chunk_pairs / 1e12, "TFLOP", MFMA_F16_PEAK_TFLOPS, "mfma"),
+        "dedup_screen": (2.0 * D * (screen_store_pairs + screen_chunk_pairs) / 1e12, "TFLOP",
+                         MFMA_F16_PEAK_TFLOPS, "mfma"),
         "score_mfma": (2.0 * D * qd.shape[0] * n_store / 1e12, "TFLOP", MFMA_F16_PEAK_TFLOPS, "mfma"),
     }
     for name, (amt, unit, peak, bound) in work.items():

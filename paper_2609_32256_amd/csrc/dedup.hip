@@ -55,17 +55,14 @@ enum Scratch { S_X16 = 0, S_ROWF, S_CHUNK, S_BITMAP, S_PAIRS, S_STATUS, S_G };
 
 struct StoreMeta {
   int32_t m;              // retained rows
-  uint32_t ebmax_bits;    // max per-row error term over retained rows (float bits)
-  uint32_t l2max_bits;
-  uint32_t pad;
+  uint32_t pad[3];
 };
 
 // Chunk-level counters (in the S_CHUNK scratch, after the per-row arrays).
 struct ChunkCounters {
   uint32_t npairs;        // ambiguous pairs appended in this chunk
-  uint32_t ebmax_bits;    // max error term over the chunk's rows (batch side)
   uint32_t n_escalate;
-  uint32_t pad;
+  uint32_t pad[2];
 };
 
 __device__ __forceinline__ bool skip_all(const DevFlags* f) {
@@ -92,7 +89,7 @@ __device__ __forceinline__ double wave_sum_f64(double v) {
 __global__ __launch_bounds__(256) void k_prep(const float* __restrict__ x, int64_t n, int D,
                                               _Float16* __restrict__ x16, float* __restrict__ hn,
                                               float* __restrict__ eterm, double K1, double K2, double K3h,
-                                              DevFlags* __restrict__ flags, uint32_t* __restrict__ ebmax_call) {
+                                              DevFlags* __restrict__ flags) {
   const int lane = threadIdx.x & 63;
   const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= n) return;
@@ -125,17 +122,21 @@ __global__ __launch_bounds__(256) void k_prep(const float* __restrict__ x, int64
     if (br) atomicAdd(&flags->out_of_range, 1u);
     hn[row] = (float)(0.5 * na);
     const double et = K1 * 0.5 * na + K2 * l1 + K3h + 0x1p-23 * (na + 1.0);
-    const float e = round_up_f32(et);
-    eterm[row] = e;
-    if (!(bn | br)) atomicMax(ebmax_call, __float_as_uint(e));
+    eterm[row] = round_up_f32(et);
   }
 }
 
 // ------------------------------------------------------------------ chunk init
+// Clears the chunk's hit/edge state; for the first chunk of a call it also
+// clears the context's status words and sets the store size (one launch
+// instead of three).
 __global__ void k_chunk_init(int nB, int W, int32_t* firstHit, uint32_t* hasEdge, uint32_t* maxcos,
-                             uint64_t* bitmap, ChunkCounters* cc) {
+                             uint64_t* bitmap, ChunkCounters* cc, DevFlags* flags, StoreMeta* meta,
+                             int32_t m_first) {
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   const int64_t t0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (m_first >= 0 && t0 < (int64_t)(sizeof(DevFlags) / 4)) reinterpret_cast<uint32_t*>(flags)[t0] = 0u;
+  if (m_first >= 0 && t0 == 0) meta->m = m_first;
   for (int64_t i = t0; i < nB; i += stride) {
     firstHit[i] = kNone;
     hasEdge[i] = 0u;
@@ -148,24 +149,20 @@ __global__ void k_chunk_init(int nB, int W, int32_t* firstHit, uint32_t* hasEdge
   }
 }
 
-__global__ void k_set_meta(StoreMeta* meta, int32_t m) {
-  if (threadIdx.x == 0 && blockIdx.x == 0) meta->m = m;
-}
-
 // ------------------------------------------------------------------ screens
 struct ScreenArgs {
-  const _Float16* A;        // rows of the "earlier" side (store rows, or chunk rows)
+  const _Float16* As;       // store rows (fp16 x 2^8)
+  const float* hnS;         // ||y||^2 / 2 of store rows
+  const float* etS;         // error term of store rows
+  const StoreMeta* meta;    // store size
   const _Float16* B;        // chunk rows (arrivals)
-  const float* hnA;         // ||a||^2 / 2 of A rows
-  const float* hnB;         // ||b||^2 / 2 of B rows
-  const float* etB;         // per-row error term of B rows
-  const uint32_t* ebmaxA;   // max error term over A rows (float bits)
-  const StoreMeta* meta;    // store size (store screen)
-  int nA;                   // A rows (chunk screen) -- store screen reads meta->m
+  const float* hnB;         // ||b||^2 / 2 of chunk rows
+  const float* etB;         // error term of chunk rows
   int nB;
   int D;
-  int ntB;                  // B tiles
-  int64_t nblocks;
+  int ntB;                  // chunk tiles
+  int64_t nb0;              // workgroups screening against the store (first in the grid)
+  int64_t nb1;              // workgroups screening inside the chunk (lower triangle)
   double half_d2;           // delta^2 / 2
   int32_t* firstHit;        // store screen
   uint32_t* maxcos;         // store screen, order-encoded (WANT_MAX)
@@ -190,38 +187,54 @@ __device__ __forceinline__ void push_pair(const ScreenArgs& a, int i, int kind, 
   }
 }
 
-// MODE 0: A = store, B = chunk.  MODE 1: A = B = chunk, pairs (ia < ib).
-template <int MODE, bool WANT_MAX>
+// One launch screens a chunk against the store (workgroups [0, nb0), MODE 0:
+// A = store rows, B = chunk rows) and against itself (workgroups
+// [nb0, nb0 + nb1), MODE 1: A = B = chunk rows, pairs ia < ib only).  The
+// A side of the error bound is the largest per-row term among the tile's own
+// A rows.
+template <bool WANT_MAX>
 __global__ __launch_bounds__(kWG) void k_screen(ScreenArgs a) {
   __shared__ _Float16 lds[4 * kTB * kLdk];
   __shared__ float hbA[kTB];
+  __shared__ float emx[2];
   if (skip_all(a.flags)) return;
-  const int64_t logical = xcd_remap(blockIdx.x, a.nblocks);
+  const int MODE = (blockIdx.x < a.nb0) ? 0 : 1;
   int ta, tb;
   if (MODE == 0) {
+    const int64_t logical = xcd_remap(blockIdx.x, a.nb0);
     ta = (int)(logical / a.ntB);
     tb = (int)(logical % a.ntB);
   } else {
     // lower-triangular tile pairs ta <= tb, row-major over tb
+    const int64_t logical = xcd_remap(blockIdx.x - a.nb0, a.nb1);
     int t = (int)((sqrt(8.0 * (double)logical + 1.0) - 1.0) * 0.5);
     while ((int64_t)(t + 1) * (t + 2) / 2 <= logical) ++t;
     while ((int64_t)t * (t + 1) / 2 > logical) --t;
     tb = t;
     ta = (int)(logical - (int64_t)t * (t + 1) / 2);
   }
-  const int nA = (MODE == 0) ? a.meta->m : a.nA;
+  const _Float16* A = MODE == 0 ? a.As : a.B;
+  const float* hnA = MODE == 0 ? a.hnS : a.hnB;
+  const float* etA = MODE == 0 ? a.etS : a.etB;
+  const int nA = (MODE == 0) ? a.meta->m : a.nB;
   const int rowsA = min(kTB, nA - ta * kTB);
   const int rowsB = min(kTB, a.nB - tb * kTB);
   if (rowsA <= 0 || rowsB <= 0) return;
-  if (threadIdx.x < kTB) hbA[threadIdx.x] = (threadIdx.x < rowsA) ? a.hnA[ta * kTB + threadIdx.x] : 0.0f;
-
-  floatx16 acc[2][2];
-  gemm_block_f16(a.A + (int64_t)ta * kTB * a.D, rowsA, a.B + (int64_t)tb * kTB * a.D, rowsB, a.D, a.D, lds, acc);
-
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
+  if (threadIdx.x < kTB) {
+    const bool v = threadIdx.x < rowsA;
+    hbA[threadIdx.x] = v ? hnA[ta * kTB + threadIdx.x] : 0.0f;
+    float e = v ? etA[ta * kTB + threadIdx.x] : 0.0f;
+    for (int o = 32; o > 0; o >>= 1) e = fmaxf(e, __shfl_xor(e, o));
+    if (lane == 0) emx[wave] = e;
+  }
+
+  floatx16 acc[2][2];
+  gemm_block_f16(A + (int64_t)ta * kTB * a.D, rowsA, a.B + (int64_t)tb * kTB * a.D, rowsB, a.D, a.D, lds, acc);
+
   const int wm = wave >> 1, wn = wave & 1;
-  const float ebA = __uint_as_float(*a.ebmaxA);
+  const float ebA = fmaxf(emx[0], emx[1]);
 #pragma unroll
   for (int tj = 0; tj < 2; ++tj) {
     const int ibl = wn * 64 + tj * 32 + (lane & 31);
@@ -373,32 +386,25 @@ struct ResolveArgs {
   DevFlags* flags;
 };
 
-// One wave.  Lane L owns bits [64L, 64L + 64) of the chunk's kept mask.
-__global__ __launch_bounds__(64) void k_resolve(ResolveArgs a) {
-  if (skip_all(a.flags)) return;
-  const int lane = threadIdx.x;
+constexpr int kResolveThreads = 1024;
+constexpr int kEdgeCap = 20480;    // in-chunk candidate entries held in LDS
+
+// Fallback when the candidate lists do not fit in LDS: one wave walks the
+// undecided rows in arrival order; lane L keeps bits [64L, 64L + 64) of the
+// kept mask in a register, and a row takes the lowest kept candidate of its
+// bitmap row.
+__device__ void resolve_sequential(const ResolveArgs& a, volatile uint8_t* st) {
+  const int lane = threadIdx.x & 63;
   const int nblk = (a.nB + 63) >> 6;
   uint64_t kept = 0ull;
+  for (int w = 0; w < nblk; ++w) {
+    const int r = w * 64 + lane;
+    const uint64_t b = __ballot(r < a.nB && st[r] == 1);
+    if (lane == w) kept = b;
+  }
   for (int blk = 0; blk < nblk; ++blk) {
     const int r = blk * 64 + lane;
-    const bool v = r < a.nB;
-    const int32_t hit = v ? a.firstHit[r] : kNone;
-    const bool edge = v && a.hasEdge[r] != 0u;
-    const bool plain_keep = v && hit == kNone && !edge;
-    const bool active = v && hit == kNone && edge;
-    const uint64_t pk = __ballot(plain_keep);
-    if (lane == blk) kept |= pk;
-    if (v && hit != kNone) {
-      a.rep[r] = a.store_ids[hit];
-      a.rep_row[r] = hit;
-    } else if (plain_keep) {
-      a.rep[r] = -1;
-      a.rep_row[r] = -1;
-    }
-    uint64_t act = __ballot(active);
-    // Active rows in increasing order; each needs every earlier row decided,
-    // which holds because rows are visited in order and decisions of plain rows
-    // (store hit / no edge) do not depend on other rows.
+    uint64_t act = __ballot(r < a.nB && st[r] == 0);
     while (act) {
       const int b = __builtin_ctzll(act);
       act &= act - 1ull;
@@ -412,40 +418,171 @@ __global__ __launch_bounds__(64) void k_resolve(ResolveArgs a) {
         const uint64_t uf = __shfl(u, F);
         const int j = F * 64 + __builtin_ctzll(uf);
         if (lane == 0) {
+          st[i] = 2;
           a.rep[i] = a.gbase + j;
           a.rep_row[i] = -(j + 2);
         }
       } else {
         if (lane == blk) kept |= 1ull << b;
         if (lane == 0) {
+          st[i] = 1;
           a.rep[i] = -1;
           a.rep_row[i] = -1;
         }
       }
     }
   }
-  // positions of kept rows
-  const int cnt = __popcll(kept);
-  int pre = cnt;
-  for (int o = 1; o < 64; o <<= 1) {
-    const int t = __shfl_up(pre, o);
-    if (lane >= o) pre += t;
-  }
-  pre -= cnt;  // exclusive prefix
-  const int total = __shfl(pre + cnt, 63);
+}
+
+// In-order resolve of one chunk by one workgroup.
+//  A. Rows with a store hit are dropped (their representative is the lowest
+//     store row); rows with no in-chunk edge are kept.  Neither depends on any
+//     other row of the chunk.  The rest are "active".
+//  B. Each active row's in-chunk candidates (bits j < i of its bitmap row) are
+//     copied into LDS as an ascending list.
+//  C. Rounds: an undecided active row walks its list past dropped rows; the
+//     first non-dropped candidate decides it (kept -> the row is dropped with
+//     that representative), or makes it wait if still undecided; an exhausted
+//     list keeps the row.  A decision is taken only once every earlier
+//     candidate is decided, so it is the one the sequential walk takes, and
+//     the lowest undecided row can always decide, so the rounds end.
+//  D. Kept rows get consecutive store positions in arrival order.
+__global__ __launch_bounds__(kResolveThreads) void k_resolve(ResolveArgs a) {
+  __shared__ uint8_t st_[kChunk];        // 0 undecided, 1 kept, 2 dropped
+  __shared__ uint16_t edges[kEdgeCap];
+  __shared__ uint32_t eoff[kChunk];
+  __shared__ uint16_t elen[kChunk];
+  __shared__ uint16_t ecur[kChunk];
+  __shared__ uint16_t active[kChunk];
+  __shared__ uint32_t n_active, n_edges, pending;
+  __shared__ int wsum[kResolveThreads / 64];
+  volatile uint8_t* st = st_;
+  if (skip_all(a.flags)) return;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int m0 = a.meta->m;
-  a.kept_words[lane] = kept;
-  for (int blk = 0; blk < nblk; ++blk) {
-    const int r = blk * 64 + lane;
-    const uint64_t w = __shfl(kept, blk);
-    const int base = __shfl(pre, blk);
-    if (r < a.nB) {
-      const bool k = (w >> lane) & 1ull;
-      a.pos[r] = k ? m0 + base + __popcll(w & ((1ull << lane) - 1ull)) : -1;
+  if (tid == 0) {
+    n_active = 0u;
+    n_edges = 0u;
+  }
+  __syncthreads();
+  for (int r = tid; r < a.nB; r += kResolveThreads) {
+    const int32_t hit = a.firstHit[r];
+    if (hit != kNone) {
+      st[r] = 2;
+      a.rep[r] = a.store_ids[hit];
+      a.rep_row[r] = hit;
+    } else if (a.hasEdge[r] == 0u) {
+      st[r] = 1;
+      a.rep[r] = -1;
+      a.rep_row[r] = -1;
+    } else {
+      st[r] = 0;
+      active[atomicAdd(&n_active, 1u)] = (uint16_t)r;
     }
   }
   __syncthreads();
-  if (lane == 0) {
+  const int na = (int)n_active;
+  for (int k = wave; k < na; k += kResolveThreads / 64) {
+    const int i = active[k];
+    const int nw = (i + 63) >> 6;
+    uint64_t e = (lane < nw) ? a.bitmap[(int64_t)i * a.W + lane] : 0ull;
+    const int c = __popcll(e);
+    int incl = c;
+    for (int o = 1; o < 64; o <<= 1) {
+      const int t = __shfl_up(incl, o);
+      if (lane >= o) incl += t;
+    }
+    const int tot = __shfl(incl, 63);
+    uint32_t base = 0u;
+    if (lane == 0) base = atomicAdd(&n_edges, (uint32_t)tot);
+    base = __shfl(base, 0);
+    if (base + (uint32_t)tot <= (uint32_t)kEdgeCap) {
+      uint32_t p = base + (uint32_t)(incl - c);
+      while (e) {
+        edges[p++] = (uint16_t)(lane * 64 + __builtin_ctzll(e));
+        e &= e - 1ull;
+      }
+    }
+    if (lane == 0) {
+      eoff[i] = base;
+      elen[i] = (uint16_t)tot;
+      ecur[i] = 0;
+    }
+  }
+  __syncthreads();
+  if (n_edges > (uint32_t)kEdgeCap) {
+    if (wave == 0) resolve_sequential(a, st);
+  } else {
+    for (;;) {
+      if (tid == 0) pending = 0u;
+      __syncthreads();
+      for (int k = tid; k < na; k += kResolveThreads) {
+        const int i = active[k];
+        if (st[i] != 0) continue;
+        const int L = elen[i];
+        const uint32_t b0 = eoff[i];
+        int p = ecur[i];
+        int dec = -1;   // -1 wait, 0 keep, 1 drop
+        int j = -1;
+        for (; p < L; ++p) {
+          j = edges[b0 + p];
+          const uint8_t s = st[j];
+          if (s == 2) continue;
+          dec = (s == 1) ? 1 : -1;
+          break;
+        }
+        if (p == L) dec = 0;
+        ecur[i] = (uint16_t)p;
+        if (dec == 1) {
+          st[i] = 2;
+          a.rep[i] = a.gbase + j;
+          a.rep_row[i] = -(j + 2);
+        } else if (dec == 0) {
+          st[i] = 1;
+          a.rep[i] = -1;
+          a.rep_row[i] = -1;
+        } else {
+          pending = 1u;
+        }
+      }
+      __syncthreads();
+      const bool done = pending == 0u;
+      __syncthreads();
+      if (done) break;
+    }
+  }
+  __syncthreads();
+  // D. store positions: exclusive scan of kept flags, 4 rows per thread
+  const int per = (a.nB + kResolveThreads - 1) / kResolveThreads;
+  const int r0 = tid * per, r1 = min(a.nB, r0 + per);
+  int c = 0;
+  for (int r = r0; r < r1; ++r) c += (st[r] == 1) ? 1 : 0;
+  int x = c;
+  for (int o = 1; o < 64; o <<= 1) {
+    const int t = __shfl_up(x, o);
+    if (lane >= o) x += t;
+  }
+  if (lane == 63) wsum[wave] = x;
+  __syncthreads();
+  if (tid == 0) {
+    int acc = 0;
+    for (int w = 0; w < kResolveThreads / 64; ++w) {
+      const int t = wsum[w];
+      wsum[w] = acc;
+      acc += t;
+    }
+    n_active = (uint32_t)acc;   // reused: kept rows of the chunk
+  }
+  __syncthreads();
+  int pos = m0 + wsum[wave] + x - c;
+  for (int r = r0; r < r1; ++r) a.pos[r] = (st[r] == 1) ? pos++ : -1;
+  for (int w = wave; w < 64; w += kResolveThreads / 64) {
+    const int r = w * 64 + lane;
+    const uint64_t b = __ballot(r < a.nB && st[r] == 1);
+    if (lane == 0) a.kept_words[w] = b;
+  }
+  if (tid == 0) {
+    const int total = (int)n_active;
     a.meta->m = m0 + total;
     atomicAdd(&a.flags->n_kept, (uint32_t)total);
   }
@@ -464,47 +601,56 @@ struct AppendArgs {
   float* xs;
   _Float16* x16s;
   float* hns;
+  float* ets;
   int64_t* ids;
-  StoreMeta* meta;
   DevFlags* flags;
 };
 
-__global__ __launch_bounds__(256) void k_append(AppendArgs a) {
+// One wave per row, four rows per workgroup.  Kept rows are copied into the
+// store; for dropped rows ||x - x_rep||^2 is formed in binary64 (fixed order)
+// and the workgroup's maximum goes to the measured bound with one atomic.
+constexpr int kAppendRows = 4;
+
+__global__ __launch_bounds__(256) void k_append(AppendArgs a, int nB) {
   if (skip_all(a.flags)) return;
-  const int r = blockIdx.x;
-  const int p = a.pos[r];
-  const float* src = a.xc + (int64_t)r * a.D;
-  if (p >= 0) {
-    float* dst = a.xs + (int64_t)p * a.D;
-    for (int d = threadIdx.x * 4; d < a.D; d += 1024)
-      *reinterpret_cast<float4*>(dst + d) = *reinterpret_cast<const float4*>(src + d);
-    const _Float16* s16 = a.x16c + (int64_t)r * a.D;
-    _Float16* d16 = a.x16s + (int64_t)p * a.D;
-    for (int d = threadIdx.x * 8; d < a.D; d += 2048)
-      *reinterpret_cast<uint4*>(d16 + d) = *reinterpret_cast<const uint4*>(s16 + d);
-    if (threadIdx.x == 0) {
-      a.hns[p] = a.hnc[r];
-      a.ids[p] = a.gbase + r;
-      atomicMax(&a.meta->ebmax_bits, __float_as_uint(a.etc[r]));
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  double dmax = 0.0;
+  for (int r = blockIdx.x * kAppendRows + wave; r < min(nB, (int)(blockIdx.x + 1) * kAppendRows); r += 4) {
+    const int p = a.pos[r];
+    const float* src = a.xc + (int64_t)r * a.D;
+    if (p >= 0) {
+      float* dst = a.xs + (int64_t)p * a.D;
+      for (int d = lane * 4; d < a.D; d += 256)
+        *reinterpret_cast<float4*>(dst + d) = *reinterpret_cast<const float4*>(src + d);
+      const _Float16* s16 = a.x16c + (int64_t)r * a.D;
+      _Float16* d16 = a.x16s + (int64_t)p * a.D;
+      for (int d = lane * 8; d < a.D; d += 512)
+        *reinterpret_cast<uint4*>(d16 + d) = *reinterpret_cast<const uint4*>(s16 + d);
+      if (lane == 0) {
+        a.hns[p] = a.hnc[r];
+        a.ets[p] = a.etc[r];
+        a.ids[p] = a.gbase + r;
+      }
+      continue;
     }
-    return;
+    const int rr = a.rep_row[r];
+    const float* b = (rr >= 0) ? a.xs + (int64_t)rr * a.D : a.xc + (int64_t)(-rr - 2) * a.D;
+    double s = 0.0;
+    for (int d = lane; d < a.D; d += 64) {
+      const double t = (double)src[d] - (double)b[d];
+      s = fma(t, t, s);
+    }
+    dmax = fmax(dmax, wave_sum_f64(s));
   }
-  // dropped: ||x - x_rep||^2 in binary64 for the measured bound
-  const int rr = a.rep_row[r];
-  const float* b = (rr >= 0) ? a.xs + (int64_t)rr * a.D : a.xc + (int64_t)(-rr - 2) * a.D;
-  double s = 0.0;
-  for (int d = threadIdx.x; d < a.D; d += 256) {
-    const double t = (double)src[d] - (double)b[d];
-    s = fma(t, t, s);
-  }
-  s = wave_sum_f64(s);
   __shared__ double part[4];
-  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = s;
+  if (lane == 0) part[wave] = dmax;
   __syncthreads();
   if (threadIdx.x == 0) {
-    const double tot = (part[0] + part[1]) + (part[2] + part[3]);
-    atomicMax(reinterpret_cast<unsigned long long*>(&a.flags->dhat2_bits),
-              (unsigned long long)__double_as_longlong(tot));
+    const double m = fmax(fmax(part[0], part[1]), fmax(part[2], part[3]));
+    if (m > 0.0)
+      atomicMax(reinterpret_cast<unsigned long long*>(&a.flags->dhat2_bits),
+                (unsigned long long)__double_as_longlong(m));
   }
 }
 
@@ -534,6 +680,7 @@ lam_status store_alloc(lam_store* st) {
   LAM_HIP(hipMalloc(&st->x32, cap * D * 4));
   LAM_HIP(hipMalloc(&st->x16, cap * D * 2));
   LAM_HIP(hipMalloc(&st->hn, cap * 4));
+  LAM_HIP(hipMalloc(&st->et, cap * 4));
   LAM_HIP(hipMalloc(&st->ids, cap * 8));
   LAM_HIP(hipMalloc(&st->stat_dev, sizeof(StoreMeta)));
   LAM_HIP(hipMemset(st->stat_dev, 0, sizeof(StoreMeta)));
@@ -542,12 +689,12 @@ lam_status store_alloc(lam_store* st) {
 }
 
 void store_free(lam_store* st) {
-  for (void* p : {(void*)st->x32, (void*)st->x16, (void*)st->hn, (void*)st->l1, (void*)st->nrm, (void*)st->ids,
+  for (void* p : {(void*)st->x32, (void*)st->x16, (void*)st->hn, (void*)st->et, (void*)st->ids,
                   (void*)st->stat_dev, (void*)st->codes})
     if (p) (void)hipFree(p);
   st->x32 = nullptr;
   st->x16 = nullptr;
-  st->hn = st->l1 = st->nrm = st->stat_dev = nullptr;
+  st->hn = st->et = st->stat_dev = nullptr;
   st->ids = nullptr;
   st->codes = nullptr;
 }
@@ -659,29 +806,30 @@ lam_status dedup_ingest(lam_ctx* ctx, lam_store* st, const float* x, int64_t n, 
     int2* pairs = ctx->scratch[S_PAIRS].as<int2>();
     uint32_t* status = ctx->scratch[S_STATUS].as<uint32_t>();
 
-    LAM_TRY(clear_flags(ctx));
-    hipLaunchKernelGGL(k_set_meta, dim3(1), dim3(64), 0, ctx->stream, meta, (int32_t)m_before);
-    {
-      ProfScope ps(ctx, "dedup_prep");
-      hipLaunchKernelGGL(k_prep, dim3((unsigned)((n + 3) / 4)), dim3(256), 0, ctx->stream, x, n, D, x16c, hnc, etc,
-                         K.K1, K.K2, K.K3h, ctx->flags_dev, &ctx->flags_dev->ebmax_call_bits);
-    }
-    LAM_HIP(hipGetLastError());
-
     for (int64_t c0 = 0; c0 < n; c0 += CH) {
       const int nB = (int)std::min<int64_t>(CH, n - c0);
       const int ntB = (nB + kTB - 1) / kTB;
       const float* xc = x + c0 * D;
       const _Float16* x16 = x16c + c0 * D;
+      // chunk 0 also clears the status words and sets the store size
       hipLaunchKernelGGL(k_chunk_init, dim3(64), dim3(256), 0, ctx->stream, nB, W, firstHit, hasEdge, maxcos,
-                         bitmap, cc);
+                         bitmap, cc, ctx->flags_dev, meta, c0 == 0 ? (int32_t)m_before : -1);
       LAM_HIP(hipGetLastError());
+      if (c0 == 0) {
+        ProfScope ps(ctx, "dedup_prep");
+        hipLaunchKernelGGL(k_prep, dim3((unsigned)((n + 3) / 4)), dim3(256), 0, ctx->stream, x, n, D, x16c, hnc,
+                           etc, K.K1, K.K2, K.K3h, ctx->flags_dev);
+        LAM_HIP(hipGetLastError());
+      }
 
       ScreenArgs sa{};
+      sa.As = st->x16;
+      sa.hnS = st->hn;
+      sa.etS = st->et;
+      sa.meta = meta;
       sa.B = x16;
       sa.hnB = hnc + c0;
       sa.etB = etc + c0;
-      sa.meta = meta;
       sa.nB = nB;
       sa.D = D;
       sa.ntB = ntB;
@@ -696,37 +844,19 @@ lam_status dedup_ingest(lam_ctx* ctx, lam_store* st, const float* x, int64_t n, 
       sa.pair_cap = cap;
       sa.cc = cc;
       sa.flags = ctx->flags_dev;
-
-      // screen against the store (rows retained before this chunk)
+      // against the store (rows retained before this chunk; the kernel reads
+      // the exact count, the grid covers an upper bound) and inside the chunk
       const int64_t m_ub = m_before + c0;
-      if (m_ub > 0) {
-        ScreenArgs s0 = sa;
-        s0.A = st->x16;
-        s0.hnA = st->hn;
-        s0.ebmaxA = &meta->ebmax_bits;
-        const int64_t ntA = (m_ub + kTB - 1) / kTB;
-        s0.nblocks = ntA * ntB;
-        LAM_CHECK(s0.nblocks < (1LL << 31), LAM_EINVAL, "screen grid too large");
-        ProfScope ps(ctx, "dedup_screen_store");
+      sa.nb0 = ((m_ub + kTB - 1) / kTB) * ntB;
+      sa.nb1 = (int64_t)ntB * (ntB + 1) / 2;
+      const int64_t grid = sa.nb0 + sa.nb1;
+      LAM_CHECK(grid < (1LL << 31), LAM_EINVAL, "screen grid too large");
+      {
+        ProfScope ps(ctx, "dedup_screen");
         if (want_max)
-          hipLaunchKernelGGL((k_screen<0, true>), dim3((unsigned)s0.nblocks), dim3(kWG), 0, ctx->stream, s0);
+          hipLaunchKernelGGL((k_screen<true>), dim3((unsigned)grid), dim3(kWG), 0, ctx->stream, sa);
         else
-          hipLaunchKernelGGL((k_screen<0, false>), dim3((unsigned)s0.nblocks), dim3(kWG), 0, ctx->stream, s0);
-        LAM_HIP(hipGetLastError());
-      }
-      // screen inside the chunk (j < i)
-      if (nB > 1) {
-        ScreenArgs s1 = sa;
-        s1.A = x16;
-        s1.hnA = hnc + c0;
-        s1.ebmaxA = &ctx->flags_dev->ebmax_call_bits;
-        s1.nA = nB;
-        s1.nblocks = (int64_t)ntB * (ntB + 1) / 2;
-        ProfScope ps(ctx, "dedup_screen_chunk");
-        if (want_max)
-          hipLaunchKernelGGL((k_screen<1, true>), dim3((unsigned)s1.nblocks), dim3(kWG), 0, ctx->stream, s1);
-        else
-          hipLaunchKernelGGL((k_screen<1, false>), dim3((unsigned)s1.nblocks), dim3(kWG), 0, ctx->stream, s1);
+          hipLaunchKernelGGL((k_screen<false>), dim3((unsigned)grid), dim3(kWG), 0, ctx->stream, sa);
         LAM_HIP(hipGetLastError());
       }
       VerifyArgs va{pairs, status, cc, cap, xc, st->x32, D, st->d2, firstHit, bitmap, W, hasEdge,
@@ -742,14 +872,15 @@ lam_status dedup_ingest(lam_ctx* ctx, lam_store* st, const float* x, int64_t n, 
                      kept_words, ctx->flags_dev};
       {
         ProfScope ps(ctx, "dedup_resolve");
-        hipLaunchKernelGGL(k_resolve, dim3(1), dim3(64), 0, ctx->stream, ra);
+        hipLaunchKernelGGL(k_resolve, dim3(1), dim3(kResolveThreads), 0, ctx->stream, ra);
         LAM_HIP(hipGetLastError());
       }
       AppendArgs aa{xc, x16, hnc + c0, etc + c0, pos, rep_row, st->n_seen + c0, D, st->x32, st->x16, st->hn,
-                    st->ids, meta, ctx->flags_dev};
+                    st->et, st->ids, ctx->flags_dev};
       {
         ProfScope ps(ctx, "dedup_append");
-        hipLaunchKernelGGL(k_append, dim3((unsigned)nB), dim3(256), 0, ctx->stream, aa);
+        hipLaunchKernelGGL(k_append, dim3((unsigned)((nB + kAppendRows - 1) / kAppendRows)), dim3(256), 0,
+                           ctx->stream, aa, nB);
         LAM_HIP(hipGetLastError());
       }
       if (want_max) {

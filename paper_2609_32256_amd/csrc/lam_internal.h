@@ -64,7 +64,7 @@ struct DevFlags {
   uint32_t n_kept;         // arrivals retained by this ingest
   uint32_t pairs_needed;   // pair-list capacity that would have sufficed
   unsigned long long dhat2_bits;  // max merged d^2 (binary64 bits, non-negative)
-  uint32_t ebmax_call_bits;       // max per-row screen error term over the call's rows
+  uint32_t reserved;
   uint32_t pad;
 };
 
@@ -103,10 +103,9 @@ struct lam_store {
   float* x32 = nullptr;       // float32 rows
   _Float16* x16 = nullptr;    // float16 rows scaled by 2^8 (screen operand)
   float* hn = nullptr;        // ||x||^2 / 2 (float32, rounded to nearest)
-  float* l1 = nullptr;        // ||x||_1 (float32, rounded up)
-  float* nrm = nullptr;       // ||x||_2 (float32, rounded up)
+  float* et = nullptr;        // per-row term of the screen's error bound (float32, rounded up)
   int64_t* ids = nullptr;     // global ids
-  float* stat_dev = nullptr;  // [0] max ||x||_2, [1] max ||x||_1 over rows (as float bits, atomic max)
+  float* stat_dev = nullptr;  // device bookkeeping block (retained-row count)
   // codes
   uint32_t* codes = nullptr;
   uint64_t codes_cap = 0;

@@ -73,7 +73,15 @@ __global__ __launch_bounds__(kThreads) void k_absmax(const float* __restrict__ x
     for (int64_t j = i; j < n; j += stride) m = max(m, __float_as_uint(x[j]) & 0x7fffffffu);
   }
   for (int o = 32; o > 0; o >>= 1) m = max(m, (uint32_t)__shfl_xor((int)m, o));
-  if ((threadIdx.x & 63) == 0) atomicMax(out, m);
+  // one atomic per block: a few hundred updates of one address, not one per wave
+  __shared__ uint32_t wm[kThreads / 64];
+  if ((threadIdx.x & 63) == 0) wm[threadIdx.x >> 6] = m;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t b = wm[0];
+    for (int w = 1; w < kThreads / 64; ++w) b = max(b, wm[w]);
+    atomicMax(out, b);
+  }
 }
 
 template <int B, bool VEC>
@@ -252,7 +260,7 @@ lam_status launch_absmax(lam_ctx* ctx, const float* x, int64_t n, uint32_t* absm
   if (n == 0) return LAM_OK;
   const bool vec = ((uintptr_t)x & 15u) == 0;
   const int64_t work = vec ? (n + 3) / 4 : n;
-  const int blocks = (int)std::min<int64_t>(4096, (work + kThreads - 1) / kThreads);
+  const int blocks = (int)std::min<int64_t>(1024, (work + kThreads - 1) / kThreads);
   ProfScope ps(ctx, prof_name);
   if (vec)
     hipLaunchKernelGGL(k_absmax<true>, dim3(blocks), dim3(kThreads), 0, ctx->stream, x, n, absmax_bits_dev);

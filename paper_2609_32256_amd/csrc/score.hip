@@ -106,6 +106,21 @@ __device__ __forceinline__ bool better(float a, int ra, float b, int rb) {
   return a > b || (a == b && ra < rb);
 }
 
+// Sorted insertion into a descending register list (entry KL-1 is dropped).
+template <int KL>
+__device__ __forceinline__ void list_insert(float (&ls)[KL], int (&lr)[KL], float sc, int row) {
+  int qpos = 0;
+#pragma unroll
+  for (int p = 0; p < KL; ++p) qpos += better(ls[p], lr[p], sc, row) ? 1 : 0;
+#pragma unroll
+  for (int p = KL - 1; p >= 0; --p) {
+    const float ps = (p > 0) ? ls[p - 1] : 0.0f;
+    const int pr = (p > 0) ? lr[p - 1] : 0;
+    ls[p] = (p > qpos) ? ps : (p == qpos ? sc : ls[p]);
+    lr[p] = (p > qpos) ? pr : (p == qpos ? row : lr[p]);
+  }
+}
+
 // Unpacks 32 b-bit codes starting at word w (element 0 at bit 0) to fp16.
 template <int B>
 __device__ __forceinline__ void unpack32(const uint32_t* __restrict__ w, _Float16* __restrict__ out) {
@@ -242,16 +257,7 @@ __global__ __launch_bounds__(kWG) void k_score(ScoreArgs a) {
           const float sc = wl[e * 64 + lane];
           const int row = (int)(rbase + rl_);
           if (!better(sc, row, ls[KL - 1], lr[KL - 1])) continue;
-          int qpos = 0;
-#pragma unroll
-          for (int p = 0; p < KL; ++p) qpos += better(ls[p], lr[p], sc, row) ? 1 : 0;
-#pragma unroll
-          for (int p = KL - 1; p >= 0; --p) {
-            const float ps = (p > 0) ? ls[p - 1] : 0.0f;
-            const int pr = (p > 0) ? lr[p - 1] : 0;
-            ls[p] = (p > qpos) ? ps : (p == qpos ? sc : ls[p]);
-            lr[p] = (p > qpos) ? pr : (p == qpos ? row : lr[p]);
-          }
+          list_insert<KL>(ls, lr, sc, row);
         }
       }
     }
@@ -268,8 +274,12 @@ __global__ __launch_bounds__(kWG) void k_score(ScoreArgs a) {
   }
 }
 
-// One wave per query: k rounds, each taking the best candidate that is worse
-// than the previous pick under (score desc, row asc).
+// One wave per query.  The candidates are the sorted per-lane lists of the
+// scoring kernel (segments of KL entries, of which only the first k can
+// matter).  Each lane folds its share into a sorted register list; then k
+// rounds take the best list head of the wave under (score desc, row asc).
+// Rows are distinct across lists, so the winning head identifies its lane.
+template <int KL>
 __global__ __launch_bounds__(256) void k_topk_merge(int64_t nq, int cands, int k, const float* __restrict__ ps,
                                                     const int32_t* __restrict__ pr, const QMeta* __restrict__ meta,
                                                     const int64_t* __restrict__ ids, float* __restrict__ out_s,
@@ -288,29 +298,42 @@ __global__ __launch_bounds__(256) void k_topk_merge(int64_t nq, int cands, int k
   }
   const float* s = ps + j * (int64_t)cands;
   const int32_t* r = pr + j * (int64_t)cands;
-  float prev_s = INFINITY;
-  int prev_r = -1;
+  float ls[KL];
+  int lr[KL];
+#pragma unroll
+  for (int p = 0; p < KL; ++p) {
+    ls[p] = -INFINITY;
+    lr[p] = kNoRow;
+  }
+  for (int c = lane; c < cands; c += 64) {
+    if ((c % KL) >= k) continue;              // below rank k of its own sorted segment
+    const int cr = r[c];
+    if (cr == kNoRow) continue;
+    const float cs = s[c];
+    if (!better(cs, cr, ls[KL - 1], lr[KL - 1])) continue;
+    list_insert<KL>(ls, lr, cs, cr);
+  }
   for (int t = 0; t < k; ++t) {
-    float bs = -INFINITY;
-    int br = kNoRow;
-    for (int c = lane; c < cands; c += 64) {
-      const float cs = s[c];
-      const int cr = r[c];
-      if (cr == kNoRow) continue;
-      if (!better(prev_s, prev_r, cs, cr)) continue;   // already taken
-      if (better(cs, cr, bs, br)) { bs = cs; br = cr; }
-    }
+    float bs = ls[0];
+    int br = lr[0];
     for (int o = 32; o > 0; o >>= 1) {
       const float os = __shfl_xor(bs, o);
       const int orr = __shfl_xor(br, o);
       if (better(os, orr, bs, br)) { bs = os; br = orr; }
     }
+    if (br != kNoRow && lr[0] == br) {        // this lane's head won: pop it
+#pragma unroll
+      for (int p = 0; p < KL - 1; ++p) {
+        ls[p] = ls[p + 1];
+        lr[p] = lr[p + 1];
+      }
+      ls[KL - 1] = -INFINITY;
+      lr[KL - 1] = kNoRow;
+    }
     if (lane == 0) {
       out_s[j * k + t] = (br == kNoRow) ? -INFINITY : bs;
       out_i[j * k + t] = (br == kNoRow) ? -1 : ids[br];
     }
-    prev_s = bs;
-    prev_r = br;
   }
 }
 
@@ -380,9 +403,14 @@ lam_status score_topk(lam_ctx* ctx, const lam_store* st, const float* q, int64_t
   }
   {
     ProfScope ps(ctx, "score_merge");
-    hipLaunchKernelGGL(k_topk_merge, dim3((unsigned)((nq + 3) / 4)), dim3(256), 0, ctx->stream, nq,
-                       ntiles > 0 ? cands : 0, k, part_s, part_r, ctx->scratch[S_QMETA].as<QMeta>(), st->ids, scores,
-                       ids, bound);
+    const dim3 g((unsigned)((nq + 3) / 4));
+    const int nc = ntiles > 0 ? cands : 0;
+    if (KL == 16)
+      hipLaunchKernelGGL((k_topk_merge<16>), g, dim3(256), 0, ctx->stream, nq, nc, k, part_s, part_r,
+                         ctx->scratch[S_QMETA].as<QMeta>(), st->ids, scores, ids, bound);
+    else
+      hipLaunchKernelGGL((k_topk_merge<64>), g, dim3(256), 0, ctx->stream, nq, nc, k, part_s, part_r,
+                         ctx->scratch[S_QMETA].as<QMeta>(), st->ids, scores, ids, bound);
     LAM_HIP(hipGetLastError());
   }
   return LAM_OK;
