@@ -36,6 +36,7 @@
 // ||a|| ||b|| <= (||a||^2 + ||b||^2)/2 makes it a sum of per-row terms, and the
 // per-row term also absorbs the float32 roundings of the epilogue.
 #include <cmath>
+#include <cstdlib>
 #include <cstring>
 #include <vector>
 
@@ -48,6 +49,7 @@ namespace {
 
 constexpr int kChunk = 4096;           // rows per resolve (64 lanes x 64 bits)
 constexpr int kNone = 0x7fffffff;       // "no store hit"
+constexpr int kGroupA = 8;              // store tiles per group in the screen's tile order
 constexpr float kScale = 256.0f;        // fp16 operands hold x * 2^8
 constexpr float kInvScale2 = 1.0f / 65536.0f;
 
@@ -192,18 +194,28 @@ __device__ __forceinline__ void push_pair(const ScreenArgs& a, int i, int kind, 
 // [nb0, nb0 + nb1), MODE 1: A = B = chunk rows, pairs ia < ib only).  The
 // A side of the error bound is the largest per-row term among the tile's own
 // A rows.
-template <bool WANT_MAX>
-__global__ __launch_bounds__(kWG) void k_screen(ScreenArgs a) {
-  __shared__ _Float16 lds[4 * kTB * kLdk];
-  __shared__ float hbA[kTB];
-  __shared__ float emx[2];
+template <class C, bool WANT_MAX>
+__global__ __launch_bounds__(C::kThreads) void k_screen(ScreenArgs a) {
+  static_assert(C::BM == C::BN, "the in-chunk triangle needs square tiles");
+  __shared__ _Float16 lds[C::kLdsHalves];
+  __shared__ float hbA[C::BM];
+  __shared__ float emx[C::kWaves];
   if (skip_all(a.flags)) return;
   const int MODE = (blockIdx.x < a.nb0) ? 0 : 1;
   int ta, tb;
   if (MODE == 0) {
+    // Grouped order: within an XCD's contiguous range, consecutive workgroups
+    // sweep a group of kGroupA store tiles against each chunk tile in turn, so
+    // the tiles in flight on one XCD (kGroupA store tiles plus a few chunk
+    // tiles) stay inside its L2 and each store tile leaves HBM once.
     const int64_t logical = xcd_remap(blockIdx.x, a.nb0);
-    ta = (int)(logical / a.ntB);
-    tb = (int)(logical % a.ntB);
+    const int64_t ntA = a.nb0 / a.ntB;
+    const int64_t per_group = (int64_t)kGroupA * a.ntB;
+    const int64_t g = logical / per_group, l = logical % per_group;
+    const int64_t ta0 = g * kGroupA;
+    const int64_t gsize = min((int64_t)kGroupA, ntA - ta0);
+    ta = (int)(ta0 + l % gsize);
+    tb = (int)(l / gsize);
   } else {
     // lower-triangular tile pairs ta <= tb, row-major over tb
     const int64_t logical = xcd_remap(blockIdx.x - a.nb0, a.nb1);
@@ -217,28 +229,34 @@ __global__ __launch_bounds__(kWG) void k_screen(ScreenArgs a) {
   const float* hnA = MODE == 0 ? a.hnS : a.hnB;
   const float* etA = MODE == 0 ? a.etS : a.etB;
   const int nA = (MODE == 0) ? a.meta->m : a.nB;
-  const int rowsA = min(kTB, nA - ta * kTB);
-  const int rowsB = min(kTB, a.nB - tb * kTB);
+  const int rowsA = min(C::BM, nA - ta * C::BM);
+  const int rowsB = min(C::BN, a.nB - tb * C::BN);
   if (rowsA <= 0 || rowsB <= 0) return;
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
-  if (threadIdx.x < kTB) {
-    const bool v = threadIdx.x < rowsA;
-    hbA[threadIdx.x] = v ? hnA[ta * kTB + threadIdx.x] : 0.0f;
-    float e = v ? etA[ta * kTB + threadIdx.x] : 0.0f;
+  {
+    // A-side row terms; the error bound uses the largest term among the tile's rows
+    float e = 0.0f;
+    for (int r = threadIdx.x; r < C::BM; r += C::kThreads) {
+      const bool v = r < rowsA;
+      hbA[r] = v ? hnA[ta * C::BM + r] : 0.0f;
+      e = fmaxf(e, v ? etA[ta * C::BM + r] : 0.0f);
+    }
     for (int o = 32; o > 0; o >>= 1) e = fmaxf(e, __shfl_xor(e, o));
     if (lane == 0) emx[wave] = e;
   }
 
-  floatx16 acc[2][2];
-  gemm_block_f16(A + (int64_t)ta * kTB * a.D, rowsA, a.B + (int64_t)tb * kTB * a.D, rowsB, a.D, a.D, lds, acc);
+  floatx16 acc[C::TI][C::TJ];
+  gemm_tile<C>(A + (int64_t)ta * C::BM * a.D, rowsA, a.B + (int64_t)tb * C::BN * a.D, rowsB, a.D, a.D, lds, acc);
 
-  const int wm = wave >> 1, wn = wave & 1;
-  const float ebA = fmaxf(emx[0], emx[1]);
+  const int wm = wave / C::WN, wn = wave % C::WN;
+  float ebA = emx[0];
 #pragma unroll
-  for (int tj = 0; tj < 2; ++tj) {
-    const int ibl = wn * 64 + tj * 32 + (lane & 31);
-    const int ib = tb * kTB + ibl;
+  for (int w = 1; w < C::kWaves; ++w) ebA = fmaxf(ebA, emx[w]);
+#pragma unroll
+  for (int tj = 0; tj < C::TJ; ++tj) {
+    const int ibl = wn * C::TJ * 32 + tj * 32 + (lane & 31);
+    const int ib = tb * C::BN + ibl;
     const bool vB = ibl < rowsB;
     float thrAmb = 3.0e38f, thrIn = 3.0e38f;
     if (vB) {
@@ -249,11 +267,11 @@ __global__ __launch_bounds__(kWG) void k_screen(ScreenArgs a) {
     }
     float mx = -3.0e38f, cmax = -3.0e38f;
 #pragma unroll
-    for (int ti = 0; ti < 2; ++ti) {
+    for (int ti = 0; ti < C::TI; ++ti) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int ial = wm * 64 + ti * 32 + acc_row(r, lane);
-        const int ia = ta * kTB + ial;
+        const int ial = wm * C::TI * 32 + ti * 32 + acc_row(r, lane);
+        const int ia = ta * C::BM + ial;
         const bool valid = vB && ial < rowsA && (MODE == 0 || ia < ib);
         const float dot = acc[ti][tj][r] * kInvScale2;
         const float v = dot - hbA[ial];
@@ -267,42 +285,56 @@ __global__ __launch_bounds__(kWG) void k_screen(ScreenArgs a) {
     if (WANT_MAX && MODE == 0 && vB && cmax > -3.0e38f) atomicMax(&a.maxcos[ib], f2ord(cmax));
     const bool hot = mx >= thrAmb;
     if (__ballot(hot) == 0ull) continue;
-    if (!hot) continue;
-    // Rare path: classify this lane's candidates in increasing row order.
-    if (MODE == 0) {
-      int ydef = kNone;
-      for (int ti = 0; ti < 2 && ydef == kNone; ++ti) {
-        for (int r = 0; r < 16; ++r) {
-          const int ial = wm * 64 + ti * 32 + acc_row(r, lane);
-          if (ial >= rowsA) continue;
-          const float v = acc[ti][tj][r] * kInvScale2 - hbA[ial];
-          if (v < thrAmb) continue;
-          const int ia = ta * kTB + ial;
-          if (v >= thrIn) { ydef = ia; break; }
-          push_pair(a, ib, 0, ia);
-        }
+    // Rare path.  Classify this lane's elements into bit masks (bit e = ti*16 + r;
+    // A rows increase with e), then walk the set bits -- the accumulators are
+    // only ever indexed statically.
+    static_assert(C::TI * 16 <= 64, "one 64-bit mask per lane and B column");
+    uint64_t cand = 0ull, def = 0ull;
+#pragma unroll
+    for (int ti = 0; ti < C::TI; ++ti) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int ial = wm * C::TI * 32 + ti * 32 + acc_row(r, lane);
+        const int ia = ta * C::BM + ial;
+        const bool valid = vB && ial < rowsA && (MODE == 0 || ia < ib);
+        const float v = acc[ti][tj][r] * kInvScale2 - hbA[ial];
+        const uint64_t bit = 1ull << (ti * 16 + r);
+        cand |= (valid && v >= thrAmb) ? bit : 0ull;
+        def |= (valid && v >= thrIn) ? bit : 0ull;
       }
-      if (ydef != kNone) atomicMin(&a.firstHit[ib], ydef);
+    }
+    if (!hot) continue;
+    auto row_of = [&](int e) { return ta * C::BM + wm * C::TI * 32 + (e >> 4) * 32 + acc_row(e & 15, lane); };
+    if (MODE == 0) {
+      // lowest definite row, and the ambiguous rows below it
+      const int edef = def ? __builtin_ctzll(def) : 64;
+      uint64_t amb = cand & ~def & (edef < 64 ? ((1ull << edef) - 1ull) : ~0ull);
+      while (amb) {
+        const int e = __builtin_ctzll(amb);
+        amb &= amb - 1ull;
+        push_pair(a, ib, 0, row_of(e));
+      }
+      if (edef < 64) atomicMin(&a.firstHit[ib], row_of(edef));
     } else {
-      for (int ti = 0; ti < 2; ++ti) {
-        for (int r = 0; r < 16; ++r) {
-          const int ial = wm * 64 + ti * 32 + acc_row(r, lane);
-          const int ia = ta * kTB + ial;
-          if (ial >= rowsA || ia >= ib) continue;
-          const float v = acc[ti][tj][r] * kInvScale2 - hbA[ial];
-          if (v < thrAmb) continue;
-          if (v >= thrIn) {
-            atomicOr(reinterpret_cast<unsigned long long*>(&a.bitmap[(int64_t)ib * a.W + (ia >> 6)]),
-                     1ull << (ia & 63));
-            a.hasEdge[ib] = 1u;
-          } else {
-            push_pair(a, ib, 1, ia);
-          }
+      uint64_t c = cand;
+      while (c) {
+        const int e = __builtin_ctzll(c);
+        c &= c - 1ull;
+        const int ia = row_of(e);
+        if ((def >> e) & 1ull) {
+          atomicOr(reinterpret_cast<unsigned long long*>(&a.bitmap[(int64_t)ib * a.W + (ia >> 6)]),
+                   1ull << (ia & 63));
+          a.hasEdge[ib] = 1u;
+        } else {
+          push_pair(a, ib, 1, ia);
         }
       }
     }
   }
 }
+
+using ScreenSmall = Tile<2, 2, 2, 2>;   // 128 x 128, four waves of 64 x 64
+using ScreenLarge = Tile<2, 2, 4, 4>;   // 256 x 256, four waves of 128 x 128
 
 // ------------------------------------------------------------------ verify
 struct VerifyArgs {
@@ -706,6 +738,16 @@ struct Consts {
   double K1, K2, K3h;
 };
 
+// Tile choice of the screen: 0 = by grid size (default), 128 or 256 forced by
+// the LAM_SCREEN_TILE environment variable (for tuning).
+int screen_tile_pref() {
+  static const int v = [] {
+    const char* e = std::getenv("LAM_SCREEN_TILE");
+    return e ? std::atoi(e) : 0;
+  }();
+  return (v == 128 || v == 256) ? v : 0;
+}
+
 Consts screen_consts(int D) {
   const double uh = std::ldexp(1.0, -11), u = std::ldexp(1.0, -24), eta = std::ldexp(1.0, -22);
   const double g = 2.0 * D * u / (1.0 - 2.0 * D * u);
@@ -847,16 +889,34 @@ lam_status dedup_ingest(lam_ctx* ctx, lam_store* st, const float* x, int64_t n, 
       // against the store (rows retained before this chunk; the kernel reads
       // the exact count, the grid covers an upper bound) and inside the chunk
       const int64_t m_ub = m_before + c0;
-      sa.nb0 = ((m_ub + kTB - 1) / kTB) * ntB;
-      sa.nb1 = (int64_t)ntB * (ntB + 1) / 2;
+      // 256 x 256 tiles once they give every CU at least one workgroup
+      const int64_t big_tiles = ((m_ub + 255) / 256) * ((nB + 255) / 256);
+      const bool large = screen_tile_pref() == 256;   // 256 x 256 only on request (slower on MI355X)
+      (void)big_tiles;
+      const int tb_rows = large ? ScreenLarge::BN : ScreenSmall::BN;
+      const int ntBt = (nB + tb_rows - 1) / tb_rows;
+      sa.ntB = ntBt;
+      sa.nb0 = ((m_ub + tb_rows - 1) / tb_rows) * ntBt;
+      sa.nb1 = (int64_t)ntBt * (ntBt + 1) / 2;
       const int64_t grid = sa.nb0 + sa.nb1;
       LAM_CHECK(grid < (1LL << 31), LAM_EINVAL, "screen grid too large");
       {
         ProfScope ps(ctx, "dedup_screen");
-        if (want_max)
-          hipLaunchKernelGGL((k_screen<true>), dim3((unsigned)grid), dim3(kWG), 0, ctx->stream, sa);
-        else
-          hipLaunchKernelGGL((k_screen<false>), dim3((unsigned)grid), dim3(kWG), 0, ctx->stream, sa);
+        if (large) {
+          if (want_max)
+            hipLaunchKernelGGL((k_screen<ScreenLarge, true>), dim3((unsigned)grid), dim3(ScreenLarge::kThreads), 0,
+                               ctx->stream, sa);
+          else
+            hipLaunchKernelGGL((k_screen<ScreenLarge, false>), dim3((unsigned)grid), dim3(ScreenLarge::kThreads), 0,
+                               ctx->stream, sa);
+        } else {
+          if (want_max)
+            hipLaunchKernelGGL((k_screen<ScreenSmall, true>), dim3((unsigned)grid), dim3(ScreenSmall::kThreads), 0,
+                               ctx->stream, sa);
+          else
+            hipLaunchKernelGGL((k_screen<ScreenSmall, false>), dim3((unsigned)grid), dim3(ScreenSmall::kThreads), 0,
+                               ctx->stream, sa);
+        }
         LAM_HIP(hipGetLastError());
       }
       VerifyArgs va{pairs, status, cc, cap, xc, st->x32, D, st->d2, firstHit, bitmap, W, hasEdge,

@@ -120,6 +120,102 @@ __device__ __forceinline__ void gemm_block_f16(const _Float16* __restrict__ A, i
   }
 }
 
+// ---------------------------------------------------------------------------
+// Generalised block: WM x WN waves, each owning TI x TJ tiles of 32 x 32, so a
+// workgroup computes (WM*TI*32) x (WN*TJ*32) of C = A . B^T.  Larger per-wave
+// tiles read fewer LDS bytes per MFMA: (TI + TJ) / (TI * TJ) KB.
+template <int WM_, int WN_, int TI_, int TJ_>
+struct Tile {
+  static constexpr int WM = WM_, WN = WN_, TI = TI_, TJ = TJ_;
+  static constexpr int kWaves = WM * WN;
+  static constexpr int kThreads = 64 * kWaves;
+  static constexpr int BM = WM * TI * 32;   // A rows per workgroup
+  static constexpr int BN = WN * TJ * 32;   // B rows per workgroup
+  static constexpr int kChunksA = BM * (kBK / 8);   // 16-byte chunks of one A slab
+  static constexpr int kChunksB = BN * (kBK / 8);
+  static constexpr int kPerA = kChunksA / kThreads;
+  static constexpr int kPerB = kChunksB / kThreads;
+  static constexpr int kLdsHalves = 2 * (BM + BN) * kLdk;   // double-buffered slabs
+  static_assert(kChunksA % kThreads == 0 && kChunksB % kThreads == 0, "slab must split evenly");
+};
+
+template <int N>
+__device__ __forceinline__ void slab_load_n(const _Float16* __restrict__ base, int rows, int64_t ld, int k0, int kmax,
+                                            uint4 (&r)[N], int nthreads) {
+#pragma unroll
+  for (int q = 0; q < N; ++q) {
+    const int c = threadIdx.x + nthreads * q;
+    const int row = c >> 3, col = (c & 7) * 8;
+    uint4 v = make_uint4(0u, 0u, 0u, 0u);
+    if (row < rows && k0 + col < kmax) v = *reinterpret_cast<const uint4*>(base + (int64_t)row * ld + k0 + col);
+    r[q] = v;
+  }
+}
+
+template <int N>
+__device__ __forceinline__ void slab_store_n(_Float16* __restrict__ s, const uint4 (&r)[N], int nthreads) {
+#pragma unroll
+  for (int q = 0; q < N; ++q) {
+    const int c = threadIdx.x + nthreads * q;
+    const int row = c >> 3, col = (c & 7) * 8;
+    *reinterpret_cast<uint4*>(s + row * kLdk + col) = r[q];
+  }
+}
+
+// C tile of one workgroup; lds holds C::kLdsHalves halves.  acc[ti][tj] holds
+// rows wm*TI*32 + ti*32 + acc_row(r, lane) of A and column wn*TJ*32 + tj*32 +
+// lane%32 of B, with wm = wave / WN, wn = wave % WN.
+template <class C>
+__device__ __forceinline__ void gemm_tile(const _Float16* __restrict__ A, int ra, const _Float16* __restrict__ B,
+                                          int rb, int64_t ld, int kdim, _Float16* lds,
+                                          floatx16 (&acc)[C::TI][C::TJ]) {
+  _Float16* sa0 = lds;
+  _Float16* sb0 = lds + 2 * C::BM * kLdk;
+  auto sa = [&](int i) -> _Float16* { return sa0 + i * (C::BM * kLdk); };
+  auto sb = [&](int i) -> _Float16* { return sb0 + i * (C::BN * kLdk); };
+  const int wave = threadIdx.x >> 6;
+  const int wm = wave / C::WN, wn = wave % C::WN;
+#pragma unroll
+  for (int a = 0; a < C::TI; ++a)
+#pragma unroll
+    for (int b = 0; b < C::TJ; ++b)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.0f;
+  uint4 ra_[C::kPerA], rb_[C::kPerB];
+  slab_load_n<C::kPerA>(A, ra, ld, 0, kdim, ra_, C::kThreads);
+  slab_load_n<C::kPerB>(B, rb, ld, 0, kdim, rb_, C::kThreads);
+  slab_store_n<C::kPerA>(sa(0), ra_, C::kThreads);
+  slab_store_n<C::kPerB>(sb(0), rb_, C::kThreads);
+  __syncthreads();
+  int cur = 0;
+  for (int k0 = 0; k0 < kdim; k0 += kBK) {
+    const bool more = k0 + kBK < kdim;
+    if (more) {
+      slab_load_n<C::kPerA>(A, ra, ld, k0 + kBK, kdim, ra_, C::kThreads);
+      slab_load_n<C::kPerB>(B, rb, ld, k0 + kBK, kdim, rb_, C::kThreads);
+    }
+#pragma unroll
+    for (int kk = 0; kk < kBK / 16; ++kk) {
+      half8 fa[C::TI], fb[C::TJ];
+#pragma unroll
+      for (int t = 0; t < C::TI; ++t) fa[t] = frag_load(sa(cur), wm * C::TI * 32 + t * 32, kk);
+#pragma unroll
+      for (int t = 0; t < C::TJ; ++t) fb[t] = frag_load(sb(cur), wn * C::TJ * 32 + t * 32, kk);
+#pragma unroll
+      for (int a = 0; a < C::TI; ++a)
+#pragma unroll
+        for (int b = 0; b < C::TJ; ++b)
+          acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fa[a], fb[b], acc[a][b], 0, 0, 0);
+    }
+    if (more) {
+      slab_store_n<C::kPerA>(sa(cur ^ 1), ra_, C::kThreads);
+      slab_store_n<C::kPerB>(sb(cur ^ 1), rb_, C::kThreads);
+    }
+    __syncthreads();
+    cur ^= 1;
+  }
+}
+
 // Workgroup index remapped so that consecutive logical tiles run on the same
 // XCD (the hardware deals workgroups to the 8 XCDs round-robin), letting tiles
 // that share operand rows share that XCD's L2.

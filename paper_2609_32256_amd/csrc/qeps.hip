@@ -11,12 +11,22 @@
 // which a second fused multiply-add gives exactly (a single rounding keeps the
 // sign, and zero only for an exact zero, i.e. a true tie).
 //
-// Memory layout.  A tile of 4096 elements (256 threads x 16) is read with
-// coalesced float4 loads, quantized in registers, and parked in LDS as int32;
-// each thread then assembles whole output words (bits [32w, 32w+32) of the
-// tile's stream) from LDS and stores them coalesced.  4096*b bits is a whole
-// number of words, so tiles never share a word.  Decode mirrors this.
-// Bytes per element: encode 4 + b/8, decode b/8 + 4 -- an HBM-bound stream.
+// Most elements never need binary64: p = x * float32(1/s) is within
+// 2^-22 (|p| + 1) of x/s (two float32 roundings), so when |p - rint(p)| is at
+// most 1/2 - 2^-21 (|p| + 1) no half-integer can separate p from x/s and
+// rint(p) is the exact answer.  Only the remaining elements (near a tie, or
+// |p| beyond float32's exact range) take the binary64 path above.
+//
+// Memory layout.  A tile of 8192 elements (256 threads x 32) is read with
+// coalesced float4 loads and quantized; the codes are parked in LDS (one pad
+// word per 32 so that a thread reading its own 32 consecutive codes hits
+// distinct banks), each thread packs its 32 codes into b words in registers
+// with compile-time shifts, and the packed words go back through LDS to
+// coalesced stores.  32 codes are exactly b words, so threads and tiles never
+// share a word.  Decode loads a tile's words into LDS, extracts each code with
+// a funnel shift, and (for b <= 12) maps it through a per-workgroup table of
+// float32(float64(c * s)).  Bytes per element: encode 4 + b/8, decode b/8 + 4
+// -- an HBM-bound stream.
 #include <cmath>
 #include <cstring>
 
@@ -26,8 +36,9 @@ namespace lam {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kPerThread = 16;
-constexpr int kTile = kThreads * kPerThread;  // 4096 elements
+constexpr int kPerThread = 32;
+constexpr int kTile = kThreads * kPerThread;  // 8192 elements
+constexpr int kPadded = kTile + kTile / 32;    // one pad word per 32 codes
 
 // Exact round-half-even of x / s, see the file comment.
 __device__ __forceinline__ int32_t q_round(float xf, double s, double inv_s, double eps) {
@@ -48,6 +59,15 @@ __device__ __forceinline__ int32_t q_round(float xf, double s, double inv_s, dou
     if (d < 0.0 || (d == 0.0 && odd)) q0 -= 1.0;
   }
   return (int32_t)q0;
+}
+
+// float32 fast path with the binary64 method as the fallback (file comment).
+__device__ __forceinline__ int32_t q_round_fast(float x, float inv_s32, double s, double inv_s, double eps) {
+  const float p = x * inv_s32;
+  const float q0 = rintf(p);
+  const float thr = fmaf(-0x1p-21f, fabsf(p), 0.5f - 0x1p-21f);
+  if (fabsf(p - q0) <= thr) return (int32_t)q0;
+  return q_round(x, s, inv_s, eps);
 }
 
 __device__ __forceinline__ void wave_flag(bool bad, uint32_t* counter) {
@@ -85,71 +105,124 @@ __global__ __launch_bounds__(kThreads) void k_absmax(const float* __restrict__ x
 }
 
 template <int B, bool VEC>
-__global__ __launch_bounds__(kThreads) void k_encode(const float* __restrict__ x, int64_t n, double s,
-                                                     double inv_s, double eps, float absmax,
+__global__ __launch_bounds__(kThreads) void k_encode(const float* __restrict__ x, int64_t n, float inv_s32,
+                                                     double s, double inv_s, double eps, float absmax,
                                                      uint32_t* __restrict__ codes, uint64_t nwords,
                                                      uint32_t* __restrict__ flags) {
-  __shared__ int32_t lq[kTile + 40];
+  __shared__ uint32_t lq[kPadded];
+  constexpr uint32_t kMask = (B == 32) ? 0xffffffffu : ((1u << B) - 1u);
   const int t = threadIdx.x;
-  const int64_t tile = blockIdx.x;
+  const int64_t ntiles = (n + kTile - 1) / kTile;
+  // Persistent workgroups: the next tile's loads are in flight while the
+  // current tile is rounded, packed and stored.
+  float4 cur[kPerThread / 4], nxt[kPerThread / 4];
+  auto load_tile = [&](int64_t tl, float4 (&v)[kPerThread / 4]) {
+    const int64_t b0 = tl * (int64_t)kTile;
+#pragma unroll
+    for (int j = 0; j < kPerThread / 4; ++j) {
+      const int64_t e = b0 + j * (kThreads * 4) + t * 4;
+      if (VEC && e + 3 < n) {
+        v[j] = *reinterpret_cast<const float4*>(x + e);
+      } else {
+        v[j].x = (e < n) ? x[e] : 0.0f;
+        v[j].y = (e + 1 < n) ? x[e + 1] : 0.0f;
+        v[j].z = (e + 2 < n) ? x[e + 2] : 0.0f;
+        v[j].w = (e + 3 < n) ? x[e + 3] : 0.0f;
+      }
+    }
+  };
+  int64_t tile = blockIdx.x;
+  if (tile < ntiles) load_tile(tile, cur);
+  for (; tile < ntiles; tile += gridDim.x) {
+  if (tile + gridDim.x < ntiles) load_tile(tile + gridDim.x, nxt);
   const int64_t base = tile * (int64_t)kTile;
-  bool nonfinite = false, range = false;
+  bool bad = false;   // NaN, Inf or |x| > absmax (absmax is finite)
 #pragma unroll
   for (int j = 0; j < kPerThread / 4; ++j) {
     const int le = j * (kThreads * 4) + t * 4;
-    const int64_t e = base + le;
-    float v[4];
-    if (VEC && e + 3 < n) {
-      const float4 f = *reinterpret_cast<const float4*>(x + e);
-      v[0] = f.x; v[1] = f.y; v[2] = f.z; v[3] = f.w;
-    } else {
-#pragma unroll
-      for (int r = 0; r < 4; ++r) v[r] = (e + r < n) ? x[e + r] : 0.0f;
-    }
+    const float v[4] = {cur[j].x, cur[j].y, cur[j].z, cur[j].w};
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const float a = fabsf(v[r]);
-      nonfinite |= !(a <= 3.402823466e38f);
-      range |= a > absmax;
-      lq[le + r] = q_round(v[r], s, inv_s, eps);
+      bad |= !(fabsf(v[r]) <= absmax);
+      const int li = le + r;
+      lq[li + (li >> 5)] = (uint32_t)q_round_fast(v[r], inv_s32, s, inv_s, eps) & kMask;
     }
   }
-  if (t < 40) lq[kTile + t] = 0;
   __syncthreads();
-
-  constexpr int kWords = kTile * B / 32;           // 128 * B words per tile
-  constexpr uint32_t kMask = (B == 32) ? 0xffffffffu : ((1u << B) - 1u);
-  constexpr int kSpan = (32 + B - 1) / B + 1;       // elements touching one word
-  const uint64_t w0 = (uint64_t)tile * kWords;
-  for (int w = t; w < kWords; w += kThreads) {
-    if (w0 + w >= nwords) break;
-    const int bit = w * 32;
-    const int e = bit / B;
-    const int sh = e * B - bit;  // in (-B, 0]
-    uint32_t acc = 0;
+  // pack this thread's 32 consecutive codes into B words
+  uint32_t w[B];
 #pragma unroll
-    for (int r = 0; r < kSpan; ++r) {
-      const int s2 = sh + r * B;
-      if (s2 < 32) {
-        const uint32_t u = (uint32_t)lq[e + r] & kMask;
-        acc |= (s2 >= 0) ? (u << s2) : (u >> (-s2));
+  for (int i = 0; i < B; ++i) w[i] = 0u;
+#pragma unroll
+  for (int k = 0; k < 32; ++k) {
+    const uint32_t u = lq[t * 33 + k];
+    const int bit = k * B, wi = bit >> 5, off = bit & 31;
+    w[wi] |= u << off;
+    if (off + B > 32) w[wi + 1] |= u >> (32 - off);
+  }
+  __syncthreads();
+  // words back through LDS (same one-per-32 padding) for coalesced stores
+#pragma unroll
+  for (int i = 0; i < B; ++i) {
+    const int wi = t * B + i;
+    lq[wi + (wi >> 5)] = w[i];
+  }
+  __syncthreads();
+  constexpr int kWords = kThreads * B;              // words per tile
+  const uint64_t w0 = (uint64_t)tile * kWords;
+  for (int i = t; i < kWords; i += kThreads)
+    if (w0 + i < nwords) codes[w0 + i] = lq[i + (i >> 5)];
+  if (__ballot(bad) != 0ull) {
+    // classify the rare failures: non-finite (EINVAL) vs merely above absmax (ERANGE)
+    bool nonfinite = false, range = false;
+    for (int j = 0; j < kPerThread / 4; ++j) {
+      const int64_t e = base + j * (kThreads * 4) + t * 4;
+      for (int r = 0; r < 4; ++r) {
+        if (e + r >= n) continue;
+        const float a = fabsf(x[e + r]);
+        nonfinite |= !(a <= 3.402823466e38f);
+        range |= a > absmax;
       }
     }
-    codes[w0 + w] = acc;
+    wave_flag(nonfinite, &flags[0]);
+    wave_flag(range, &flags[1]);
   }
-  wave_flag(nonfinite, &flags[0]);
-  wave_flag(range, &flags[1]);
+  __syncthreads();   // lq is rewritten by the next tile
+#pragma unroll
+  for (int j = 0; j < kPerThread / 4; ++j) cur[j] = nxt[j];
+  }
 }
 
 template <int B, bool VEC>
 __global__ __launch_bounds__(kThreads) void k_decode(const uint32_t* __restrict__ codes, int64_t n,
                                                      uint64_t nwords, double s, float* __restrict__ xhat) {
   constexpr int kWords = kTile * B / 32;
+  constexpr bool kLut = B <= 12;                    // decode table of 2^B entries
+  constexpr int kLutN = kLut ? (1 << (B > 12 ? 0 : B)) : 1;
   __shared__ uint32_t lw[kWords + 2];
+  __shared__ float lut[kLutN];
   const int t = threadIdx.x;
   const int64_t tile = blockIdx.x;
   const uint64_t w0 = (uint64_t)tile * kWords;
-  for (int w = t; w < kWords + 2; w += kThreads) lw[w] = (w0 + w < nwords) ? codes[w0 + w] : 0u;
+  {
+    // all of this thread's loads in flight before the first LDS store
+    constexpr int kIt = (kWords + 2 + kThreads - 1) / kThreads;
+    uint32_t tmp[kIt];
+#pragma unroll
+    for (int i = 0; i < kIt; ++i) {
+      const int w = t + i * kThreads;
+      tmp[i] = (w < kWords + 2 && w0 + w < nwords) ? codes[w0 + w] : 0u;
+    }
+#pragma unroll
+    for (int i = 0; i < kIt; ++i) {
+      const int w = t + i * kThreads;
+      if (w < kWords + 2) lw[w] = tmp[i];
+    }
+  }
+  if (kLut) {
+    // entry c + 2^(B-1) holds float32(float64(c * s)), the decode definition
+    for (int c = t; c < kLutN; c += kThreads) lut[c] = (float)((double)(c - kLutN / 2) * s);
+  }
   __syncthreads();
   const int64_t base = tile * (int64_t)kTile;
 #pragma unroll
@@ -160,10 +233,13 @@ __global__ __launch_bounds__(kThreads) void k_decode(const uint32_t* __restrict_
     for (int r = 0; r < 4; ++r) {
       const int bit = (le + r) * B;
       const int wi = bit >> 5, off = bit & 31;
-      const uint64_t pair = ((uint64_t)lw[wi + 1] << 32) | lw[wi];
-      const uint32_t u = (uint32_t)(pair >> off);
-      const int32_t q = (int32_t)(u << (32 - B)) >> (32 - B);
-      v[r] = (float)((double)q * s);
+      const uint32_t u = __builtin_amdgcn_alignbit(lw[wi + 1], lw[wi], (uint32_t)off);
+      if (kLut) {
+        v[r] = lut[(u ^ (1u << (B - 1))) & (uint32_t)(kLutN - 1)];   // offset binary index
+      } else {
+        const int32_t q = (int32_t)(u << (32 - B)) >> (32 - B);
+        v[r] = (float)((double)q * s);
+      }
     }
     const int64_t e = base + le;
     if (VEC && e + 3 < n) {
@@ -201,11 +277,11 @@ void encode_dispatch(int b, bool vec, dim3 grid, hipStream_t st, const float* x,
                      double eps, float absmax, uint32_t* codes, uint64_t nwords, uint32_t* flags) {
   if (b == B) {
     if (vec)
-      hipLaunchKernelGGL((k_encode<B, true>), grid, dim3(kThreads), 0, st, x, n, s, 1.0 / s, eps, absmax,
-                         codes, nwords, flags);
+      hipLaunchKernelGGL((k_encode<B, true>), grid, dim3(kThreads), 0, st, x, n, (float)(1.0 / s), s, 1.0 / s, eps,
+                         absmax, codes, nwords, flags);
     else
-      hipLaunchKernelGGL((k_encode<B, false>), grid, dim3(kThreads), 0, st, x, n, s, 1.0 / s, eps, absmax,
-                         codes, nwords, flags);
+      hipLaunchKernelGGL((k_encode<B, false>), grid, dim3(kThreads), 0, st, x, n, (float)(1.0 / s), s, 1.0 / s,
+                         eps, absmax, codes, nwords, flags);
     return;
   }
   if constexpr (B < 32) encode_dispatch<B + 1>(b, vec, grid, st, x, n, s, eps, absmax, codes, nwords, flags);
@@ -279,7 +355,9 @@ lam_status launch_encode(lam_ctx* ctx, const float* x, int64_t n, const lam_qpar
   LAM_CHECK(tiles < (1LL << 31), LAM_EINVAL, "too many elements");
   const uint64_t nwords = p.code_bytes / 4u;
   ProfScope ps(ctx, prof_name);
-  encode_dispatch<1>(p.bits, vec, dim3((unsigned)tiles), ctx->stream, x, n, p.step, p.eps, p.absmax, codes,
+  // persistent grid: four 33 KB-LDS workgroups fit each of the 256 CUs
+  const unsigned grid = (unsigned)std::min<int64_t>(tiles, 1024);
+  encode_dispatch<1>(p.bits, vec, dim3(grid), ctx->stream, x, n, p.step, p.eps, p.absmax, codes,
                      nwords, flags2);
   LAM_HIP(hipGetLastError());
   return LAM_OK;

@@ -29,7 +29,7 @@ namespace {
 
 constexpr int kNoRow = 0x7fffffff;
 
-enum ScoreScratch { S_QHI = 7, S_QLO, S_QMETA, S_PART };
+enum ScoreScratch { S_QHI = 7, S_QLO, S_QMETA, S_PART, S_CAND };
 
 struct QMeta {
   float osc;     // float32(s * 2^-e): multiplies the raw accumulator
@@ -86,20 +86,29 @@ __global__ __launch_bounds__(256) void k_score_prep(const float* __restrict__ q,
   }
 }
 
+
 struct ScoreArgs {
   const uint32_t* codes;
-  int64_t n;            // store rows
+  int64_t n;                 // store rows
   int D;
-  int64_t row_words;    // D * b / 32
+  int64_t row_words;         // D * b / 32
   const _Float16* qhi;
   const _Float16* qlo;
   const QMeta* meta;
   int64_t nq;
-  int nqt;              // query tiles
-  int splits;
+  int nqt;                   // query tiles of 128
+  int64_t tile_begin;        // store tiles [tile_begin, tile_end) scanned by this launch
+  int64_t tile_end;
+  int splits;                // contiguous tile ranges per query tile
   int64_t tiles_per_split;
-  float* part_s;        // [nq][splits][2][KL]
+  float* part_s;             // list modes: [nq][splits][2][KL]
   int32_t* part_r;
+  const float* thr;          // filter mode: per-query threshold
+  float* cand_s;             // filter mode: [nq][cap]
+  int32_t* cand_r;
+  uint32_t* cand_cnt;
+  uint32_t cap;
+  const uint32_t* tflag;     // fallback mode: query tiles to redo
 };
 
 __device__ __forceinline__ bool better(float a, int ra, float b, int rb) {
@@ -138,100 +147,116 @@ __device__ __forceinline__ void unpack32(const uint32_t* __restrict__ w, _Float1
   }
 }
 
-template <int B, int KL>
+// acc[t] (t = 0..3) <- the 128 x 128 tile of raw scores: store rows
+// [rbase, rbase + rows) against the workgroup's 128 queries (wave w holds
+// queries [32w, 32w + 32), lane j % 32, store rows t*32 + acc_row(r, lane)).
+// Codes are unpacked straight into an fp16 LDS slab; queries enter as hi/lo.
+template <int B>
+__device__ __forceinline__ void score_tile(const ScoreArgs& a, int64_t rbase, int rows, const _Float16* QH,
+                                           const _Float16* QL, int qrows, _Float16* lds, floatx16 (&acc)[4]) {
+  auto buf = [&](int i) -> _Float16* { return lds + i * (kTB * kLdk); };  // codes 0/1, hi 2/3, lo 4/5
+  const int wave = threadIdx.x >> 6;
+  const int urow = threadIdx.x >> 1, uhalf = threadIdx.x & 1;   // unpack: 2 threads per row
+#pragma unroll
+  for (int t = 0; t < 4; ++t)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[t][r] = 0.0f;
+  auto load_codes = [&](int k0, uint32_t (&cw)[B]) {
+    if (urow < rows && k0 + 32 * uhalf < a.D) {
+      const uint32_t* src = a.codes + (rbase + urow) * a.row_words + (int64_t)(k0 / 32 + uhalf) * B;
+#pragma unroll
+      for (int i = 0; i < B; ++i) cw[i] = src[i];
+    } else {
+#pragma unroll
+      for (int i = 0; i < B; ++i) cw[i] = 0u;
+    }
+  };
+  auto store_codes = [&](_Float16* s, const uint32_t (&cw)[B]) {
+    _Float16 h[32];
+    unpack32<B>(cw, h);
+    _Float16* dst = s + urow * kLdk + uhalf * 32;
+#pragma unroll
+    for (int i = 0; i < 32; i += 8) *reinterpret_cast<uint4*>(dst + i) = *reinterpret_cast<const uint4*>(h + i);
+  };
+  uint32_t cw[B];
+  SlabRegs rh, rl;
+  load_codes(0, cw);
+  slab_load(QH, qrows, a.D, 0, a.D, rh);
+  slab_load(QL, qrows, a.D, 0, a.D, rl);
+  store_codes(buf(0), cw);
+  slab_store(buf(2), rh);
+  slab_store(buf(4), rl);
+  __syncthreads();
+  int cur = 0;
+  for (int k0 = 0; k0 < a.D; k0 += kBK) {
+    const bool more = k0 + kBK < a.D;
+    if (more) {
+      load_codes(k0 + kBK, cw);
+      slab_load(QH, qrows, a.D, k0 + kBK, a.D, rh);
+      slab_load(QL, qrows, a.D, k0 + kBK, a.D, rl);
+    }
+#pragma unroll
+    for (int kk = 0; kk < kBK / 16; ++kk) {
+      const half8 bh = frag_load(buf(2 + cur), wave * 32, kk);
+      const half8 bl = frag_load(buf(4 + cur), wave * 32, kk);
+      half8 fa[4];
+#pragma unroll
+      for (int t = 0; t < 4; ++t) fa[t] = frag_load(buf(cur), t * 32, kk);
+#pragma unroll
+      for (int t = 0; t < 4; ++t) acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fa[t], bh, acc[t], 0, 0, 0);
+#pragma unroll
+      for (int t = 0; t < 4; ++t) acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fa[t], bl, acc[t], 0, 0, 0);
+    }
+    if (more) {
+      store_codes(buf(cur ^ 1), cw);
+      slab_store(buf(2 + (cur ^ 1)), rh);
+      slab_store(buf(4 + (cur ^ 1)), rl);
+    }
+    __syncthreads();
+    cur ^= 1;
+  }
+}
+
+enum { kModeLists = 0, kModeFilter = 1, kModeFallback = 2 };
+
+// MODE kModeLists / kModeFallback: each lane keeps a sorted private list of its
+// best KL (score, row) pairs; the lists go to part_s/part_r.  kModeFallback
+// only runs query tiles flagged in tflag.  MODE kModeFilter: every score at or
+// above the query's threshold is appended to its candidate buffer.
+template <int B, int KL, int MODE>
 __global__ __launch_bounds__(kWG) void k_score(ScoreArgs a) {
   __shared__ _Float16 lds[6 * kTB * kLdk];
-  // slab buffers: codes (A) at 0 / 1, query hi at 2 / 3, query lo at 4 / 5
-  auto buf = [&](int i) -> _Float16* { return lds + i * (kTB * kLdk); };
   const int qt = blockIdx.x % a.nqt;
   const int split = blockIdx.x / a.nqt;
-  const int64_t ntiles = (a.n + kTB - 1) / kTB;
-  const int64_t t0 = (int64_t)split * a.tiles_per_split;
-  const int64_t t1 = min(ntiles, t0 + a.tiles_per_split);
+  if (MODE == kModeFallback && a.tflag[qt] == 0u) return;
+  const int64_t t0 = a.tile_begin + (int64_t)split * a.tiles_per_split;
+  const int64_t t1 = min(a.tile_end, t0 + a.tiles_per_split);
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int64_t qbase = (int64_t)qt * kTB;
   const int qrows = (int)min<int64_t>(kTB, a.nq - qbase);
   const int64_t j = qbase + wave * 32 + (lane & 31);
   const float osc = (j < a.nq) ? a.meta[j].osc : 0.0f;
+  const float th = (MODE == kModeFilter && j < a.nq) ? a.thr[j] : 0.0f;
   const _Float16* QH = a.qhi + qbase * a.D;
   const _Float16* QL = a.qlo + qbase * a.D;
 
-  float ls[KL];
-  int lr[KL];
+  float ls[MODE == kModeFilter ? 1 : KL];
+  int lr[MODE == kModeFilter ? 1 : KL];
+  if constexpr (MODE != kModeFilter) {
 #pragma unroll
-  for (int p = 0; p < KL; ++p) {
-    ls[p] = -INFINITY;
-    lr[p] = kNoRow;
+    for (int p = 0; p < KL; ++p) {
+      ls[p] = -INFINITY;
+      lr[p] = kNoRow;
+    }
   }
 
-  const int urow = threadIdx.x >> 1, uhalf = threadIdx.x & 1;   // unpack: 2 threads per row
   for (int64_t tile = t0; tile < t1; ++tile) {
     const int64_t rbase = tile * kTB;
     const int rows = (int)min<int64_t>(kTB, a.n - rbase);
     floatx16 acc[4];
-#pragma unroll
-    for (int t = 0; t < 4; ++t)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[t][r] = 0.0f;
+    score_tile<B>(a, rbase, rows, QH, QL, qrows, lds, acc);
 
-    // stage 0
-    auto load_codes = [&](int k0, uint32_t (&cw)[B]) {
-      if (urow < rows && k0 + 32 * uhalf < a.D) {
-        const uint32_t* src = a.codes + (rbase + urow) * a.row_words + (int64_t)(k0 / 32 + uhalf) * B;
-#pragma unroll
-        for (int i = 0; i < B; ++i) cw[i] = src[i];
-      } else {
-#pragma unroll
-        for (int i = 0; i < B; ++i) cw[i] = 0u;
-      }
-    };
-    auto store_codes = [&](_Float16* s, const uint32_t (&cw)[B]) {
-      _Float16 h[32];
-      unpack32<B>(cw, h);
-      _Float16* dst = s + urow * kLdk + uhalf * 32;
-#pragma unroll
-      for (int i = 0; i < 32; i += 8) *reinterpret_cast<uint4*>(dst + i) = *reinterpret_cast<const uint4*>(h + i);
-    };
-    uint32_t cw[B];
-    SlabRegs rh, rl;
-    load_codes(0, cw);
-    slab_load(QH, qrows, a.D, 0, a.D, rh);
-    slab_load(QL, qrows, a.D, 0, a.D, rl);
-    store_codes(buf(0), cw);
-    slab_store(buf(2), rh);
-    slab_store(buf(4), rl);
-    __syncthreads();
-    int cur = 0;
-    for (int k0 = 0; k0 < a.D; k0 += kBK) {
-      const bool more = k0 + kBK < a.D;
-      if (more) {
-        load_codes(k0 + kBK, cw);
-        slab_load(QH, qrows, a.D, k0 + kBK, a.D, rh);
-        slab_load(QL, qrows, a.D, k0 + kBK, a.D, rl);
-      }
-#pragma unroll
-      for (int kk = 0; kk < kBK / 16; ++kk) {
-        const half8 bh = frag_load(buf(2 + cur), wave * 32, kk);
-        const half8 bl = frag_load(buf(4 + cur), wave * 32, kk);
-        half8 fa[4];
-#pragma unroll
-        for (int t = 0; t < 4; ++t) fa[t] = frag_load(buf(cur), t * 32, kk);
-#pragma unroll
-        for (int t = 0; t < 4; ++t) acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fa[t], bh, acc[t], 0, 0, 0);
-#pragma unroll
-        for (int t = 0; t < 4; ++t) acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fa[t], bl, acc[t], 0, 0, 0);
-      }
-      if (more) {
-        store_codes(buf(cur ^ 1), cw);
-        slab_store(buf(2 + (cur ^ 1)), rh);
-        slab_store(buf(4 + (cur ^ 1)), rl);
-      }
-      __syncthreads();
-      cur ^= 1;
-    }
-
-    // epilogue: candidates against this lane's list threshold
     float mx = -INFINITY;
 #pragma unroll
     for (int t = 0; t < 4; ++t)
@@ -241,6 +266,26 @@ __global__ __launch_bounds__(kWG) void k_score(ScoreArgs a) {
         const float sc = acc[t][r] * osc;
         mx = (rl_ < rows) ? fmaxf(mx, sc) : mx;
       }
+    if constexpr (MODE == kModeFilter) {
+      const bool hot = j < a.nq && mx >= th;
+      if (__ballot(hot) != 0ull && hot) {
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int rl_ = t * 32 + acc_row(r, lane);
+            const float sc = acc[t][r] * osc;
+            if (rl_ < rows && sc >= th) {
+              const uint32_t idx = atomicAdd(&a.cand_cnt[j], 1u);
+              if (idx < a.cap) {
+                a.cand_s[j * a.cap + idx] = sc;
+                a.cand_r[j * a.cap + idx] = (int)(rbase + rl_);
+              }
+            }
+          }
+      }
+      // no LDS use here: the K loop's last barrier already protects the slabs
+    } else {
     const bool hot = mx >= ls[KL - 1];
     if (__ballot(hot) != 0ull) {
       // Park this wave's 64 scores per lane in LDS (free after the K loop) and
@@ -262,8 +307,10 @@ __global__ __launch_bounds__(kWG) void k_score(ScoreArgs a) {
       }
     }
     __syncthreads();   // LDS is reused by the next tile's first slab
+    }
   }
-  if (j < a.nq) {
+  if constexpr (MODE != kModeFilter) {
+    if (j >= a.nq) return;
     const int slot = lane >> 5;
     const int64_t o = ((j * a.splits + split) * 2 + slot) * (int64_t)KL;
 #pragma unroll
@@ -274,26 +321,70 @@ __global__ __launch_bounds__(kWG) void k_score(ScoreArgs a) {
   }
 }
 
-// One wave per query.  The candidates are the sorted per-lane lists of the
-// scoring kernel (segments of KL entries, of which only the first k can
-// matter).  Each lane folds its share into a sorted register list; then k
-// rounds take the best list head of the wave under (score desc, row asc).
-// Rows are distinct across lists, so the winning head identifies its lane.
+// Fold a lane's share of candidates into a sorted register list, then take k
+// rounds of the best list head of the wave under (score desc, row asc).  Rows
+// are distinct, so the winning head identifies its lane.  Writes the k picks
+// (ids mapped to global ids) and/or the k-th score.
 template <int KL>
-__global__ __launch_bounds__(256) void k_topk_merge(int64_t nq, int cands, int k, const float* __restrict__ ps,
-                                                    const int32_t* __restrict__ pr, const QMeta* __restrict__ meta,
-                                                    const int64_t* __restrict__ ids, float* __restrict__ out_s,
-                                                    int64_t* __restrict__ out_i, float* __restrict__ bound) {
+__device__ __forceinline__ void wave_select(int k, float (&ls)[KL], int (&lr)[KL], int64_t j,
+                                            const int64_t* __restrict__ ids, float* __restrict__ out_s,
+                                            int64_t* __restrict__ out_i, float* __restrict__ kth) {
   const int lane = threadIdx.x & 63;
-  const int64_t j = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (j >= nq) return;
-  const QMeta m = meta[j];
+  for (int t = 0; t < k; ++t) {
+    float bs = ls[0];
+    int br = lr[0];
+    for (int o = 32; o > 0; o >>= 1) {
+      const float os = __shfl_xor(bs, o);
+      const int orr = __shfl_xor(br, o);
+      if (better(os, orr, bs, br)) { bs = os; br = orr; }
+    }
+    if (br != kNoRow && lr[0] == br) {        // this lane's head won: pop it
+#pragma unroll
+      for (int p = 0; p < KL - 1; ++p) {
+        ls[p] = ls[p + 1];
+        lr[p] = lr[p + 1];
+      }
+      ls[KL - 1] = -INFINITY;
+      lr[KL - 1] = kNoRow;
+    }
+    if (lane == 0) {
+      if (out_s) {
+        out_s[j * k + t] = (br == kNoRow) ? -INFINITY : bs;
+        out_i[j * k + t] = (br == kNoRow) ? -1 : ids[br];
+      }
+      if (kth && t == k - 1) kth[j] = (br == kNoRow) ? -INFINITY : bs;
+    }
+  }
+}
+
+__device__ __forceinline__ bool write_bad(const QMeta& m, int64_t j, int k, float* out_s, int64_t* out_i,
+                                          float* bound) {
+  const int lane = threadIdx.x & 63;
   if (lane == 0 && bound) bound[j] = m.bound;
-  if (m.bad) {
+  if (!m.bad) return false;
+  if (out_s)
     for (int t = lane; t < k; t += 64) {
       out_s[j * k + t] = __builtin_nanf("");
       out_i[j * k + t] = -1;
     }
+  return true;
+}
+
+// One wave per query: the k best of the per-lane lists (segments of KL sorted
+// entries, of which only the first k can matter).  With qflag set, only
+// flagged queries are processed (the fallback after a candidate overflow).
+template <int KL>
+__global__ __launch_bounds__(256) void k_topk_merge(int64_t nq, int cands, int k, const float* __restrict__ ps,
+                                                    const int32_t* __restrict__ pr, const QMeta* __restrict__ meta,
+                                                    const int64_t* __restrict__ ids, float* __restrict__ out_s,
+                                                    int64_t* __restrict__ out_i, float* __restrict__ bound,
+                                                    float* __restrict__ kth, const uint32_t* __restrict__ qflag) {
+  const int lane = threadIdx.x & 63;
+  const int64_t j = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (j >= nq) return;
+  if (qflag && qflag[j] == 0u) return;
+  if (write_bad(meta[j], j, k, out_s, out_i, bound)) {
+    if (kth && lane == 0) kth[j] = __builtin_nanf("");
     return;
   }
   const float* s = ps + j * (int64_t)cands;
@@ -313,52 +404,97 @@ __global__ __launch_bounds__(256) void k_topk_merge(int64_t nq, int cands, int k
     if (!better(cs, cr, ls[KL - 1], lr[KL - 1])) continue;
     list_insert<KL>(ls, lr, cs, cr);
   }
-  for (int t = 0; t < k; ++t) {
-    float bs = ls[0];
-    int br = lr[0];
-    for (int o = 32; o > 0; o >>= 1) {
-      const float os = __shfl_xor(bs, o);
-      const int orr = __shfl_xor(br, o);
-      if (better(os, orr, bs, br)) { bs = os; br = orr; }
-    }
-    if (br != kNoRow && lr[0] == br) {        // this lane's head won: pop it
-#pragma unroll
-      for (int p = 0; p < KL - 1; ++p) {
-        ls[p] = ls[p + 1];
-        lr[p] = lr[p + 1];
-      }
-      ls[KL - 1] = -INFINITY;
-      lr[KL - 1] = kNoRow;
-    }
-    if (lane == 0) {
-      out_s[j * k + t] = (br == kNoRow) ? -INFINITY : bs;
-      out_i[j * k + t] = (br == kNoRow) ? -1 : ids[br];
-    }
+  wave_select<KL>(k, ls, lr, j, ids, out_s, out_i, kth);
+}
+
+// One wave per query: the k best of the query's candidate buffer.  A buffer
+// that overflowed is flagged (query and query tile) for the exact fallback.
+template <int KL>
+__global__ __launch_bounds__(256) void k_cand_select(int64_t nq, uint32_t cap, int k, const uint32_t* __restrict__ cnt,
+                                                     const float* __restrict__ cs, const int32_t* __restrict__ cr,
+                                                     const QMeta* __restrict__ meta, const int64_t* __restrict__ ids,
+                                                     float* __restrict__ out_s, int64_t* __restrict__ out_i,
+                                                     float* __restrict__ bound, uint32_t* __restrict__ qflag,
+                                                     uint32_t* __restrict__ tflag) {
+  const int lane = threadIdx.x & 63;
+  const int64_t j = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (j >= nq) return;
+  const uint32_t c = cnt[j];
+  const bool over = c > cap;
+  if (lane == 0) {
+    qflag[j] = over ? 1u : 0u;
+    if (over) atomicOr(&tflag[j / kTB], 1u);
   }
+  if (write_bad(meta[j], j, k, out_s, out_i, bound) || over) return;
+  float ls[KL];
+  int lr[KL];
+#pragma unroll
+  for (int p = 0; p < KL; ++p) {
+    ls[p] = -INFINITY;
+    lr[p] = kNoRow;
+  }
+  for (uint32_t i = lane; i < c; i += 64) {
+    const int row = cr[j * cap + i];
+    const float sc = cs[j * cap + i];
+    if (!better(sc, row, ls[KL - 1], lr[KL - 1])) continue;
+    list_insert<KL>(ls, lr, sc, row);
+  }
+  wave_select<KL>(k, ls, lr, j, ids, out_s, out_i, nullptr);
+}
+
+__global__ void k_clear_u32(uint32_t* a, int64_t na, uint32_t* b, int64_t nb) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t st = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t t = i; t < na; t += st) a[t] = 0u;
+  for (int64_t t = i; t < nb; t += st) b[t] = 0u;
 }
 
 template <int B, int KL>
-void launch_score_b(dim3 grid, hipStream_t st, const ScoreArgs& a) {
-  hipLaunchKernelGGL((k_score<B, KL>), grid, dim3(kWG), 0, st, a);
+void launch_mode(int mode, dim3 grid, hipStream_t st, const ScoreArgs& a) {
+  if (mode == kModeLists) hipLaunchKernelGGL((k_score<B, KL, kModeLists>), grid, dim3(kWG), 0, st, a);
+  else if (mode == kModeFilter) hipLaunchKernelGGL((k_score<B, KL, kModeFilter>), grid, dim3(kWG), 0, st, a);
+  else hipLaunchKernelGGL((k_score<B, KL, kModeFallback>), grid, dim3(kWG), 0, st, a);
 }
 
 template <int B>
-lam_status launch_score(int kl, dim3 grid, hipStream_t st, const ScoreArgs& a) {
-  if (kl == 16) launch_score_b<B, 16>(grid, st, a);
-  else launch_score_b<B, 64>(grid, st, a);
-  return LAM_OK;
-}
-
-template <int B>
-lam_status dispatch_bits(int b, int kl, dim3 grid, hipStream_t st, const ScoreArgs& a) {
-  if (b == B) return launch_score<B>(kl, grid, st, a);
-  if constexpr (B < 12) return dispatch_bits<B + 1>(b, kl, grid, st, a);
+lam_status dispatch_bits(int b, int kl, int mode, dim3 grid, hipStream_t st, const ScoreArgs& a) {
+  if (b == B) {
+    if (kl == 16) launch_mode<B, 16>(mode, grid, st, a);
+    else launch_mode<B, 64>(mode, grid, st, a);
+    return LAM_OK;
+  }
+  if constexpr (B < 12) return dispatch_bits<B + 1>(b, kl, mode, grid, st, a);
   set_error("scoring supports codes of at most 12 bits (got %d)", b);
   return LAM_ESTATE;
 }
 
+// Split a tile range over query tiles so that the grid holds about 1024
+// workgroups; returns (splits, tiles per split).
+void plan_splits(int nqt, int64_t ntiles, int* splits, int64_t* tps) {
+  if (ntiles <= 0) {
+    *splits = 1;
+    *tps = 0;
+    return;
+  }
+  const int64_t want = std::max<int64_t>(1, (1024 + nqt - 1) / nqt);
+  int64_t s = std::min<int64_t>(want, ntiles);
+  const int64_t t = (ntiles + s - 1) / s;
+  *tps = t;
+  *splits = (int)((ntiles + t - 1) / t);
+}
+
 }  // namespace
 
+// Scoring plan.  With at most S store rows (S = k * n / 1024, at least 4,096)
+// one pass of per-lane lists gives the exact top-k.  Beyond that:
+//   1. exact top-k of the first S rows: its k-th score theta_j is a lower
+//      bound of the k-th best score over the whole store;
+//   2. a full scan appends every row scoring >= theta_j to query j's candidate
+//      buffer (about k * n / S = 1,024 entries expected; capacity 4,096);
+//   3. the k best candidates by (score desc, id asc) are the answer;
+//   4. a query whose buffer overflowed (many equal scores, say) is redone with
+//      per-lane lists over the whole store; launched always, it returns at once
+//      when nothing overflowed, so the call stays asynchronous.
 lam_status score_topk(lam_ctx* ctx, const lam_store* st, const float* q, int64_t nq, int32_t k, float* scores,
                       int64_t* ids, float* bound) {
   if (nq == 0) return LAM_OK;
@@ -371,46 +507,125 @@ lam_status score_topk(lam_ctx* ctx, const lam_store* st, const float* q, int64_t
   LAM_TRY(ctx->scratch[S_QHI].ensure((size_t)nq * D * 2));
   LAM_TRY(ctx->scratch[S_QLO].ensure((size_t)nq * D * 2));
   LAM_TRY(ctx->scratch[S_QMETA].ensure((size_t)nq * sizeof(QMeta)));
+  QMeta* qmeta = ctx->scratch[S_QMETA].as<QMeta>();
   {
     ProfScope ps(ctx, "score_prep");
     hipLaunchKernelGGL(k_score_prep, dim3((unsigned)((nq + 3) / 4)), dim3(256), 0, ctx->stream, q, nq, D, st->q.step,
-                       st->q.eps, ctx->scratch[S_QHI].as<_Float16>(), ctx->scratch[S_QLO].as<_Float16>(),
-                       ctx->scratch[S_QMETA].as<QMeta>());
+                       st->q.eps, ctx->scratch[S_QHI].as<_Float16>(), ctx->scratch[S_QLO].as<_Float16>(), qmeta);
     LAM_HIP(hipGetLastError());
   }
   const int nqt = (int)((nq + kTB - 1) / kTB);
   const int64_t ntiles = (n + kTB - 1) / kTB;
-  int splits = 1;
-  if (ntiles > 0) {
-    const int64_t want = std::max<int64_t>(1, (1024 + nqt - 1) / nqt);
-    splits = (int)std::min<int64_t>(want, ntiles);
-  }
-  const int64_t tps = ntiles > 0 ? (ntiles + splits - 1) / splits : 0;
-  if (ntiles > 0) splits = (int)((ntiles + tps - 1) / tps);
-  const int cands = splits * 2 * KL;
-  LAM_TRY(ctx->scratch[S_PART].ensure((size_t)nq * cands * 8));
+  const int64_t sample_rows = std::max<int64_t>(4096, ((int64_t)k * n + 1023) / 1024);
+  const int64_t stiles = std::min<int64_t>(ntiles, (sample_rows + kTB - 1) / kTB);
+  const bool two_pass = stiles < ntiles;
+
+  int sp1 = 1, sp2 = 1;
+  int64_t tps1 = 0, tps2 = 0;
+  plan_splits(nqt, stiles, &sp1, &tps1);
+  plan_splits(nqt, ntiles, &sp2, &tps2);
+  const int cands_max = std::max(sp1, sp2) * 2 * KL;
+  LAM_TRY(ctx->scratch[S_PART].ensure((size_t)nq * cands_max * 8));
   float* part_s = ctx->scratch[S_PART].as<float>();
-  int32_t* part_r = reinterpret_cast<int32_t*>(part_s + (size_t)nq * cands);
-  if (ntiles > 0) {
-    ScoreArgs a{st->codes, n, D, (int64_t)D * b / 32, ctx->scratch[S_QHI].as<_Float16>(),
-                ctx->scratch[S_QLO].as<_Float16>(), ctx->scratch[S_QMETA].as<QMeta>(), nq, nqt, splits, tps,
-                part_s, part_r};
-    const int64_t grid = (int64_t)nqt * splits;
-    LAM_CHECK(grid < (1LL << 31), LAM_EINVAL, "scoring grid too large");
+  int32_t* part_r = reinterpret_cast<int32_t*>(part_s + (size_t)nq * cands_max);
+
+  ScoreArgs a{};
+  a.codes = st->codes;
+  a.n = n;
+  a.D = D;
+  a.row_words = (int64_t)D * b / 32;
+  a.qhi = ctx->scratch[S_QHI].as<_Float16>();
+  a.qlo = ctx->scratch[S_QLO].as<_Float16>();
+  a.meta = qmeta;
+  a.nq = nq;
+  a.nqt = nqt;
+  a.part_s = part_s;
+  a.part_r = part_r;
+  const dim3 gq((unsigned)((nq + 3) / 4));
+
+  if (!two_pass) {
+    if (ntiles > 0) {
+      a.tile_begin = 0;
+      a.tile_end = ntiles;
+      a.splits = sp2;
+      a.tiles_per_split = tps2;
+      ProfScope ps(ctx, "score_mfma");
+      LAM_TRY(dispatch_bits<1>(b, KL, kModeLists, dim3((unsigned)(nqt * sp2)), ctx->stream, a));
+      LAM_HIP(hipGetLastError());
+    }
+    ProfScope ps(ctx, "score_merge");
+    const int nc = ntiles > 0 ? sp2 * 2 * KL : 0;
+    if (KL == 16)
+      hipLaunchKernelGGL((k_topk_merge<16>), gq, dim3(256), 0, ctx->stream, nq, nc, k, part_s, part_r, qmeta, st->ids,
+                         scores, ids, bound, nullptr, nullptr);
+    else
+      hipLaunchKernelGGL((k_topk_merge<64>), gq, dim3(256), 0, ctx->stream, nq, nc, k, part_s, part_r, qmeta, st->ids,
+                         scores, ids, bound, nullptr, nullptr);
+    LAM_HIP(hipGetLastError());
+    return LAM_OK;
+  }
+
+  const uint32_t cap = 4096;
+  LAM_TRY(ctx->scratch[S_CAND].ensure((size_t)nq * cap * 8 + (size_t)nq * 12 + (size_t)nqt * 4 + 256));
+  float* cand_s = ctx->scratch[S_CAND].as<float>();
+  int32_t* cand_r = reinterpret_cast<int32_t*>(cand_s + (size_t)nq * cap);
+  uint32_t* cand_cnt = reinterpret_cast<uint32_t*>(cand_r + (size_t)nq * cap);
+  float* thr = reinterpret_cast<float*>(cand_cnt + nq);
+  uint32_t* qflag = reinterpret_cast<uint32_t*>(thr + nq);
+  uint32_t* tflag = qflag + nq;
+  hipLaunchKernelGGL(k_clear_u32, dim3(64), dim3(256), 0, ctx->stream, cand_cnt, nq, tflag, (int64_t)nqt);
+  LAM_HIP(hipGetLastError());
+  {  // 1. exact top-k of the sample -> thresholds
+    ProfScope ps(ctx, "score_sample");
+    a.tile_begin = 0;
+    a.tile_end = stiles;
+    a.splits = sp1;
+    a.tiles_per_split = tps1;
+    LAM_TRY(dispatch_bits<1>(b, KL, kModeLists, dim3((unsigned)(nqt * sp1)), ctx->stream, a));
+    const int nc = sp1 * 2 * KL;
+    if (KL == 16)
+      hipLaunchKernelGGL((k_topk_merge<16>), gq, dim3(256), 0, ctx->stream, nq, nc, k, part_s, part_r, qmeta, st->ids,
+                         nullptr, nullptr, nullptr, thr, nullptr);
+    else
+      hipLaunchKernelGGL((k_topk_merge<64>), gq, dim3(256), 0, ctx->stream, nq, nc, k, part_s, part_r, qmeta, st->ids,
+                         nullptr, nullptr, nullptr, thr, nullptr);
+    LAM_HIP(hipGetLastError());
+  }
+  a.tile_begin = 0;
+  a.tile_end = ntiles;
+  a.splits = sp2;
+  a.tiles_per_split = tps2;
+  a.thr = thr;
+  a.cand_s = cand_s;
+  a.cand_r = cand_r;
+  a.cand_cnt = cand_cnt;
+  a.cap = cap;
+  a.tflag = tflag;
+  {  // 2. full scan with the thresholds
     ProfScope ps(ctx, "score_mfma");
-    LAM_TRY(dispatch_bits<1>(b, KL, dim3((unsigned)grid), ctx->stream, a));
+    LAM_TRY(dispatch_bits<1>(b, KL, kModeFilter, dim3((unsigned)(nqt * sp2)), ctx->stream, a));
+    LAM_HIP(hipGetLastError());
+  }
+  {  // 3. select; 4. exact fallback for overflowed buffers (returns at once otherwise)
+    ProfScope ps(ctx, "score_merge");
+    if (KL == 16)
+      hipLaunchKernelGGL((k_cand_select<16>), gq, dim3(256), 0, ctx->stream, nq, cap, k, cand_cnt, cand_s, cand_r,
+                         qmeta, st->ids, scores, ids, bound, qflag, tflag);
+    else
+      hipLaunchKernelGGL((k_cand_select<64>), gq, dim3(256), 0, ctx->stream, nq, cap, k, cand_cnt, cand_s, cand_r,
+                         qmeta, st->ids, scores, ids, bound, qflag, tflag);
     LAM_HIP(hipGetLastError());
   }
   {
-    ProfScope ps(ctx, "score_merge");
-    const dim3 g((unsigned)((nq + 3) / 4));
-    const int nc = ntiles > 0 ? cands : 0;
+    ProfScope ps(ctx, "score_fallback");
+    LAM_TRY(dispatch_bits<1>(b, KL, kModeFallback, dim3((unsigned)(nqt * sp2)), ctx->stream, a));
+    const int nc = sp2 * 2 * KL;
     if (KL == 16)
-      hipLaunchKernelGGL((k_topk_merge<16>), g, dim3(256), 0, ctx->stream, nq, nc, k, part_s, part_r,
-                         ctx->scratch[S_QMETA].as<QMeta>(), st->ids, scores, ids, bound);
+      hipLaunchKernelGGL((k_topk_merge<16>), gq, dim3(256), 0, ctx->stream, nq, nc, k, part_s, part_r, qmeta, st->ids,
+                         scores, ids, bound, nullptr, qflag);
     else
-      hipLaunchKernelGGL((k_topk_merge<64>), g, dim3(256), 0, ctx->stream, nq, nc, k, part_s, part_r,
-                         ctx->scratch[S_QMETA].as<QMeta>(), st->ids, scores, ids, bound);
+      hipLaunchKernelGGL((k_topk_merge<64>), gq, dim3(256), 0, ctx->stream, nq, nc, k, part_s, part_r, qmeta, st->ids,
+                         scores, ids, bound, nullptr, qflag);
     LAM_HIP(hipGetLastError());
   }
   return LAM_OK;

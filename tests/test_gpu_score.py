@@ -146,3 +146,24 @@ def test_corpus_sampled(lam):
     sample = np.random.default_rng(0).choice(q.shape[0], 64, replace=False)
     worst = _compare(gs[sample], gi[sample], c, np.arange(x.shape[0]), q[sample], eps, k)
     print(f"corpus: max |score - oracle| = {worst:.3g}")
+
+
+@pytest.mark.parametrize("k", [10, 50])
+def test_two_pass_and_overflow_fallback(lam, k):
+    """A store beyond the sample size takes the threshold/candidate plan; an
+    all-zero query ties every row at score 0, overflows its candidate buffer
+    and must come back exact from the fallback (the k lowest ids)."""
+    rng = np.random.default_rng(11)
+    n = 20000
+    x = synth.unit_rows(rng, n, 64).astype(np.float32)
+    s = _store_from_rows(lam, x)
+    s.quantize(1e-3)
+    q = synth.unit_rows(rng, 40, 64).astype(np.float32)
+    q[[3, 17]] = 0.0
+    gs, gi, gb = s.score_topk(_dev(q), k)
+    gs, gi = gs.cpu().numpy(), gi.cpu().numpy()
+    assert np.all(gi[3] == np.arange(k)) and np.all(gs[3] == 0.0)
+    assert np.all(gi[17] == np.arange(k))
+    c = qeps.codes(x, 1e-3).reshape(n, -1)
+    keep = [j for j in range(q.shape[0]) if j not in (3, 17)]
+    _compare(gs[keep], gi[keep], c, np.arange(n), q[keep], 1e-3, k)
