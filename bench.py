@@ -44,7 +44,42 @@ def parse():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true", help="skip timing the CPU oracle")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="after the timed steps, run a plain 1 GiB device-to-device copy three times (a "
+                         "known-size reference for hardware byte counters)")
     return ap.parse_args()
+
+
+KERNELS = ("qeps_encode", "qeps_decode", "dedup_prep", "dedup_screen", "dedup_verify", "dedup_resolve",
+           "dedup_append", "store_absmax", "store_encode", "store_decode", "score_prep", "score_mfma",
+           "score_merge")
+HERE = os.path.dirname(os.path.abspath(__file__))
+TRAFFIC_FILE = os.path.join(HERE, "profiles", "traffic.json")
+
+
+def _sha256(path):
+    import hashlib
+    with open(os.path.join(HERE, path), "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def measured_traffic(kernel):
+    """HBM bytes per launch of `kernel` from the committed rocprofv3 counter
+    runs (FETCH_SIZE and WRITE_SIZE, each scaled by what the counter reads for a
+    plain copy of known size), or None when there are none or the kernel's
+    sources have changed since they were taken."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+        k = t["kernels"][kernel]
+        if any(_sha256(p) != h for p, h in k["sources"].items()):
+            return None
+        cal = t["copy_calibration"]
+        ff = cal["bytes"] / 1024.0 / cal["fetch_kib"]
+        wf = cal["bytes"] / 1024.0 / cal["write_kib"]
+        return (k["fetch_kib_per_dispatch"] * ff + k["write_kib_per_dispatch"] * wf) * 1024.0
+    except (OSError, KeyError, ValueError):
+        return None
 
 
 def cpu_baseline(x, pairs):
@@ -135,50 +170,77 @@ def main():
     n_store = int(kept.sum())
     info = store.info()
 
+    # 1. instrumented pass: HIP events around every launch, for the per-kernel
+    #    breakdown (the events cost time of their own, so this pass is not timed)
+    prof_steps = max(2, min(args.steps, 10))
     ctx.profile_reset()
+    ctx.profile_only(None)
+    ctx.profile(True)
+    for i in range(prof_steps):
+        step(args.warmup + i)
+    torch.cuda.synchronize()
+    ctx.profile(False)
+    kinfo = {}
+    for name in KERNELS:
+        tot, cnt = ctx.profile_read(name)
+        if cnt:
+            kinfo[name] = {"ms_per_step": tot / prof_steps, "launches_per_step": cnt / prof_steps,
+                           "avg_launch_ms": tot / cnt}
+    dominant = max(kinfo, key=lambda k: kinfo[k]["ms_per_step"])
+
+    # 2. timed pass: events on the dominant kernel's launches only
+    ctx.profile_reset()
+    ctx.profile_only(dominant)
     ctx.profile(True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
-        step(args.warmup + i)
+        step(args.warmup + prof_steps + i)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     ctx.profile(False)
+    ctx.profile_only(None)
     ms = (t1 - t0) * 1e3 / args.steps
+    dom_tot, dom_cnt = ctx.profile_read(dominant)
 
-    kinfo = {}
-    for name in ("qeps_encode", "qeps_decode", "dedup_prep", "dedup_screen",
-                 "dedup_verify", "dedup_resolve", "dedup_append", "store_absmax", "store_encode", "store_decode",
-                 "score_prep", "score_mfma", "score_merge"):
-        tot, cnt = ctx.profile_read(name)
-        if cnt:
-            kinfo[name] = {"ms_per_step": tot / args.steps, "launches_per_step": cnt / args.steps,
-                           "avg_launch_ms": tot / cnt}
+    if args.copy_calibration:
+        src = torch.ones(1 << 28, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+
     bq = p_raw.bits / 8.0
     store_elems = n_store * D
     bs = info.q.bits / 8.0
-    work = {  # algorithmic units per step: (amount, unit, peak, bound)
-        "qeps_encode": ((4 + bq) * n_raw / 1e9, "GB", HBM_PEAK_GBS, "hbm"),
-        "qeps_decode": ((4 + bq) * n_raw / 1e9, "GB", HBM_PEAK_GBS, "hbm"),
-        "store_encode": ((4 + bs) * store_elems / 1e9, "GB", HBM_PEAK_GBS, "hbm"),
-        "store_decode": ((4 + bs) * store_elems / 1e9, "GB", HBM_PEAK_GBS, "hbm"),
+    screen_bytes = 2.0 * D * (screen_store_pairs / BATCH + n) + 8.0 * n   # fp16 store + chunk rows, norms
+    work = {  # algorithmic units per step: (amount, unit, peak, bound, algorithmic bytes)
+        "qeps_encode": ((4 + bq) * n_raw / 1e9, "GB", HBM_PEAK_GBS, "hbm", (4 + bq) * n_raw),
+        "qeps_decode": ((4 + bq) * n_raw / 1e9, "GB", HBM_PEAK_GBS, "hbm", (4 + bq) * n_raw),
+        "store_encode": ((4 + bs) * store_elems / 1e9, "GB", HBM_PEAK_GBS, "hbm", (4 + bs) * store_elems),
+        "store_decode": ((4 + bs) * store_elems / 1e9, "GB", HBM_PEAK_GBS, "hbm", (4 + bs) * store_elems),
         "dedup_screen": (2.0 * D * (screen_store_pairs + screen_chunk_pairs) / 1e12, "TFLOP",
-                         MFMA_F16_PEAK_TFLOPS, "mfma"),
-        "score_mfma": (2.0 * D * qd.shape[0] * n_store / 1e12, "TFLOP", MFMA_F16_PEAK_TFLOPS, "mfma"),
+                         MFMA_F16_PEAK_TFLOPS, "mfma", screen_bytes),
+        "score_mfma": (2.0 * D * qd.shape[0] * n_store / 1e12, "TFLOP", MFMA_F16_PEAK_TFLOPS, "mfma", None),
     }
-    for name, (amt, unit, peak, bound) in work.items():
+    for name, (amt, unit, peak, bound, _) in work.items():
         if name in kinfo:
             rate = amt / (kinfo[name]["ms_per_step"] / 1e3)
             kinfo[name].update({"achieved": rate, "unit": unit + "/s", "peak": peak, "frac": rate / peak})
-    dominant = max(kinfo, key=lambda k: kinfo[k]["ms_per_step"])
     dom_work = work.get(dominant)
-    if dom_work:
-        d = kinfo[dominant]
-        per_launch = dom_work[0] / d["launches_per_step"]
-        achieved = per_launch / (d["avg_launch_ms"] / 1e3)
+    if dom_work and dom_cnt:
+        launches = dom_cnt / args.steps
+        per_launch = dom_work[0] / launches
+        avg_s = dom_tot / dom_cnt / 1e3
+        achieved = per_launch / avg_s
         roofline = {"kernel": dominant, "bound": dom_work[3], "achieved": achieved,
                     "peak": dom_work[2], "unit": "GB/s" if dom_work[1] == "GB" else "TFLOP/s",
-                    "frac": achieved / dom_work[2], "traffic": None}
+                    "frac": achieved / dom_work[2], "traffic": measured_traffic(dominant),
+                    "avg_launch_us": avg_s * 1e6, "launches_per_step": launches,
+                    "algorithmic_per_launch": per_launch * (1e3 if dom_work[1] == "GB" else 1.0),
+                    "algorithmic_unit": "MB" if dom_work[1] == "GB" else "TFLOP",
+                    "algorithmic_bytes_per_launch": (dom_work[4] / launches if dom_work[4] else None)}
     else:
         roofline = {"kernel": dominant, "bound": "latency", "achieved": None, "peak": None, "unit": None,
                     "frac": None, "traffic": None}
@@ -213,6 +275,8 @@ def main():
                                           / 1e3)),
         "roofline": roofline,
         "kernels": kinfo,
+        "kernels_note": (f"per-kernel breakdown from {prof_steps} separate steps with HIP events around every "
+                         f"launch; the timed steps carry events on the dominant kernel only"),
     }
     if not args.no_cpu_baseline:
         ref, cb = cpu_baseline(x, pairs)

@@ -76,6 +76,10 @@ lam_status lam_ctx_synchronize(lam_ctx* ctx);
  * returns the summed elapsed milliseconds and launch count of one kernel name
  * (0 / 0 if never launched).  For benchmarks; off by default. */
 lam_status lam_ctx_profile(lam_ctx* ctx, int enable);
+/* Restricts the timing to the launches of one kernel name (NULL or "": every
+ * kernel), so that a timed run carries only that kernel's events.  The name is
+ * copied. */
+lam_status lam_ctx_profile_only(lam_ctx* ctx, const char* kernel);
 lam_status lam_ctx_profile_reset(lam_ctx* ctx);
 lam_status lam_ctx_profile_read(lam_ctx* ctx, const char* kernel, double* total_ms, int64_t* launches);
 

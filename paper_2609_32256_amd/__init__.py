@@ -76,6 +76,7 @@ _SIGS = {
     "lam_ctx_destroy": ([_P], None),
     "lam_ctx_synchronize": ([_P], ctypes.c_int),
     "lam_ctx_profile": ([_P, ctypes.c_int], ctypes.c_int),
+    "lam_ctx_profile_only": ([_P, ctypes.c_char_p], ctypes.c_int),
     "lam_ctx_profile_reset": ([_P], ctypes.c_int),
     "lam_ctx_profile_read": ([_P, ctypes.c_char_p, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(_I64)],
                              ctypes.c_int),
@@ -140,6 +141,10 @@ class Context:
 
     def profile(self, enable: bool = True):
         _check(_lib.lam_ctx_profile(self._h, 1 if enable else 0))
+
+    def profile_only(self, kernel: str | None):
+        """Time only the launches of one kernel name (None: every kernel)."""
+        _check(_lib.lam_ctx_profile_only(self._h, (kernel or "").encode()))
 
     def profile_reset(self):
         _check(_lib.lam_ctx_profile_reset(self._h))

@@ -61,6 +61,7 @@ struct DeviceGuard {
 lam_status prof_begin(lam_ctx* ctx, const char* name, size_t* slot) {
   *slot = (size_t)-1;
   if (!ctx->profiling) return LAM_OK;
+  if (!ctx->prof_only.empty() && ctx->prof_only != name) return LAM_OK;
   ProfRec r{name, nullptr, nullptr};
   for (hipEvent_t* ev : {&r.a, &r.b}) {
     if (!ctx->event_pool.empty()) {
@@ -90,6 +91,7 @@ __global__ void k_zero_words(uint32_t* p, int n) {
 }
 
 lam_status clear_flags(lam_ctx* ctx) {
+  ctx->flags_zero = false;   // the caller's kernels write them next
   hipLaunchKernelGGL(k_zero_words, dim3(1), dim3(64), 0, ctx->stream,
                      reinterpret_cast<uint32_t*>(ctx->flags_dev), (int)(sizeof(DevFlags) / 4));
   LAM_HIP(hipGetLastError());
@@ -174,8 +176,10 @@ lam_status lam_ctx_create(int device, void* hip_stream, lam_ctx** out) {
   c->device = device;
   c->stream = static_cast<hipStream_t>(hip_stream);
   if (hipMalloc(&c->flags_dev, sizeof(DevFlags)) != hipSuccess ||
-      hipHostMalloc(&c->flags_host, sizeof(DevFlags), hipHostMallocDefault) != hipSuccess) {
+      hipHostMalloc(&c->flags_host, sizeof(DevFlags), hipHostMallocCoherent) != hipSuccess ||
+      hipHostGetDevicePointer(reinterpret_cast<void**>(&c->flags_host_dev), c->flags_host, 0) != hipSuccess) {
     if (c->flags_dev) (void)hipFree(c->flags_dev);
+    if (c->flags_host) (void)hipHostFree(c->flags_host);
     delete c;
     set_error("could not allocate the context status words");
     return LAM_ENOMEM;
@@ -210,6 +214,12 @@ lam_status lam_ctx_synchronize(lam_ctx* ctx) {
 lam_status lam_ctx_profile(lam_ctx* ctx, int enable) {
   LAM_CHECK(ctx != nullptr, LAM_EINVAL, "ctx is NULL");
   ctx->profiling = enable != 0;
+  return LAM_OK;
+}
+
+lam_status lam_ctx_profile_only(lam_ctx* ctx, const char* kernel) {
+  LAM_CHECK(ctx != nullptr, LAM_EINVAL, "ctx is NULL");
+  ctx->prof_only = kernel ? kernel : "";
   return LAM_OK;
 }
 

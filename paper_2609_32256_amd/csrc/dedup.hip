@@ -64,7 +64,8 @@ struct StoreMeta {
 struct ChunkCounters {
   uint32_t npairs;        // ambiguous pairs appended in this chunk
   uint32_t n_escalate;
-  uint32_t pad[2];
+  uint32_t blocks_done;   // append workgroups finished (last one exports the status words)
+  uint32_t pad;
 };
 
 __device__ __forceinline__ bool skip_all(const DevFlags* f) {
@@ -88,12 +89,43 @@ __device__ __forceinline__ double wave_sum_f64(double v) {
 }
 
 // ------------------------------------------------------------------ prep
+// Per-chunk state: the first store hit, the in-chunk edge flag, the order-
+// encoded max cosine and the row's edge bitmap words.  Rows of the first chunk
+// are initialised by k_prep, the others by k_chunk_init.
+struct ChunkState {
+  int32_t* firstHit;
+  uint32_t* hasEdge;
+  uint32_t* maxcos;
+  uint64_t* bitmap;
+  int W;
+  int nB;                  // rows of the first chunk
+  ChunkCounters* cc;
+  StoreMeta* meta;
+  int32_t m_first;         // store size at the start of the call
+};
+
+__device__ __forceinline__ void init_chunk_row(const ChunkState& c, int64_t r, int lane) {
+  for (int w = lane; w < c.W; w += 64) c.bitmap[r * c.W + w] = 0ull;
+  if (lane == 0) {
+    c.firstHit[r] = kNone;
+    c.hasEdge[r] = 0u;
+    c.maxcos[r] = 0x007fffffu;  // order-encoded -inf
+  }
+}
+
 __global__ __launch_bounds__(256) void k_prep(const float* __restrict__ x, int64_t n, int D,
                                               _Float16* __restrict__ x16, float* __restrict__ hn,
                                               float* __restrict__ eterm, double K1, double K2, double K3h,
-                                              DevFlags* __restrict__ flags) {
+                                              DevFlags* __restrict__ flags, ChunkState cs) {
   const int lane = threadIdx.x & 63;
   const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    cs.cc->npairs = 0u;
+    cs.cc->n_escalate = 0u;
+    cs.cc->blocks_done = 0u;
+    cs.meta->m = cs.m_first;
+  }
+  if (row < cs.nB) init_chunk_row(cs, row, lane);
   if (row >= n) return;
   const float* p = x + row * D;
   _Float16* q = x16 + row * D;
@@ -129,25 +161,16 @@ __global__ __launch_bounds__(256) void k_prep(const float* __restrict__ x, int64
 }
 
 // ------------------------------------------------------------------ chunk init
-// Clears the chunk's hit/edge state; for the first chunk of a call it also
-// clears the context's status words and sets the store size (one launch
-// instead of three).
-__global__ void k_chunk_init(int nB, int W, int32_t* firstHit, uint32_t* hasEdge, uint32_t* maxcos,
-                             uint64_t* bitmap, ChunkCounters* cc, DevFlags* flags, StoreMeta* meta,
-                             int32_t m_first) {
-  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  const int64_t t0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (m_first >= 0 && t0 < (int64_t)(sizeof(DevFlags) / 4)) reinterpret_cast<uint32_t*>(flags)[t0] = 0u;
-  if (m_first >= 0 && t0 == 0) meta->m = m_first;
-  for (int64_t i = t0; i < nB; i += stride) {
-    firstHit[i] = kNone;
-    hasEdge[i] = 0u;
-    maxcos[i] = 0x007fffffu;  // order-encoded -inf
-  }
-  for (int64_t i = t0; i < (int64_t)nB * W; i += stride) bitmap[i] = 0ull;
-  if (t0 == 0) {
-    cc->npairs = 0u;
-    cc->n_escalate = 0u;
+// Clears the chunk state for the second and later chunks of a call.
+__global__ void k_chunk_init(ChunkState cs) {
+  const int lane = threadIdx.x & 63;
+  const int64_t waves = (int64_t)gridDim.x * (blockDim.x >> 6);
+  for (int64_t r = (int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6); r < cs.nB; r += waves)
+    init_chunk_row(cs, r, lane);
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    cs.cc->npairs = 0u;
+    cs.cc->n_escalate = 0u;
+    cs.cc->blocks_done = 0u;
   }
 }
 
@@ -514,31 +537,49 @@ __global__ __launch_bounds__(kResolveThreads) void k_resolve(ResolveArgs a) {
   }
   __syncthreads();
   const int na = (int)n_active;
-  for (int k = wave; k < na; k += kResolveThreads / 64) {
-    const int i = active[k];
-    const int nw = (i + 63) >> 6;
-    uint64_t e = (lane < nw) ? a.bitmap[(int64_t)i * a.W + lane] : 0ull;
-    const int c = __popcll(e);
-    int incl = c;
-    for (int o = 1; o < 64; o <<= 1) {
-      const int t = __shfl_up(incl, o);
-      if (lane >= o) incl += t;
+  // B. A row's bitmap words (bits j < i) are read by G lanes, G = W rounded up
+  //    to a power of two, so a wave covers 64 / G rows at once; four such sets
+  //    are loaded before any is used, which keeps several loads in flight.
+  const int G = a.W <= 1 ? 1 : 1 << (32 - __clz(a.W - 1));
+  const int sub = lane / G, wl = lane % G;
+  const int rstep = (kResolveThreads / 64) * (64 / G);
+  for (int kb = wave * (64 / G); kb < na; kb += 4 * rstep) {
+    uint64_t e[4];
+    int ir[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int k = kb + u * rstep + sub;
+      ir[u] = k < na ? (int)active[k] : -1;
+      const int nw = (ir[u] + 63) >> 6;
+      e[u] = (ir[u] >= 0 && wl < nw) ? a.bitmap[(int64_t)ir[u] * a.W + wl] : 0ull;
     }
-    const int tot = __shfl(incl, 63);
-    uint32_t base = 0u;
-    if (lane == 0) base = atomicAdd(&n_edges, (uint32_t)tot);
-    base = __shfl(base, 0);
-    if (base + (uint32_t)tot <= (uint32_t)kEdgeCap) {
-      uint32_t p = base + (uint32_t)(incl - c);
-      while (e) {
-        edges[p++] = (uint16_t)(lane * 64 + __builtin_ctzll(e));
-        e &= e - 1ull;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      uint64_t eu = e[u];
+      const int c = __popcll(eu);
+      int incl = c;
+      for (int o = 1; o < G; o <<= 1) {
+        const int t = __shfl_up(incl, o, G);
+        if (wl >= o) incl += t;
       }
-    }
-    if (lane == 0) {
-      eoff[i] = base;
-      elen[i] = (uint16_t)tot;
-      ecur[i] = 0;
+      const int tot = __shfl(incl, sub * G + G - 1);
+      uint32_t base = 0u;
+      if (wl == 0 && ir[u] >= 0) base = atomicAdd(&n_edges, (uint32_t)tot);
+      base = __shfl(base, sub * G);
+      if (ir[u] >= 0) {
+        if (base + (uint32_t)tot <= (uint32_t)kEdgeCap) {
+          uint32_t p = base + (uint32_t)(incl - c);
+          while (eu) {
+            edges[p++] = (uint16_t)(wl * 64 + __builtin_ctzll(eu));
+            eu &= eu - 1ull;
+          }
+        }
+        if (wl == 0) {
+          eoff[ir[u]] = base;
+          elen[ir[u]] = (uint16_t)tot;
+          ecur[ir[u]] = 0;
+        }
+      }
     }
   }
   __syncthreads();
@@ -636,6 +677,8 @@ struct AppendArgs {
   float* ets;
   int64_t* ids;
   DevFlags* flags;
+  ChunkCounters* cc;
+  DevFlags* flags_out;      // host-mapped copy of the status words, or NULL
 };
 
 // One wave per row, four rows per workgroup.  Kept rows are copied into the
@@ -644,11 +687,12 @@ struct AppendArgs {
 constexpr int kAppendRows = 4;
 
 __global__ __launch_bounds__(256) void k_append(AppendArgs a, int nB) {
-  if (skip_all(a.flags)) return;
+  const bool skip = skip_all(a.flags);
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   double dmax = 0.0;
-  for (int r = blockIdx.x * kAppendRows + wave; r < min(nB, (int)(blockIdx.x + 1) * kAppendRows); r += 4) {
+  for (int r = blockIdx.x * kAppendRows + wave; !skip && r < min(nB, (int)(blockIdx.x + 1) * kAppendRows);
+       r += 4) {
     const int p = a.pos[r];
     const float* src = a.xc + (int64_t)r * a.D;
     if (p >= 0) {
@@ -684,6 +728,27 @@ __global__ __launch_bounds__(256) void k_append(AppendArgs a, int nB) {
       atomicMax(reinterpret_cast<unsigned long long*>(&a.flags->dhat2_bits),
                 (unsigned long long)__double_as_longlong(m));
   }
+  if (a.flags_out == nullptr) return;
+  // The last workgroup to finish copies the status words to host memory and
+  // clears them for the next call (every other workgroup's updates are
+  // ordered before its count by the fence).
+  __shared__ bool last;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    __threadfence();
+    last = atomicAdd(&a.cc->blocks_done, 1u) == gridDim.x - 1;
+  }
+  __syncthreads();
+  if (!last) return;
+  __threadfence();
+  constexpr int kWords = (int)(sizeof(DevFlags) / 4);
+  if (threadIdx.x < kWords) {
+    uint32_t* f = reinterpret_cast<uint32_t*>(a.flags);
+    const uint32_t v = __hip_atomic_load(f + threadIdx.x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    reinterpret_cast<uint32_t*>(a.flags_out)[threadIdx.x] = v;
+    f[threadIdx.x] = 0u;
+  }
+  if (threadIdx.x == 0) a.cc->blocks_done = 0u;
 }
 
 // ------------------------------------------------------------------ max cos
@@ -853,14 +918,19 @@ lam_status dedup_ingest(lam_ctx* ctx, lam_store* st, const float* x, int64_t n, 
       const int ntB = (nB + kTB - 1) / kTB;
       const float* xc = x + c0 * D;
       const _Float16* x16 = x16c + c0 * D;
-      // chunk 0 also clears the status words and sets the store size
-      hipLaunchKernelGGL(k_chunk_init, dim3(64), dim3(256), 0, ctx->stream, nB, W, firstHit, hasEdge, maxcos,
-                         bitmap, cc, ctx->flags_dev, meta, c0 == 0 ? (int32_t)m_before : -1);
-      LAM_HIP(hipGetLastError());
+      const bool last_chunk = c0 + CH >= n;
+      const ChunkState cs{firstHit, hasEdge, maxcos, bitmap, W, nB, cc, meta, (int32_t)m_before};
       if (c0 == 0) {
+        // the status words must be zero before prep counts into them; the
+        // last append of every completed call leaves them zero
+        if (!ctx->flags_zero) LAM_TRY(clear_flags(ctx));
+        ctx->flags_zero = false;
         ProfScope ps(ctx, "dedup_prep");
         hipLaunchKernelGGL(k_prep, dim3((unsigned)((n + 3) / 4)), dim3(256), 0, ctx->stream, x, n, D, x16c, hnc,
-                           etc, K.K1, K.K2, K.K3h, ctx->flags_dev);
+                           etc, K.K1, K.K2, K.K3h, ctx->flags_dev, cs);
+        LAM_HIP(hipGetLastError());
+      } else {
+        hipLaunchKernelGGL(k_chunk_init, dim3(64), dim3(256), 0, ctx->stream, cs);
         LAM_HIP(hipGetLastError());
       }
 
@@ -889,10 +959,8 @@ lam_status dedup_ingest(lam_ctx* ctx, lam_store* st, const float* x, int64_t n, 
       // against the store (rows retained before this chunk; the kernel reads
       // the exact count, the grid covers an upper bound) and inside the chunk
       const int64_t m_ub = m_before + c0;
-      // 256 x 256 tiles once they give every CU at least one workgroup
-      const int64_t big_tiles = ((m_ub + 255) / 256) * ((nB + 255) / 256);
-      const bool large = screen_tile_pref() == 256;   // 256 x 256 only on request (slower on MI355X)
-      (void)big_tiles;
+      // 128 x 128 tiles; 256 x 256 (one workgroup per CU) only on request
+      const bool large = screen_tile_pref() == 256;
       const int tb_rows = large ? ScreenLarge::BN : ScreenSmall::BN;
       const int ntBt = (nB + tb_rows - 1) / tb_rows;
       sa.ntB = ntBt;
@@ -935,21 +1003,23 @@ lam_status dedup_ingest(lam_ctx* ctx, lam_store* st, const float* x, int64_t n, 
         hipLaunchKernelGGL(k_resolve, dim3(1), dim3(kResolveThreads), 0, ctx->stream, ra);
         LAM_HIP(hipGetLastError());
       }
+      if (want_max) {
+        hipLaunchKernelGGL(k_maxcos, dim3((unsigned)((nB + 3) / 4)), dim3(256), 0, ctx->stream, nB, maxcos, G,
+                           kept_words, max_cos + c0, ctx->flags_dev);
+        LAM_HIP(hipGetLastError());
+      }
       AppendArgs aa{xc, x16, hnc + c0, etc + c0, pos, rep_row, st->n_seen + c0, D, st->x32, st->x16, st->hn,
-                    st->et, st->ids, ctx->flags_dev};
+                    st->et, st->ids, ctx->flags_dev, cc, last_chunk ? ctx->flags_host_dev : nullptr};
       {
         ProfScope ps(ctx, "dedup_append");
         hipLaunchKernelGGL(k_append, dim3((unsigned)((nB + kAppendRows - 1) / kAppendRows)), dim3(256), 0,
                            ctx->stream, aa, nB);
         LAM_HIP(hipGetLastError());
       }
-      if (want_max) {
-        hipLaunchKernelGGL(k_maxcos, dim3((unsigned)((nB + 3) / 4)), dim3(256), 0, ctx->stream, nB, maxcos, G,
-                           kept_words, max_cos + c0, ctx->flags_dev);
-        LAM_HIP(hipGetLastError());
-      }
     }
-    LAM_TRY(read_flags(ctx));
+    // the last append wrote the status words to host memory and zeroed them
+    LAM_HIP(hipStreamSynchronize(ctx->stream));
+    ctx->flags_zero = true;
     const DevFlags f = *ctx->flags_host;
     LAM_CHECK(f.nonfinite == 0, LAM_EINVAL, "input holds NaN or Inf (%u rows)", f.nonfinite);
     LAM_CHECK(f.out_of_range == 0, LAM_EINVAL, "input has coordinates with |x| >= 256 (%u rows)", f.out_of_range);

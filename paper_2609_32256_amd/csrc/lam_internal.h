@@ -80,12 +80,15 @@ struct lam_ctx {
   int device = 0;
   hipStream_t stream = nullptr;
   lam::DevFlags* flags_dev = nullptr;   // device status words
-  lam::DevFlags* flags_host = nullptr;  // pinned mirror
+  lam::DevFlags* flags_host = nullptr;  // pinned, coherent mirror
+  lam::DevFlags* flags_host_dev = nullptr;  // its device-side address (kernels write it directly)
+  bool flags_zero = false;              // flags_dev known to hold zeros
   // scratch arena, grown on demand
   lam::DevBuf scratch[12];
   // profiling
   uint32_t pair_cap = 1u << 20;         // ambiguous-pair list capacity (grows on overflow)
   bool profiling = false;
+  std::string prof_only;                // empty: every kernel
   std::vector<lam::ProfRec> prof;
   std::vector<hipEvent_t> event_pool;
 };

@@ -4,6 +4,7 @@ delta_hat within 1e-12, max-cos within the screen bound; invariance to how the
 stream is split into calls; exact ties; error paths."""
 import numpy as np
 import pytest
+import torch
 
 import synth
 from oracle import dedup, invariants
@@ -89,18 +90,52 @@ def test_inclusive_threshold_pair(lam):
     assert stats[-1]["delta_hat_call"] == 0.5
 
 
+_SUBSET_REF = {}
+
+
+def _subset_ref(tau):
+    if tau not in _SUBSET_REF:
+        x = synth.subset_ingest()["x"]
+        _SUBSET_REF[tau] = (x, dedup.greedy(x, tau, block=512))
+    return _SUBSET_REF[tau]
+
+
 @pytest.mark.parametrize("tau", [0.95, 0.99])
 def test_subset_parity(lam, tau):
     """27,986 clustered rows in batches of 1,024 (the benchmark's launch
     configuration), exhaustive parity with the oracle."""
-    cfg = synth.subset_ingest()
-    x = cfg["x"]
-    ref = dedup.greedy(x, tau, block=512)
+    x, ref = _subset_ref(tau)
     _, rep, stats, _ = _ingest(lam, x, tau, 1024)
     assert np.array_equal(rep, ref["rep"])
     assert abs(stats[-1]["delta_hat_run"] - ref["delta_hat"]) <= 1e-12
     amb = sum(st["n_ambiguous_pairs"] for st in stats)
     print(f"tau={tau}: kept {np.count_nonzero(rep < 0)} of {rep.size}, ambiguous pairs {amb}")
+
+
+def test_subset_multi_chunk_calls(lam):
+    """Calls of 10,000 rows: each is split into chunks of 4,096, 4,096 and
+    1,808 rows inside the library (the last call is ragged)."""
+    x, ref = _subset_ref(0.95)
+    _, rep, stats, _ = _ingest(lam, x, 0.95, 10000)
+    assert np.array_equal(rep, ref["rep"])
+    assert abs(stats[-1]["delta_hat_run"] - ref["delta_hat"]) <= 1e-12
+
+
+def test_ingest_after_failed_quantize(lam):
+    """A quantize call that fails on the device in between two ingests leaves
+    the second ingest's decisions unchanged."""
+    x, ref = _subset_ref(0.95)
+    s = lam.Store(x.shape[1], 0.95, x.shape[0])
+    xd = _dev(x)
+    r1, _ = s.ingest(xd[:5000])
+    bad = torch.zeros(4096, dtype=torch.float32, device="cuda")
+    bad[17] = float("nan")
+    with pytest.raises(lam.LamError):
+        lam.quantize(bad, 1e-3, absmax=1.0)
+    r2, _ = s.ingest(xd[5000:12000])
+    rep = torch.cat([r1, r2]).cpu().numpy()
+    ref12 = dedup.greedy(x[:12000], 0.95, block=512)
+    assert np.array_equal(rep, ref12["rep"])
 
 
 def test_gpu_output_invariants(lam):
