@@ -180,6 +180,7 @@ struct ScreenArgs {
   const float* hnS;         // ||y||^2 / 2 of store rows
   const float* etS;         // error term of store rows
   const StoreMeta* meta;    // store size
+  int m_exact;              // store size when the host knows it, else -1 (read meta)
   const _Float16* B;        // chunk rows (arrivals)
   const float* hnB;         // ||b||^2 / 2 of chunk rows
   const float* etB;         // error term of chunk rows
@@ -218,30 +219,34 @@ __device__ __forceinline__ void push_pair(const ScreenArgs& a, int i, int kind, 
 // A side of the error bound is the largest per-row term among the tile's own
 // A rows.
 template <class C, bool WANT_MAX>
-__global__ __launch_bounds__(C::kThreads) void k_screen(ScreenArgs a) {
+__global__ __launch_bounds__(C::kThreads, C::kMinWaves) void k_screen(ScreenArgs a) {
   static_assert(C::BM == C::BN, "the in-chunk triangle needs square tiles");
+  static_assert(C::BM <= C::kThreads, "one thread per A row for the row terms");
   __shared__ _Float16 lds[C::kLdsHalves];
   __shared__ float hbA[C::BM];
   __shared__ float emx[C::kWaves];
-  if (skip_all(a.flags)) return;
-  const int MODE = (blockIdx.x < a.nb0) ? 0 : 1;
+  // (no early exit on the status words: the screen writes only chunk scratch,
+  // and every kernel that writes caller outputs or the store checks them)
+  const int bid = (int)blockIdx.x;
+  const int nb0 = (int)a.nb0;
+  const int MODE = bid < nb0 ? 0 : 1;
   int ta, tb;
   if (MODE == 0) {
     // Grouped order: within an XCD's contiguous range, consecutive workgroups
     // sweep a group of kGroupA store tiles against each chunk tile in turn, so
     // the tiles in flight on one XCD (kGroupA store tiles plus a few chunk
     // tiles) stay inside its L2 and each store tile leaves HBM once.
-    const int64_t logical = xcd_remap(blockIdx.x, a.nb0);
-    const int64_t ntA = a.nb0 / a.ntB;
-    const int64_t per_group = (int64_t)kGroupA * a.ntB;
-    const int64_t g = logical / per_group, l = logical % per_group;
-    const int64_t ta0 = g * kGroupA;
-    const int64_t gsize = min((int64_t)kGroupA, ntA - ta0);
-    ta = (int)(ta0 + l % gsize);
-    tb = (int)(l / gsize);
+    const int logical = xcd_remap32(bid, nb0);
+    const int ntA = nb0 / a.ntB;
+    const int per_group = kGroupA * a.ntB;
+    const int g = logical / per_group, l = logical - g * per_group;
+    const int ta0 = g * kGroupA;
+    const int gsize = min(kGroupA, ntA - ta0);
+    ta = ta0 + l % gsize;
+    tb = l / gsize;
   } else {
     // lower-triangular tile pairs ta <= tb, row-major over tb
-    const int64_t logical = xcd_remap(blockIdx.x - a.nb0, a.nb1);
+    const int64_t logical = xcd_remap(bid - nb0, a.nb1);
     int t = (int)((sqrt(8.0 * (double)logical + 1.0) - 1.0) * 0.5);
     while ((int64_t)(t + 1) * (t + 2) / 2 <= logical) ++t;
     while ((int64_t)t * (t + 1) / 2 > logical) --t;
@@ -251,27 +256,50 @@ __global__ __launch_bounds__(C::kThreads) void k_screen(ScreenArgs a) {
   const _Float16* A = MODE == 0 ? a.As : a.B;
   const float* hnA = MODE == 0 ? a.hnS : a.hnB;
   const float* etA = MODE == 0 ? a.etS : a.etB;
-  const int nA = (MODE == 0) ? a.meta->m : a.nB;
+  const int nA = (MODE == 0) ? (a.m_exact >= 0 ? a.m_exact : a.meta->m) : a.nB;
   const int rowsA = min(C::BM, nA - ta * C::BM);
   const int rowsB = min(C::BN, a.nB - tb * C::BN);
   if (rowsA <= 0 || rowsB <= 0) return;
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
-  {
-    // A-side row terms; the error bound uses the largest term among the tile's rows
-    float e = 0.0f;
-    for (int r = threadIdx.x; r < C::BM; r += C::kThreads) {
-      const bool v = r < rowsA;
-      hbA[r] = v ? hnA[ta * C::BM + r] : 0.0f;
-      e = fmaxf(e, v ? etA[ta * C::BM + r] : 0.0f);
-    }
-    for (int o = 32; o > 0; o >>= 1) e = fmaxf(e, __shfl_xor(e, o));
-    if (lane == 0) emx[wave] = e;
+  const int wn0 = wave % C::WN;
+
+  // Row terms of both sides: loaded before the GEMM, used after it, so their
+  // latency hides behind the first slabs.
+  const __amdgpu_buffer_rsrc_t rhA = f32_rsrc(hnA + (int64_t)ta * C::BM, rowsA);
+  const __amdgpu_buffer_rsrc_t reA = f32_rsrc(etA + (int64_t)ta * C::BM, rowsA);
+  const __amdgpu_buffer_rsrc_t rhB = f32_rsrc(a.hnB + (int64_t)tb * C::BN, rowsB);
+  const __amdgpu_buffer_rsrc_t reB = f32_rsrc(a.etB + (int64_t)tb * C::BN, rowsB);
+  const bool rowA = (int)threadIdx.x < rowsA;
+  const float hA = buf_f32(rhA, rowA, threadIdx.x);
+  const float eA = buf_f32(reA, rowA, threadIdx.x);
+  float hB[C::TJ], eB[C::TJ];
+#pragma unroll
+  for (int tj = 0; tj < C::TJ; ++tj) {
+    const int ibl = wn0 * C::TJ * 32 + tj * 32 + (lane & 31);
+    hB[tj] = buf_f32(rhB, ibl < rowsB, ibl);
+    eB[tj] = buf_f32(reB, ibl < rowsB, ibl);
   }
 
   floatx16 acc[C::TI][C::TJ];
-  gemm_tile<C>(A + (int64_t)ta * C::BM * a.D, rowsA, a.B + (int64_t)tb * C::BN * a.D, rowsB, a.D, a.D, lds, acc);
+  const _Float16* tA = A + (int64_t)ta * C::BM * a.D;
+  const _Float16* tB = a.B + (int64_t)tb * C::BN * a.D;
+  // the common dims get a fully unrolled reduction
+  if (a.D == 768)
+    gemm_tile<C, 12>(tA, rowsA, tB, rowsB, a.D, a.D, lds, acc);
+  else if (a.D == 1024)
+    gemm_tile<C, 16>(tA, rowsA, tB, rowsB, a.D, a.D, lds, acc);
+  else
+    gemm_tile<C>(tA, rowsA, tB, rowsB, a.D, a.D, lds, acc);
 
+  {
+    // A-side row terms; the error bound uses the largest term among the tile's rows
+    if ((int)threadIdx.x < C::BM) hbA[threadIdx.x] = hA;
+    float e = eA;
+    for (int o = 32; o > 0; o >>= 1) e = fmaxf(e, __shfl_xor(e, o));
+    if (lane == 0) emx[wave] = e;
+  }
+  __syncthreads();
   const int wm = wave / C::WN, wn = wave % C::WN;
   float ebA = emx[0];
 #pragma unroll
@@ -283,8 +311,8 @@ __global__ __launch_bounds__(C::kThreads) void k_screen(ScreenArgs a) {
     const bool vB = ibl < rowsB;
     float thrAmb = 3.0e38f, thrIn = 3.0e38f;
     if (vB) {
-      const double base = (double)a.hnB[ib] - a.half_d2;
-      const double e = (double)a.etB[ib] + (double)ebA;
+      const double base = (double)hB[tj] - a.half_d2;
+      const double e = (double)eB[tj] + (double)ebA;
       thrAmb = round_down_f32(base - e);
       thrIn = round_up_f32(base + e);
     }
@@ -356,8 +384,7 @@ __global__ __launch_bounds__(C::kThreads) void k_screen(ScreenArgs a) {
   }
 }
 
-using ScreenSmall = Tile<2, 2, 2, 2>;   // 128 x 128, four waves of 64 x 64
-using ScreenLarge = Tile<2, 2, 4, 4>;   // 256 x 256, four waves of 128 x 128
+using ScreenTile = Tile<2, 2, 2, 2>;   // 128 x 128, four waves of 64 x 64
 
 // ------------------------------------------------------------------ verify
 struct VerifyArgs {
@@ -803,16 +830,6 @@ struct Consts {
   double K1, K2, K3h;
 };
 
-// Tile choice of the screen: 0 = by grid size (default), 128 or 256 forced by
-// the LAM_SCREEN_TILE environment variable (for tuning).
-int screen_tile_pref() {
-  static const int v = [] {
-    const char* e = std::getenv("LAM_SCREEN_TILE");
-    return e ? std::atoi(e) : 0;
-  }();
-  return (v == 128 || v == 256) ? v : 0;
-}
-
 Consts screen_consts(int D) {
   const double uh = std::ldexp(1.0, -11), u = std::ldexp(1.0, -24), eta = std::ldexp(1.0, -22);
   const double g = 2.0 * D * u / (1.0 - 2.0 * D * u);
@@ -939,6 +956,7 @@ lam_status dedup_ingest(lam_ctx* ctx, lam_store* st, const float* x, int64_t n, 
       sa.hnS = st->hn;
       sa.etS = st->et;
       sa.meta = meta;
+      sa.m_exact = c0 == 0 ? (int)m_before : -1;   // later chunks: read the kernel-maintained count
       sa.B = x16;
       sa.hnB = hnc + c0;
       sa.etB = etc + c0;
@@ -959,9 +977,7 @@ lam_status dedup_ingest(lam_ctx* ctx, lam_store* st, const float* x, int64_t n, 
       // against the store (rows retained before this chunk; the kernel reads
       // the exact count, the grid covers an upper bound) and inside the chunk
       const int64_t m_ub = m_before + c0;
-      // 128 x 128 tiles; 256 x 256 (one workgroup per CU) only on request
-      const bool large = screen_tile_pref() == 256;
-      const int tb_rows = large ? ScreenLarge::BN : ScreenSmall::BN;
+      const int tb_rows = ScreenTile::BN;
       const int ntBt = (nB + tb_rows - 1) / tb_rows;
       sa.ntB = ntBt;
       sa.nb0 = ((m_ub + tb_rows - 1) / tb_rows) * ntBt;
@@ -970,21 +986,12 @@ lam_status dedup_ingest(lam_ctx* ctx, lam_store* st, const float* x, int64_t n, 
       LAM_CHECK(grid < (1LL << 31), LAM_EINVAL, "screen grid too large");
       {
         ProfScope ps(ctx, "dedup_screen");
-        if (large) {
-          if (want_max)
-            hipLaunchKernelGGL((k_screen<ScreenLarge, true>), dim3((unsigned)grid), dim3(ScreenLarge::kThreads), 0,
-                               ctx->stream, sa);
-          else
-            hipLaunchKernelGGL((k_screen<ScreenLarge, false>), dim3((unsigned)grid), dim3(ScreenLarge::kThreads), 0,
-                               ctx->stream, sa);
-        } else {
-          if (want_max)
-            hipLaunchKernelGGL((k_screen<ScreenSmall, true>), dim3((unsigned)grid), dim3(ScreenSmall::kThreads), 0,
-                               ctx->stream, sa);
-          else
-            hipLaunchKernelGGL((k_screen<ScreenSmall, false>), dim3((unsigned)grid), dim3(ScreenSmall::kThreads), 0,
-                               ctx->stream, sa);
-        }
+        if (want_max)
+          hipLaunchKernelGGL((k_screen<ScreenTile, true>), dim3((unsigned)grid), dim3(ScreenTile::kThreads), 0,
+                             ctx->stream, sa);
+        else
+          hipLaunchKernelGGL((k_screen<ScreenTile, false>), dim3((unsigned)grid), dim3(ScreenTile::kThreads), 0,
+                             ctx->stream, sa);
         LAM_HIP(hipGetLastError());
       }
       VerifyArgs va{pairs, status, cc, cap, xc, st->x32, D, st->d2, firstHit, bitmap, W, hasEdge,

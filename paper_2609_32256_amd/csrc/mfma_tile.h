@@ -5,8 +5,8 @@
 // contiguous ("K-major" on both sides).  Waves sit on a 2 x 2 grid; each wave
 // owns 64 x 64 of C as 2 x 2 tiles of v_mfma_f32_32x32x16_f16 (CDNA4), i.e.
 // 64 fp32 accumulators per lane.  Operands are staged through LDS in K-slabs
-// of 64 halves per row, double-buffered, with rows padded by 8 halves so that
-// the 32 rows read by one fragment load fall on distinct LDS banks.
+// of 64 halves per row (two stages), with rows padded by 8 halves so that the
+// 32 rows read by one fragment load fall on distinct LDS banks.
 //
 // Fragment layout of the 32x32x16 instruction (wave64):
 //   A operand: lane l supplies A[i = l % 32][k = 8 * (l / 32) + e], e = 0..7
@@ -35,19 +35,44 @@ struct SlabRegs {
   uint4 v[4];  // 4 x 16 B per thread = one 128 x 64 fp16 slab per workgroup
 };
 
+// Slab loads go through buffer resources: a descriptor bounds the tile's rows
+// in bytes and the hardware returns zeros for an offset past the bound, so a
+// chunk outside the tile costs no branch (an offset select instead).  Keeping
+// every load off divergent branches also lets the compiler count outstanding
+// loads exactly rather than waiting for all of them.
+constexpr uint32_t kOffOOB = 0x80000000u;   // beyond every tile's bound
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_rsrc(const _Float16* base, int rows, int64_t ld) {
+  // gfx9 raw buffer: stride 0, num_records in bytes, 32-bit data format word
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<_Float16*>(base), (short)0, (int)(rows * ld * 2), 0x00020000);
+}
+
+// Per-row float32 terms of a tile through a buffer resource (zeros past
+// `count` rows), for the same reason as the slab loads.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t f32_rsrc(const float* base, int count) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(base), (short)0, count * 4, 0x00020000);
+}
+
+__device__ __forceinline__ float buf_f32(__amdgpu_buffer_rsrc_t rs, bool ok, int idx) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, ok ? (uint32_t)idx * 4u : kOffOOB, 0, 0));
+}
+
+__device__ __forceinline__ uint4 chunk_load(__amdgpu_buffer_rsrc_t rs, bool ok, int64_t off_halves) {
+  const uint32_t off = ok ? (uint32_t)(off_halves * 2) : kOffOOB;
+  return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0));
+}
+
 // Loads rows [0, rows) x halves [k0, k0 + 64) of a row-major fp16 matrix with
 // leading dimension ld (halves); rows past `rows` and columns past `kmax` read
-// as zero.
+// as zero.  rows * ld * 2 must fit in 31 bits.
 __device__ __forceinline__ void slab_load(const _Float16* __restrict__ base, int rows, int64_t ld, int k0,
                                           int kmax, SlabRegs& r) {
+  const __amdgpu_buffer_rsrc_t rs = tile_rsrc(base, rows, ld);
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     const int c = threadIdx.x + kWG * q;
     const int row = c >> 3, col = (c & 7) * 8;
-    uint4 v = make_uint4(0u, 0u, 0u, 0u);
-    if (row < rows && k0 + col < kmax)
-      v = *reinterpret_cast<const uint4*>(base + (int64_t)row * ld + k0 + col);
-    r.v[q] = v;
+    r.v[q] = chunk_load(rs, row < rows && k0 + col < kmax, (int64_t)row * ld + k0 + col);
   }
 }
 
@@ -68,60 +93,8 @@ __device__ __forceinline__ half8 frag_load(const _Float16* __restrict__ s, int r
 // Row of C (within a 32x32 tile) held in accumulator register r of this lane.
 __device__ __forceinline__ int acc_row(int r, int lane) { return 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3); }
 
-// 128x128 block of C = A . B^T over reduction length kdim.  A rows [0, ra),
-// B rows [0, rb) (zero beyond).  lds must hold 2 * 2 * 128 * kLdk halves.
-__device__ __forceinline__ void gemm_block_f16(const _Float16* __restrict__ A, int ra,
-                                               const _Float16* __restrict__ B, int rb, int64_t ld, int kdim,
-                                               _Float16* lds, floatx16 (&acc)[2][2]) {
-  // slab buffers: A at 0 / 1, B at 2 / 3
-  auto buf = [&](int i) -> _Float16* { return lds + i * (kTB * kLdk); };
-  const int wave = threadIdx.x >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
-#pragma unroll
-  for (int a = 0; a < 2; ++a)
-#pragma unroll
-    for (int b = 0; b < 2; ++b)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.0f;
-
-  SlabRegs ra_, rb_;
-  slab_load(A, ra, ld, 0, kdim, ra_);
-  slab_load(B, rb, ld, 0, kdim, rb_);
-  slab_store(buf(0), ra_);
-  slab_store(buf(2), rb_);
-  __syncthreads();
-  int cur = 0;
-  for (int k0 = 0; k0 < kdim; k0 += kBK) {
-    const bool more = k0 + kBK < kdim;
-    if (more) {
-      slab_load(A, ra, ld, k0 + kBK, kdim, ra_);
-      slab_load(B, rb, ld, k0 + kBK, kdim, rb_);
-    }
-#pragma unroll
-    for (int kk = 0; kk < kBK / 16; ++kk) {
-      half8 fa[2], fb[2];
-#pragma unroll
-      for (int t = 0; t < 2; ++t) {
-        fa[t] = frag_load(buf(cur), wm * 64 + t * 32, kk);
-        fb[t] = frag_load(buf(2 + cur), wn * 64 + t * 32, kk);
-      }
-#pragma unroll
-      for (int a = 0; a < 2; ++a)
-#pragma unroll
-        for (int b = 0; b < 2; ++b)
-          acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fa[a], fb[b], acc[a][b], 0, 0, 0);
-    }
-    if (more) {
-      slab_store(buf(cur ^ 1), ra_);
-      slab_store(buf(2 + (cur ^ 1)), rb_);
-    }
-    __syncthreads();
-    cur ^= 1;
-  }
-}
-
 // ---------------------------------------------------------------------------
-// Generalised block: WM x WN waves, each owning TI x TJ tiles of 32 x 32, so a
+// Block shape: WM x WN waves, each owning TI x TJ tiles of 32 x 32, so a
 // workgroup computes (WM*TI*32) x (WN*TJ*32) of C = A . B^T.  Larger per-wave
 // tiles read fewer LDS bytes per MFMA: (TI + TJ) / (TI * TJ) KB.
 template <int WM_, int WN_, int TI_, int TJ_>
@@ -135,20 +108,20 @@ struct Tile {
   static constexpr int kChunksB = BN * (kBK / 8);
   static constexpr int kPerA = kChunksA / kThreads;
   static constexpr int kPerB = kChunksB / kThreads;
-  static constexpr int kLdsHalves = 2 * (BM + BN) * kLdk;   // double-buffered slabs
+  static constexpr int kLdsHalves = 2 * (BM + BN) * kLdk;   // two K-slab stages of A and B
+  // waves per SIMD the register budget is held to (256 registers per lane)
+  static constexpr int kMinWaves = 2;
   static_assert(kChunksA % kThreads == 0 && kChunksB % kThreads == 0, "slab must split evenly");
 };
 
 template <int N>
-__device__ __forceinline__ void slab_load_n(const _Float16* __restrict__ base, int rows, int64_t ld, int k0, int kmax,
+__device__ __forceinline__ void slab_load_n(__amdgpu_buffer_rsrc_t rs, int rows, int64_t ld, int k0, int kmax,
                                             uint4 (&r)[N], int nthreads) {
 #pragma unroll
   for (int q = 0; q < N; ++q) {
     const int c = threadIdx.x + nthreads * q;
     const int row = c >> 3, col = (c & 7) * 8;
-    uint4 v = make_uint4(0u, 0u, 0u, 0u);
-    if (row < rows && k0 + col < kmax) v = *reinterpret_cast<const uint4*>(base + (int64_t)row * ld + k0 + col);
-    r[q] = v;
+    r[q] = chunk_load(rs, row < rows && k0 + col < kmax, (int64_t)row * ld + k0 + col);
   }
 }
 
@@ -162,17 +135,26 @@ __device__ __forceinline__ void slab_store_n(_Float16* __restrict__ s, const uin
   }
 }
 
-// C tile of one workgroup; lds holds C::kLdsHalves halves.  acc[ti][tj] holds
-// rows wm*TI*32 + ti*32 + acc_row(r, lane) of A and column wn*TJ*32 + tj*32 +
-// lane%32 of B, with wm = wave / WN, wn = wave % WN.
-template <class C>
+// C tile of one workgroup; lds holds C::kLdsHalves halves (two K-slab stages
+// of A and B).  acc[ti][tj] holds rows wm*TI*32 + ti*32 + acc_row(r, lane) of A
+// and column wn*TJ*32 + tj*32 + lane%32 of B, with wm = wave / WN, wn = wave %
+// WN.
+//
+// Pipeline: global loads run two slabs ahead of the MFMAs in two register
+// sets; slab s is multiplied from LDS stage s % 2 while slab s + 1 is written
+// to the other stage, so one barrier per slab suffices and the LDS writes
+// overlap the MFMAs.  Loads past the last slab are issued too (they fall
+// outside the buffer bound, read zeros and touch no memory), so that no load
+// sits behind a branch.  With NS > 0 the reduction has exactly NS slabs and the
+// loop is unrolled, which lets the compiler wait for exactly the loads each
+// LDS store needs (across a loop back edge it waits for all of them); NS = 0
+// takes kdim at run time.
+template <class C, int NS = 0>
 __device__ __forceinline__ void gemm_tile(const _Float16* __restrict__ A, int ra, const _Float16* __restrict__ B,
                                           int rb, int64_t ld, int kdim, _Float16* lds,
                                           floatx16 (&acc)[C::TI][C::TJ]) {
-  _Float16* sa0 = lds;
-  _Float16* sb0 = lds + 2 * C::BM * kLdk;
-  auto sa = [&](int i) -> _Float16* { return sa0 + i * (C::BM * kLdk); };
-  auto sb = [&](int i) -> _Float16* { return sb0 + i * (C::BN * kLdk); };
+  auto sa = [&](int i) -> _Float16* { return lds + i * ((C::BM + C::BN) * kLdk); };
+  auto sb = [&](int i) -> _Float16* { return lds + i * ((C::BM + C::BN) * kLdk) + C::BM * kLdk; };
   const int wave = threadIdx.x >> 6;
   const int wm = wave / C::WN, wn = wave % C::WN;
 #pragma unroll
@@ -181,38 +163,50 @@ __device__ __forceinline__ void gemm_tile(const _Float16* __restrict__ A, int ra
     for (int b = 0; b < C::TJ; ++b)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.0f;
-  uint4 ra_[C::kPerA], rb_[C::kPerB];
-  slab_load_n<C::kPerA>(A, ra, ld, 0, kdim, ra_, C::kThreads);
-  slab_load_n<C::kPerB>(B, rb, ld, 0, kdim, rb_, C::kThreads);
-  slab_store_n<C::kPerA>(sa(0), ra_, C::kThreads);
-  slab_store_n<C::kPerB>(sb(0), rb_, C::kThreads);
-  __syncthreads();
-  int cur = 0;
-  for (int k0 = 0; k0 < kdim; k0 += kBK) {
-    const bool more = k0 + kBK < kdim;
-    if (more) {
-      slab_load_n<C::kPerA>(A, ra, ld, k0 + kBK, kdim, ra_, C::kThreads);
-      slab_load_n<C::kPerB>(B, rb, ld, k0 + kBK, kdim, rb_, C::kThreads);
-    }
+  auto compute = [&](int st) {
 #pragma unroll
     for (int kk = 0; kk < kBK / 16; ++kk) {
       half8 fa[C::TI], fb[C::TJ];
 #pragma unroll
-      for (int t = 0; t < C::TI; ++t) fa[t] = frag_load(sa(cur), wm * C::TI * 32 + t * 32, kk);
+      for (int t = 0; t < C::TI; ++t) fa[t] = frag_load(sa(st), wm * C::TI * 32 + t * 32, kk);
 #pragma unroll
-      for (int t = 0; t < C::TJ; ++t) fb[t] = frag_load(sb(cur), wn * C::TJ * 32 + t * 32, kk);
+      for (int t = 0; t < C::TJ; ++t) fb[t] = frag_load(sb(st), wn * C::TJ * 32 + t * 32, kk);
 #pragma unroll
       for (int a = 0; a < C::TI; ++a)
 #pragma unroll
         for (int b = 0; b < C::TJ; ++b)
           acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fa[a], fb[b], acc[a][b], 0, 0, 0);
     }
-    if (more) {
-      slab_store_n<C::kPerA>(sa(cur ^ 1), ra_, C::kThreads);
-      slab_store_n<C::kPerB>(sb(cur ^ 1), rb_, C::kThreads);
-    }
+  };
+  const int S = NS > 0 ? NS : (kdim + kBK - 1) / kBK;
+  const __amdgpu_buffer_rsrc_t rsA = tile_rsrc(A, ra, ld), rsB = tile_rsrc(B, rb, ld);
+  uint4 a0[C::kPerA], b0[C::kPerB], a1[C::kPerA], b1[C::kPerB];
+  slab_load_n<C::kPerA>(rsA, ra, ld, 0, kdim, a0, C::kThreads);
+  slab_load_n<C::kPerB>(rsB, rb, ld, 0, kdim, b0, C::kThreads);
+  slab_load_n<C::kPerA>(rsA, ra, ld, kBK, kdim, a1, C::kThreads);
+  slab_load_n<C::kPerB>(rsB, rb, ld, kBK, kdim, b1, C::kThreads);
+  slab_store_n<C::kPerA>(sa(0), a0, C::kThreads);
+  slab_store_n<C::kPerB>(sb(0), b0, C::kThreads);
+  slab_load_n<C::kPerA>(rsA, ra, ld, 2 * kBK, kdim, a0, C::kThreads);
+  slab_load_n<C::kPerB>(rsB, rb, ld, 2 * kBK, kdim, b0, C::kThreads);
+  __syncthreads();
+#pragma unroll
+  for (int s = 0; s < (NS > 0 ? NS : S); s += 2) {
+    // even slab s from stage 0; slab s + 1 (a1/b1) goes to stage 1
+    compute(0);
+    slab_store_n<C::kPerA>(sa(1), a1, C::kThreads);
+    slab_store_n<C::kPerB>(sb(1), b1, C::kThreads);
+    slab_load_n<C::kPerA>(rsA, ra, ld, (s + 3) * kBK, kdim, a1, C::kThreads);
+    slab_load_n<C::kPerB>(rsB, rb, ld, (s + 3) * kBK, kdim, b1, C::kThreads);
     __syncthreads();
-    cur ^= 1;
+    if (s + 1 >= S) break;
+    // odd slab s + 1 from stage 1; slab s + 2 (a0/b0) goes to stage 0
+    compute(1);
+    slab_store_n<C::kPerA>(sa(0), a0, C::kThreads);
+    slab_store_n<C::kPerB>(sb(0), b0, C::kThreads);
+    slab_load_n<C::kPerA>(rsA, ra, ld, (s + 4) * kBK, kdim, a0, C::kThreads);
+    slab_load_n<C::kPerB>(rsB, rb, ld, (s + 4) * kBK, kdim, b0, C::kThreads);
+    __syncthreads();
   }
 }
 
@@ -225,6 +219,12 @@ __host__ __device__ inline int64_t xcd_remap(int64_t bid, int64_t nblocks) {
   const int64_t q = nblocks / 8, rem = nblocks % 8;
   const int64_t x = bid % 8;
   return x * q + (x < rem ? x : rem) + bid / 8;
+}
+
+__device__ __forceinline__ int xcd_remap32(int bid, int nblocks) {
+  const int q = nblocks >> 3, rem = nblocks & 7;
+  const int x = bid & 7;
+  return x * q + (x < rem ? x : rem) + (bid >> 3);
 }
 
 // Order-preserving map of float to uint32 for atomicMax.
