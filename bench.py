@@ -8,7 +8,7 @@ the paper's workloads:
      input sets rotate so that no pass reads from the 256 MB last-level cache;
   2. the greedy near-duplicate test over the 27,986-row subset stream (600
      trajectories of ~47 chunks, D = 768) in batches of 1,024, tau = 0.95,
-     into a cleared store;
+     into a cleared store (calls that do not wait for the device);
   3. Q_eps of the retained store at eps = 1e-3 (absmax measured on the GPU),
      and its decode;
   4. top-10 scoring of 1,024 queries against the quantized store.
@@ -147,7 +147,7 @@ def main():
         lam.dequantize(raw_codes[k], p, out=raw_out[k], ctx=ctx)
         store.clear()
         for bi, b0 in enumerate(range(0, n, BATCH)):
-            store.ingest(xd[b0:b0 + BATCH], rep=reps[bi])
+            store.ingest(xd[b0:b0 + BATCH], rep=reps[bi], sync=False)   # store.quantize waits for them
         store.quantize(EPS)
         store.dequantize(out=xhat)
         store.score_topk(qd, TOPK, out=topk_out)

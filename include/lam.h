@@ -142,10 +142,13 @@ typedef struct lam_store_info {
   lam_qparams q;         /* valid when quantized                                */
 } lam_store_info;
 
+/* Synchronous: waits for ingest calls that did not wait (see lam_dedup_ingest)
+ * and returns EINVAL, once, if any of them met invalid input. */
 lam_status lam_store_get_info(const lam_store* store, lam_store_info* out);
 
 /* Empty the store (size, n_seen, delta_hat and codes reset; memory kept), as
- * if newly created.  Asynchronous. */
+ * if newly created.  Asynchronous; drops the pending error report of earlier
+ * calls that did not wait. */
 lam_status lam_store_clear(lam_ctx* ctx, lam_store* store);
 
 typedef struct lam_ingest_stats {
@@ -156,8 +159,8 @@ typedef struct lam_ingest_stats {
   int64_t n_ambiguous_pairs;    /* pairs whose screened distance lay within the
                                    screen's error bound of delta^2 and were
                                    decided by the exact binary64 test           */
-  int64_t n_exact_escalations;  /* pairs within 1e-12 of delta^2 in binary64,
-                                   decided on exact integers on the host        */
+  int64_t n_exact_escalations;  /* pairs within binary64 rounding distance of
+                                   delta^2, decided on exact integers (device)  */
   double delta_hat_call;        /* max ||x_i - x_rep|| over this call's merges  */
   double delta_hat_run;         /* same over the store's lifetime               */
 } lam_ingest_stats;
@@ -169,10 +172,23 @@ typedef struct lam_ingest_stats {
  * or -1, and i is appended to the store with global id n_seen + i.
  * max_cos_dev (optional, NULL to skip): max over rows retained at i's arrival
  * of the dot product x_i . y in the screen's precision (|error| <= 1.1e-3 for
- * unit rows), -inf if none.  stats (optional) is filled synchronously; rep and
- * max_cos are written asynchronously unless stats is requested.
+ * unit rows), -inf if none.
+ *
+ * With stats (host struct) the call waits for the device and fills it; errors
+ * are returned by the call itself.  With stats == NULL the call returns as soon
+ * as its kernels are queued on the context's stream (rep and max_cos are
+ * written in stream order) whenever the library can guarantee that no host
+ * step is needed: the ambiguous-pair list can hold every pair the call's
+ * chunks could produce (n (size + n) entries, at most 2^26) and the store has
+ * room even if every earlier row was kept.  Otherwise it waits as above.  An
+ * asynchronous call whose input turns out invalid leaves the store unchanged,
+ * writes no outputs, and is reported (EINVAL, once for all such calls) by the
+ * next call on the store that waits: lam_store_get_info, lam_store_quantize,
+ * lam_store_dequantize, lam_store_export, lam_score_topk or an ingest with
+ * stats; later calls are decided as if it had not happened.
  * EINVAL: n < 0, NaN/Inf or |x| >= 256 in a coordinate (store unchanged).
- * ECAPACITY: size + n > capacity (checked before any work). */
+ * ECAPACITY: size + n > capacity (checked before any work; a call that does
+ * not wait checks an upper bound of the size and waits if that bound is over). */
 lam_status lam_dedup_ingest(lam_ctx* ctx, lam_store* store, const float* x_dev, int64_t n,
                             int64_t* rep_dev, float* max_cos_dev, lam_ingest_stats* stats);
 

@@ -243,9 +243,12 @@ class Store:
     def size(self) -> int:
         return self.info().size
 
-    def ingest(self, x: torch.Tensor, max_cos: bool = False, rep: torch.Tensor | None = None):
+    def ingest(self, x: torch.Tensor, max_cos: bool = False, rep: torch.Tensor | None = None, sync: bool = True):
         """Algorithm "admit" over the rows of x (n x dim float32).  Returns
-        (rep int64[n], stats dict[, max_cos float32[n]])."""
+        (rep int64[n], stats dict[, max_cos float32[n]]).  With sync=False the
+        call may return before the device has finished (stats is then None);
+        invalid input of such a call is raised by the next call that waits
+        (size, info, quantize, scoring or a synchronous ingest)."""
         x = _dev_tensor(x, torch.float32, "x")
         if x.dim() != 2 or x.shape[1] != self.dim:
             raise ValueError(f"x must be (n, {self.dim})")
@@ -253,10 +256,11 @@ class Store:
         if rep is None:
             rep = torch.empty(n, dtype=torch.int64, device=x.device)
         mc = torch.empty(n, dtype=torch.float32, device=x.device) if max_cos else None
-        st = IngestStats()
+        st = IngestStats() if sync else None
         _check(_lib.lam_dedup_ingest(self.ctx.handle, self._h, _ptr(x), n, _ptr(rep), _ptr(mc),
-                                     ctypes.byref(st)))
-        return (rep, st.as_dict(), mc) if max_cos else (rep, st.as_dict())
+                                     ctypes.byref(st) if st is not None else None))
+        stats = st.as_dict() if st is not None else None
+        return (rep, stats, mc) if max_cos else (rep, stats)
 
     def quantize(self, eps: float, absmax: float | None = None, mode: str = "bits") -> QParams:
         p = QParams()

@@ -316,6 +316,10 @@ void lam_store_destroy(lam_store* st) {
 
 lam_status lam_store_get_info(const lam_store* st, lam_store_info* out) {
   LAM_CHECK(st != nullptr && out != nullptr, LAM_EINVAL, "store or out is NULL");
+  {
+    DeviceGuard g(st->ctx->device);
+    LAM_TRY(store_settle(const_cast<lam_store*>(st)));
+  }
   lam_store_info i{};
   i.size = st->size;
   i.capacity = st->capacity;
@@ -336,9 +340,8 @@ lam_status lam_dedup_ingest(lam_ctx* ctx, lam_store* st, const float* x_dev, int
   LAM_CHECK(n >= 0, LAM_EINVAL, "n must be >= 0");
   LAM_CHECK((x_dev != nullptr && rep_dev != nullptr) || n == 0, LAM_EINVAL, "x or rep is NULL");
   LAM_CHECK(((uintptr_t)x_dev & 15u) == 0, LAM_EINVAL, "x must be 16-byte aligned");
-  LAM_CHECK(n <= st->capacity - st->size, LAM_ECAPACITY,
-            "store holds %lld of %lld rows; a batch of %lld may not fit", (long long)st->size,
-            (long long)st->capacity, (long long)n);
+  LAM_CHECK(n <= st->capacity, LAM_ECAPACITY, "a batch of %lld rows exceeds the store's capacity %lld",
+            (long long)n, (long long)st->capacity);
   DeviceGuard g(ctx->device);
   return dedup_ingest(ctx, st, x_dev, n, rep_dev, max_cos_dev, stats);
 }
@@ -347,6 +350,7 @@ lam_status lam_store_quantize(lam_ctx* ctx, lam_store* st, double eps, float abs
                               lam_qparams* out) {
   LAM_CHECK(ctx != nullptr && st != nullptr, LAM_EINVAL, "ctx or store is NULL");
   DeviceGuard g(ctx->device);
+  LAM_TRY(store_settle(st));
   const int64_t n = st->size * (int64_t)st->dim;
   DevBuf holder{st->codes, st->codes_cap};
   lam_qparams p{};
@@ -369,6 +373,8 @@ lam_status lam_store_clear(lam_ctx* ctx, lam_store* st) {
   hipLaunchKernelGGL(k_zero_words, dim3(1), dim3(64), 0, ctx->stream, reinterpret_cast<uint32_t*>(st->stat_dev),
                      (int)(store_meta_bytes() / 4));
   LAM_HIP(hipGetLastError());
+  st->pending = false;   // errors of earlier calls that did not wait are dropped with the contents
+  st->size_ub = 0;
   st->size = 0;
   st->n_seen = 0;
   st->delta_hat_run = 0.0;
@@ -379,6 +385,10 @@ lam_status lam_store_clear(lam_ctx* ctx, lam_store* st) {
 
 lam_status lam_store_dequantize(lam_ctx* ctx, const lam_store* st, float* xhat_dev) {
   LAM_CHECK(ctx != nullptr && st != nullptr, LAM_EINVAL, "ctx or store is NULL");
+  {
+    DeviceGuard g(ctx->device);
+    LAM_TRY(store_settle(const_cast<lam_store*>(st)));
+  }
   LAM_CHECK(st->codes != nullptr && st->coded_rows == st->size, LAM_ESTATE, "store is not quantized");
   LAM_CHECK(xhat_dev != nullptr || st->size == 0, LAM_EINVAL, "xhat is NULL");
   LAM_CHECK(((uintptr_t)xhat_dev & 3u) == 0, LAM_EINVAL, "xhat must be 4-byte aligned");
@@ -390,6 +400,7 @@ lam_status lam_store_export(lam_ctx* ctx, const lam_store* st, int64_t* ids_dev,
                             uint64_t codes_cap_bytes) {
   LAM_CHECK(ctx != nullptr && st != nullptr, LAM_EINVAL, "ctx or store is NULL");
   DeviceGuard g(ctx->device);
+  LAM_TRY(store_settle(const_cast<lam_store*>(st)));
   if (ids_dev && st->size > 0)
     LAM_HIP(hipMemcpyAsync(ids_dev, st->ids, (size_t)st->size * 8, hipMemcpyDeviceToDevice, ctx->stream));
   if (codes_dev) {
@@ -409,6 +420,10 @@ lam_status lam_score_topk(lam_ctx* ctx, const lam_store* st, const float* q_dev,
   LAM_CHECK((q_dev != nullptr && scores_dev != nullptr && ids_dev != nullptr) || nq == 0, LAM_EINVAL,
             "NULL buffer");
   LAM_CHECK(((uintptr_t)q_dev & 15u) == 0, LAM_EINVAL, "q must be 16-byte aligned");
+  {
+    DeviceGuard g(ctx->device);
+    LAM_TRY(store_settle(const_cast<lam_store*>(st)));
+  }
   LAM_CHECK(st->codes != nullptr && st->coded_rows == st->size, LAM_ESTATE,
             "store must be quantized (lam_store_quantize) after its last ingest");
   DeviceGuard g(ctx->device);

@@ -40,6 +40,7 @@
 #include <cstring>
 #include <vector>
 
+#include "exact.h"
 #include "lam_internal.h"
 #include "mfma_tile.h"
 
@@ -55,9 +56,16 @@ constexpr float kInvScale2 = 1.0f / 65536.0f;
 
 enum Scratch { S_X16 = 0, S_ROWF, S_CHUNK, S_BITMAP, S_PAIRS, S_STATUS, S_G };
 
+// Device bookkeeping of a store.  Kernels keep it current, so calls that do
+// not wait for the device need no host round trip: the host reads it when a
+// call needs exact values (lam_store_get_info, capacity near full, ...).
 struct StoreMeta {
-  int32_t m;              // retained rows
-  uint32_t pad[3];
+  int32_t m;                       // retained rows
+  uint32_t err_calls;              // calls since the host last looked that had invalid input
+  int64_t n_seen;                  // arrivals taken so far (global id of the next arrival)
+  unsigned long long dhat2_bits;   // max merged squared distance of the run (binary64 bits)
+  uint32_t err_bits;               // bit 0: non-finite input, bit 1: a coordinate with |x| >= 256
+  uint32_t pad;
 };
 
 // Chunk-level counters (in the S_CHUNK scratch, after the per-row arrays).
@@ -101,7 +109,7 @@ struct ChunkState {
   int nB;                  // rows of the first chunk
   ChunkCounters* cc;
   StoreMeta* meta;
-  int32_t m_first;         // store size at the start of the call
+  int32_t m_first;         // store size at the start of the call, or -1 to leave it
 };
 
 __device__ __forceinline__ void init_chunk_row(const ChunkState& c, int64_t r, int lane) {
@@ -123,7 +131,7 @@ __global__ __launch_bounds__(256) void k_prep(const float* __restrict__ x, int64
     cs.cc->npairs = 0u;
     cs.cc->n_escalate = 0u;
     cs.cc->blocks_done = 0u;
-    cs.meta->m = cs.m_first;
+    if (cs.m_first >= 0) cs.meta->m = cs.m_first;   // a retried call starts from the store as it was
   }
   if (row < cs.nB) init_chunk_row(cs, row, lane);
   if (row >= n) return;
@@ -181,6 +189,7 @@ struct ScreenArgs {
   const float* etS;         // error term of store rows
   const StoreMeta* meta;    // store size
   int m_exact;              // store size when the host knows it, else -1 (read meta)
+  int capA;                 // store capacity (rows that may be read before the size is known)
   const _Float16* B;        // chunk rows (arrivals)
   const float* hnB;         // ||b||^2 / 2 of chunk rows
   const float* etB;         // error term of chunk rows
@@ -256,23 +265,28 @@ __global__ __launch_bounds__(C::kThreads, C::kMinWaves) void k_screen(ScreenArgs
   const _Float16* A = MODE == 0 ? a.As : a.B;
   const float* hnA = MODE == 0 ? a.hnS : a.hnB;
   const float* etA = MODE == 0 ? a.etS : a.etB;
-  const int nA = (MODE == 0) ? (a.m_exact >= 0 ? a.m_exact : a.meta->m) : a.nB;
-  const int rowsA = min(C::BM, nA - ta * C::BM);
   const int rowsB = min(C::BN, a.nB - tb * C::BN);
-  if (rowsA <= 0 || rowsB <= 0) return;
+  // When the host does not know the store size, loads start against the
+  // capacity bound and the size is read while they are in flight; tiles past
+  // it stop before the main loop.  Rows between size and capacity only reach
+  // accumulators the epilogue masks out.
+  const bool known = MODE == 1 || a.m_exact >= 0;
+  const int nA0 = MODE == 1 ? a.nB : (known ? a.m_exact : a.capA);
+  const int rowsLim = min(C::BM, nA0 - ta * C::BM);
+  if (rowsLim <= 0 || rowsB <= 0) return;
+  int rowsA = rowsLim;
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int wn0 = wave % C::WN;
 
   // Row terms of both sides: loaded before the GEMM, used after it, so their
   // latency hides behind the first slabs.
-  const __amdgpu_buffer_rsrc_t rhA = f32_rsrc(hnA + (int64_t)ta * C::BM, rowsA);
-  const __amdgpu_buffer_rsrc_t reA = f32_rsrc(etA + (int64_t)ta * C::BM, rowsA);
+  const __amdgpu_buffer_rsrc_t rhA = f32_rsrc(hnA + (int64_t)ta * C::BM, rowsLim);
+  const __amdgpu_buffer_rsrc_t reA = f32_rsrc(etA + (int64_t)ta * C::BM, rowsLim);
   const __amdgpu_buffer_rsrc_t rhB = f32_rsrc(a.hnB + (int64_t)tb * C::BN, rowsB);
   const __amdgpu_buffer_rsrc_t reB = f32_rsrc(a.etB + (int64_t)tb * C::BN, rowsB);
-  const bool rowA = (int)threadIdx.x < rowsA;
-  const float hA = buf_f32(rhA, rowA, threadIdx.x);
-  const float eA = buf_f32(reA, rowA, threadIdx.x);
+  const float hA = buf_f32(rhA, (int)threadIdx.x < rowsLim, threadIdx.x);
+  float eA = buf_f32(reA, (int)threadIdx.x < rowsLim, threadIdx.x);
   float hB[C::TJ], eB[C::TJ];
 #pragma unroll
   for (int tj = 0; tj < C::TJ; ++tj) {
@@ -284,13 +298,21 @@ __global__ __launch_bounds__(C::kThreads, C::kMinWaves) void k_screen(ScreenArgs
   floatx16 acc[C::TI][C::TJ];
   const _Float16* tA = A + (int64_t)ta * C::BM * a.D;
   const _Float16* tB = a.B + (int64_t)tb * C::BN * a.D;
+  auto go_on = [&]() {
+    if (known) return true;
+    rowsA = min(C::BM, a.meta->m - ta * C::BM);
+    return rowsA > 0;
+  };
+  bool ran;
   // the common dims get a fully unrolled reduction
   if (a.D == 768)
-    gemm_tile<C, 12>(tA, rowsA, tB, rowsB, a.D, a.D, lds, acc);
+    ran = gemm_tile<C, 12>(tA, rowsLim, tB, rowsB, a.D, a.D, lds, acc, go_on);
   else if (a.D == 1024)
-    gemm_tile<C, 16>(tA, rowsA, tB, rowsB, a.D, a.D, lds, acc);
+    ran = gemm_tile<C, 16>(tA, rowsLim, tB, rowsB, a.D, a.D, lds, acc, go_on);
   else
-    gemm_tile<C>(tA, rowsA, tB, rowsB, a.D, a.D, lds, acc);
+    ran = gemm_tile<C>(tA, rowsLim, tB, rowsB, a.D, a.D, lds, acc, go_on);
+  if (!ran) return;
+  if ((int)threadIdx.x >= rowsA) eA = 0.0f;
 
   {
     // A-side row terms; the error bound uses the largest term among the tile's rows
@@ -389,22 +411,26 @@ using ScreenTile = Tile<2, 2, 2, 2>;   // 128 x 128, four waves of 64 x 64
 // ------------------------------------------------------------------ verify
 struct VerifyArgs {
   const int2* pairs;
-  uint32_t* status;       // 0 out, 1 in, 2 escalate, 3 skipped
+  uint32_t* status;       // 0 out, 1 in, 3 skipped (above the row's definite hit)
   const ChunkCounters* cc;
   uint32_t pair_cap;
   const float* xc;        // chunk rows, float32 (caller memory)
   const float* xs;        // store rows, float32
   int D;
   double d2;              // delta^2 in binary64
+  Big6 thr;               // floor((2 - 2 tau) * 2^298), the exact right-hand side
   int32_t* firstHit;
   uint64_t* bitmap;
   int W;
   uint32_t* hasEdge;
   DevFlags* flags;
   ChunkCounters* ccw;
-  int careful;
 };
 
+// One wave per ambiguous pair: the squared distance in binary64 (error below
+// (D + 2) u64 d^2 in any order); a pair within that distance of delta^2 is
+// decided on exact integers by the same wave (exact.h), so every decision is
+// the exact one.
 __global__ __launch_bounds__(256) void k_verify(VerifyArgs a) {
   if (skip_all(a.flags)) return;
   const uint32_t n = min(a.cc->npairs, a.pair_cap);
@@ -427,27 +453,39 @@ __global__ __launch_bounds__(256) void k_verify(VerifyArgs a) {
       const double t = (double)pa[d] - (double)pb[d];
       s = fma(t, t, s);
     }
-    s = wave_sum_f64(s);
-    if (lane != 0) continue;
+    s = wave_sum_f64(s);   // every lane holds the sum
     const double margin = (double)(a.D + 8) * 2.5e-16 * fmax(a.d2, s) + 1e-300;
-    uint32_t st;
+    bool in;
     if (fabs(s - a.d2) <= margin) {
-      st = 2u;
-      atomicAdd(&a.ccw->n_escalate, 1u);
-      atomicAdd(&a.flags->n_escalate, 1u);
-      if (!a.careful) atomicOr(&a.flags->pair_overflow, 2u);
-    } else if (s <= a.d2) {
-      st = 1u;
+      Big6 acc;
+      big_zero(acc);
+      for (int d = lane; d < a.D; d += 64)
+        big_add(acc, big_sq_diff(__float_as_uint(pa[d]), __float_as_uint(pb[d])));
+      for (int o = 32; o > 0; o >>= 1) {
+        Big6 other;
+#pragma unroll
+        for (int l = 0; l < kExactLimbs; ++l)
+          other.w[l] = (uint64_t)__shfl_xor((unsigned long long)acc.w[l], o);
+        big_add(acc, other);
+      }
+      in = big_cmp(acc, a.thr) <= 0;
+      if (lane == 0) {
+        atomicAdd(&a.ccw->n_escalate, 1u);
+        atomicAdd(&a.flags->n_escalate, 1u);
+      }
+    } else {
+      in = s <= a.d2;
+    }
+    if (lane != 0) continue;
+    if (in) {
       if (kind == 0) {
         atomicMin(&a.firstHit[i], y);
       } else {
         atomicOr(reinterpret_cast<unsigned long long*>(&a.bitmap[(int64_t)i * a.W + (y >> 6)]), 1ull << (y & 63));
         a.hasEdge[i] = 1u;
       }
-    } else {
-      st = 0u;
     }
-    a.status[p] = st;
+    a.status[p] = in ? 1u : 0u;
   }
 }
 
@@ -460,7 +498,7 @@ struct ResolveArgs {
   const uint64_t* bitmap;
   const int64_t* store_ids;
   StoreMeta* meta;
-  int64_t gbase;            // global id of chunk row 0
+  int64_t c0;               // offset of the chunk in the call (global id = meta->n_seen + c0 + row)
   int64_t* rep;             // caller output for the chunk (global ids, -1 kept)
   int32_t* pos;             // store position of kept rows, -1 if dropped
   int32_t* rep_row;         // >= 0 store row, <= -2 chunk row (-(j+2)), -1 kept
@@ -475,7 +513,7 @@ constexpr int kEdgeCap = 20480;    // in-chunk candidate entries held in LDS
 // undecided rows in arrival order; lane L keeps bits [64L, 64L + 64) of the
 // kept mask in a register, and a row takes the lowest kept candidate of its
 // bitmap row.
-__device__ void resolve_sequential(const ResolveArgs& a, volatile uint8_t* st) {
+__device__ void resolve_sequential(const ResolveArgs& a, volatile uint8_t* st, int64_t gbase) {
   const int lane = threadIdx.x & 63;
   const int nblk = (a.nB + 63) >> 6;
   uint64_t kept = 0ull;
@@ -501,7 +539,7 @@ __device__ void resolve_sequential(const ResolveArgs& a, volatile uint8_t* st) {
         const int j = F * 64 + __builtin_ctzll(uf);
         if (lane == 0) {
           st[i] = 2;
-          a.rep[i] = a.gbase + j;
+          a.rep[i] = gbase + j;
           a.rep_row[i] = -(j + 2);
         }
       } else {
@@ -542,6 +580,7 @@ __global__ __launch_bounds__(kResolveThreads) void k_resolve(ResolveArgs a) {
   if (skip_all(a.flags)) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int m0 = a.meta->m;
+  const int64_t gbase = a.meta->n_seen + a.c0;   // updated only at the end of a call
   if (tid == 0) {
     n_active = 0u;
     n_edges = 0u;
@@ -611,7 +650,7 @@ __global__ __launch_bounds__(kResolveThreads) void k_resolve(ResolveArgs a) {
   }
   __syncthreads();
   if (n_edges > (uint32_t)kEdgeCap) {
-    if (wave == 0) resolve_sequential(a, st);
+    if (wave == 0) resolve_sequential(a, st, gbase);
   } else {
     for (;;) {
       if (tid == 0) pending = 0u;
@@ -635,7 +674,7 @@ __global__ __launch_bounds__(kResolveThreads) void k_resolve(ResolveArgs a) {
         ecur[i] = (uint16_t)p;
         if (dec == 1) {
           st[i] = 2;
-          a.rep[i] = a.gbase + j;
+          a.rep[i] = gbase + j;
           a.rep_row[i] = -(j + 2);
         } else if (dec == 0) {
           st[i] = 1;
@@ -696,7 +735,7 @@ struct AppendArgs {
   const float* etc;
   const int32_t* pos;
   const int32_t* rep_row;
-  int64_t gbase;
+  int64_t c0;               // offset of the chunk in the call
   int D;
   float* xs;
   _Float16* x16s;
@@ -705,6 +744,10 @@ struct AppendArgs {
   int64_t* ids;
   DevFlags* flags;
   ChunkCounters* cc;
+  StoreMeta* meta;
+  int64_t n_call;           // rows of the whole call
+  int last_chunk;           // the call's last chunk: fold the call into the store's bookkeeping
+  int async_call;           // no host check follows: a full pair list is reported as an error
   DevFlags* flags_out;      // host-mapped copy of the status words, or NULL
 };
 
@@ -717,6 +760,8 @@ __global__ __launch_bounds__(256) void k_append(AppendArgs a, int nB) {
   const bool skip = skip_all(a.flags);
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
+  // every workgroup reads n_seen before the last one (below) advances it
+  const int64_t gbase = a.meta->n_seen + a.c0;
   double dmax = 0.0;
   for (int r = blockIdx.x * kAppendRows + wave; !skip && r < min(nB, (int)(blockIdx.x + 1) * kAppendRows);
        r += 4) {
@@ -733,7 +778,7 @@ __global__ __launch_bounds__(256) void k_append(AppendArgs a, int nB) {
       if (lane == 0) {
         a.hns[p] = a.hnc[r];
         a.ets[p] = a.etc[r];
-        a.ids[p] = a.gbase + r;
+        a.ids[p] = gbase + r;
       }
       continue;
     }
@@ -755,10 +800,12 @@ __global__ __launch_bounds__(256) void k_append(AppendArgs a, int nB) {
       atomicMax(reinterpret_cast<unsigned long long*>(&a.flags->dhat2_bits),
                 (unsigned long long)__double_as_longlong(m));
   }
-  if (a.flags_out == nullptr) return;
-  // The last workgroup to finish copies the status words to host memory and
-  // clears them for the next call (every other workgroup's updates are
-  // ordered before its count by the fence).
+  if (!a.last_chunk) return;
+  // The last workgroup to finish folds the call into the store's bookkeeping
+  // (arrival count and delta_hat if the call went through, an error count if
+  // its input was invalid), copies the status words to host memory when asked,
+  // and clears them for the next call.  Every other workgroup's updates are
+  // ordered before its count by the fence.
   __shared__ bool last;
   __syncthreads();
   if (threadIdx.x == 0) {
@@ -769,12 +816,28 @@ __global__ __launch_bounds__(256) void k_append(AppendArgs a, int nB) {
   if (!last) return;
   __threadfence();
   constexpr int kWords = (int)(sizeof(DevFlags) / 4);
-  if (threadIdx.x < kWords) {
-    uint32_t* f = reinterpret_cast<uint32_t*>(a.flags);
-    const uint32_t v = __hip_atomic_load(f + threadIdx.x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    reinterpret_cast<uint32_t*>(a.flags_out)[threadIdx.x] = v;
-    f[threadIdx.x] = 0u;
+  uint32_t* f = reinterpret_cast<uint32_t*>(a.flags);
+  if (threadIdx.x == 0) {
+    // atomic loads: this workgroup may hold the words in its L1 from its start
+    auto ld = [](uint32_t* p) { return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); };
+    const uint32_t bad = (ld(&a.flags->nonfinite) ? 1u : 0u) | (ld(&a.flags->out_of_range) ? 2u : 0u);
+    const bool overflow = (ld(&a.flags->pair_overflow) & 1u) != 0u;
+    if (bad != 0u || (overflow && a.async_call)) {
+      a.meta->err_calls += 1u;
+      a.meta->err_bits |= bad | (overflow ? 4u : 0u);
+    } else if (!overflow) {
+      a.meta->n_seen += a.n_call;
+      const unsigned long long d2 =
+          __hip_atomic_load(&a.flags->dhat2_bits, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (d2 > a.meta->dhat2_bits) a.meta->dhat2_bits = d2;   // non-negative doubles order as their bits
+    }
   }
+  if ((int)threadIdx.x < kWords) {
+    const uint32_t v = __hip_atomic_load(f + threadIdx.x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (a.flags_out) reinterpret_cast<uint32_t*>(a.flags_out)[threadIdx.x] = v;
+  }
+  __syncthreads();
+  if ((int)threadIdx.x < kWords) f[threadIdx.x] = 0u;
   if (threadIdx.x == 0) a.cc->blocks_done = 0u;
 }
 
@@ -808,7 +871,9 @@ lam_status store_alloc(lam_store* st) {
   LAM_HIP(hipMalloc(&st->ids, cap * 8));
   LAM_HIP(hipMalloc(&st->stat_dev, sizeof(StoreMeta)));
   LAM_HIP(hipMemset(st->stat_dev, 0, sizeof(StoreMeta)));
+  LAM_HIP(hipEventCreateWithFlags(&st->done, hipEventDisableTiming));
   LAM_HIP(hipDeviceSynchronize());
+  st->thr = exact_threshold(st->tau);
   return LAM_OK;
 }
 
@@ -816,6 +881,8 @@ void store_free(lam_store* st) {
   for (void* p : {(void*)st->x32, (void*)st->x16, (void*)st->hn, (void*)st->et, (void*)st->ids,
                   (void*)st->stat_dev, (void*)st->codes})
     if (p) (void)hipFree(p);
+  if (st->done) (void)hipEventDestroy(st->done);
+  st->done = nullptr;
   st->x32 = nullptr;
   st->x16 = nullptr;
   st->hn = st->et = st->stat_dev = nullptr;
@@ -840,55 +907,45 @@ Consts screen_consts(int D) {
   return c;
 }
 
-// Exact decisions for the pairs the binary64 test could not separate from
-// delta^2 (status 2), patched into the chunk's hit/edge state.
-lam_status escalate_chunk(lam_ctx* ctx, lam_store* st, const float* xc, int64_t c_rows, int32_t* firstHit,
-                          uint64_t* bitmap, int W, uint32_t* hasEdge, const int2* pairs_dev,
-                          const uint32_t* status_dev, const ChunkCounters* cc_dev, uint32_t cap) {
-  ChunkCounters cc{};
-  LAM_HIP(hipMemcpyAsync(&cc, cc_dev, sizeof cc, hipMemcpyDeviceToHost, ctx->stream));
-  LAM_HIP(hipStreamSynchronize(ctx->stream));
-  if (cc.n_escalate == 0) return LAM_OK;
-  const uint32_t n = std::min(cc.npairs, cap);
-  std::vector<int2> pairs(n);
-  std::vector<uint32_t> status(n);
-  LAM_HIP(hipMemcpy(pairs.data(), pairs_dev, n * sizeof(int2), hipMemcpyDeviceToHost));
-  LAM_HIP(hipMemcpy(status.data(), status_dev, n * 4, hipMemcpyDeviceToHost));
-  const int D = st->dim;
-  std::vector<float> ra(D), rb(D);
-  for (uint32_t p = 0; p < n; ++p) {
-    if (status[p] != 2u) continue;
-    const int kind = (int)((uint32_t)pairs[p].x >> 31);
-    const int i = pairs[p].x & 0x7fffffff;
-    const int y = pairs[p].y;
-    (void)c_rows;
-    LAM_HIP(hipMemcpy(ra.data(), xc + (int64_t)i * D, D * 4, hipMemcpyDeviceToHost));
-    LAM_HIP(hipMemcpy(rb.data(), (kind ? xc : st->x32) + (int64_t)y * D, D * 4, hipMemcpyDeviceToHost));
-    if (!exact_within(ra.data(), rb.data(), D, st->tau)) continue;
-    if (kind == 0) {
-      int32_t cur = 0;
-      LAM_HIP(hipMemcpy(&cur, firstHit + i, 4, hipMemcpyDeviceToHost));
-      if (y < cur) LAM_HIP(hipMemcpy(firstHit + i, &y, 4, hipMemcpyHostToDevice));
-    } else {
-      uint64_t w = 0;
-      LAM_HIP(hipMemcpy(&w, bitmap + (int64_t)i * W + (y >> 6), 8, hipMemcpyDeviceToHost));
-      w |= 1ull << (y & 63);
-      LAM_HIP(hipMemcpy(bitmap + (int64_t)i * W + (y >> 6), &w, 8, hipMemcpyHostToDevice));
-      const uint32_t one = 1u;
-      LAM_HIP(hipMemcpy(hasEdge + i, &one, 4, hipMemcpyHostToDevice));
-    }
+// Ambiguous-pair entries (12 bytes each) reserved for a call that does not
+// wait for the device: such a call needs room for every pair one chunk can
+// produce, n (m + n).
+constexpr uint64_t kAsyncPairLimit = 1ull << 26;
+
+}  // namespace
+
+lam_status store_settle(lam_store* st) {
+  if (!st->pending) return LAM_OK;
+  LAM_HIP(hipEventSynchronize(st->done));
+  StoreMeta m{};
+  LAM_HIP(hipMemcpy(&m, st->stat_dev, sizeof m, hipMemcpyDeviceToHost));
+  st->pending = false;
+  st->size = m.m;
+  st->size_ub = m.m;
+  st->n_seen = m.n_seen;
+  double dh2 = 0.0;
+  memcpy(&dh2, &m.dhat2_bits, 8);
+  st->delta_hat_run = std::sqrt(dh2);
+  if (m.err_calls != 0u) {
+    const uint32_t calls = m.err_calls, bits = m.err_bits;
+    m.err_calls = 0u;
+    m.err_bits = 0u;
+    LAM_HIP(hipMemcpy(st->stat_dev, &m, sizeof m, hipMemcpyHostToDevice));
+    set_error("%u earlier ingest call(s) that did not wait for the device had %s; they left the store "
+              "unchanged and wrote no outputs", calls,
+              (bits & 4u) ? "too many ambiguous pairs (internal)"
+                          : (bits & 1u) ? "NaN or Inf in the input" : "coordinates with |x| >= 256");
+    return LAM_EINVAL;
   }
   return LAM_OK;
 }
 
-}  // namespace
-
 lam_status dedup_ingest(lam_ctx* ctx, lam_store* st, const float* x, int64_t n, int64_t* rep, float* max_cos,
                         lam_ingest_stats* stats) {
   const int D = st->dim;
-  const int64_t m_before = st->size;
   if (n == 0) {
     if (stats) {
+      LAM_TRY(store_settle(st));
       *stats = lam_ingest_stats{};
       stats->store_size = st->size;
       stats->delta_hat_run = st->delta_hat_run;
@@ -897,6 +954,24 @@ lam_status dedup_ingest(lam_ctx* ctx, lam_store* st, const float* x, int64_t n, 
   }
   const int CH = (int)std::min<int64_t>(n, kChunk);
   const int W = (CH + 63) / 64;
+
+  // A call without stats does not wait for the device when the ambiguous-pair
+  // list can hold every pair its chunks could produce (so it cannot overflow)
+  // and the store has room even if every earlier row was kept.  Otherwise the
+  // call waits, checks the status words and, on an overflow, repeats with a
+  // larger list.
+  const int64_t m_ub = st->pending ? st->size_ub : st->size;
+  const uint64_t worst = (uint64_t)CH * (uint64_t)(m_ub + n);
+  const bool async = stats == nullptr && worst <= kAsyncPairLimit && m_ub + n <= st->capacity;
+  if (!async) {
+    LAM_TRY(store_settle(st));
+    LAM_CHECK(n <= st->capacity - st->size, LAM_ECAPACITY, "store holds %lld of %lld rows; a batch of %lld may not fit",
+              (long long)st->size, (long long)st->capacity, (long long)n);
+  } else if (ctx->pair_cap < worst) {
+    // grow geometrically: every growth reallocates, which waits for the device
+    ctx->pair_cap = (uint32_t)std::min<uint64_t>(kAsyncPairLimit, std::max<uint64_t>(worst, 2ull * ctx->pair_cap));
+  }
+  const int64_t m_before = async ? m_ub : st->size;   // exact when waiting, an upper bound otherwise
   const Consts K = screen_consts(D);
   StoreMeta* meta = reinterpret_cast<StoreMeta*>(st->stat_dev);
   const bool want_max = max_cos != nullptr;
@@ -922,7 +997,6 @@ lam_status dedup_ingest(lam_ctx* ctx, lam_store* st, const float* x, int64_t n, 
   uint64_t* bitmap = ctx->scratch[S_BITMAP].as<uint64_t>();
   float* G = want_max ? ctx->scratch[S_G].as<float>() : nullptr;
 
-  bool careful = false;
   for (int attempt = 0; attempt < 4; ++attempt) {
     const uint32_t cap = ctx->pair_cap;
     LAM_TRY(ctx->scratch[S_PAIRS].ensure((size_t)cap * sizeof(int2)));
@@ -932,14 +1006,15 @@ lam_status dedup_ingest(lam_ctx* ctx, lam_store* st, const float* x, int64_t n, 
 
     for (int64_t c0 = 0; c0 < n; c0 += CH) {
       const int nB = (int)std::min<int64_t>(CH, n - c0);
-      const int ntB = (nB + kTB - 1) / kTB;
       const float* xc = x + c0 * D;
       const _Float16* x16 = x16c + c0 * D;
       const bool last_chunk = c0 + CH >= n;
-      const ChunkState cs{firstHit, hasEdge, maxcos, bitmap, W, nB, cc, meta, (int32_t)m_before};
+      // a waiting call sets the store size (so a repeated attempt starts from
+      // the store as it was); otherwise the kernels keep it
+      const ChunkState cs{firstHit, hasEdge, maxcos, bitmap, W, nB, cc, meta, async ? -1 : (int32_t)m_before};
       if (c0 == 0) {
         // the status words must be zero before prep counts into them; the
-        // last append of every completed call leaves them zero
+        // last append of every call leaves them zero
         if (!ctx->flags_zero) LAM_TRY(clear_flags(ctx));
         ctx->flags_zero = false;
         ProfScope ps(ctx, "dedup_prep");
@@ -956,13 +1031,13 @@ lam_status dedup_ingest(lam_ctx* ctx, lam_store* st, const float* x, int64_t n, 
       sa.hnS = st->hn;
       sa.etS = st->et;
       sa.meta = meta;
-      sa.m_exact = c0 == 0 ? (int)m_before : -1;   // later chunks: read the kernel-maintained count
+      sa.m_exact = (!async && c0 == 0) ? (int)m_before : -1;   // otherwise read the kernel-maintained count
+      sa.capA = (int)std::min<int64_t>(st->capacity, INT32_MAX);
       sa.B = x16;
       sa.hnB = hnc + c0;
       sa.etB = etc + c0;
       sa.nB = nB;
       sa.D = D;
-      sa.ntB = ntB;
       sa.half_d2 = 0.5 * st->d2;
       sa.firstHit = firstHit;
       sa.maxcos = maxcos;
@@ -976,11 +1051,11 @@ lam_status dedup_ingest(lam_ctx* ctx, lam_store* st, const float* x, int64_t n, 
       sa.flags = ctx->flags_dev;
       // against the store (rows retained before this chunk; the kernel reads
       // the exact count, the grid covers an upper bound) and inside the chunk
-      const int64_t m_ub = m_before + c0;
+      const int64_t m_grid = m_before + c0;
       const int tb_rows = ScreenTile::BN;
       const int ntBt = (nB + tb_rows - 1) / tb_rows;
       sa.ntB = ntBt;
-      sa.nb0 = ((m_ub + tb_rows - 1) / tb_rows) * ntBt;
+      sa.nb0 = ((m_grid + tb_rows - 1) / tb_rows) * ntBt;
       sa.nb1 = (int64_t)ntBt * (ntBt + 1) / 2;
       const int64_t grid = sa.nb0 + sa.nb1;
       LAM_CHECK(grid < (1LL << 31), LAM_EINVAL, "screen grid too large");
@@ -994,17 +1069,15 @@ lam_status dedup_ingest(lam_ctx* ctx, lam_store* st, const float* x, int64_t n, 
                              ctx->stream, sa);
         LAM_HIP(hipGetLastError());
       }
-      VerifyArgs va{pairs, status, cc, cap, xc, st->x32, D, st->d2, firstHit, bitmap, W, hasEdge,
-                    ctx->flags_dev, cc, careful ? 1 : 0};
+      VerifyArgs va{pairs, status, cc, cap, xc, st->x32, D, st->d2, st->thr, firstHit, bitmap, W, hasEdge,
+                    ctx->flags_dev, cc};
       {
         ProfScope ps(ctx, "dedup_verify");
         hipLaunchKernelGGL(k_verify, dim3(256), dim3(256), 0, ctx->stream, va);
         LAM_HIP(hipGetLastError());
       }
-      if (careful)
-        LAM_TRY(escalate_chunk(ctx, st, xc, nB, firstHit, bitmap, W, hasEdge, pairs, status, cc, cap));
-      ResolveArgs ra{nB, W, firstHit, hasEdge, bitmap, st->ids, meta, st->n_seen + c0, rep + c0, pos, rep_row,
-                     kept_words, ctx->flags_dev};
+      ResolveArgs ra{nB, W, firstHit, hasEdge, bitmap, st->ids, meta, c0, rep + c0, pos, rep_row, kept_words,
+                     ctx->flags_dev};
       {
         ProfScope ps(ctx, "dedup_resolve");
         hipLaunchKernelGGL(k_resolve, dim3(1), dim3(kResolveThreads), 0, ctx->stream, ra);
@@ -1015,8 +1088,9 @@ lam_status dedup_ingest(lam_ctx* ctx, lam_store* st, const float* x, int64_t n, 
                            kept_words, max_cos + c0, ctx->flags_dev);
         LAM_HIP(hipGetLastError());
       }
-      AppendArgs aa{xc, x16, hnc + c0, etc + c0, pos, rep_row, st->n_seen + c0, D, st->x32, st->x16, st->hn,
-                    st->et, st->ids, ctx->flags_dev, cc, last_chunk ? ctx->flags_host_dev : nullptr};
+      AppendArgs aa{xc, x16, hnc + c0, etc + c0, pos, rep_row, c0, D, st->x32, st->x16, st->hn, st->et, st->ids,
+                    ctx->flags_dev, cc, meta, n, last_chunk ? 1 : 0, async ? 1 : 0,
+                    (last_chunk && !async) ? ctx->flags_host_dev : nullptr};
       {
         ProfScope ps(ctx, "dedup_append");
         hipLaunchKernelGGL(k_append, dim3((unsigned)((nB + kAppendRows - 1) / kAppendRows)), dim3(256), 0,
@@ -1024,9 +1098,15 @@ lam_status dedup_ingest(lam_ctx* ctx, lam_store* st, const float* x, int64_t n, 
         LAM_HIP(hipGetLastError());
       }
     }
-    // the last append wrote the status words to host memory and zeroed them
+    ctx->flags_zero = true;   // the last append clears the status words
+    if (async) {
+      LAM_HIP(hipEventRecord(st->done, ctx->stream));
+      st->pending = true;
+      st->size_ub = m_before + n;
+      return LAM_OK;
+    }
+    // the last append wrote the status words to host memory
     LAM_HIP(hipStreamSynchronize(ctx->stream));
-    ctx->flags_zero = true;
     const DevFlags f = *ctx->flags_host;
     LAM_CHECK(f.nonfinite == 0, LAM_EINVAL, "input holds NaN or Inf (%u rows)", f.nonfinite);
     LAM_CHECK(f.out_of_range == 0, LAM_EINVAL, "input has coordinates with |x| >= 256 (%u rows)", f.out_of_range);
@@ -1034,14 +1114,11 @@ lam_status dedup_ingest(lam_ctx* ctx, lam_store* st, const float* x, int64_t n, 
       ctx->pair_cap = std::max<uint32_t>(ctx->pair_cap * 2u, f.pairs_needed + (f.pairs_needed >> 2));
       continue;
     }
-    if (f.pair_overflow & 2u) {
-      careful = true;
-      continue;
-    }
     double dh2 = 0.0;
     memcpy(&dh2, &f.dhat2_bits, 8);
     const double dh_call = std::sqrt(dh2);
     st->size = m_before + f.n_kept;
+    st->size_ub = st->size;
     st->n_seen += n;
     st->delta_hat_run = std::max(st->delta_hat_run, dh_call);
     if (stats) {

@@ -8,6 +8,7 @@
 #include <string>
 #include <vector>
 
+#include "exact.h"
 #include "lam.h"
 
 namespace lam {
@@ -99,9 +100,13 @@ struct lam_store {
   double tau = 0.0;
   double d2 = 0.0;          // delta^2 = 2 - 2 tau (binary64)
   int64_t capacity = 0;
-  int64_t size = 0;
-  int64_t n_seen = 0;
-  double delta_hat_run = 0.0;
+  int64_t size = 0;           // exact when !pending
+  int64_t n_seen = 0;         // exact when !pending
+  double delta_hat_run = 0.0; // exact when !pending
+  bool pending = false;       // ingest calls ran without waiting; the device bookkeeping holds the truth
+  int64_t size_ub = 0;        // upper bound of the size while pending
+  hipEvent_t done = nullptr;  // recorded after the last call that did not wait
+  lam::Big6 thr{};            // floor((2 - 2 tau) * 2^298), the exact predicate's right side
   // retained rows (capacity rows each)
   float* x32 = nullptr;       // float32 rows
   _Float16* x16 = nullptr;    // float16 rows scaled by 2^8 (screen operand)
@@ -156,6 +161,8 @@ lam_status score_topk(lam_ctx* ctx, const lam_store* st, const float* q, int64_t
 
 // ------------------------------------------------------------------ exact host predicate (exact.cpp)
 // sum_d (a_d - b_d)^2 <= 2 - 2 tau on exact reals, float32 rows a, b of length d.
-bool exact_within(const float* a, const float* b, int d, double tau);
+// Waits for ingest calls that did not wait, copies the device bookkeeping into
+// the host fields and reports (once) invalid input those calls met.
+lam_status store_settle(lam_store* st);
 
 }  // namespace lam

@@ -148,11 +148,13 @@ __device__ __forceinline__ void slab_store_n(_Float16* __restrict__ s, const uin
 // sits behind a branch.  With NS > 0 the reduction has exactly NS slabs and the
 // loop is unrolled, which lets the compiler wait for exactly the loads each
 // LDS store needs (across a loop back edge it waits for all of them); NS = 0
-// takes kdim at run time.
-template <class C, int NS = 0>
-__device__ __forceinline__ void gemm_tile(const _Float16* __restrict__ A, int ra, const _Float16* __restrict__ B,
+// takes kdim at run time.  go_on() runs once the first two slabs' loads are in
+// flight; if it returns false the tile is abandoned and gemm_tile returns
+// false.
+template <class C, int NS = 0, class Go>
+__device__ __forceinline__ bool gemm_tile(const _Float16* __restrict__ A, int ra, const _Float16* __restrict__ B,
                                           int rb, int64_t ld, int kdim, _Float16* lds,
-                                          floatx16 (&acc)[C::TI][C::TJ]) {
+                                          floatx16 (&acc)[C::TI][C::TJ], Go&& go_on) {
   auto sa = [&](int i) -> _Float16* { return lds + i * ((C::BM + C::BN) * kLdk); };
   auto sb = [&](int i) -> _Float16* { return lds + i * ((C::BM + C::BN) * kLdk) + C::BM * kLdk; };
   const int wave = threadIdx.x >> 6;
@@ -164,18 +166,34 @@ __device__ __forceinline__ void gemm_tile(const _Float16* __restrict__ A, int ra
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.0f;
   auto compute = [&](int st) {
+    // fragments double-buffered in registers: step kk + 1's LDS reads are
+    // issued between step kk's MFMAs
+    half8 fa[2][C::TI], fb[2][C::TJ];
+#pragma unroll
+    for (int t = 0; t < C::TI; ++t) fa[0][t] = frag_load(sa(st), wm * C::TI * 32 + t * 32, 0);
+#pragma unroll
+    for (int t = 0; t < C::TJ; ++t) fb[0][t] = frag_load(sb(st), wn * C::TJ * 32 + t * 32, 0);
 #pragma unroll
     for (int kk = 0; kk < kBK / 16; ++kk) {
-      half8 fa[C::TI], fb[C::TJ];
+      const int cb = kk & 1, nb = cb ^ 1;
+      if (kk + 1 < kBK / 16) {
 #pragma unroll
-      for (int t = 0; t < C::TI; ++t) fa[t] = frag_load(sa(st), wm * C::TI * 32 + t * 32, kk);
+        for (int t = 0; t < C::TI; ++t) fa[nb][t] = frag_load(sa(st), wm * C::TI * 32 + t * 32, kk + 1);
 #pragma unroll
-      for (int t = 0; t < C::TJ; ++t) fb[t] = frag_load(sb(st), wn * C::TJ * 32 + t * 32, kk);
+        for (int t = 0; t < C::TJ; ++t) fb[nb][t] = frag_load(sb(st), wn * C::TJ * 32 + t * 32, kk + 1);
+      }
 #pragma unroll
       for (int a = 0; a < C::TI; ++a)
 #pragma unroll
         for (int b = 0; b < C::TJ; ++b)
-          acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fa[a], fb[b], acc[a][b], 0, 0, 0);
+          acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fa[cb][a], fb[cb][b], acc[a][b], 0, 0, 0);
+      if (kk + 1 < kBK / 16) {
+#pragma unroll
+        for (int i = 0; i < C::TI + C::TJ; ++i) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one MFMA
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // one LDS read
+        }
+      }
     }
   };
   const int S = NS > 0 ? NS : (kdim + kBK - 1) / kBK;
@@ -185,6 +203,8 @@ __device__ __forceinline__ void gemm_tile(const _Float16* __restrict__ A, int ra
   slab_load_n<C::kPerB>(rsB, rb, ld, 0, kdim, b0, C::kThreads);
   slab_load_n<C::kPerA>(rsA, ra, ld, kBK, kdim, a1, C::kThreads);
   slab_load_n<C::kPerB>(rsB, rb, ld, kBK, kdim, b1, C::kThreads);
+  // the caller may stop here (its check's own loads overlap the first slabs')
+  if (!go_on()) return false;
   slab_store_n<C::kPerA>(sa(0), a0, C::kThreads);
   slab_store_n<C::kPerB>(sb(0), b0, C::kThreads);
   slab_load_n<C::kPerA>(rsA, ra, ld, 2 * kBK, kdim, a0, C::kThreads);
@@ -208,6 +228,7 @@ __device__ __forceinline__ void gemm_tile(const _Float16* __restrict__ A, int ra
     slab_load_n<C::kPerB>(rsB, rb, ld, (s + 4) * kBK, kdim, b0, C::kThreads);
     __syncthreads();
   }
+  return true;
 }
 
 // Workgroup index remapped so that consecutive logical tiles run on the same

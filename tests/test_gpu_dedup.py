@@ -177,3 +177,73 @@ def test_empty_batch(lam):
     s = lam.Store(64, 0.95, 10)
     rep, st = s.ingest(torch.empty((0, 64), dtype=torch.float32, device="cuda"))
     assert rep.numel() == 0 and st["n_in"] == 0 and s.size == 0
+
+
+# ----------------------------------------------------------------- calls that do not wait
+
+def _ingest_async(lam, x, tau, batch, sync_every=0):
+    """Ingest in batches with sync=False (every `sync_every`-th call waits)."""
+    s = lam.Store(x.shape[1], tau, x.shape[0])
+    xd = _dev(x)
+    reps = []
+    for k, b0 in enumerate(range(0, x.shape[0], batch)):
+        sync = sync_every > 0 and k % sync_every == sync_every - 1
+        reps.append(s.ingest(xd[b0:b0 + batch], sync=sync)[0])
+    info = s.info()
+    rep = torch.cat(reps).cpu().numpy() if reps else np.zeros(0, np.int64)
+    return s, rep, info
+
+
+def test_subset_async_parity(lam):
+    """The benchmark's stream with calls that return before the device is done."""
+    x, ref = _subset_ref(0.95)
+    _, rep, info = _ingest_async(lam, x, 0.95, 1024)
+    assert np.array_equal(rep, ref["rep"])
+    assert info.size == int(np.count_nonzero(ref["rep"] < 0)) and info.n_seen == x.shape[0]
+    assert abs(info.delta_hat_run - ref["delta_hat"]) <= 1e-12
+
+
+def test_async_mixed_with_waiting_calls(lam):
+    x, ref = _subset_ref(0.95)
+    _, rep, info = _ingest_async(lam, x[:9000], 0.95, 700, sync_every=3)
+    ref9 = dedup.greedy(x[:9000], 0.95, block=512)
+    assert np.array_equal(rep, ref9["rep"])
+    assert info.size == int(np.count_nonzero(ref9["rep"] < 0))
+
+
+def test_async_exact_ties(lam):
+    """Exact ties decided on the device inside calls that do not wait."""
+    rng = np.random.default_rng(5)
+    a, b, b_in, b_out, tau = synth.dyadic_ties(rng, 200, 128)
+    x = np.concatenate([a, b, b_in, b_out, synth.unit_rows(rng, 300, 128).astype(np.float32)])
+    x = x[rng.permutation(x.shape[0])]
+    ref = dedup.greedy(x, tau)
+    assert ref["n_exact"] > 0
+    _, rep, info = _ingest_async(lam, x, tau, 256)
+    assert np.array_equal(rep, ref["rep"])
+    assert abs(info.delta_hat_run - ref["delta_hat"]) <= 1e-12
+
+
+def test_async_invalid_input_reported_later(lam):
+    """A call that did not wait and met NaN leaves the store and its outputs
+    untouched; the next waiting call reports it once; later calls are decided
+    as if it had not happened."""
+    rng = np.random.default_rng(3)
+    x = synth.unit_rows(rng, 900, 64).astype(np.float32)
+    bad = x[300:600].copy()
+    bad[123, 7] = np.nan
+    s = lam.Store(64, 0.95, 2000)
+    r1, st1 = s.ingest(_dev(x[:300]), sync=False)
+    assert st1 is None
+    rb = torch.full((300,), -7, dtype=torch.int64, device="cuda")
+    s.ingest(_dev(bad), rep=rb, sync=False)
+    r3, _ = s.ingest(_dev(x[600:]), sync=False)
+    with pytest.raises(lam.LamError) as e:
+        s.info()
+    assert e.value.name == "LAM_EINVAL"
+    info = s.info()   # reported once
+    good = np.concatenate([x[:300], x[600:]])
+    ref = dedup.greedy(good, 0.95)
+    assert info.n_seen == 600 and info.size == int(np.count_nonzero(ref["rep"] < 0))
+    assert np.array_equal(torch.cat([r1, r3]).cpu().numpy(), ref["rep"])
+    assert (rb.cpu().numpy() == -7).all()
