@@ -118,7 +118,7 @@ __host__ __device__ inline Big6 big_sq_diff(uint32_t ua, uint32_t ub) {
       const uint64_t t = s + carry;
       c += t < s ? 1u : 0u;
       r.w[i + j] = t;
-      carry = hi + c;   // hi <= 2^64 - 2, so no wrap
+      carry = hi + c;   // d_i d_j + r + carry < 2^128, so this high word cannot wrap
     }
     for (int k = i + 3; k < kExactLimbs && carry != 0u; ++k) {
       const uint64_t s = r.w[k] + carry;

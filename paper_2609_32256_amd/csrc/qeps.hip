@@ -70,6 +70,15 @@ __device__ __forceinline__ int32_t q_round_fast(float x, float inv_s32, double s
   return q_round(x, s, inv_s, eps);
 }
 
+// Buffer resource over `bytes` bytes from base: loads at offsets past the
+// bound return zeros without touching memory, so a load never needs a branch
+// (a load under a branch makes the compiler wait for every outstanding load,
+// which serialises a prefetching loop).  gfx9 raw buffer: stride 0, 32-bit data
+// format word.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t span_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+
 __device__ __forceinline__ void wave_flag(bool bad, uint32_t* counter) {
   const unsigned long long m = __ballot(bad);
   if (m != 0ull && (threadIdx.x & 63) == 0) atomicAdd(counter, (uint32_t)__popcll(m));
@@ -82,11 +91,23 @@ __global__ __launch_bounds__(kThreads) void k_absmax(const float* __restrict__ x
   const int64_t stride = (int64_t)gridDim.x * kThreads;
   int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
   if (VEC) {
+    // float4 loads, four per trip and all in flight together; each trip reads
+    // a window of 4 * stride float4 through a resource that ends at the data,
+    // so the tail reads zeros (which do not change the maximum)
     const int64_t n4 = n >> 2;
-    const uint4* x4 = reinterpret_cast<const uint4*>(x);
-    for (int64_t j = i; j < n4; j += stride) {
-      const uint4 v = x4[j];
-      m = max(m, max(max(v.x & 0x7fffffffu, v.y & 0x7fffffffu), max(v.z & 0x7fffffffu, v.w & 0x7fffffffu)));
+    for (int64_t j0 = (int64_t)blockIdx.x * kThreads; j0 < n4; j0 += 4 * stride) {
+      const int64_t left = n4 - j0;
+      const uint32_t nbytes = (uint32_t)((left < 4 * stride ? left : 4 * stride) * 16);
+      const __amdgpu_buffer_rsrc_t rs = span_rsrc(x + j0 * 4, nbytes);
+      uint4 v[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        v[u] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(
+                                             rs, (uint32_t)(u * stride + threadIdx.x) * 16u, 0, 0));
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        m = max(m, max(max(v[u].x & 0x7fffffffu, v[u].y & 0x7fffffffu),
+                       max(v[u].z & 0x7fffffffu, v[u].w & 0x7fffffffu)));
     }
     for (int64_t j = (n4 << 2) + i; j < n; j += stride) m = max(m, __float_as_uint(x[j]) & 0x7fffffffu);
   } else {
@@ -104,46 +125,26 @@ __global__ __launch_bounds__(kThreads) void k_absmax(const float* __restrict__ x
   }
 }
 
-template <int B, bool VEC>
-__global__ __launch_bounds__(kThreads) void k_encode(const float* __restrict__ x, int64_t n, float inv_s32,
-                                                     double s, double inv_s, double eps, float absmax,
-                                                     uint32_t* __restrict__ codes, uint64_t nwords,
-                                                     uint32_t* __restrict__ flags) {
-  __shared__ uint32_t lq[kPadded];
+// Quantize, pack and store one tile whose values are in v (thread t holds
+// elements j * 1024 + 4t .. +3 of the tile for j = 0..7).  FULL: all kTile
+// elements exist.
+template <int B, bool FULL>
+__device__ __forceinline__ void encode_tile(const float4 (&v4)[kPerThread / 4], int64_t tile, int64_t n,
+                                            float inv_s32, double s, double inv_s, double eps, float absmax,
+                                            uint32_t* __restrict__ codes, uint64_t nwords,
+                                            uint32_t* __restrict__ flags, uint32_t* lq) {
   constexpr uint32_t kMask = (B == 32) ? 0xffffffffu : ((1u << B) - 1u);
   const int t = threadIdx.x;
-  const int64_t ntiles = (n + kTile - 1) / kTile;
-  // Persistent workgroups: the next tile's loads are in flight while the
-  // current tile is rounded, packed and stored.
-  float4 cur[kPerThread / 4], nxt[kPerThread / 4];
-  auto load_tile = [&](int64_t tl, float4 (&v)[kPerThread / 4]) {
-    const int64_t b0 = tl * (int64_t)kTile;
-#pragma unroll
-    for (int j = 0; j < kPerThread / 4; ++j) {
-      const int64_t e = b0 + j * (kThreads * 4) + t * 4;
-      if (VEC && e + 3 < n) {
-        v[j] = *reinterpret_cast<const float4*>(x + e);
-      } else {
-        v[j].x = (e < n) ? x[e] : 0.0f;
-        v[j].y = (e + 1 < n) ? x[e + 1] : 0.0f;
-        v[j].z = (e + 2 < n) ? x[e + 2] : 0.0f;
-        v[j].w = (e + 3 < n) ? x[e + 3] : 0.0f;
-      }
-    }
-  };
-  int64_t tile = blockIdx.x;
-  if (tile < ntiles) load_tile(tile, cur);
-  for (; tile < ntiles; tile += gridDim.x) {
-  if (tile + gridDim.x < ntiles) load_tile(tile + gridDim.x, nxt);
   const int64_t base = tile * (int64_t)kTile;
   bool bad = false;   // NaN, Inf or |x| > absmax (absmax is finite)
 #pragma unroll
   for (int j = 0; j < kPerThread / 4; ++j) {
     const int le = j * (kThreads * 4) + t * 4;
-    const float v[4] = {cur[j].x, cur[j].y, cur[j].z, cur[j].w};
+    const float v[4] = {v4[j].x, v4[j].y, v4[j].z, v4[j].w};
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      bad |= !(fabsf(v[r]) <= absmax);
+      const bool real = FULL || base + le + r < n;
+      bad |= real && !(fabsf(v[r]) <= absmax);
       const int li = le + r;
       lq[li + (li >> 5)] = (uint32_t)q_round_fast(v[r], inv_s32, s, inv_s, eps) & kMask;
     }
@@ -170,16 +171,21 @@ __global__ __launch_bounds__(kThreads) void k_encode(const float* __restrict__ x
   __syncthreads();
   constexpr int kWords = kThreads * B;              // words per tile
   const uint64_t w0 = (uint64_t)tile * kWords;
+#pragma unroll
   for (int i = t; i < kWords; i += kThreads)
-    if (w0 + i < nwords) codes[w0 + i] = lq[i + (i >> 5)];
+    if (FULL || w0 + i < nwords) codes[w0 + i] = lq[i + (i >> 5)];
   if (__ballot(bad) != 0ull) {
-    // classify the rare failures: non-finite (EINVAL) vs merely above absmax (ERANGE)
+    // classify the rare failures from the values at hand: non-finite (EINVAL)
+    // vs merely above absmax (ERANGE)
     bool nonfinite = false, range = false;
+#pragma unroll
     for (int j = 0; j < kPerThread / 4; ++j) {
-      const int64_t e = base + j * (kThreads * 4) + t * 4;
+      const int le = j * (kThreads * 4) + t * 4;
+      const float v[4] = {v4[j].x, v4[j].y, v4[j].z, v4[j].w};
+#pragma unroll
       for (int r = 0; r < 4; ++r) {
-        if (e + r >= n) continue;
-        const float a = fabsf(x[e + r]);
+        if (!(FULL || base + le + r < n)) continue;
+        const float a = fabsf(v[r]);
         nonfinite |= !(a <= 3.402823466e38f);
         range |= a > absmax;
       }
@@ -188,8 +194,52 @@ __global__ __launch_bounds__(kThreads) void k_encode(const float* __restrict__ x
     wave_flag(range, &flags[1]);
   }
   __syncthreads();   // lq is rewritten by the next tile
+}
+
+// Persistent workgroups over the full tiles: the next tile's loads are in
+// flight while the current tile is rounded, packed and stored.  The partial
+// last tile, and every tile of an input that is not 16-byte aligned, take the
+// element-wise path.
+template <int B, bool VEC>
+__global__ __launch_bounds__(kThreads) void k_encode(const float* __restrict__ x, int64_t n, float inv_s32,
+                                                     double s, double inv_s, double eps, float absmax,
+                                                     uint32_t* __restrict__ codes, uint64_t nwords,
+                                                     uint32_t* __restrict__ flags) {
+  __shared__ uint32_t lq[kPadded];
+  const int t = threadIdx.x;
+  const int64_t ntiles = (n + kTile - 1) / kTile;
+  const int64_t nfull = VEC ? n / kTile : 0;
+  if (VEC) {
+    float4 cur[kPerThread / 4], nxt[kPerThread / 4];
+    auto load_full = [&](int64_t tl, float4 (&v)[kPerThread / 4]) {
+      const bool ok = tl < nfull;   // uniform: past the end the resource is empty
+      const __amdgpu_buffer_rsrc_t rs = span_rsrc(x + (ok ? tl * (int64_t)kTile : 0), ok ? kTile * 4u : 0u);
 #pragma unroll
-  for (int j = 0; j < kPerThread / 4; ++j) cur[j] = nxt[j];
+      for (int j = 0; j < kPerThread / 4; ++j)
+        v[j] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(
+                                              rs, (uint32_t)(j * (kThreads * 4) + t * 4) * 4u, 0, 0));
+    };
+    int64_t tile = blockIdx.x;
+    load_full(tile, cur);
+    for (; tile < nfull; tile += gridDim.x) {
+      load_full(tile + gridDim.x, nxt);
+      encode_tile<B, true>(cur, tile, n, inv_s32, s, inv_s, eps, absmax, codes, nwords, flags, lq);
+#pragma unroll
+      for (int j = 0; j < kPerThread / 4; ++j) cur[j] = nxt[j];
+    }
+  }
+  for (int64_t tile = nfull + blockIdx.x; tile < ntiles; tile += gridDim.x) {
+    float4 v[kPerThread / 4];
+    const int64_t b0 = tile * (int64_t)kTile;
+#pragma unroll
+    for (int j = 0; j < kPerThread / 4; ++j) {
+      const int64_t e = b0 + j * (kThreads * 4) + t * 4;
+      v[j].x = (e < n) ? x[e] : 0.0f;
+      v[j].y = (e + 1 < n) ? x[e + 1] : 0.0f;
+      v[j].z = (e + 2 < n) ? x[e + 2] : 0.0f;
+      v[j].w = (e + 3 < n) ? x[e + 3] : 0.0f;
+    }
+    encode_tile<B, false>(v, tile, n, inv_s32, s, inv_s, eps, absmax, codes, nwords, flags, lq);
   }
 }
 
@@ -205,14 +255,16 @@ __global__ __launch_bounds__(kThreads) void k_decode(const uint32_t* __restrict_
   const int64_t tile = blockIdx.x;
   const uint64_t w0 = (uint64_t)tile * kWords;
   {
-    // all of this thread's loads in flight before the first LDS store
+    // all of this thread's loads in flight before the first LDS store; words
+    // past the tile's end (and past the stream) read as zero from the bound
     constexpr int kIt = (kWords + 2 + kThreads - 1) / kThreads;
+    const uint64_t avail = nwords > w0 ? nwords - w0 : 0u;
+    const uint32_t nw = (uint32_t)(avail < (uint64_t)(kWords + 2) ? avail : (uint64_t)(kWords + 2));
+    const __amdgpu_buffer_rsrc_t rs = span_rsrc(codes + w0, nw * 4u);
     uint32_t tmp[kIt];
 #pragma unroll
-    for (int i = 0; i < kIt; ++i) {
-      const int w = t + i * kThreads;
-      tmp[i] = (w < kWords + 2 && w0 + w < nwords) ? codes[w0 + w] : 0u;
-    }
+    for (int i = 0; i < kIt; ++i)
+      tmp[i] = (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(rs, (uint32_t)(t + i * kThreads) * 4u, 0, 0);
 #pragma unroll
     for (int i = 0; i < kIt; ++i) {
       const int w = t + i * kThreads;
