@@ -219,6 +219,41 @@ def decide_one(x, i: int, kept_before, tau: float):
     return -1
 
 
+def decide_many(x, samples, kept, tau: float, block: int = 1 << 16):
+    """decide_one for several arrivals at once: for each i in `samples`, the
+    lowest id y in `kept` (ascending ids of the retained set) with y < i and
+    x[y] within delta of x[i], else -1.  The retained rows are visited in
+    ascending blocks, so the first qualifying id found is the lowest; the
+    predicate is decided as in decide_one (binary64 distance, exact integers
+    within 1e-11 of delta^2).  For checking sampled decisions of a stream too
+    large for `greedy`."""
+    x = np.asarray(x, dtype=np.float32)
+    kept = np.asarray(kept, dtype=np.int64)
+    samples = np.asarray(samples, dtype=np.int64)
+    d2f = float(delta2(tau))
+    xs = x[samples].astype(np.float64)
+    sn = np.einsum("ij,ij->i", xs, xs)
+    best = np.full(samples.size, -1, dtype=np.int64)
+    for b0 in range(0, kept.size, block):
+        ids = kept[b0:b0 + block]
+        open_ = (best < 0) & (samples > ids[0])
+        if not open_.any():
+            continue
+        rows = x[ids].astype(np.float64)
+        rn = np.einsum("ij,ij->i", rows, rows)
+        cols = np.nonzero(open_)[0]
+        d2 = rn[:, None] + sn[None, cols] - 2.0 * (rows @ xs[cols].T)
+        for c, sidx in enumerate(cols):
+            i = int(samples[sidx])
+            tol = 1e-11 * max(1.0, 2.0 * float(sn[sidx]))
+            for r in np.nonzero((ids < i) & (d2[:, c] <= d2f + tol))[0].tolist():
+                if d2[r, c] < d2f - 1e-11 * max(1.0, float(sn[sidx] + rn[r])) \
+                        or within(x[i], x[ids[r]], tau):
+                    best[sidx] = int(ids[r])
+                    break
+    return best
+
+
 def deletion_digest(rep) -> str:
     """SHA-256 over the (id, rep) pairs of dropped arrivals, little-endian
     int64, in id order (the deletion-set digest of Section "Determinism")."""

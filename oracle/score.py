@@ -54,3 +54,35 @@ def score_topk(q, codes_rows, ids, eps: float, k: int):
     s = scores(q, codes_rows, eps)
     ts, ti = topk(s, ids, k)
     return ts, ti, bound(q, eps)
+
+
+def score_topk_blocked(q, x_rows, ids, eps: float, k: int, block: int = 1 << 16):
+    """score_topk over a store given by its float32 rows: each block of rows is
+    coded by the Q_eps oracle (oracle.qeps.codes) and scored in binary64, and
+    the per-query best k of all blocks are merged by (score desc, id asc).  The
+    same definition as score_topk(q, codes(x_rows), ...), without holding every
+    code or score at once."""
+    from oracle import qeps
+    q = np.asarray(q, dtype=np.float32)
+    ids = np.asarray(ids, dtype=np.int64)
+    nq = q.shape[0]
+    best_s = np.full((nq, 0), -np.inf)
+    best_i = np.full((nq, 0), -1, dtype=np.int64)
+    for b0 in range(0, ids.size, block):
+        rows = np.asarray(x_rows[b0:b0 + block], dtype=np.float32)
+        c = qeps.codes(rows.reshape(-1), eps).reshape(rows.shape)
+        s = scores(q, c, eps)
+        bs, bi = topk(s, ids[b0:b0 + block], k)
+        best_s = np.concatenate([best_s, bs], axis=1)
+        best_i = np.concatenate([best_i, bi], axis=1)
+        keep = best_i >= 0
+        ms = np.where(keep, best_s, -np.inf)
+        out_s = np.full((nq, k), -np.inf)
+        out_i = np.full((nq, k), -1, dtype=np.int64)
+        for j in range(nq):
+            valid = np.nonzero(keep[j])[0]
+            order = valid[np.lexsort((best_i[j, valid], -ms[j, valid]))][:k]
+            out_s[j, :order.size] = ms[j, order]
+            out_i[j, :order.size] = best_i[j, order]
+        best_s, best_i = out_s, out_i
+    return best_s, best_i, bound(q, eps)

@@ -171,6 +171,54 @@ def online_store(seed: int = 5, n: int = 1 << 20, n_clusters: int = 16384,
                 name=f"online store n={n} D={d} dups={n_dup}")
 
 
+def online_store_device(seed: int = 5, device: str = "cuda", n: int = 1 << 20, n_clusters: int = 16384,
+                        d: int = 1024, dup_frac: float = 0.2, nq: int = 16384):
+    """The online-store recipe of `online_store` drawn on a device with torch's
+    seeded generator (binary64 draws, float32 at the end), for tests at the
+    full 1,048,576 x 1,024 size where drawing on the host takes minutes.  The
+    values differ from `online_store` (another random stream); the recipe,
+    shapes and distributions are the same.  Returns torch tensors on `device`."""
+    import torch
+    g = torch.Generator(device=device)
+    g.manual_seed(seed)
+    f64 = dict(device=device, dtype=torch.float64)
+
+    def normalize(v):
+        return v / torch.linalg.vector_norm(v, dim=1, keepdim=True)
+
+    def members_dev(mu, c):
+        gg = torch.randn(mu.shape, generator=g, **f64)
+        gg -= (gg * mu).sum(dim=1, keepdim=True) * mu
+        u = normalize(gg)
+        c = c.reshape(-1, 1)
+        return normalize(c * mu + torch.sqrt(1.0 - c * c) * u)
+
+    def uniform(lo, hi, m):
+        return lo + (hi - lo) * torch.rand(m, generator=g, **f64)
+
+    n_dup = int(round(dup_frac * n))
+    n_base = n - n_dup
+    sizes = torch.from_numpy(cluster_sizes(n_base, n_clusters)).to(device)
+    cent = normalize(torch.randn((n_clusters, d), generator=g, **f64))
+    labels = torch.repeat_interleave(torch.arange(n_clusters, device=device), sizes)
+    x = torch.empty((n, d), device=device, dtype=torch.float32)
+    chunk = 1 << 16
+    for s in range(0, n_base, chunk):
+        lab = labels[s:s + chunk]
+        x[s:s + lab.numel()] = members_dev(cent[lab], uniform(0.80, 0.999, lab.numel())).float()
+    src = torch.randint(0, n_base, (n_dup,), generator=g, device=device)
+    for s in range(0, n_dup, chunk):
+        rows = x[src[s:s + chunk]].double()
+        # the planted copies start from the float32 base rows
+        x[n_base + s:n_base + s + rows.shape[0]] = members_dev(rows, uniform(0.96, 0.995, rows.shape[0])).float()
+    perm = torch.randperm(n, generator=g, device=device)
+    x = x[perm]
+    pick = torch.randint(0, n_clusters, (nq,), generator=g, device=device)
+    q = members_dev(cent[pick], uniform(0.5, 0.9, nq)).float()
+    return dict(x=x, q=q, tau=0.95, eps=1e-3, k=50, batch=4096,
+                name=f"online store (device draw) n={n} D={d} dups={n_dup}")
+
+
 def near_threshold_pairs(rng: np.random.Generator, n_pairs: int, d: int, tau: float,
                          spread: float = 1e-7):
     """Pairs (a, b) of unit rows whose cosine is tau + U(-spread, spread), to

@@ -215,3 +215,18 @@ def test_decide_one_matches_stream(tiny, tiny_result):
     kept = rep < 0
     for i in (0, 1, 10, 500, 2000, 4095):
         assert dedup.decide_one(x, i, np.nonzero(kept[:i])[0], tau) == rep[i]
+
+
+def test_decide_many_matches_decide_one():
+    """The blocked form gives decide_one's answer for every sampled arrival,
+    including exact ties on the threshold and blocks smaller than the set."""
+    rng = np.random.default_rng(11)
+    a, b, b_in, b_out, tau = synth.dyadic_ties(rng, 40, 64)
+    x = np.concatenate([a, b, b_in, b_out, synth.unit_rows(rng, 120, 64).astype(np.float32)])
+    x = x[rng.permutation(x.shape[0])]
+    ref = dedup.greedy(x, tau)
+    kept = np.nonzero(ref["rep"] < 0)[0]
+    samples = np.arange(x.shape[0])
+    got = dedup.decide_many(x, samples, kept, tau, block=17)
+    one = [dedup.decide_one(x, int(i), kept[kept < i], tau) for i in samples]
+    assert got.tolist() == one == ref["rep"].tolist()

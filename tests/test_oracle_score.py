@@ -91,3 +91,21 @@ def test_dedup_plus_quantization_bound():
     qn = np.linalg.norm(q.astype(np.float64), axis=1)
     assert np.all(gap >= -beta - 1e-12)
     assert np.all(gap <= qn * r["delta_hat"] + beta + 1e-12)
+
+
+def test_blocked_topk_matches_whole_store():
+    """score_topk_blocked over float32 rows equals score_topk over their codes,
+    with ties planted across block boundaries."""
+    rng = np.random.default_rng(4)
+    x = synth.unit_rows(rng, 200, 64).astype(np.float32)
+    x[150] = x[3]            # equal scores in different blocks
+    x[77] = x[40]
+    q = synth.unit_rows(rng, 12, 64).astype(np.float32)
+    q[5] = x[3]
+    eps = 1e-3
+    ids = np.arange(200, dtype=np.int64) * 2 + 1
+    c = qeps.codes(x, eps).reshape(x.shape)
+    for k in (1, 7, 50, 250):
+        ws, wi, wb = score.score_topk(q, c, ids, eps, k)
+        bs, bi, bb = score.score_topk_blocked(q, x, ids, eps, k, block=37)
+        assert np.array_equal(wi, bi) and np.array_equal(ws, bs) and np.array_equal(wb, bb)
