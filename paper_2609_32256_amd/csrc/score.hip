@@ -151,70 +151,72 @@ __device__ __forceinline__ void unpack32(const uint32_t* __restrict__ w, _Float1
 // [rbase, rbase + rows) against the workgroup's 128 queries (wave w holds
 // queries [32w, 32w + 32), lane j % 32, store rows t*32 + acc_row(r, lane)).
 // Codes are unpacked straight into an fp16 LDS slab; queries enter as hi/lo.
+//
+// One LDS stage (codes, hi, lo: 3 x 128 rows of kLdk halves) is refilled
+// between two barriers while the next slab's loads are in flight in
+// registers; loads go through buffer resources (zeros past the tile) so none
+// sits behind a branch.  With one slab in flight, the wait at the top of each
+// step is for all outstanding loads, which is exactly the slab being stored.
+// Ends with a barrier, so the caller may reuse the LDS.
 template <int B>
 __device__ __forceinline__ void score_tile(const ScoreArgs& a, int64_t rbase, int rows, const _Float16* QH,
                                            const _Float16* QL, int qrows, _Float16* lds, floatx16 (&acc)[4]) {
-  auto buf = [&](int i) -> _Float16* { return lds + i * (kTB * kLdk); };  // codes 0/1, hi 2/3, lo 4/5
+  _Float16* sc = lds;
+  _Float16* sh = lds + kTB * kLdk;
+  _Float16* sl = lds + 2 * kTB * kLdk;
   const int wave = threadIdx.x >> 6;
   const int urow = threadIdx.x >> 1, uhalf = threadIdx.x & 1;   // unpack: 2 threads per row
 #pragma unroll
   for (int t = 0; t < 4; ++t)
 #pragma unroll
     for (int r = 0; r < 16; ++r) acc[t][r] = 0.0f;
-  auto load_codes = [&](int k0, uint32_t (&cw)[B]) {
-    if (urow < rows && k0 + 32 * uhalf < a.D) {
-      const uint32_t* src = a.codes + (rbase + urow) * a.row_words + (int64_t)(k0 / 32 + uhalf) * B;
+  const __amdgpu_buffer_rsrc_t rsC = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint32_t*>(a.codes + rbase * a.row_words), (short)0, (int)(rows * a.row_words * 4), 0x00020000);
+  const __amdgpu_buffer_rsrc_t rsH = tile_rsrc(QH, qrows, a.D), rsL = tile_rsrc(QL, qrows, a.D);
+  auto load_slab = [&](int k0, uint32_t (&cw)[B], uint4 (&rh)[4], uint4 (&rl)[4]) {
+    const bool ok = urow < rows && k0 + 32 * uhalf < a.D;
+    const uint32_t w0 = (uint32_t)(urow * a.row_words + (int64_t)(k0 / 32 + uhalf) * B);
 #pragma unroll
-      for (int i = 0; i < B; ++i) cw[i] = src[i];
-    } else {
-#pragma unroll
-      for (int i = 0; i < B; ++i) cw[i] = 0u;
-    }
+    for (int i = 0; i < B; ++i)
+      cw[i] = (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(rsC, ok ? (w0 + i) * 4u : kOffOOB, 0, 0);
+    slab_load_n<4>(rsH, qrows, a.D, k0, a.D, rh, kWG);
+    slab_load_n<4>(rsL, qrows, a.D, k0, a.D, rl, kWG);
   };
-  auto store_codes = [&](_Float16* s, const uint32_t (&cw)[B]) {
-    _Float16 h[32];
-    unpack32<B>(cw, h);
-    _Float16* dst = s + urow * kLdk + uhalf * 32;
-#pragma unroll
-    for (int i = 0; i < 32; i += 8) *reinterpret_cast<uint4*>(dst + i) = *reinterpret_cast<const uint4*>(h + i);
-  };
-  uint32_t cw[B];
-  SlabRegs rh, rl;
-  load_codes(0, cw);
-  slab_load(QH, qrows, a.D, 0, a.D, rh);
-  slab_load(QL, qrows, a.D, 0, a.D, rl);
-  store_codes(buf(0), cw);
-  slab_store(buf(2), rh);
-  slab_store(buf(4), rl);
-  __syncthreads();
-  int cur = 0;
-  for (int k0 = 0; k0 < a.D; k0 += kBK) {
-    const bool more = k0 + kBK < a.D;
-    if (more) {
-      load_codes(k0 + kBK, cw);
-      slab_load(QH, qrows, a.D, k0 + kBK, a.D, rh);
-      slab_load(QL, qrows, a.D, k0 + kBK, a.D, rl);
-    }
+  auto compute = [&]() {
 #pragma unroll
     for (int kk = 0; kk < kBK / 16; ++kk) {
-      const half8 bh = frag_load(buf(2 + cur), wave * 32, kk);
-      const half8 bl = frag_load(buf(4 + cur), wave * 32, kk);
+      const half8 bh = frag_load(sh, wave * 32, kk);
+      const half8 bl = frag_load(sl, wave * 32, kk);
       half8 fa[4];
 #pragma unroll
-      for (int t = 0; t < 4; ++t) fa[t] = frag_load(buf(cur), t * 32, kk);
+      for (int t = 0; t < 4; ++t) fa[t] = frag_load(sc, t * 32, kk);
 #pragma unroll
       for (int t = 0; t < 4; ++t) acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fa[t], bh, acc[t], 0, 0, 0);
 #pragma unroll
       for (int t = 0; t < 4; ++t) acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fa[t], bl, acc[t], 0, 0, 0);
     }
-    if (more) {
-      store_codes(buf(cur ^ 1), cw);
-      slab_store(buf(2 + (cur ^ 1)), rh);
-      slab_store(buf(4 + (cur ^ 1)), rl);
+  };
+  const int S = (a.D + kBK - 1) / kBK;
+  uint32_t cw[B];
+  uint4 rh[4], rl[4];
+  load_slab(0, cw, rh, rl);
+  for (int s = 0; s < S; ++s) {
+    __syncthreads();   // every wave is done with the previous slab (or tile)
+    {
+      _Float16 h[32];
+      unpack32<B>(cw, h);
+      _Float16* dst = sc + urow * kLdk + uhalf * 32;
+#pragma unroll
+      for (int i = 0; i < 32; i += 8) *reinterpret_cast<uint4*>(dst + i) = *reinterpret_cast<const uint4*>(h + i);
     }
+    slab_store_n<4>(sh, rh, kWG);
+    slab_store_n<4>(sl, rl, kWG);
     __syncthreads();
-    cur ^= 1;
+    load_slab((s + 1) * kBK, cw, rh, rl);   // past the last slab: zeros, no memory touched
+    __builtin_amdgcn_sched_barrier(0);      // issue the loads before the MFMAs
+    compute();
   }
+  __syncthreads();
 }
 
 enum { kModeLists = 0, kModeFilter = 1, kModeFallback = 2 };
@@ -224,8 +226,10 @@ enum { kModeLists = 0, kModeFilter = 1, kModeFallback = 2 };
 // only runs query tiles flagged in tflag.  MODE kModeFilter: every score at or
 // above the query's threshold is appended to its candidate buffer.
 template <int B, int KL, int MODE>
-__global__ __launch_bounds__(kWG) void k_score(ScoreArgs a) {
-  __shared__ _Float16 lds[6 * kTB * kLdk];
+__global__ __launch_bounds__(kWG, 2) void k_score(ScoreArgs a) {
+  // one slab stage (3 x 128 rows) or the list epilogue's 4 x 64 x 64 scores
+  constexpr int kLdsHalves = (3 * kTB * kLdk > 2 * 4 * 64 * 64) ? 3 * kTB * kLdk : 2 * 4 * 64 * 64;
+  __shared__ __attribute__((aligned(16))) _Float16 lds[kLdsHalves];
   const int qt = blockIdx.x % a.nqt;
   const int split = blockIdx.x / a.nqt;
   if (MODE == kModeFallback && a.tflag[qt] == 0u) return;
@@ -284,7 +288,7 @@ __global__ __launch_bounds__(kWG) void k_score(ScoreArgs a) {
             }
           }
       }
-      // no LDS use here: the K loop's last barrier already protects the slabs
+      // no LDS use here: score_tile's barriers protect the slabs
     } else {
     const bool hot = mx >= ls[KL - 1];
     if (__ballot(hot) != 0ull) {
