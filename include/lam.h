@@ -221,6 +221,47 @@ lam_status lam_store_export(lam_ctx* ctx, const lam_store* store, int64_t* ids_d
 lam_status lam_score_topk(lam_ctx* ctx, const lam_store* store, const float* q_dev, int64_t nq,
                           int32_t k, float* scores_dev, int64_t* ids_dev, float* bound_dev);
 
+/* Top-k with the rank-invariance certificate (Appendix "Rank invariance, in
+ * full"): as lam_score_topk (1 <= k <= 63), plus per query certified_dev[j] = 1
+ * when the float32 margin m_j = s_k - s_{k+1} between ranks k and k+1 exceeds
+ *   2 (beta_j + ||q_j||_2 delta_hat + e_j),
+ * beta_j = eps ||q_j||_1, delta_hat the store's measured bound, and e_j =
+ * kappa ||q_j||_1 (A + eps) a bound on the float32 score's error (A the store's
+ * absmax, kappa = 1.01 (2^-22 + gamma_2D + 2^-23)).  A flag implies that the
+ * exact margin exceeds 2 (beta_j + ||q_j||_2 delta_hat), so no record crosses
+ * the rank-k boundary when every score moves by the substitution and
+ * quantization bounds.  A store with at most k rows certifies every valid
+ * query; a NaN/Inf query row is never certified.  margin_dev (optional): m_j
+ * (+inf past the store size, NaN for an invalid query).  Asynchronous. */
+lam_status lam_score_topk_certified(lam_ctx* ctx, const lam_store* store, const float* q_dev, int64_t nq,
+                                    int32_t k, float* scores_dev, int64_t* ids_dev, float* bound_dev,
+                                    uint8_t* certified_dev, float* margin_dev);
+
+/* ------------------------------------------------------------------ removal ceiling */
+
+typedef struct lam_ceiling_stats {
+  int64_t n;               /* arrivals                                               */
+  int64_t kept;            /* |R(delta)|: greedy at tau                               */
+  int64_t kept_2delta;     /* |R(2 delta)|: greedy at tau' = 4 tau - 3                */
+  double tau, tau_2delta;
+  double removal;          /* attained: 1 - kept / n                                  */
+  double ceiling;          /* 1 - kept_2delta / n, an upper bound on the removal of
+                              any delta-bounded compactor of this stream             */
+  double frac_of_ceiling;  /* removal / ceiling (0 when the ceiling is 0)             */
+  double bits_lo, bits_hi; /* log2 kept_2delta <= H_delta(S) <= log2 kept             */
+  double delta_hat, delta_hat_2delta;   /* measured bounds of the two passes          */
+} lam_ceiling_stats;
+
+/* Theorem "removal ceiling" and Corollary "measured bracket": greedy
+ * first-occurrence over x_dev (n rows of dim float32, arrival order, the same
+ * input contract as lam_dedup_ingest) at radius delta = sqrt(2 - 2 tau) and at
+ * radius 2 delta (threshold 4 tau - 3, exact in binary64), in batches of
+ * `batch`, on two temporary stores of capacity n that the call frees.
+ * Synchronous.  EINVAL: tau outside (1/2, 1], n < 1, batch < 1, or invalid rows
+ * (as lam_dedup_ingest); ENOMEM if the two stores do not fit. */
+lam_status lam_removal_ceiling(lam_ctx* ctx, const float* x_dev, int64_t n, int32_t dim, double tau,
+                               int64_t batch, lam_ceiling_stats* out);
+
 #ifdef __cplusplus
 }
 #endif

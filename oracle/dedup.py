@@ -254,6 +254,24 @@ def decide_many(x, samples, kept, tau: float, block: int = 1 << 16):
     return best
 
 
+def removal_ceiling(x, tau: float):
+    """Theorem "removal ceiling" and Corollary "measured bracket": greedy at
+    radius delta (tau) and at radius 2 delta (tau' = 4 tau - 3; exact in
+    binary64 for tau in [1/2, 1]).  Returns the counts, the attained removal
+    1 - |R(delta)|/n, the ceiling 1 - |R(2 delta)|/n and the bracket
+    (log2 |R(2 delta)|, log2 |R(delta)|)."""
+    tau2 = 4.0 * tau - 3.0
+    assert Fraction(tau2) == 4 * Fraction(tau) - 3
+    n = np.asarray(x).shape[0]
+    r1 = greedy(x, tau)
+    r2 = greedy(x, tau2)
+    k1 = int(np.count_nonzero(r1["rep"] < 0))
+    k2 = int(np.count_nonzero(r2["rep"] < 0))
+    return dict(n=n, kept=k1, kept_2delta=k2, tau=tau, tau_2delta=tau2, removal=1.0 - k1 / n,
+                ceiling=1.0 - k2 / n, bits_lo=math.log2(k2), bits_hi=math.log2(k1),
+                kept_ids=r1["kept"], kept_ids_2delta=r2["kept"])
+
+
 def deletion_digest(rep) -> str:
     """SHA-256 over the (id, rep) pairs of dropped arrivals, little-endian
     int64, in id order (the deletion-set digest of Section "Determinism")."""

@@ -86,3 +86,17 @@ def score_topk_blocked(q, x_rows, ids, eps: float, k: int, block: int = 1 << 16)
             out_i[j, :order.size] = best_i[j, order]
         best_s, best_i = out_s, out_i
     return best_s, best_i, bound(q, eps)
+
+
+def certify(q, codes_rows, ids, eps: float, k: int, delta_hat: float):
+    """Rank-invariance certificate (Appendix "Rank invariance, in full") on the
+    exact dequantized scores: query j's top-k cannot change when every score
+    moves by at most beta_j + ||q_j||_2 delta_hat iff the margin between ranks
+    k and k+1 exceeds twice that (a store with at most k records always
+    qualifies).  Returns (flags bool[nq], margins float64[nq], thresholds)."""
+    s = scores(q, codes_rows, eps)
+    ts, _ = topk(s, ids, k + 1)
+    q64 = np.asarray(q, dtype=np.float32).astype(np.float64)
+    thr = 2.0 * (bound(q, eps) + np.sqrt(np.sum(q64 * q64, axis=1)) * float(delta_hat))
+    margin = np.where(np.isfinite(ts[:, k]), ts[:, k - 1] - ts[:, k], np.inf)
+    return margin > thr, margin, thr

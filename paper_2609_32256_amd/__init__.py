@@ -68,6 +68,16 @@ class StoreInfo(ctypes.Structure):
 
 _P = ctypes.c_void_p
 _I64 = ctypes.c_int64
+class CeilingStats(ctypes.Structure):
+    _fields_ = [("n", _I64), ("kept", _I64), ("kept_2delta", _I64), ("tau", ctypes.c_double),
+                ("tau_2delta", ctypes.c_double), ("removal", ctypes.c_double), ("ceiling", ctypes.c_double),
+                ("frac_of_ceiling", ctypes.c_double), ("bits_lo", ctypes.c_double), ("bits_hi", ctypes.c_double),
+                ("delta_hat", ctypes.c_double), ("delta_hat_2delta", ctypes.c_double)]
+
+    def as_dict(self):
+        return {f: getattr(self, f) for f, _ in self._fields_}
+
+
 _SIGS = {
     "lam_abi_version": ([], ctypes.c_int),
     "lam_status_name": ([ctypes.c_int], ctypes.c_char_p),
@@ -93,6 +103,9 @@ _SIGS = {
     "lam_store_clear": ([_P, _P], ctypes.c_int),
     "lam_store_dequantize": ([_P, _P, _P], ctypes.c_int),
     "lam_store_export": ([_P, _P, _P, _P, ctypes.c_uint64], ctypes.c_int),
+    "lam_score_topk_certified": ([_P, _P, _P, _I64, ctypes.c_int32, _P, _P, _P, _P, _P], ctypes.c_int),
+    "lam_removal_ceiling": ([_P, _P, _I64, ctypes.c_int32, ctypes.c_double, _I64, ctypes.POINTER(CeilingStats)],
+                            ctypes.c_int),
     "lam_score_topk": ([_P, _P, _P, _I64, ctypes.c_int32, _P, _P, _P], ctypes.c_int),
 }
 for _name, (_args, _res) in _SIGS.items():
@@ -110,6 +123,21 @@ def _check(status: int):
 
 def abi_version() -> int:
     return _lib.lam_abi_version()
+
+
+def removal_ceiling(x: torch.Tensor, tau: float, batch: int = 4096, ctx: Context | None = None) -> dict:
+    """Theorem "removal ceiling" / Corollary "measured bracket": greedy over the
+    rows of x at tau and at 4 tau - 3 (radius 2 delta).  Returns the counts,
+    the attained removal, the ceiling and the bracket log2|R(2 delta)| <=
+    H_delta <= log2|R(delta)|."""
+    ctx = ctx or default_context()
+    x = _dev_tensor(x, torch.float32, "x")
+    if x.dim() != 2:
+        raise ValueError("x must be (n, dim)")
+    out = CeilingStats()
+    _check(_lib.lam_removal_ceiling(ctx.handle, _ptr(x), x.shape[0], x.shape[1], float(tau), int(batch),
+                                    ctypes.byref(out)))
+    return out.as_dict()
 
 
 def qeps_plan(eps: float, absmax: float, mode: str = "bits", n: int = 0) -> QParams:
@@ -292,6 +320,23 @@ class Store:
         _check(_lib.lam_store_export(self.ctx.handle, self._h, _P(None), _ptr(out), out.numel() * 4))
         return out[: p.code_bytes // 4]
 
+    def score_topk_certified(self, q: torch.Tensor, k: int):
+        """Top-k plus the rank-invariance certificate: (scores, ids, bound,
+        certified bool[nq], margin float32[nq]); see lam_score_topk_certified."""
+        q = _dev_tensor(q, torch.float32, "q")
+        if q.dim() != 2 or q.shape[1] != self.dim:
+            raise ValueError(f"q must be (nq, {self.dim})")
+        nq = q.shape[0]
+        dev = q.device
+        scores = torch.empty((nq, k), dtype=torch.float32, device=dev)
+        ids = torch.empty((nq, k), dtype=torch.int64, device=dev)
+        bound = torch.empty(nq, dtype=torch.float32, device=dev)
+        cert = torch.empty(nq, dtype=torch.uint8, device=dev)
+        margin = torch.empty(nq, dtype=torch.float32, device=dev)
+        _check(_lib.lam_score_topk_certified(self.ctx.handle, self._h, _ptr(q), nq, int(k), _ptr(scores), _ptr(ids),
+                                             _ptr(bound), _ptr(cert), _ptr(margin)))
+        return scores, ids, bound, cert.bool(), margin
+
     def score_topk(self, q: torch.Tensor, k: int, out=None):
         """Top-k (scores float32[nq, k], ids int64[nq, k], bound float32[nq])."""
         q = _dev_tensor(q, torch.float32, "q")
@@ -319,4 +364,4 @@ class Store:
 
 
 __all__ = ["LamError", "QParams", "IngestStats", "StoreInfo", "Context", "default_context", "quantize",
-           "dequantize", "Store", "qeps_plan", "abi_version", "EXPORTED", "LIB_PATH"]
+           "dequantize", "Store", "qeps_plan", "removal_ceiling", "CeilingStats", "abi_version", "EXPORTED", "LIB_PATH"]

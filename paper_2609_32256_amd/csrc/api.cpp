@@ -430,4 +430,23 @@ lam_status lam_score_topk(lam_ctx* ctx, const lam_store* st, const float* q_dev,
   return score_topk(ctx, st, q_dev, nq, k, scores_dev, ids_dev, bound_dev);
 }
 
+lam_status lam_score_topk_certified(lam_ctx* ctx, const lam_store* st, const float* q_dev, int64_t nq, int32_t k,
+                                    float* scores_dev, int64_t* ids_dev, float* bound_dev, uint8_t* certified_dev,
+                                    float* margin_dev) {
+  LAM_CHECK(ctx != nullptr && st != nullptr, LAM_EINVAL, "ctx or store is NULL");
+  LAM_CHECK(nq >= 0, LAM_EINVAL, "nq must be >= 0");
+  LAM_CHECK(k >= 1 && k <= 63, LAM_EINVAL, "k must be in [1, 63]");
+  LAM_CHECK((q_dev != nullptr && scores_dev != nullptr && ids_dev != nullptr && certified_dev != nullptr) || nq == 0,
+            LAM_EINVAL, "NULL buffer");
+  LAM_CHECK(((uintptr_t)q_dev & 15u) == 0, LAM_EINVAL, "q must be 16-byte aligned");
+  {
+    DeviceGuard g(ctx->device);
+    LAM_TRY(store_settle(const_cast<lam_store*>(st)));
+  }
+  LAM_CHECK(st->codes != nullptr && st->coded_rows == st->size, LAM_ESTATE,
+            "store must be quantized (lam_store_quantize) after its last ingest");
+  DeviceGuard g(ctx->device);
+  return score_certify(ctx, st, q_dev, nq, k, scores_dev, ids_dev, bound_dev, certified_dev, margin_dev);
+}
+
 }  // extern "C"

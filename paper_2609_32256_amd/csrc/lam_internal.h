@@ -45,6 +45,12 @@ struct Status {
   } while (0)
 
 // ------------------------------------------------------------------ device buffer
+// Context scratch slots: 0-6 ingest (dedup.hip), 7-11 scoring (score.hip),
+// then the ones below.
+constexpr int kScratchCeilingRep = 12;   // representatives of the ceiling passes (not returned)
+constexpr int kScratchCertify = 13;      // top-(k+1) lists of the certified scoring
+constexpr int kScratchSlots = 14;
+
 struct DevBuf {
   void* p = nullptr;
   size_t bytes = 0;
@@ -59,9 +65,9 @@ struct DevFlags {
   uint32_t nonfinite;      // NaN/Inf seen in an input
   uint32_t out_of_range;   // |x| > declared absmax, or |x| >= 256 for the screen
   uint32_t absmax_bits;    // max |x| as float bits (measured absmax)
-  uint32_t pair_overflow;  // bit 0: ambiguous-pair list overflowed; bit 1: a pair needs the exact host test
+  uint32_t pair_overflow;  // bit 0: ambiguous-pair list overflowed
   uint32_t n_pairs;        // ambiguous pairs found
-  uint32_t n_escalate;     // pairs decided by the exact host test
+  uint32_t n_escalate;     // pairs decided on exact integers
   uint32_t n_kept;         // arrivals retained by this ingest
   uint32_t pairs_needed;   // pair-list capacity that would have sufficed
   unsigned long long dhat2_bits;  // max merged d^2 (binary64 bits, non-negative)
@@ -85,7 +91,7 @@ struct lam_ctx {
   lam::DevFlags* flags_host_dev = nullptr;  // its device-side address (kernels write it directly)
   bool flags_zero = false;              // flags_dev known to hold zeros
   // scratch arena, grown on demand
-  lam::DevBuf scratch[12];
+  lam::DevBuf scratch[lam::kScratchSlots];
   // profiling
   uint32_t pair_cap = 1u << 20;         // ambiguous-pair list capacity (grows on overflow)
   bool profiling = false;
@@ -158,6 +164,8 @@ void store_free(lam_store* st);
 // ------------------------------------------------------------------ scoring (score.hip)
 lam_status score_topk(lam_ctx* ctx, const lam_store* st, const float* q, int64_t nq, int32_t k,
                       float* scores, int64_t* ids, float* bound);
+lam_status score_certify(lam_ctx* ctx, const lam_store* st, const float* q, int64_t nq, int32_t k, float* scores,
+                         int64_t* ids, float* bound, uint8_t* certified, float* margin);
 
 // ------------------------------------------------------------------ exact host predicate (exact.cpp)
 // sum_d (a_d - b_d)^2 <= 2 - 2 tau on exact reals, float32 rows a, b of length d.

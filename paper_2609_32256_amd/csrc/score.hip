@@ -635,4 +635,78 @@ lam_status score_topk(lam_ctx* ctx, const lam_store* st, const float* q, int64_t
   return LAM_OK;
 }
 
+// ------------------------------------------------------------------ certificate
+namespace {
+
+// Rank-invariance certificate (Appendix "Rank invariance, in full"): one wave
+// per query copies the first k of its top-(k+1) and flags the query when the
+// float32 margin between ranks k and k+1 exceeds
+//   2 (beta + ||q||_2 delta_hat + e),   e = kappa ||q||_1 (A + eps),
+// where e bounds the float32 score's error against the exact dequantized score
+// (hi/lo residual 2^-22, float32 accumulation of 2 D terms gamma_2D, output
+// scaling 2^-23, all relative to sum |q_d x_hat_d| <= ||q||_1 (A + eps)).  A
+// flag therefore implies that the exact margin exceeds 2 (beta + ||q||_2
+// delta_hat): no record can cross the rank-k boundary when every score moves
+// by at most beta + ||q||_2 delta_hat.  A store with at most k rows certifies
+// every valid query (nothing can cross).
+__global__ __launch_bounds__(256) void k_certify(int64_t nq, int k, const float* __restrict__ s1,
+                                                 const int64_t* __restrict__ i1, const float* __restrict__ b1,
+                                                 const float* __restrict__ q, int D, double eps, double dhat,
+                                                 double err_per_l1, float* __restrict__ scores,
+                                                 int64_t* __restrict__ ids, float* __restrict__ bound,
+                                                 uint8_t* __restrict__ cert, float* __restrict__ margin) {
+  const int lane = threadIdx.x & 63;
+  const int64_t j = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (j >= nq) return;
+  const float* p = q + j * D;
+  double l1 = 0.0, l2 = 0.0;
+  for (int d = lane; d < D; d += 64) {
+    const double v = (double)p[d];
+    l1 += fabs(v);
+    l2 = fma(v, v, l2);
+  }
+  for (int o = 32; o > 0; o >>= 1) {
+    l1 += __shfl_xor(l1, o);
+    l2 += __shfl_xor(l2, o);
+  }
+  const int64_t o1 = j * (k + 1);
+  for (int t = lane; t < k; t += 64) {
+    scores[j * k + t] = s1[o1 + t];
+    ids[j * k + t] = i1[o1 + t];
+  }
+  if (lane != 0) return;
+  if (bound) bound[j] = b1[j];
+  const float sk = s1[o1 + k - 1], sk1 = s1[o1 + k];
+  const bool valid = !isnan(b1[j]);   // NaN bound: the query row holds NaN/Inf
+  const double m = (i1[o1 + k] < 0) ? INFINITY : (double)sk - (double)sk1;
+  // (1 + 2^-50) rounds the threshold up past its own evaluation error
+  const double thr = 2.0 * (eps * l1 + sqrt(l2) * dhat + err_per_l1 * l1) * (1.0 + 0x1p-50);
+  cert[j] = (valid && m > thr) ? 1 : 0;
+  if (margin) margin[j] = valid ? (float)m : __builtin_nanf("");
+}
+
+}  // namespace
+
+lam_status score_certify(lam_ctx* ctx, const lam_store* st, const float* q, int64_t nq, int32_t k, float* scores,
+                         int64_t* ids, float* bound, uint8_t* certified, float* margin) {
+  if (nq == 0) return LAM_OK;
+  const int K1 = k + 1;
+  const size_t per = (size_t)K1 * (4 + 8);
+  LAM_TRY(ctx->scratch[kScratchCertify].ensure((size_t)nq * per + (size_t)nq * 4 + 64));
+  char* base = ctx->scratch[kScratchCertify].as<char>();
+  int64_t* i1 = reinterpret_cast<int64_t*>(base);
+  float* s1 = reinterpret_cast<float*>(base + (size_t)nq * K1 * 8);
+  float* b1 = s1 + (size_t)nq * K1;
+  LAM_TRY(score_topk(ctx, st, q, nq, K1, s1, i1, b1));
+  // error bound of the float32 score per unit of ||q||_1: kappa (A + eps)
+  const double u = std::ldexp(1.0, -24);
+  const double g2d = 2.0 * st->dim * u / (1.0 - 2.0 * st->dim * u);
+  const double kappa = 1.01 * (std::ldexp(1.0, -22) + g2d + std::ldexp(1.0, -23));
+  const double err_per_l1 = kappa * ((double)st->q.absmax + st->q.eps);
+  hipLaunchKernelGGL(k_certify, dim3((unsigned)((nq + 3) / 4)), dim3(256), 0, ctx->stream, nq, k, s1, i1, b1, q,
+                     st->dim, st->q.eps, st->delta_hat_run, err_per_l1, scores, ids, bound, certified, margin);
+  LAM_HIP(hipGetLastError());
+  return LAM_OK;
+}
+
 }  // namespace lam

@@ -247,3 +247,27 @@ def test_async_invalid_input_reported_later(lam):
     assert info.n_seen == 600 and info.size == int(np.count_nonzero(ref["rep"] < 0))
     assert np.array_equal(torch.cat([r1, r3]).cpu().numpy(), ref["rep"])
     assert (rb.cpu().numpy() == -7).all()
+
+
+@pytest.mark.parametrize("tau", [0.95, 0.99])
+def test_removal_ceiling_subset(lam, tau):
+    """Theorem "removal ceiling" on the subset stream: both greedy passes
+    (tau and 4 tau - 3) match the oracle's counts exactly."""
+    x = synth.subset_ingest()["x"]
+    ref = dedup.removal_ceiling(x, tau)
+    got = lam.removal_ceiling(_dev(x), tau, batch=1024)
+    for key in ("n", "kept", "kept_2delta", "tau_2delta", "removal", "ceiling", "bits_lo", "bits_hi"):
+        assert got[key] == ref[key], key
+    assert got["delta_hat"] <= dedup.delta(tau) and got["delta_hat_2delta"] <= 2 * dedup.delta(tau)
+    print(f"tau={tau}: removal {got['removal']:.4f} ceiling {got['ceiling']:.4f} "
+          f"({got['frac_of_ceiling']:.3f} of it), bits [{got['bits_lo']:.3f}, {got['bits_hi']:.3f}]")
+
+
+def test_removal_ceiling_errors(lam):
+    x = _dev(np.eye(64, dtype=np.float32)[:10])
+    for tau in (0.5, 1.5, float("nan")):
+        with pytest.raises(lam.LamError) as e:
+            lam.removal_ceiling(x, tau)
+        assert e.value.name == "LAM_EINVAL"
+    r = lam.removal_ceiling(x, 0.6, batch=3)
+    assert (r["kept"], r["kept_2delta"]) == (10, 1)

@@ -167,3 +167,57 @@ def test_two_pass_and_overflow_fallback(lam, k):
     c = qeps.codes(x, 1e-3).reshape(n, -1)
     keep = [j for j in range(q.shape[0]) if j not in (3, 17)]
     _compare(gs[keep], gi[keep], c, np.arange(n), q[keep], 1e-3, k)
+
+
+def test_rank_invariance_certificate(lam):
+    """Certified queries have an exact margin above 2 (beta + ||q|| delta_hat)
+    (soundness); queries whose exact margin clears that by more than the
+    float32 error bound are certified; the top-k equals lam_score_topk's."""
+    import torch
+    rng = np.random.default_rng(21)
+    d, n = 768, 3000
+    x = synth.unit_rows(rng, n, d).astype(np.float32)
+    x[1500:1600] = synth.near_dups(rng, x[:100].astype(np.float64)).astype(np.float32)
+    tau, eps = 0.95, 1e-3
+    s = lam.Store(d, tau, n)
+    s.ingest(_dev(x))
+    info = s.info()
+    p = s.quantize(eps)
+    kept = s.ids().cpu().numpy()
+    codes = qeps.codes(x[kept], eps).reshape(kept.size, d)
+    q = np.concatenate([synth.unit_rows(rng, 40, d).astype(np.float32), x[kept[rng.choice(kept.size, 24)]]])
+    qd = _dev(q)
+    u = 2.0 ** -24
+    kappa = 1.01 * (2.0 ** -22 + 2 * d * u / (1 - 2 * d * u) + 2.0 ** -23)
+    e = kappa * np.abs(q.astype(np.float64)).sum(axis=1) * (p.absmax + eps)
+    n_cert = 0
+    for k in (1, 5, 20):
+        gs, gi, gb, gc, gm = s.score_topk_certified(qd, k)
+        ps, pi, pb = s.score_topk(qd, k)
+        assert torch.equal(gi, pi) and torch.equal(gs, ps) and torch.equal(gb, pb)
+        flags, margin, thr = score.certify(q, codes, kept, eps, k, info.delta_hat_run)
+        gc = gc.cpu().numpy()
+        assert np.all(margin[gc] > thr[gc])                         # sound
+        assert np.all(gc[margin > thr + 2 * e + 4 * TOL])           # complete away from the error band
+        gmn = gm.cpu().numpy().astype(np.float64)
+        fin = np.isfinite(margin)
+        assert np.all(np.abs(gmn[fin] - margin[fin]) <= 2 * TOL)
+        n_cert += int(gc.sum())
+    assert 0 < n_cert < 3 * q.shape[0]
+
+
+def test_certificate_small_store_and_invalid_rows(lam):
+    import torch
+    rng = np.random.default_rng(22)
+    x = synth.unit_rows(rng, 3, 64).astype(np.float32)
+    s = lam.Store(64, 1.0, 8)
+    s.ingest(_dev(x))
+    s.quantize(1e-3)
+    q = synth.unit_rows(rng, 4, 64).astype(np.float32)
+    q[2, 5] = np.nan
+    _, gi, gb, gc, gm = s.score_topk_certified(_dev(q), 3)
+    assert gc.cpu().tolist() == [True, True, False, True]
+    assert torch.isinf(gm[[0, 1, 3]]).all() and torch.isnan(gm[2])
+    for k in (0, 64):
+        with pytest.raises(lam.LamError):
+            s.score_topk_certified(_dev(q), k)

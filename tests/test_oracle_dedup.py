@@ -230,3 +230,36 @@ def test_decide_many_matches_decide_one():
     got = dedup.decide_many(x, samples, kept, tau, block=17)
     one = [dedup.decide_one(x, int(i), kept[kept < i], tau) for i in samples]
     assert got.tolist() == one == ref["rep"].tolist()
+
+
+def test_removal_ceiling_closed_forms():
+    """Orthonormal rows are sqrt(2) apart: at tau = 0.95 (2 delta = 0.63)
+    nothing merges in either pass; at tau = 0.6 (delta = 0.89 < sqrt(2) < 2
+    delta = 1.79) nothing merges at delta and everything merges into the
+    first row at 2 delta.  Identical rows merge at any radius."""
+    e = np.eye(64, dtype=np.float32)[:40]
+    r = dedup.removal_ceiling(e, 0.95)
+    assert (r["kept"], r["kept_2delta"], r["removal"], r["ceiling"]) == (40, 40, 0.0, 0.0)
+    r = dedup.removal_ceiling(e, 0.6)
+    assert (r["kept"], r["kept_2delta"]) == (40, 1)
+    assert r["ceiling"] == 1 - 1 / 40 and r["bits_lo"] == 0.0 and r["bits_hi"] == math.log2(40)
+    same = np.repeat(e[:1], 9, axis=0)
+    r = dedup.removal_ceiling(same, 0.99)
+    assert (r["kept"], r["kept_2delta"]) == (1, 1)
+
+
+def test_removal_ceiling_packing_and_order():
+    """Theorem "removal ceiling": the 2 delta pass returns a 2 delta-packing
+    (every pair of its survivors is more than 2 delta apart, brute force), no
+    larger than the delta pass, so the ceiling bounds the attained removal."""
+    t = synth.tiny_ingest()
+    x = t["x"][:700]
+    for tau in (0.95, 0.9, 0.75):
+        r = dedup.removal_ceiling(x, tau)
+        p = x[r["kept_ids_2delta"]].astype(np.float64)
+        nn = np.einsum("ij,ij->i", p, p)
+        d2 = nn[:, None] + nn[None, :] - 2.0 * (p @ p.T)   # binary64, error ~1e-13
+        iu = np.triu_indices(p.shape[0], 1)
+        assert np.all(d2[iu] > 4 * float(dedup.delta2(tau)) - 1e-9)
+        assert r["kept_2delta"] <= r["kept"] and r["ceiling"] >= r["removal"]
+        assert r["bits_lo"] <= r["bits_hi"]

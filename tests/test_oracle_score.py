@@ -109,3 +109,27 @@ def test_blocked_topk_matches_whole_store():
         ws, wi, wb = score.score_topk(q, c, ids, eps, k)
         bs, bi, bb = score.score_topk_blocked(q, x, ids, eps, k, block=37)
         assert np.array_equal(wi, bi) and np.array_equal(ws, bs) and np.array_equal(wb, bb)
+
+
+def test_certify_closed_forms():
+    """A query equal to one stored row, the others orthogonal to it, has margin
+    |q|^2 - 0 at k = 1: certified for small eps and delta_hat, not once
+    delta_hat exceeds half the margin.  A duplicated best row has margin 0
+    (never certified at k = 1); a store of at most k rows always qualifies."""
+    d = 64
+    x = np.eye(d, dtype=np.float32)[:10] * np.float32(0.5)
+    ids = np.arange(10, dtype=np.int64)
+    eps = 2.0 ** -10                       # dyadic: codes are exact, scores exact
+    c = qeps.codes(x, eps).reshape(x.shape)
+    q = np.zeros((1, d), np.float32)
+    q[0, 3] = 1.0
+    f, m, t = score.certify(q, c, ids, eps, 1, 0.0)
+    assert f[0] and m[0] == 0.5 and t[0] == 2 * eps
+    f, m, t = score.certify(q, c, ids, eps, 1, 0.25)
+    assert not f[0] and t[0] == 2 * (eps + 0.25)
+    x2 = np.concatenate([x, x[3:4]])
+    c2 = qeps.codes(x2, eps).reshape(x2.shape)
+    f, m, _ = score.certify(q, c2, np.arange(11), eps, 1, 0.0)
+    assert not f[0] and m[0] == 0.0
+    f, m, _ = score.certify(q, c[:3], ids[:3], eps, 3, 10.0)
+    assert f[0] and m[0] == np.inf
