@@ -245,6 +245,14 @@ def main():
         roofline = {"kernel": dominant, "bound": "latency", "achieved": None, "peak": None, "unit": None,
                     "frac": None, "traffic": None}
 
+    # beside the timed step (not in it): the removal ceiling of the stream and
+    # the share of benchmark queries whose top-10 is certified rank-invariant
+    ceil = lam.removal_ceiling(xd, TAU, batch=BATCH, ctx=ctx)
+    cert = store.score_topk_certified(qd, TOPK)[3]
+    extras = {"removal_ceiling": {k: ceil[k] for k in ("kept", "kept_2delta", "removal", "ceiling",
+                                                         "frac_of_ceiling", "bits_lo", "bits_hi")},
+              "certified_top10_frac": float(cert.float().mean().item())}
+
     value = pairs / (ms / 1e3) / 1e6
     enc = kinfo.get("qeps_encode", {})
     out = {
@@ -274,6 +282,7 @@ def main():
                                                                                 "score_merge") if k in kinfo)
                                           / 1e3)),
         "roofline": roofline,
+        **extras,
         "kernels": kinfo,
         "kernels_note": (f"per-kernel breakdown from {prof_steps} separate steps with HIP events around every "
                          f"launch; the timed steps carry events on the dominant kernel only"),
