@@ -237,6 +237,49 @@ lam_status lam_score_topk_certified(lam_ctx* ctx, const lam_store* store, const 
                                     int32_t k, float* scores_dev, int64_t* ids_dev, float* bound_dev,
                                     uint8_t* certified_dev, float* margin_dev);
 
+/* ------------------------------------------------------------------ block codec */
+
+typedef struct lam_block_stats {
+  int64_t rows;             /* retained rows encoded                                 */
+  int64_t blocks;           /* rows x dim / 32                                       */
+  uint64_t data_bytes;      /* bit-plane words                                       */
+  uint64_t meta_bytes;      /* one width byte per block + (rows + 1) 64-bit offsets   */
+  uint64_t total_bytes;
+  double bits_per_code;     /* 8 total_bytes / (rows x dim)                          */
+  int32_t plain_bits;       /* b of the fixed-width codes                            */
+  int32_t pad;
+  double codec_ratio;       /* 32 / bits_per_code: float32 rows over encoded rows     */
+  double composite_ratio;   /* n_seen x dim x 4 / total_bytes: deduplication x codec  */
+} lam_block_stats;
+
+/* Section 2.2 (L2) and Section "Composite reduction": encode the store's Q_eps
+ * codes in blocks of 32 codes of a row: zigzag values (u = 2q, or -2q - 1 for
+ * q < 0), each block with the bit width w of its largest u (0 if all zero) as w
+ * 32-bit bit planes (bit j of word t = bit t of code j), one width byte per
+ * block and a 64-bit word offset per row.  Lossless on the codes, so the
+ * reconstruction and the score bound are those of Q_eps.  Requires a store
+ * quantized after its last ingest (ESTATE otherwise); an encoding lasts until
+ * the store is re-quantized or cleared.  Synchronous (fills out). */
+lam_status lam_store_block_encode(lam_ctx* ctx, lam_store* store, lam_block_stats* out);
+
+/* Decode the block encoding to x_hat (size x dim float32), bit for bit the
+ * values lam_store_dequantize gives.  ESTATE without a current encoding.
+ * Asynchronous. */
+lam_status lam_store_block_decode(lam_ctx* ctx, const lam_store* store, float* xhat_dev);
+
+/* Copy the encoding out: widths (size x dim/32 bytes), row offsets (size + 1
+ * uint64 word offsets; the last is the total word count) and the bit-plane
+ * words (data_cap_bytes must hold them).  NULL pointers are skipped.  Async. */
+lam_status lam_store_block_export(lam_ctx* ctx, const lam_store* store, uint8_t* widths_dev, uint64_t* row_off_dev,
+                                  uint32_t* data_dev, uint64_t data_cap_bytes);
+
+/* lam_score_topk over the block encoding: the blocks are expanded to the
+ * fixed-width code stream in context scratch (one pass) and scored by the same
+ * fused kernel, so the results equal lam_score_topk's.  ESTATE without a current
+ * encoding.  Asynchronous. */
+lam_status lam_score_topk_blocks(lam_ctx* ctx, const lam_store* store, const float* q_dev, int64_t nq, int32_t k,
+                                 float* scores_dev, int64_t* ids_dev, float* bound_dev);
+
 /* ------------------------------------------------------------------ removal ceiling */
 
 typedef struct lam_ceiling_stats {

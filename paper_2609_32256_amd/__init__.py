@@ -68,6 +68,15 @@ class StoreInfo(ctypes.Structure):
 
 _P = ctypes.c_void_p
 _I64 = ctypes.c_int64
+class BlockStats(ctypes.Structure):
+    _fields_ = [("rows", _I64), ("blocks", _I64), ("data_bytes", ctypes.c_uint64), ("meta_bytes", ctypes.c_uint64),
+                ("total_bytes", ctypes.c_uint64), ("bits_per_code", ctypes.c_double), ("plain_bits", ctypes.c_int32),
+                ("pad", ctypes.c_int32), ("codec_ratio", ctypes.c_double), ("composite_ratio", ctypes.c_double)]
+
+    def as_dict(self):
+        return {f: getattr(self, f) for f, _ in self._fields_ if f != "pad"}
+
+
 class CeilingStats(ctypes.Structure):
     _fields_ = [("n", _I64), ("kept", _I64), ("kept_2delta", _I64), ("tau", ctypes.c_double),
                 ("tau_2delta", ctypes.c_double), ("removal", ctypes.c_double), ("ceiling", ctypes.c_double),
@@ -104,6 +113,10 @@ _SIGS = {
     "lam_store_dequantize": ([_P, _P, _P], ctypes.c_int),
     "lam_store_export": ([_P, _P, _P, _P, ctypes.c_uint64], ctypes.c_int),
     "lam_score_topk_certified": ([_P, _P, _P, _I64, ctypes.c_int32, _P, _P, _P, _P, _P], ctypes.c_int),
+    "lam_store_block_encode": ([_P, _P, ctypes.POINTER(BlockStats)], ctypes.c_int),
+    "lam_store_block_decode": ([_P, _P, _P], ctypes.c_int),
+    "lam_store_block_export": ([_P, _P, _P, _P, _P, ctypes.c_uint64], ctypes.c_int),
+    "lam_score_topk_blocks": ([_P, _P, _P, _I64, ctypes.c_int32, _P, _P, _P], ctypes.c_int),
     "lam_removal_ceiling": ([_P, _P, _I64, ctypes.c_int32, ctypes.c_double, _I64, ctypes.POINTER(CeilingStats)],
                             ctypes.c_int),
     "lam_score_topk": ([_P, _P, _P, _I64, ctypes.c_int32, _P, _P, _P], ctypes.c_int),
@@ -319,6 +332,42 @@ class Store:
         out = torch.empty(max(1, p.code_bytes // 4), dtype=torch.int32, device=f"cuda:{self.ctx.device}")
         _check(_lib.lam_store_export(self.ctx.handle, self._h, _P(None), _ptr(out), out.numel() * 4))
         return out[: p.code_bytes // 4]
+
+    def block_encode(self) -> dict:
+        """Per-block codec of the current codes (lam_store_block_encode)."""
+        st = BlockStats()
+        _check(_lib.lam_store_block_encode(self.ctx.handle, self._h, ctypes.byref(st)))
+        self._blocks = st.as_dict()
+        return self._blocks
+
+    def block_decode(self, out: torch.Tensor | None = None) -> torch.Tensor:
+        n = self.size
+        if out is None:
+            out = torch.empty((max(1, n), self.dim), dtype=torch.float32, device=f"cuda:{self.ctx.device}")
+        _check(_lib.lam_store_block_decode(self.ctx.handle, self._h, _ptr(out)))
+        return out[:n]
+
+    def block_export(self):
+        """(widths uint8[size, dim/32], row_off int64[size + 1], data int32[words])."""
+        n = self.size
+        dev = f"cuda:{self.ctx.device}"
+        words = int(self._blocks["data_bytes"] // 4)
+        w = torch.empty((max(1, n), self.dim // 32), dtype=torch.uint8, device=dev)
+        ro = torch.empty(n + 1, dtype=torch.int64, device=dev)
+        d = torch.empty(max(1, words), dtype=torch.int32, device=dev)
+        _check(_lib.lam_store_block_export(self.ctx.handle, self._h, _ptr(w), _ptr(ro), _ptr(d), d.numel() * 4))
+        return w[:n], ro, d[:words]
+
+    def score_topk_blocks(self, q: torch.Tensor, k: int):
+        """lam_score_topk over the block encoding."""
+        q = _dev_tensor(q, torch.float32, "q")
+        nq = q.shape[0]
+        scores = torch.empty((nq, k), dtype=torch.float32, device=q.device)
+        ids = torch.empty((nq, k), dtype=torch.int64, device=q.device)
+        bound = torch.empty(nq, dtype=torch.float32, device=q.device)
+        _check(_lib.lam_score_topk_blocks(self.ctx.handle, self._h, _ptr(q), nq, int(k), _ptr(scores), _ptr(ids),
+                                          _ptr(bound)))
+        return scores, ids, bound
 
     def score_topk_certified(self, q: torch.Tensor, k: int):
         """Top-k plus the rank-invariance certificate: (scores, ids, bound,

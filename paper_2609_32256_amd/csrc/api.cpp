@@ -354,6 +354,7 @@ lam_status lam_store_quantize(lam_ctx* ctx, lam_store* st, double eps, float abs
   const int64_t n = st->size * (int64_t)st->dim;
   DevBuf holder{st->codes, st->codes_cap};
   lam_qparams p{};
+  st->blk_rows = -1;   // any block encoding describes the previous codes
   lam_status s = quantize_impl(ctx, st->x32, n, eps, absmax, mode, nullptr, 0, &p, &holder, true);
   st->codes = holder.as<uint32_t>();
   st->codes_cap = holder.bytes;
@@ -374,6 +375,7 @@ lam_status lam_store_clear(lam_ctx* ctx, lam_store* st) {
                      (int)(store_meta_bytes() / 4));
   LAM_HIP(hipGetLastError());
   st->pending = false;   // errors of earlier calls that did not wait are dropped with the contents
+  st->blk_rows = -1;
   st->size_ub = 0;
   st->size = 0;
   st->n_seen = 0;
@@ -428,6 +430,66 @@ lam_status lam_score_topk(lam_ctx* ctx, const lam_store* st, const float* q_dev,
             "store must be quantized (lam_store_quantize) after its last ingest");
   DeviceGuard g(ctx->device);
   return score_topk(ctx, st, q_dev, nq, k, scores_dev, ids_dev, bound_dev);
+}
+
+lam_status lam_store_block_encode(lam_ctx* ctx, lam_store* st, lam_block_stats* out) {
+  LAM_CHECK(ctx != nullptr && st != nullptr, LAM_EINVAL, "ctx or store is NULL");
+  DeviceGuard g(ctx->device);
+  LAM_TRY(store_settle(st));
+  LAM_CHECK(st->codes != nullptr && st->coded_rows == st->size, LAM_ESTATE,
+            "store must be quantized (lam_store_quantize) after its last ingest");
+  return block_encode(ctx, st, out);
+}
+
+static bool blocks_current(const lam_store* st) {
+  return st->codes != nullptr && st->coded_rows == st->size && st->blk_rows == st->size;
+}
+
+lam_status lam_store_block_decode(lam_ctx* ctx, const lam_store* st, float* xhat_dev) {
+  LAM_CHECK(ctx != nullptr && st != nullptr, LAM_EINVAL, "ctx or store is NULL");
+  DeviceGuard g(ctx->device);
+  LAM_TRY(store_settle(const_cast<lam_store*>(st)));
+  LAM_CHECK(blocks_current(st), LAM_ESTATE, "store has no block encoding of its current codes");
+  LAM_CHECK(xhat_dev != nullptr || st->size == 0, LAM_EINVAL, "xhat is NULL");
+  return block_decode(ctx, st, xhat_dev, nullptr);
+}
+
+lam_status lam_store_block_export(lam_ctx* ctx, const lam_store* st, uint8_t* widths_dev, uint64_t* row_off_dev,
+                                  uint32_t* data_dev, uint64_t data_cap_bytes) {
+  LAM_CHECK(ctx != nullptr && st != nullptr, LAM_EINVAL, "ctx or store is NULL");
+  DeviceGuard g(ctx->device);
+  LAM_TRY(store_settle(const_cast<lam_store*>(st)));
+  LAM_CHECK(blocks_current(st), LAM_ESTATE, "store has no block encoding of its current codes");
+  const int64_t m = st->blk_rows;
+  const size_t nb = (size_t)st->dim / 32;
+  if (widths_dev && m > 0)
+    LAM_HIP(hipMemcpyAsync(widths_dev, st->blk_w, (size_t)m * nb, hipMemcpyDeviceToDevice, ctx->stream));
+  if (row_off_dev)
+    LAM_HIP(hipMemcpyAsync(row_off_dev, st->blk_row_off, (size_t)(m + 1) * 8, hipMemcpyDeviceToDevice, ctx->stream));
+  if (data_dev) {
+    LAM_CHECK(data_cap_bytes >= st->blk_words * 4, LAM_EINVAL, "data capacity too small");
+    if (st->blk_words)
+      LAM_HIP(hipMemcpyAsync(data_dev, st->blk_data, st->blk_words * 4, hipMemcpyDeviceToDevice, ctx->stream));
+  }
+  return LAM_OK;
+}
+
+lam_status lam_score_topk_blocks(lam_ctx* ctx, const lam_store* st, const float* q_dev, int64_t nq, int32_t k,
+                                 float* scores_dev, int64_t* ids_dev, float* bound_dev) {
+  LAM_CHECK(ctx != nullptr && st != nullptr, LAM_EINVAL, "ctx or store is NULL");
+  LAM_CHECK(nq >= 0, LAM_EINVAL, "nq must be >= 0");
+  LAM_CHECK(k >= 1 && k <= 64, LAM_EINVAL, "k must be in [1, 64]");
+  LAM_CHECK((q_dev != nullptr && scores_dev != nullptr && ids_dev != nullptr) || nq == 0, LAM_EINVAL,
+            "NULL buffer");
+  LAM_CHECK(((uintptr_t)q_dev & 15u) == 0, LAM_EINVAL, "q must be 16-byte aligned");
+  DeviceGuard g(ctx->device);
+  LAM_TRY(store_settle(const_cast<lam_store*>(st)));
+  LAM_CHECK(blocks_current(st), LAM_ESTATE, "store has no block encoding of its current codes");
+  // the blocks are expanded back to the fixed-width stream the fused scorer reads
+  LAM_TRY(ctx->scratch[kScratchExpand].ensure(std::max<uint64_t>(st->q.code_bytes, 4)));
+  uint32_t* codes = ctx->scratch[kScratchExpand].as<uint32_t>();
+  LAM_TRY(block_decode(ctx, st, nullptr, codes));
+  return score_topk(ctx, st, q_dev, nq, k, scores_dev, ids_dev, bound_dev, codes);
 }
 
 lam_status lam_score_topk_certified(lam_ctx* ctx, const lam_store* st, const float* q_dev, int64_t nq, int32_t k,

@@ -881,6 +881,13 @@ void store_free(lam_store* st) {
   for (void* p : {(void*)st->x32, (void*)st->x16, (void*)st->hn, (void*)st->et, (void*)st->ids,
                   (void*)st->stat_dev, (void*)st->codes})
     if (p) (void)hipFree(p);
+  for (void* p : {(void*)st->blk_w, (void*)st->blk_row_off, (void*)st->blk_data})
+    if (p) (void)hipFree(p);
+  st->blk_w = nullptr;
+  st->blk_row_off = nullptr;
+  st->blk_data = nullptr;
+  st->blk_cap = 0;
+  st->blk_rows = -1;
   if (st->done) (void)hipEventDestroy(st->done);
   st->done = nullptr;
   st->x32 = nullptr;

@@ -49,7 +49,9 @@ struct Status {
 // then the ones below.
 constexpr int kScratchCeilingRep = 12;   // representatives of the ceiling passes (not returned)
 constexpr int kScratchCertify = 13;      // top-(k+1) lists of the certified scoring
-constexpr int kScratchSlots = 14;
+constexpr int kScratchBlocks = 14;       // block codec: row word counts and scan sums
+constexpr int kScratchExpand = 15;       // block codec: codes expanded back to the b-bit stream for scoring
+constexpr int kScratchSlots = 16;
 
 struct DevBuf {
   void* p = nullptr;
@@ -124,6 +126,13 @@ struct lam_store {
   uint32_t* codes = nullptr;
   uint64_t codes_cap = 0;
   int64_t coded_rows = 0;     // rows covered by the current codes
+  // per-block codec of the codes (blockcodec.hip); valid when blk_rows == coded_rows
+  uint8_t* blk_w = nullptr;          // widths, capacity x dim/32
+  uint64_t* blk_row_off = nullptr;   // word offset of each row, capacity + 1
+  uint32_t* blk_data = nullptr;      // bit planes
+  uint64_t blk_cap = 0;              // bytes allocated for blk_data
+  uint64_t blk_words = 0;
+  int64_t blk_rows = -1;             // rows encoded, -1 when none or stale
   lam_qparams q{};
 };
 
@@ -162,10 +171,14 @@ size_t store_meta_bytes();   // device bookkeeping block of a store (cleared by 
 void store_free(lam_store* st);
 
 // ------------------------------------------------------------------ scoring (score.hip)
+// codes: the b-bit code stream to score (NULL: the store's own)
 lam_status score_topk(lam_ctx* ctx, const lam_store* st, const float* q, int64_t nq, int32_t k,
-                      float* scores, int64_t* ids, float* bound);
+                      float* scores, int64_t* ids, float* bound, const uint32_t* codes = nullptr);
 lam_status score_certify(lam_ctx* ctx, const lam_store* st, const float* q, int64_t nq, int32_t k, float* scores,
                          int64_t* ids, float* bound, uint8_t* certified, float* margin);
+lam_status block_encode(lam_ctx* ctx, lam_store* st, lam_block_stats* out);
+// decode the blocks to float32 (xhat) or back to the b-bit code stream (codes_out)
+lam_status block_decode(lam_ctx* ctx, const lam_store* st, float* xhat, uint32_t* codes_out);
 
 // ------------------------------------------------------------------ exact host predicate (exact.cpp)
 // sum_d (a_d - b_d)^2 <= 2 - 2 tau on exact reals, float32 rows a, b of length d.

@@ -500,7 +500,7 @@ void plan_splits(int nqt, int64_t ntiles, int* splits, int64_t* tps) {
 //      per-lane lists over the whole store; launched always, it returns at once
 //      when nothing overflowed, so the call stays asynchronous.
 lam_status score_topk(lam_ctx* ctx, const lam_store* st, const float* q, int64_t nq, int32_t k, float* scores,
-                      int64_t* ids, float* bound) {
+                      int64_t* ids, float* bound, const uint32_t* codes) {
   if (nq == 0) return LAM_OK;
   const int D = st->dim;
   const int b = st->q.bits;
@@ -534,7 +534,7 @@ lam_status score_topk(lam_ctx* ctx, const lam_store* st, const float* q, int64_t
   int32_t* part_r = reinterpret_cast<int32_t*>(part_s + (size_t)nq * cands_max);
 
   ScoreArgs a{};
-  a.codes = st->codes;
+  a.codes = codes ? codes : st->codes;
   a.n = n;
   a.D = D;
   a.row_words = (int64_t)D * b / 32;
