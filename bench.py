@@ -245,13 +245,16 @@ def main():
         roofline = {"kernel": dominant, "bound": "latency", "achieved": None, "peak": None, "unit": None,
                     "frac": None, "traffic": None}
 
-    # beside the timed step (not in it): the removal ceiling of the stream and
-    # the share of benchmark queries whose top-10 is certified rank-invariant
+    # beside the timed step (not in it): the removal ceiling of the stream, the
+    # share of benchmark queries whose top-10 is certified rank-invariant, and
+    # the per-block codec's size on the retained store
     ceil = lam.removal_ceiling(xd, TAU, batch=BATCH, ctx=ctx)
     cert = store.score_topk_certified(qd, TOPK)[3]
+    blk = store.block_encode()
     extras = {"removal_ceiling": {k: ceil[k] for k in ("kept", "kept_2delta", "removal", "ceiling",
                                                          "frac_of_ceiling", "bits_lo", "bits_hi")},
-              "certified_top10_frac": float(cert.float().mean().item())}
+              "certified_top10_frac": float(cert.float().mean().item()),
+              "block_codec": {k: blk[k] for k in ("bits_per_code", "plain_bits", "codec_ratio", "composite_ratio")}}
 
     value = pairs / (ms / 1e3) / 1e6
     enc = kinfo.get("qeps_encode", {})
