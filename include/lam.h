@@ -129,6 +129,29 @@ lam_status lam_dequantize(lam_ctx* ctx, const uint32_t* codes_dev, const lam_qpa
 typedef struct lam_store lam_store;
 
 lam_status lam_store_create(lam_ctx* ctx, int32_t dim, double tau, int64_t capacity, lam_store** out);
+
+/* A store whose ingest takes its candidates from a band index over Q_eps codes
+ * (Section 2.2, the candidate layer L1; Appendix "Band width and quantizer
+ * step") instead of screening every retained row.  Each row's codes at step
+ * eps_band (code = round-half-even of the exact x / (2 eps_band), as
+ * lam_quantize) are cut into dim / band_width bands of band_width consecutive
+ * coordinates; a retained row is a candidate of an arrival when the codes of
+ * at least one band are equal in both (a 64-bit digest only finds equal bands;
+ * the codes are compared before a pair counts).  Every candidate is decided by
+ * the exact merge predicate and the lowest-indexed candidate within delta is
+ * the representative; an arrival with none is kept and its bands enter the
+ * index.  So rep is that of Algorithm "admit" with the retained set cut down
+ * to the candidates; a coarse enough step (every code 0) gives exhaustive
+ * greedy.  The index holds retained rows only.  Library-owned device memory
+ * grows by about 28 bytes per (row of capacity, band).
+ * band_width must divide dim; eps_band in [2^-23, 2^40];
+ * capacity * (dim / band_width) < 2^31.  On such a store lam_dedup_ingest
+ * rejects max_cos_dev (EINVAL), and n_ambiguous_pairs counts candidate pairs:
+ * the arrival against retained rows of earlier chunks (a chunk is 4,096
+ * arrivals of a call), plus pairs of arrivals j < i within one chunk with an
+ * equal band, whether or not j is later kept. */
+lam_status lam_store_create_banded(lam_ctx* ctx, int32_t dim, double tau, int64_t capacity, double eps_band,
+                                   int32_t band_width, lam_store** out);
 void lam_store_destroy(lam_store* store);
 
 typedef struct lam_store_info {

@@ -104,6 +104,8 @@ _SIGS = {
                       ctypes.POINTER(QParams)], ctypes.c_int),
     "lam_dequantize": ([_P, _P, ctypes.POINTER(QParams), _P], ctypes.c_int),
     "lam_store_create": ([_P, ctypes.c_int32, ctypes.c_double, _I64, ctypes.POINTER(_P)], ctypes.c_int),
+    "lam_store_create_banded": ([_P, ctypes.c_int32, ctypes.c_double, _I64, ctypes.c_double, ctypes.c_int32,
+                                 ctypes.POINTER(_P)], ctypes.c_int),
     "lam_store_destroy": ([_P], None),
     "lam_store_get_info": ([_P, ctypes.POINTER(StoreInfo)], ctypes.c_int),
     "lam_dedup_ingest": ([_P, _P, _P, _I64, _P, _P, ctypes.POINTER(IngestStats)], ctypes.c_int),
@@ -267,11 +269,22 @@ def dequantize(codes: torch.Tensor, p: QParams, out: torch.Tensor | None = None,
 class Store:
     """The retained set of the greedy near-duplicate test, on one device."""
 
-    def __init__(self, dim: int, tau: float, capacity: int, ctx: Context | None = None):
+    def __init__(self, dim: int, tau: float, capacity: int, ctx: Context | None = None,
+                 eps_band: float | None = None, band_width: int | None = None):
+        """With eps_band and band_width the store takes its candidates from a
+        band index over Q_eps codes (lam_store_create_banded); otherwise every
+        retained row is screened."""
         self.ctx = ctx or default_context()
         h = _P()
-        _check(_lib.lam_store_create(self.ctx.handle, int(dim), float(tau), int(capacity), ctypes.byref(h)))
+        if (eps_band is None) != (band_width is None):
+            raise ValueError("give both eps_band and band_width, or neither")
+        if band_width is None:
+            _check(_lib.lam_store_create(self.ctx.handle, int(dim), float(tau), int(capacity), ctypes.byref(h)))
+        else:
+            _check(_lib.lam_store_create_banded(self.ctx.handle, int(dim), float(tau), int(capacity),
+                                                float(eps_band), int(band_width), ctypes.byref(h)))
         self._h = h
+        self.banded = band_width is not None
         self.dim = int(dim)
         self.tau = float(tau)
 

@@ -282,12 +282,22 @@ lam_status lam_dequantize(lam_ctx* ctx, const uint32_t* codes_dev, const lam_qpa
   return launch_decode(ctx, codes_dev, *p, xhat_dev);
 }
 
-lam_status lam_store_create(lam_ctx* ctx, int32_t dim, double tau, int64_t capacity, lam_store** out) {
+namespace {
+
+lam_status store_create(lam_ctx* ctx, int32_t dim, double tau, int64_t capacity, double eps_band,
+                        int32_t band_width, lam_store** out) {
   LAM_CHECK(ctx != nullptr && out != nullptr, LAM_EINVAL, "ctx or out is NULL");
   *out = nullptr;
   LAM_CHECK(dim > 0 && dim % 32 == 0 && dim <= 4096, LAM_EINVAL, "dim must be a multiple of 32 in [32, 4096]");
   LAM_CHECK(std::isfinite(tau) && tau > -1.0 && tau <= 1.0, LAM_EINVAL, "tau must be in (-1, 1]");
   LAM_CHECK(capacity > 0 && capacity < (1LL << 31), LAM_EINVAL, "capacity must be in [1, 2^31)");
+  if (band_width > 0) {
+    LAM_CHECK(dim % band_width == 0, LAM_EINVAL, "band_width must divide dim");
+    LAM_CHECK(std::isfinite(eps_band) && eps_band >= 0x1p-23 && eps_band <= 0x1p40, LAM_EINVAL,
+              "eps_band must be in [2^-23, 2^40]");
+    LAM_CHECK(capacity * (int64_t)(dim / band_width) < (1LL << 31), LAM_EINVAL,
+              "capacity * (dim / band_width) must be below 2^31");
+  }
   DeviceGuard g(ctx->device);
   lam_store* st = new (std::nothrow) lam_store();
   LAM_CHECK(st != nullptr, LAM_ENOMEM, "out of host memory");
@@ -296,6 +306,11 @@ lam_status lam_store_create(lam_ctx* ctx, int32_t dim, double tau, int64_t capac
   st->tau = tau;
   st->d2 = 2.0 - 2.0 * tau;
   st->capacity = capacity;
+  if (band_width > 0) {
+    st->lsh_r = band_width;
+    st->lsh_nb = dim / band_width;
+    st->lsh_eps = eps_band;
+  }
   lam_status s = store_alloc(st);
   if (s != LAM_OK) {
     store_free(st);
@@ -304,6 +319,18 @@ lam_status lam_store_create(lam_ctx* ctx, int32_t dim, double tau, int64_t capac
   }
   *out = st;
   return LAM_OK;
+}
+
+}  // namespace
+
+lam_status lam_store_create(lam_ctx* ctx, int32_t dim, double tau, int64_t capacity, lam_store** out) {
+  return store_create(ctx, dim, tau, capacity, 0.0, 0, out);
+}
+
+lam_status lam_store_create_banded(lam_ctx* ctx, int32_t dim, double tau, int64_t capacity, double eps_band,
+                                   int32_t band_width, lam_store** out) {
+  LAM_CHECK(band_width > 0, LAM_EINVAL, "band_width must be positive");
+  return store_create(ctx, dim, tau, capacity, eps_band, band_width, out);
 }
 
 void lam_store_destroy(lam_store* st) {
@@ -374,6 +401,7 @@ lam_status lam_store_clear(lam_ctx* ctx, lam_store* st) {
   hipLaunchKernelGGL(k_zero_words, dim3(1), dim3(64), 0, ctx->stream, reinterpret_cast<uint32_t*>(st->stat_dev),
                      (int)(store_meta_bytes() / 4));
   LAM_HIP(hipGetLastError());
+  LAM_TRY(lsh_reset(ctx, st, 0));
   st->pending = false;   // errors of earlier calls that did not wait are dropped with the contents
   st->blk_rows = -1;
   st->size_ub = 0;

@@ -43,6 +43,7 @@
 #include "exact.h"
 #include "lam_internal.h"
 #include "mfma_tile.h"
+#include "qround.h"
 
 namespace lam {
 
@@ -407,6 +408,202 @@ __global__ __launch_bounds__(C::kThreads, C::kMinWaves) void k_screen(ScreenArgs
 }
 
 using ScreenTile = Tile<2, 2, 2, 2>;   // 128 x 128, four waves of 64 x 64
+
+// ------------------------------------------------------------------ banded candidates
+// Algorithm "admit" with a band index (Section 2.2, L1): the codes of a row at
+// the band step are cut into bands of r coordinates; a retained row is a
+// candidate of an arrival when some band holds equal codes in both.  A 64-bit
+// key of (band, codes) finds equal bands through an open-addressing index; the
+// codes themselves are compared before a pair counts, so key collisions never
+// make candidates.  A candidate pair is emitted only for the lowest band whose
+// codes agree, so each pair is verified once; the pairs enter the same exact
+// verification as the screen's ambiguous pairs.
+struct LshArgs {
+  const float* xc;            // chunk rows (float32)
+  const float* xs;            // store rows (float32)
+  int nB;
+  int D;
+  int r, nb;                  // band width, bands per row
+  double s, inv_s, eps;       // band step 2 eps, its inverse, eps
+  float inv_s32;
+  unsigned long long* ckey;   // chunk band keys (nB x nb)
+  // the store's index
+  const unsigned long long* skey;
+  const int32_t* shead;
+  const int32_t* snext;
+  const unsigned long long* srowkey;
+  uint64_t smask;
+  // the chunk's own index (rebuilt per chunk)
+  unsigned long long* bkey;
+  int32_t* bhead;
+  int32_t* bnext;
+  uint64_t bmask;
+  uint64_t bslots;            // slots of the chunk's index
+  const StoreMeta* meta;
+  int m_exact;                // store size when known, else -1
+  int2* pairs;
+  uint32_t pair_cap;
+  ChunkCounters* cc;
+  DevFlags* flags;
+};
+
+__device__ __forceinline__ unsigned long long mix64(unsigned long long z) {
+  z += 0x9e3779b97f4a7c15ull;
+  z = (z ^ (z >> 30)) * 0xbf58476d1ce4e5b9ull;
+  z = (z ^ (z >> 27)) * 0x94d049bb133111ebull;
+  return z ^ (z >> 31);
+}
+
+__device__ __forceinline__ int32_t band_code(const LshArgs& a, float v) {
+  return q_round_fast(v, a.inv_s32, a.s, a.inv_s, a.eps);
+}
+
+// codes of band b of row p equal those of row q (both float32 rows of dim D)
+__device__ __forceinline__ bool band_equal(const LshArgs& a, const float* p, const float* q, int b) {
+  for (int t = b * a.r; t < (b + 1) * a.r; ++t)
+    if (band_code(a, p[t]) != band_code(a, q[t])) return false;
+  return true;
+}
+
+// first band below b whose codes agree (-1 if none): a key match is confirmed
+// on the codes
+__device__ __forceinline__ bool earlier_band_equal(const LshArgs& a, const unsigned long long* ki,
+                                                   const unsigned long long* ky, const float* p, const float* q,
+                                                   int b) {
+  for (int b2 = 0; b2 < b; ++b2)
+    if (ki[b2] == ky[b2] && band_equal(a, p, q, b2)) return true;
+  return false;
+}
+
+// Band keys of the chunk's rows; the same grid clears the chunk's index.
+__global__ __launch_bounds__(256) void k_lsh_keys(LshArgs a) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if ((uint64_t)t < a.bslots) {
+    a.bkey[t] = 0ull;
+    a.bhead[t] = -1;
+  }
+  if (t >= (int64_t)a.nB * a.nb) return;
+  const int i = (int)(t / a.nb), b = (int)(t % a.nb);
+  const float* p = a.xc + (int64_t)i * a.D + b * a.r;
+  unsigned long long h = mix64((unsigned long long)b + 1ull);
+  for (int k = 0; k < a.r; ++k) h = mix64(h ^ (unsigned long long)(uint32_t)band_code(a, p[k]));
+  a.ckey[t] = h ? h : 1ull;   // 0 marks an empty slot
+}
+
+__device__ __forceinline__ void push_cand(const LshArgs& a, int i, int kind, int y) {
+  const uint32_t idx = atomicAdd(&a.cc->npairs, 1u);
+  atomicAdd(&a.flags->n_pairs, 1u);
+  if (idx < a.pair_cap) {
+    a.pairs[idx] = make_int2(i | (kind << 31), y);
+  } else {
+    atomicOr(&a.flags->pair_overflow, 1u);
+    atomicMax(&a.flags->pairs_needed, idx + 1u);
+  }
+}
+
+// Slot holding key h in an index (linear probing), or -1 if absent.
+__device__ __forceinline__ int64_t find_slot(const unsigned long long* keys, uint64_t mask, unsigned long long h) {
+  uint64_t sl = h & mask;
+  for (;;) {
+    const unsigned long long k = keys[sl];
+    if (k == h) return (int64_t)sl;
+    if (k == 0ull) return -1;
+    sl = (sl + 1) & mask;
+  }
+}
+
+// Inserts entry e under key h (the index is at most half full, so a free or
+// matching slot is always found).
+__device__ __forceinline__ void index_insert(unsigned long long* keys, int32_t* head, int32_t* next, uint64_t mask,
+                                             unsigned long long h, int32_t e) {
+  uint64_t sl = h & mask;
+  for (;;) {
+    const unsigned long long k = atomicCAS(&keys[sl], 0ull, h);
+    if (k == 0ull || k == h) break;
+    sl = (sl + 1) & mask;
+  }
+  next[e] = atomicExch(&head[sl], e);
+}
+
+// One thread per (arrival, band): retained candidates from the store's index.
+__global__ __launch_bounds__(256) void k_lsh_query_store(LshArgs a) {
+  if (skip_all(a.flags)) return;
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= (int64_t)a.nB * a.nb) return;
+  const int i = (int)(t / a.nb), b = (int)(t % a.nb);
+  const int m = a.m_exact >= 0 ? a.m_exact : a.meta->m;
+  const unsigned long long h = a.ckey[t];
+  const int64_t sl = find_slot(a.skey, a.smask, h);
+  if (sl < 0) return;
+  const float* p = a.xc + (int64_t)i * a.D;
+  for (int32_t e = a.shead[sl]; e >= 0; e = a.snext[e]) {
+    const int pos = e / a.nb;
+    if (e % a.nb != b || pos >= m) continue;
+    const float* q = a.xs + (int64_t)pos * a.D;
+    if (!band_equal(a, p, q, b)) continue;
+    if (earlier_band_equal(a, a.ckey + (int64_t)i * a.nb, a.srowkey + (int64_t)pos * a.nb, p, q, b)) continue;
+    push_cand(a, i, 0, pos);
+  }
+}
+
+// The chunk's own index over all its rows (cleared beforehand).
+__global__ __launch_bounds__(256) void k_lsh_index_chunk(LshArgs a) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= (int64_t)a.nB * a.nb) return;
+  index_insert(a.bkey, a.bhead, a.bnext, a.bmask, a.ckey[t], (int32_t)t);
+}
+
+// One thread per (arrival, band): earlier arrivals of the chunk sharing a band.
+__global__ __launch_bounds__(256) void k_lsh_query_chunk(LshArgs a) {
+  if (skip_all(a.flags)) return;
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= (int64_t)a.nB * a.nb) return;
+  const int i = (int)(t / a.nb), b = (int)(t % a.nb);
+  const int64_t sl = find_slot(a.bkey, a.bmask, a.ckey[t]);
+  const float* p = a.xc + (int64_t)i * a.D;
+  for (int32_t e = sl >= 0 ? a.bhead[sl] : -1; e >= 0; e = a.bnext[e]) {
+    const int j = e / a.nb;
+    if (e % a.nb != b || j >= i) continue;
+    const float* q = a.xc + (int64_t)j * a.D;
+    if (!band_equal(a, p, q, b)) continue;
+    if (earlier_band_equal(a, a.ckey + (int64_t)i * a.nb, a.ckey + (int64_t)j * a.nb, p, q, b)) continue;
+    push_cand(a, i, 1, j);
+  }
+}
+
+// Kept rows of the chunk join the store's index under their store positions.
+__global__ __launch_bounds__(256) void k_lsh_insert(LshArgs a, const int32_t* __restrict__ pos,
+                                                    unsigned long long* skey, int32_t* shead, int32_t* snext,
+                                                    unsigned long long* srowkey) {
+  if (skip_all(a.flags)) return;
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= (int64_t)a.nB * a.nb) return;
+  const int i = (int)(t / a.nb), b = (int)(t % a.nb);
+  const int p = pos[i];
+  if (p < 0) return;
+  const unsigned long long h = a.ckey[t];
+  const int32_t e = p * a.nb + b;
+  srowkey[e] = h;
+  index_insert(skey, shead, snext, a.smask, h, e);
+}
+
+// Empties the store's index, then (second kernel) puts back the entries of the
+// first rows of the store from their recorded band keys.
+__global__ __launch_bounds__(256) void k_lsh_clear_index(unsigned long long* key, int32_t* head, uint64_t slots) {
+  const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+  for (uint64_t t = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; t < slots; t += stride) {
+    key[t] = 0ull;
+    head[t] = -1;
+  }
+}
+
+__global__ __launch_bounds__(256) void k_lsh_reinsert(unsigned long long* key, int32_t* head, int32_t* next,
+                                                      const unsigned long long* rowkey, uint64_t mask,
+                                                      int64_t n_entries) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < n_entries; e += stride)
+    index_insert(key, head, next, mask, rowkey[e], (int32_t)e);
+}
 
 // ------------------------------------------------------------------ verify
 struct VerifyArgs {
@@ -871,9 +1068,37 @@ lam_status store_alloc(lam_store* st) {
   LAM_HIP(hipMalloc(&st->ids, cap * 8));
   LAM_HIP(hipMalloc(&st->stat_dev, sizeof(StoreMeta)));
   LAM_HIP(hipMemset(st->stat_dev, 0, sizeof(StoreMeta)));
+  if (st->lsh_r > 0) {
+    const uint64_t entries = (uint64_t)cap * (uint64_t)st->lsh_nb;
+    uint64_t slots = 1;
+    while (slots < 2 * entries) slots <<= 1;
+    st->lsh_slots = slots;
+    LAM_HIP(hipMalloc(&st->lsh_key, slots * 8));
+    LAM_HIP(hipMalloc(&st->lsh_head, slots * 4));
+    LAM_HIP(hipMalloc(&st->lsh_next, entries * 4));
+    LAM_HIP(hipMalloc(&st->lsh_rowkey, entries * 8));
+    LAM_HIP(hipMemset(st->lsh_key, 0, slots * 8));
+    LAM_HIP(hipMemset(st->lsh_head, 0xff, slots * 4));   // -1: empty list
+  }
   LAM_HIP(hipEventCreateWithFlags(&st->done, hipEventDisableTiming));
   LAM_HIP(hipDeviceSynchronize());
   st->thr = exact_threshold(st->tau);
+  return LAM_OK;
+}
+
+lam_status lsh_reset(lam_ctx* ctx, lam_store* st, int64_t keep_rows) {
+  if (st->lsh_r <= 0) return LAM_OK;
+  const unsigned g = (unsigned)std::min<uint64_t>((st->lsh_slots + 255) / 256, 8192);
+  hipLaunchKernelGGL(k_lsh_clear_index, dim3(g), dim3(256), 0, ctx->stream, st->lsh_key, st->lsh_head,
+                     st->lsh_slots);
+  LAM_HIP(hipGetLastError());
+  const int64_t ne = keep_rows * st->lsh_nb;
+  if (ne > 0) {
+    const unsigned g2 = (unsigned)std::min<int64_t>((ne + 255) / 256, 8192);
+    hipLaunchKernelGGL(k_lsh_reinsert, dim3(g2), dim3(256), 0, ctx->stream, st->lsh_key, st->lsh_head,
+                       st->lsh_next, st->lsh_rowkey, (uint64_t)(st->lsh_slots - 1), ne);
+    LAM_HIP(hipGetLastError());
+  }
   return LAM_OK;
 }
 
@@ -881,8 +1106,11 @@ void store_free(lam_store* st) {
   for (void* p : {(void*)st->x32, (void*)st->x16, (void*)st->hn, (void*)st->et, (void*)st->ids,
                   (void*)st->stat_dev, (void*)st->codes})
     if (p) (void)hipFree(p);
-  for (void* p : {(void*)st->blk_w, (void*)st->blk_row_off, (void*)st->blk_data})
+  for (void* p : {(void*)st->blk_w, (void*)st->blk_row_off, (void*)st->blk_data, (void*)st->lsh_key,
+                  (void*)st->lsh_head, (void*)st->lsh_next, (void*)st->lsh_rowkey})
     if (p) (void)hipFree(p);
+  st->lsh_key = st->lsh_rowkey = nullptr;
+  st->lsh_head = st->lsh_next = nullptr;
   st->blk_w = nullptr;
   st->blk_row_off = nullptr;
   st->blk_data = nullptr;
@@ -961,6 +1189,8 @@ lam_status dedup_ingest(lam_ctx* ctx, lam_store* st, const float* x, int64_t n, 
   }
   const int CH = (int)std::min<int64_t>(n, kChunk);
   const int W = (CH + 63) / 64;
+  const bool lsh = st->lsh_r > 0;
+  LAM_CHECK(!(lsh && max_cos), LAM_EINVAL, "max_cos is not available on a store with a band index");
 
   // A call without stats does not wait for the device when the ambiguous-pair
   // list can hold every pair its chunks could produce (so it cannot overflow)
@@ -1004,12 +1234,48 @@ lam_status dedup_ingest(lam_ctx* ctx, lam_store* st, const float* x, int64_t n, 
   uint64_t* bitmap = ctx->scratch[S_BITMAP].as<uint64_t>();
   float* G = want_max ? ctx->scratch[S_G].as<float>() : nullptr;
 
+  // banded candidates: chunk keys and the chunk's own index
+  LshArgs la{};
+  if (lsh) {
+    const int nb = st->lsh_nb;
+    const uint64_t ce = (uint64_t)CH * nb;
+    uint64_t bslots = 1;
+    while (bslots < 2 * ce) bslots <<= 1;
+    LAM_TRY(ctx->scratch[kScratchLsh].ensure(ce * 8 + bslots * 8 + bslots * 4 + ce * 4));
+    char* lb = ctx->scratch[kScratchLsh].as<char>();
+    la.ckey = reinterpret_cast<unsigned long long*>(lb);
+    la.bkey = reinterpret_cast<unsigned long long*>(lb + ce * 8);
+    la.bhead = reinterpret_cast<int32_t*>(lb + ce * 8 + bslots * 8);
+    la.bnext = reinterpret_cast<int32_t*>(lb + ce * 8 + bslots * 12);
+    la.bslots = bslots;
+    la.bmask = bslots - 1;
+    la.xs = st->x32;
+    la.D = D;
+    la.r = st->lsh_r;
+    la.nb = nb;
+    la.eps = st->lsh_eps;
+    la.s = 2.0 * st->lsh_eps;
+    la.inv_s = 1.0 / la.s;
+    la.inv_s32 = (float)la.inv_s;
+    la.skey = st->lsh_key;
+    la.shead = st->lsh_head;
+    la.snext = st->lsh_next;
+    la.srowkey = st->lsh_rowkey;
+    la.smask = st->lsh_slots - 1;
+    la.meta = meta;
+    la.cc = cc;
+    la.flags = ctx->flags_dev;
+  }
+
   for (int attempt = 0; attempt < 4; ++attempt) {
     const uint32_t cap = ctx->pair_cap;
     LAM_TRY(ctx->scratch[S_PAIRS].ensure((size_t)cap * sizeof(int2)));
     LAM_TRY(ctx->scratch[S_STATUS].ensure((size_t)cap * 4));
     int2* pairs = ctx->scratch[S_PAIRS].as<int2>();
     uint32_t* status = ctx->scratch[S_STATUS].as<uint32_t>();
+    // a repeated attempt starts from the store as it was: the band index is
+    // rebuilt from the rows retained before the call
+    if (lsh && attempt > 0) LAM_TRY(lsh_reset(ctx, st, m_before));
 
     for (int64_t c0 = 0; c0 < n; c0 += CH) {
       const int nB = (int)std::min<int64_t>(CH, n - c0);
@@ -1033,6 +1299,27 @@ lam_status dedup_ingest(lam_ctx* ctx, lam_store* st, const float* x, int64_t n, 
         LAM_HIP(hipGetLastError());
       }
 
+      if (lsh) {
+        la.xc = xc;
+        la.nB = nB;
+        la.m_exact = (!async && c0 == 0) ? (int)m_before : -1;
+        la.pairs = pairs;
+        la.pair_cap = cap;
+        const int64_t ne = (int64_t)nB * la.nb;
+        const int64_t nt = std::max<int64_t>(ne, (int64_t)la.bslots);
+        ProfScope ps(ctx, "dedup_lsh");
+        hipLaunchKernelGGL(k_lsh_keys, dim3((unsigned)((nt + 255) / 256)), dim3(256), 0, ctx->stream, la);
+        LAM_HIP(hipGetLastError());
+        const unsigned ge = (unsigned)((ne + 255) / 256);
+        if (m_before + c0 > 0) {
+          hipLaunchKernelGGL(k_lsh_query_store, dim3(ge), dim3(256), 0, ctx->stream, la);
+          LAM_HIP(hipGetLastError());
+        }
+        hipLaunchKernelGGL(k_lsh_index_chunk, dim3(ge), dim3(256), 0, ctx->stream, la);
+        LAM_HIP(hipGetLastError());
+        hipLaunchKernelGGL(k_lsh_query_chunk, dim3(ge), dim3(256), 0, ctx->stream, la);
+        LAM_HIP(hipGetLastError());
+      }
       ScreenArgs sa{};
       sa.As = st->x16;
       sa.hnS = st->hn;
@@ -1066,7 +1353,7 @@ lam_status dedup_ingest(lam_ctx* ctx, lam_store* st, const float* x, int64_t n, 
       sa.nb1 = (int64_t)ntBt * (ntBt + 1) / 2;
       const int64_t grid = sa.nb0 + sa.nb1;
       LAM_CHECK(grid < (1LL << 31), LAM_EINVAL, "screen grid too large");
-      {
+      if (!lsh) {
         ProfScope ps(ctx, "dedup_screen");
         if (want_max)
           hipLaunchKernelGGL((k_screen<ScreenTile, true>), dim3((unsigned)grid), dim3(ScreenTile::kThreads), 0,
@@ -1093,6 +1380,13 @@ lam_status dedup_ingest(lam_ctx* ctx, lam_store* st, const float* x, int64_t n, 
       if (want_max) {
         hipLaunchKernelGGL(k_maxcos, dim3((unsigned)((nB + 3) / 4)), dim3(256), 0, ctx->stream, nB, maxcos, G,
                            kept_words, max_cos + c0, ctx->flags_dev);
+        LAM_HIP(hipGetLastError());
+      }
+      if (lsh) {
+        // kept rows join the store's index before the append of the last
+        // chunk hands the status words back (and zeroes them)
+        hipLaunchKernelGGL(k_lsh_insert, dim3((unsigned)(((int64_t)nB * la.nb + 255) / 256)), dim3(256), 0,
+                           ctx->stream, la, pos, st->lsh_key, st->lsh_head, st->lsh_next, st->lsh_rowkey);
         LAM_HIP(hipGetLastError());
       }
       AppendArgs aa{xc, x16, hnc + c0, etc + c0, pos, rep_row, c0, D, st->x32, st->x16, st->hn, st->et, st->ids,

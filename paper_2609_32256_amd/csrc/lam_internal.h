@@ -51,7 +51,8 @@ constexpr int kScratchCeilingRep = 12;   // representatives of the ceiling passe
 constexpr int kScratchCertify = 13;      // top-(k+1) lists of the certified scoring
 constexpr int kScratchBlocks = 14;       // block codec: row word counts and scan sums
 constexpr int kScratchExpand = 15;       // block codec: codes expanded back to the b-bit stream for scoring
-constexpr int kScratchSlots = 16;
+constexpr int kScratchLsh = 16;          // banded candidates: chunk keys and the chunk's own index
+constexpr int kScratchSlots = 17;
 
 struct DevBuf {
   void* p = nullptr;
@@ -108,6 +109,16 @@ struct lam_store {
   double tau = 0.0;
   double d2 = 0.0;          // delta^2 = 2 - 2 tau (binary64)
   int64_t capacity = 0;
+  // banded candidates (Algorithm "admit" with a band index); lsh_r == 0: every
+  // retained row is a candidate (the MFMA screen)
+  int32_t lsh_r = 0;                 // band width (coordinates per band)
+  int32_t lsh_nb = 0;                // bands per row
+  double lsh_eps = 0.0;              // Q_eps step of the band codes
+  uint64_t lsh_slots = 0;            // index slots (a power of two)
+  unsigned long long* lsh_key = nullptr;   // slot key (0 = empty)
+  int32_t* lsh_head = nullptr;       // slot -> newest entry (entry = store position * nb + band)
+  int32_t* lsh_next = nullptr;       // entry -> older entry with the same key, -1 at the end
+  unsigned long long* lsh_rowkey = nullptr;  // band keys of retained rows (position * nb + band)
   int64_t size = 0;           // exact when !pending
   int64_t n_seen = 0;         // exact when !pending
   double delta_hat_run = 0.0; // exact when !pending
@@ -180,8 +191,10 @@ lam_status block_encode(lam_ctx* ctx, lam_store* st, lam_block_stats* out);
 // decode the blocks to float32 (xhat) or back to the b-bit code stream (codes_out)
 lam_status block_decode(lam_ctx* ctx, const lam_store* st, float* xhat, uint32_t* codes_out);
 
-// ------------------------------------------------------------------ exact host predicate (exact.cpp)
-// sum_d (a_d - b_d)^2 <= 2 - 2 tau on exact reals, float32 rows a, b of length d.
+// Empties the band index of a store and puts back the entries of its first
+// keep_rows rows (no-op for a store without a band index).
+lam_status lsh_reset(lam_ctx* ctx, lam_store* st, int64_t keep_rows);
+
 // Waits for ingest calls that did not wait, copies the device bookkeeping into
 // the host fields and reports (once) invalid input those calls met.
 lam_status store_settle(lam_store* st);

@@ -31,6 +31,7 @@
 #include <cstring>
 
 #include "lam_internal.h"
+#include "qround.h"
 
 namespace lam {
 namespace {
@@ -39,36 +40,6 @@ constexpr int kThreads = 256;
 constexpr int kPerThread = 32;
 constexpr int kTile = kThreads * kPerThread;  // 8192 elements
 constexpr int kPadded = kTile + kTile / 32;    // one pad word per 32 codes
-
-// Exact round-half-even of x / s, see the file comment.
-__device__ __forceinline__ int32_t q_round(float xf, double s, double inv_s, double eps) {
-  const double xd = (double)xf;
-  double q0 = rint(xd * inv_s);
-  const double t = fma(-q0, s, xd);
-  if (t > eps) {
-    q0 += 1.0;
-  } else if (t < -eps) {
-    q0 -= 1.0;
-  } else if (t == eps) {
-    const double d = fma(-(q0 + 0.5), s, xd);
-    const bool odd = ((long long)q0 & 1LL) != 0;
-    if (d > 0.0 || (d == 0.0 && odd)) q0 += 1.0;
-  } else if (t == -eps) {
-    const double d = fma(-(q0 - 0.5), s, xd);
-    const bool odd = ((long long)q0 & 1LL) != 0;
-    if (d < 0.0 || (d == 0.0 && odd)) q0 -= 1.0;
-  }
-  return (int32_t)q0;
-}
-
-// float32 fast path with the binary64 method as the fallback (file comment).
-__device__ __forceinline__ int32_t q_round_fast(float x, float inv_s32, double s, double inv_s, double eps) {
-  const float p = x * inv_s32;
-  const float q0 = rintf(p);
-  const float thr = fmaf(-0x1p-21f, fabsf(p), 0.5f - 0x1p-21f);
-  if (fabsf(p - q0) <= thr) return (int32_t)q0;
-  return q_round(x, s, inv_s, eps);
-}
 
 // Buffer resource over `bytes` bytes from base: loads at offsets past the
 // bound return zeros without touching memory, so a load never needs a branch
