@@ -409,15 +409,59 @@ __global__ __launch_bounds__(C::kThreads, C::kMinWaves) void k_screen(ScreenArgs
 
 using ScreenTile = Tile<2, 2, 2, 2>;   // 128 x 128, four waves of 64 x 64
 
+// ------------------------------------------------------------------ merge predicate of one pair
+// sum_d (a_d - b_d)^2 <= delta^2 for float32 rows a, b, by one wave: the
+// squared distance in binary64 (error below (D + 2) u64 d^2 in any order); a
+// pair within that distance of delta^2 is decided on exact integers
+// (exact.h), so every decision is the exact one.  Every lane returns the
+// decision; *escalated tells whether the exact path ran.
+__device__ bool pair_within(const float* pa, const float* pb, int D, double d2, const Big6& thr, bool* escalated) {
+  const int lane = threadIdx.x & 63;
+  double s = 0.0;
+  for (int d = lane; d < D; d += 64) {
+    const double t = (double)pa[d] - (double)pb[d];
+    s = fma(t, t, s);
+  }
+  s = wave_sum_f64(s);   // every lane holds the sum
+  const double margin = (double)(D + 8) * 2.5e-16 * fmax(d2, s) + 1e-300;
+  if (fabs(s - d2) > margin) {
+    *escalated = false;
+    return s <= d2;
+  }
+  Big6 acc;
+  big_zero(acc);
+  for (int d = lane; d < D; d += 64) big_add(acc, big_sq_diff(__float_as_uint(pa[d]), __float_as_uint(pb[d])));
+  for (int o = 32; o > 0; o >>= 1) {
+    Big6 other;
+#pragma unroll
+    for (int l = 0; l < kExactLimbs; ++l) other.w[l] = (uint64_t)__shfl_xor((unsigned long long)acc.w[l], o);
+    big_add(acc, other);
+  }
+  *escalated = true;
+  return big_cmp(acc, thr) <= 0;
+}
+
 // ------------------------------------------------------------------ banded candidates
 // Algorithm "admit" with a band index (Section 2.2, L1): the codes of a row at
 // the band step are cut into bands of r coordinates; a retained row is a
 // candidate of an arrival when some band holds equal codes in both.  A 64-bit
-// key of (band, codes) finds equal bands through an open-addressing index; the
-// codes themselves are compared before a pair counts, so key collisions never
-// make candidates.  A candidate pair is emitted only for the lowest band whose
-// codes agree, so each pair is verified once; the pairs enter the same exact
-// verification as the screen's ambiguous pairs.
+// key of (band, codes) finds equal bands through open-addressing indexes (one
+// over the retained rows, one over the chunk); the codes themselves are
+// compared before a pair counts, so key collisions never make candidates.
+//
+// One workgroup per arrival collects its distinct candidates in an LDS set,
+// then decides them with the merge predicate: retained rows first, where the
+// lowest one within delta is the representative (a candidate above the lowest
+// hit found so far is skipped); only when none is within are the chunk's
+// earlier arrivals decided, for the in-order resolve.  An arrival with more
+// candidates than the set holds instead lists each pair once, for its lowest
+// equal band, for the separate verification kernel.
+constexpr int kAdmitThreads = 256;
+constexpr int kSetSlots = 4096;               // LDS candidate set (a power of two)
+constexpr int kSetMax = 3072;                 // entries before an arrival takes the pair list
+constexpr uint32_t kSetEmpty = 0xffffffffu;
+constexpr uint32_t kChunkBit = 0x80000000u;   // set entry of a chunk row (else a store position)
+
 struct LshArgs {
   const float* xc;            // chunk rows (float32)
   const float* xs;            // store rows (float32)
@@ -441,6 +485,14 @@ struct LshArgs {
   uint64_t bslots;            // slots of the chunk's index
   const StoreMeta* meta;
   int m_exact;                // store size when known, else -1
+  // decisions
+  double d2;                  // delta^2 in binary64
+  Big6 thr;                   // exact right-hand side (exact.h)
+  int32_t* firstHit;
+  uint64_t* bitmap;
+  int W;
+  uint32_t* hasEdge;
+  // pair list of arrivals whose candidates overflow the set
   int2* pairs;
   uint32_t pair_cap;
   ChunkCounters* cc;
@@ -458,21 +510,35 @@ __device__ __forceinline__ int32_t band_code(const LshArgs& a, float v) {
   return q_round_fast(v, a.inv_s32, a.s, a.inv_s, a.eps);
 }
 
-// codes of band b of row p equal those of row q (both float32 rows of dim D)
-__device__ __forceinline__ bool band_equal(const LshArgs& a, const float* p, const float* q, int b) {
+// band b of float32 row q has the codes held in code[] (the arrival's)
+__device__ __forceinline__ bool band_matches(const LshArgs& a, const int32_t* code, const float* q, int b) {
   for (int t = b * a.r; t < (b + 1) * a.r; ++t)
-    if (band_code(a, p[t]) != band_code(a, q[t])) return false;
+    if (band_code(a, q[t]) != code[t]) return false;
   return true;
 }
 
-// first band below b whose codes agree (-1 if none): a key match is confirmed
-// on the codes
-__device__ __forceinline__ bool earlier_band_equal(const LshArgs& a, const unsigned long long* ki,
-                                                   const unsigned long long* ky, const float* p, const float* q,
-                                                   int b) {
-  for (int b2 = 0; b2 < b; ++b2)
-    if (ki[b2] == ky[b2] && band_equal(a, p, q, b2)) return true;
-  return false;
+// Slot holding key h in an index (linear probing), or -1 if absent.
+__device__ __forceinline__ int64_t find_slot(const unsigned long long* keys, uint64_t mask, unsigned long long h) {
+  uint64_t sl = h & mask;
+  for (;;) {
+    const unsigned long long k = keys[sl];
+    if (k == h) return (int64_t)sl;
+    if (k == 0ull) return -1;
+    sl = (sl + 1) & mask;
+  }
+}
+
+// Inserts entry e under key h (an index is at most half full, so a free or
+// matching slot is always found).
+__device__ __forceinline__ void index_insert(unsigned long long* keys, int32_t* head, int32_t* next, uint64_t mask,
+                                             unsigned long long h, int32_t e) {
+  uint64_t sl = h & mask;
+  for (;;) {
+    const unsigned long long k = atomicCAS(&keys[sl], 0ull, h);
+    if (k == 0ull || k == h) break;
+    sl = (sl + 1) & mask;
+  }
+  next[e] = atomicExch(&head[sl], e);
 }
 
 // Band keys of the chunk's rows; the same grid clears the chunk's index.
@@ -490,84 +556,153 @@ __global__ __launch_bounds__(256) void k_lsh_keys(LshArgs a) {
   a.ckey[t] = h ? h : 1ull;   // 0 marks an empty slot
 }
 
-__device__ __forceinline__ void push_cand(const LshArgs& a, int i, int kind, int y) {
-  const uint32_t idx = atomicAdd(&a.cc->npairs, 1u);
-  atomicAdd(&a.flags->n_pairs, 1u);
-  if (idx < a.pair_cap) {
-    a.pairs[idx] = make_int2(i | (kind << 31), y);
-  } else {
-    atomicOr(&a.flags->pair_overflow, 1u);
-    atomicMax(&a.flags->pairs_needed, idx + 1u);
-  }
-}
-
-// Slot holding key h in an index (linear probing), or -1 if absent.
-__device__ __forceinline__ int64_t find_slot(const unsigned long long* keys, uint64_t mask, unsigned long long h) {
-  uint64_t sl = h & mask;
-  for (;;) {
-    const unsigned long long k = keys[sl];
-    if (k == h) return (int64_t)sl;
-    if (k == 0ull) return -1;
-    sl = (sl + 1) & mask;
-  }
-}
-
-// Inserts entry e under key h (the index is at most half full, so a free or
-// matching slot is always found).
-__device__ __forceinline__ void index_insert(unsigned long long* keys, int32_t* head, int32_t* next, uint64_t mask,
-                                             unsigned long long h, int32_t e) {
-  uint64_t sl = h & mask;
-  for (;;) {
-    const unsigned long long k = atomicCAS(&keys[sl], 0ull, h);
-    if (k == 0ull || k == h) break;
-    sl = (sl + 1) & mask;
-  }
-  next[e] = atomicExch(&head[sl], e);
-}
-
-// One thread per (arrival, band): retained candidates from the store's index.
-__global__ __launch_bounds__(256) void k_lsh_query_store(LshArgs a) {
-  if (skip_all(a.flags)) return;
-  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (t >= (int64_t)a.nB * a.nb) return;
-  const int i = (int)(t / a.nb), b = (int)(t % a.nb);
-  const int m = a.m_exact >= 0 ? a.m_exact : a.meta->m;
-  const unsigned long long h = a.ckey[t];
-  const int64_t sl = find_slot(a.skey, a.smask, h);
-  if (sl < 0) return;
-  const float* p = a.xc + (int64_t)i * a.D;
-  for (int32_t e = a.shead[sl]; e >= 0; e = a.snext[e]) {
-    const int pos = e / a.nb;
-    if (e % a.nb != b || pos >= m) continue;
-    const float* q = a.xs + (int64_t)pos * a.D;
-    if (!band_equal(a, p, q, b)) continue;
-    if (earlier_band_equal(a, a.ckey + (int64_t)i * a.nb, a.srowkey + (int64_t)pos * a.nb, p, q, b)) continue;
-    push_cand(a, i, 0, pos);
-  }
-}
-
-// The chunk's own index over all its rows (cleared beforehand).
+// The chunk's own index over all its rows (cleared by k_lsh_keys).
 __global__ __launch_bounds__(256) void k_lsh_index_chunk(LshArgs a) {
   const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (t >= (int64_t)a.nB * a.nb) return;
   index_insert(a.bkey, a.bhead, a.bnext, a.bmask, a.ckey[t], (int32_t)t);
 }
 
-// One thread per (arrival, band): earlier arrivals of the chunk sharing a band.
-__global__ __launch_bounds__(256) void k_lsh_query_chunk(LshArgs a) {
-  if (skip_all(a.flags)) return;
-  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (t >= (int64_t)a.nB * a.nb) return;
-  const int i = (int)(t / a.nb), b = (int)(t % a.nb);
-  const int64_t sl = find_slot(a.bkey, a.bmask, a.ckey[t]);
-  const float* p = a.xc + (int64_t)i * a.D;
+// Walks the store's and the chunk's lists of arrival i's band b and hands each
+// row whose band codes equal the arrival's to f(entry) (entry: store position,
+// or kChunkBit | chunk row j for j < i).  Stops early when f returns false.
+template <class F>
+__device__ __forceinline__ void band_rows(const LshArgs& a, int i, int b, int m, const int32_t* code, F&& f) {
+  const unsigned long long h = a.ckey[(int64_t)i * a.nb + b];
+  if (m > 0) {
+    const int64_t sl = find_slot(a.skey, a.smask, h);
+    for (int32_t e = sl >= 0 ? a.shead[sl] : -1; e >= 0; e = a.snext[e]) {
+      const int pos = e / a.nb;
+      if (e - pos * a.nb != b || pos >= m) continue;
+      if (band_matches(a, code, a.xs + (int64_t)pos * a.D, b) && !f((uint32_t)pos)) return;
+    }
+  }
+  const int64_t sl = find_slot(a.bkey, a.bmask, h);
   for (int32_t e = sl >= 0 ? a.bhead[sl] : -1; e >= 0; e = a.bnext[e]) {
     const int j = e / a.nb;
-    if (e % a.nb != b || j >= i) continue;
-    const float* q = a.xc + (int64_t)j * a.D;
-    if (!band_equal(a, p, q, b)) continue;
-    if (earlier_band_equal(a, a.ckey + (int64_t)i * a.nb, a.ckey + (int64_t)j * a.nb, p, q, b)) continue;
-    push_cand(a, i, 1, j);
+    if (e - j * a.nb != b || j >= i) continue;
+    if (band_matches(a, code, a.xc + (int64_t)j * a.D, b) && !f(kChunkBit | (uint32_t)j)) return;
+  }
+}
+
+__device__ __forceinline__ uint32_t set_hash(uint32_t v) { return (v * 0x9e3779b1u) >> (32 - 12); }
+static_assert(kSetSlots == 1 << 12, "set_hash yields 12 bits");
+
+__global__ __launch_bounds__(kAdmitThreads) void k_lsh_admit(LshArgs a) {
+  extern __shared__ int32_t s_code[];   // the arrival's band codes (D)
+  __shared__ uint32_t set[kSetSlots];
+  __shared__ uint32_t list[kSetMax + kAdmitThreads];
+  __shared__ uint32_t n_set, n_store, n_chunk;
+  __shared__ int32_t hit, skip;
+  const int i = (int)blockIdx.x;
+  const int tid = (int)threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // one reading of the status words for the whole workgroup (another
+  // workgroup's pair-list overflow may set them meanwhile)
+  if (tid == 0) skip = skip_all(a.flags) ? 1 : 0;
+  __syncthreads();
+  if (skip) return;
+  const int m = a.m_exact >= 0 ? a.m_exact : a.meta->m;
+  const float* p = a.xc + (int64_t)i * a.D;
+  for (int d = tid; d < a.D; d += kAdmitThreads) s_code[d] = band_code(a, p[d]);
+  for (int k = tid; k < kSetSlots; k += kAdmitThreads) set[k] = kSetEmpty;
+  if (tid == 0) {
+    n_set = 0u;
+    n_store = 0u;
+    n_chunk = 0u;
+    hit = kNone;
+  }
+  __syncthreads();
+
+  // 1. distinct candidates into the set (at most kSetMax + one per thread:
+  //    an insert starts only while the count is below kSetMax)
+  volatile uint32_t* vn = &n_set;
+  for (int b = tid; b < a.nb && *vn < (uint32_t)kSetMax; b += kAdmitThreads) {
+    band_rows(a, i, b, m, s_code, [&](uint32_t v) {
+      if (*vn >= (uint32_t)kSetMax) return false;
+      uint32_t sl = set_hash(v);
+      for (;;) {
+        const uint32_t old = atomicCAS(&set[sl], kSetEmpty, v);
+        if (old == kSetEmpty) {
+          atomicAdd(&n_set, 1u);
+          break;
+        }
+        if (old == v) break;
+        sl = (sl + 1) & (kSetSlots - 1);
+      }
+      return true;
+    });
+  }
+  __syncthreads();
+
+  if (n_set >= (uint32_t)kSetMax) {
+    // 2'. too many candidates: each pair once, for its lowest equal band, to
+    //     the pair list (decided by k_verify)
+    for (int b = tid; b < a.nb; b += kAdmitThreads) {
+      band_rows(a, i, b, m, s_code, [&](uint32_t v) {
+        const bool chunk = (v & kChunkBit) != 0u;
+        const int y = (int)(v & ~kChunkBit);
+        const float* q = (chunk ? a.xc : a.xs) + (int64_t)y * a.D;
+        for (int b2 = 0; b2 < b; ++b2)
+          if (band_matches(a, s_code, q, b2)) return true;   // listed by band b2
+        const uint32_t idx = atomicAdd(&a.cc->npairs, 1u);
+        atomicAdd(&a.flags->n_pairs, 1u);
+        atomicAdd(&a.flags->n_cand, 1ull);
+        if (idx < a.pair_cap) {
+          a.pairs[idx] = make_int2(i | ((chunk ? 1 : 0) << 31), y);
+        } else {
+          atomicOr(&a.flags->pair_overflow, 1u);
+          atomicMax(&a.flags->pairs_needed, idx + 1u);
+        }
+        return true;
+      });
+    }
+    return;
+  }
+
+  // 2. the set as two lists: store positions from the front, chunk rows from the back
+  for (int k = tid; k < kSetSlots; k += kAdmitThreads) {
+    const uint32_t v = set[k];
+    if (v == kSetEmpty) continue;
+    if (v & kChunkBit)
+      list[kSetMax + kAdmitThreads - 1 - atomicAdd(&n_chunk, 1u)] = v & ~kChunkBit;
+    else
+      list[atomicAdd(&n_store, 1u)] = v;
+  }
+  __syncthreads();
+  const int ns = (int)n_store, nc = (int)n_chunk;
+  if (tid == 0) atomicAdd(&a.flags->n_cand, (unsigned long long)(ns + nc));
+
+  // 3. retained candidates: the lowest within delta is the representative
+  volatile int32_t* vh = &hit;
+  uint32_t esc = 0u;
+  for (int k = wave; k < ns; k += kAdmitThreads / 64) {
+    const int y = (int)list[k];
+    if (y >= __builtin_amdgcn_readfirstlane(*vh)) continue;   // wave-uniform: the wave then shuffles
+    bool e = false;
+    const bool in = pair_within(p, a.xs + (int64_t)y * a.D, a.D, a.d2, a.thr, &e);
+    esc += e ? 1u : 0u;
+    if (in && lane == 0) atomicMin(&hit, y);
+  }
+  __syncthreads();
+  if (hit != kNone) {
+    if (tid == 0) a.firstHit[i] = hit;
+  } else {
+    // 4. no retained row within delta: the chunk's earlier arrivals, for the resolve
+    const uint32_t* cl = list + kSetMax + kAdmitThreads - nc;
+    for (int k = wave; k < nc; k += kAdmitThreads / 64) {
+      const int j = (int)cl[k];
+      bool e = false;
+      const bool in = pair_within(p, a.xc + (int64_t)j * a.D, a.D, a.d2, a.thr, &e);
+      esc += e ? 1u : 0u;
+      if (in && lane == 0) {
+        atomicOr(reinterpret_cast<unsigned long long*>(&a.bitmap[(int64_t)i * a.W + (j >> 6)]), 1ull << (j & 63));
+        a.hasEdge[i] = 1u;
+      }
+    }
+  }
+  if (lane == 0 && esc) {
+    atomicAdd(&a.cc->n_escalate, esc);
+    atomicAdd(&a.flags->n_escalate, esc);
   }
 }
 
@@ -624,10 +759,7 @@ struct VerifyArgs {
   ChunkCounters* ccw;
 };
 
-// One wave per ambiguous pair: the squared distance in binary64 (error below
-// (D + 2) u64 d^2 in any order); a pair within that distance of delta^2 is
-// decided on exact integers by the same wave (exact.h), so every decision is
-// the exact one.
+// One wave per listed pair, decided by the merge predicate (pair_within).
 __global__ __launch_bounds__(256) void k_verify(VerifyArgs a) {
   if (skip_all(a.flags)) return;
   const uint32_t n = min(a.cc->npairs, a.pair_cap);
@@ -645,33 +777,11 @@ __global__ __launch_bounds__(256) void k_verify(VerifyArgs a) {
     }
     const float* pa = a.xc + (int64_t)i * a.D;
     const float* pb = (kind == 0 ? a.xs : a.xc) + (int64_t)y * a.D;
-    double s = 0.0;
-    for (int d = lane; d < a.D; d += 64) {
-      const double t = (double)pa[d] - (double)pb[d];
-      s = fma(t, t, s);
-    }
-    s = wave_sum_f64(s);   // every lane holds the sum
-    const double margin = (double)(a.D + 8) * 2.5e-16 * fmax(a.d2, s) + 1e-300;
-    bool in;
-    if (fabs(s - a.d2) <= margin) {
-      Big6 acc;
-      big_zero(acc);
-      for (int d = lane; d < a.D; d += 64)
-        big_add(acc, big_sq_diff(__float_as_uint(pa[d]), __float_as_uint(pb[d])));
-      for (int o = 32; o > 0; o >>= 1) {
-        Big6 other;
-#pragma unroll
-        for (int l = 0; l < kExactLimbs; ++l)
-          other.w[l] = (uint64_t)__shfl_xor((unsigned long long)acc.w[l], o);
-        big_add(acc, other);
-      }
-      in = big_cmp(acc, a.thr) <= 0;
-      if (lane == 0) {
-        atomicAdd(&a.ccw->n_escalate, 1u);
-        atomicAdd(&a.flags->n_escalate, 1u);
-      }
-    } else {
-      in = s <= a.d2;
+    bool escalated = false;
+    const bool in = pair_within(pa, pb, a.D, a.d2, a.thr, &escalated);
+    if (escalated && lane == 0) {
+      atomicAdd(&a.ccw->n_escalate, 1u);
+      atomicAdd(&a.flags->n_escalate, 1u);
     }
     if (lane != 0) continue;
     if (in) {
@@ -1263,6 +1373,12 @@ lam_status dedup_ingest(lam_ctx* ctx, lam_store* st, const float* x, int64_t n, 
     la.srowkey = st->lsh_rowkey;
     la.smask = st->lsh_slots - 1;
     la.meta = meta;
+    la.d2 = st->d2;
+    la.thr = st->thr;
+    la.firstHit = firstHit;
+    la.bitmap = bitmap;
+    la.W = W;
+    la.hasEdge = hasEdge;
     la.cc = cc;
     la.flags = ctx->flags_dev;
   }
@@ -1307,18 +1423,18 @@ lam_status dedup_ingest(lam_ctx* ctx, lam_store* st, const float* x, int64_t n, 
         la.pair_cap = cap;
         const int64_t ne = (int64_t)nB * la.nb;
         const int64_t nt = std::max<int64_t>(ne, (int64_t)la.bslots);
-        ProfScope ps(ctx, "dedup_lsh");
-        hipLaunchKernelGGL(k_lsh_keys, dim3((unsigned)((nt + 255) / 256)), dim3(256), 0, ctx->stream, la);
-        LAM_HIP(hipGetLastError());
-        const unsigned ge = (unsigned)((ne + 255) / 256);
-        if (m_before + c0 > 0) {
-          hipLaunchKernelGGL(k_lsh_query_store, dim3(ge), dim3(256), 0, ctx->stream, la);
+        {
+          ProfScope ps(ctx, "lsh_keys");
+          hipLaunchKernelGGL(k_lsh_keys, dim3((unsigned)((nt + 255) / 256)), dim3(256), 0, ctx->stream, la);
+          LAM_HIP(hipGetLastError());
+          hipLaunchKernelGGL(k_lsh_index_chunk, dim3((unsigned)((ne + 255) / 256)), dim3(256), 0, ctx->stream, la);
           LAM_HIP(hipGetLastError());
         }
-        hipLaunchKernelGGL(k_lsh_index_chunk, dim3(ge), dim3(256), 0, ctx->stream, la);
-        LAM_HIP(hipGetLastError());
-        hipLaunchKernelGGL(k_lsh_query_chunk, dim3(ge), dim3(256), 0, ctx->stream, la);
-        LAM_HIP(hipGetLastError());
+        {
+          ProfScope ps(ctx, "lsh_admit");
+          hipLaunchKernelGGL(k_lsh_admit, dim3((unsigned)nB), dim3(kAdmitThreads), (size_t)D * 4, ctx->stream, la);
+          LAM_HIP(hipGetLastError());
+        }
       }
       ScreenArgs sa{};
       sa.As = st->x16;
@@ -1385,6 +1501,7 @@ lam_status dedup_ingest(lam_ctx* ctx, lam_store* st, const float* x, int64_t n, 
       if (lsh) {
         // kept rows join the store's index before the append of the last
         // chunk hands the status words back (and zeroes them)
+        ProfScope ps(ctx, "lsh_insert");
         hipLaunchKernelGGL(k_lsh_insert, dim3((unsigned)(((int64_t)nB * la.nb + 255) / 256)), dim3(256), 0,
                            ctx->stream, la, pos, st->lsh_key, st->lsh_head, st->lsh_next, st->lsh_rowkey);
         LAM_HIP(hipGetLastError());
@@ -1427,7 +1544,7 @@ lam_status dedup_ingest(lam_ctx* ctx, lam_store* st, const float* x, int64_t n, 
       stats->n_kept = f.n_kept;
       stats->n_dropped = n - f.n_kept;
       stats->store_size = st->size;
-      stats->n_ambiguous_pairs = f.n_pairs;
+      stats->n_ambiguous_pairs = lsh ? (int64_t)f.n_cand : (int64_t)f.n_pairs;
       stats->n_exact_escalations = f.n_escalate;
       stats->delta_hat_call = dh_call;
       stats->delta_hat_run = st->delta_hat_run;

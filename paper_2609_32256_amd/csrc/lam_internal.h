@@ -74,8 +74,7 @@ struct DevFlags {
   uint32_t n_kept;         // arrivals retained by this ingest
   uint32_t pairs_needed;   // pair-list capacity that would have sufficed
   unsigned long long dhat2_bits;  // max merged d^2 (binary64 bits, non-negative)
-  uint32_t reserved;
-  uint32_t pad;
+  unsigned long long n_cand;      // candidate pairs of a banded store
 };
 
 // ------------------------------------------------------------------ profiling
