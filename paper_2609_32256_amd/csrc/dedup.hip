@@ -410,19 +410,29 @@ __global__ __launch_bounds__(C::kThreads, C::kMinWaves) void k_screen(ScreenArgs
 using ScreenTile = Tile<2, 2, 2, 2>;   // 128 x 128, four waves of 64 x 64
 
 // ------------------------------------------------------------------ merge predicate of one pair
-// sum_d (a_d - b_d)^2 <= delta^2 for float32 rows a, b, by one wave: the
-// squared distance in binary64 (error below (D + 2) u64 d^2 in any order); a
-// pair within that distance of delta^2 is decided on exact integers
-// (exact.h), so every decision is the exact one.  Every lane returns the
-// decision; *escalated tells whether the exact path ran.
+// sum_d (a_d - b_d)^2 <= delta^2 for float32 rows a, b (16-byte aligned, D a
+// multiple of 4) by a group of G lanes of one wave: the squared distance in
+// binary64 (error below (D + 2) u64 d^2 in any order); a pair within that
+// distance of delta^2 is decided on exact integers (exact.h), so every
+// decision is the exact one.  Every lane of the group returns the decision;
+// *escalated tells whether the exact path ran.  The G lanes of a group must
+// run it together.
+template <int G>
 __device__ bool pair_within(const float* pa, const float* pb, int D, double d2, const Big6& thr, bool* escalated) {
-  const int lane = threadIdx.x & 63;
+  static_assert(G == 16 || G == 32 || G == 64, "a group is a power of two within one wave");
+  const int gl = (int)threadIdx.x & (G - 1);
   double s = 0.0;
-  for (int d = lane; d < D; d += 64) {
-    const double t = (double)pa[d] - (double)pb[d];
-    s = fma(t, t, s);
+  for (int d = gl * 4; d < D; d += 4 * G) {
+    const float4 u = *reinterpret_cast<const float4*>(pa + d);
+    const float4 v = *reinterpret_cast<const float4*>(pb + d);
+    const double t0 = (double)u.x - (double)v.x, t1 = (double)u.y - (double)v.y;
+    const double t2 = (double)u.z - (double)v.z, t3 = (double)u.w - (double)v.w;
+    s = fma(t0, t0, s);
+    s = fma(t1, t1, s);
+    s = fma(t2, t2, s);
+    s = fma(t3, t3, s);
   }
-  s = wave_sum_f64(s);   // every lane holds the sum
+  for (int o = G / 2; o > 0; o >>= 1) s += __shfl_xor(s, o);   // every lane of the group holds the sum
   const double margin = (double)(D + 8) * 2.5e-16 * fmax(d2, s) + 1e-300;
   if (fabs(s - d2) > margin) {
     *escalated = false;
@@ -430,8 +440,15 @@ __device__ bool pair_within(const float* pa, const float* pb, int D, double d2, 
   }
   Big6 acc;
   big_zero(acc);
-  for (int d = lane; d < D; d += 64) big_add(acc, big_sq_diff(__float_as_uint(pa[d]), __float_as_uint(pb[d])));
-  for (int o = 32; o > 0; o >>= 1) {
+  for (int d = gl * 4; d < D; d += 4 * G) {
+    const uint4 u = *reinterpret_cast<const uint4*>(pa + d);
+    const uint4 v = *reinterpret_cast<const uint4*>(pb + d);
+    big_add(acc, big_sq_diff(u.x, v.x));
+    big_add(acc, big_sq_diff(u.y, v.y));
+    big_add(acc, big_sq_diff(u.z, v.z));
+    big_add(acc, big_sq_diff(u.w, v.w));
+  }
+  for (int o = G / 2; o > 0; o >>= 1) {
     Big6 other;
 #pragma unroll
     for (int l = 0; l < kExactLimbs; ++l) other.w[l] = (uint64_t)__shfl_xor((unsigned long long)acc.w[l], o);
@@ -461,6 +478,7 @@ constexpr int kSetSlots = 4096;               // LDS candidate set (a power of t
 constexpr int kSetMax = 3072;                 // entries before an arrival takes the pair list
 constexpr uint32_t kSetEmpty = 0xffffffffu;
 constexpr uint32_t kChunkBit = 0x80000000u;   // set entry of a chunk row (else a store position)
+static_assert(kSetMax + kAdmitThreads < kSetSlots, "the set always keeps an empty slot");
 
 struct LshArgs {
   const float* xc;            // chunk rows (float32)
@@ -595,7 +613,7 @@ __global__ __launch_bounds__(kAdmitThreads) void k_lsh_admit(LshArgs a) {
   __shared__ uint32_t n_set, n_store, n_chunk;
   __shared__ int32_t hit, skip;
   const int i = (int)blockIdx.x;
-  const int tid = (int)threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = (int)threadIdx.x;
   // one reading of the status words for the whole workgroup (another
   // workgroup's pair-list overflow may set them meanwhile)
   if (tid == 0) skip = skip_all(a.flags) ? 1 : 0;
@@ -635,7 +653,7 @@ __global__ __launch_bounds__(kAdmitThreads) void k_lsh_admit(LshArgs a) {
   __syncthreads();
 
   if (n_set >= (uint32_t)kSetMax) {
-    // 2'. too many candidates: each pair once, for its lowest equal band, to
+    // 1'. too many candidates: each pair once, for its lowest equal band, to
     //     the pair list (decided by k_verify)
     for (int b = tid; b < a.nb; b += kAdmitThreads) {
       band_rows(a, i, b, m, s_code, [&](uint32_t v) {
@@ -658,6 +676,7 @@ __global__ __launch_bounds__(kAdmitThreads) void k_lsh_admit(LshArgs a) {
     }
     return;
   }
+  if (tid == 0) atomicAdd(&a.flags->n_cand, (unsigned long long)n_set);
 
   // 2. the set as two lists: store positions from the front, chunk rows from the back
   for (int k = tid; k < kSetSlots; k += kAdmitThreads) {
@@ -670,18 +689,24 @@ __global__ __launch_bounds__(kAdmitThreads) void k_lsh_admit(LshArgs a) {
   }
   __syncthreads();
   const int ns = (int)n_store, nc = (int)n_chunk;
-  if (tid == 0) atomicAdd(&a.flags->n_cand, (unsigned long long)(ns + nc));
 
-  // 3. retained candidates: the lowest within delta is the representative
+  // 3. retained candidates, by groups of kGroup lanes (a wave's groups take
+  //    consecutive entries): the lowest within delta is the representative,
+  //    so a candidate above the lowest hit so far is skipped.  (Each reading
+  //    of hit is the same for every lane of a group: they read it in one
+  //    instruction.)
+  constexpr int kGroup = 16, kGroups = kAdmitThreads / kGroup;
+  const int grp = tid / kGroup;
+  const bool glead = (tid & (kGroup - 1)) == 0;
   volatile int32_t* vh = &hit;
   uint32_t esc = 0u;
-  for (int k = wave; k < ns; k += kAdmitThreads / 64) {
+  for (int k = grp; k < ns; k += kGroups) {
     const int y = (int)list[k];
-    if (y >= __builtin_amdgcn_readfirstlane(*vh)) continue;   // wave-uniform: the wave then shuffles
+    if (y >= *vh) continue;
     bool e = false;
-    const bool in = pair_within(p, a.xs + (int64_t)y * a.D, a.D, a.d2, a.thr, &e);
+    const bool in = pair_within<kGroup>(p, a.xs + (int64_t)y * a.D, a.D, a.d2, a.thr, &e);
     esc += e ? 1u : 0u;
-    if (in && lane == 0) atomicMin(&hit, y);
+    if (in && glead) atomicMin(&hit, y);
   }
   __syncthreads();
   if (hit != kNone) {
@@ -689,18 +714,18 @@ __global__ __launch_bounds__(kAdmitThreads) void k_lsh_admit(LshArgs a) {
   } else {
     // 4. no retained row within delta: the chunk's earlier arrivals, for the resolve
     const uint32_t* cl = list + kSetMax + kAdmitThreads - nc;
-    for (int k = wave; k < nc; k += kAdmitThreads / 64) {
+    for (int k = grp; k < nc; k += kGroups) {
       const int j = (int)cl[k];
       bool e = false;
-      const bool in = pair_within(p, a.xc + (int64_t)j * a.D, a.D, a.d2, a.thr, &e);
+      const bool in = pair_within<kGroup>(p, a.xc + (int64_t)j * a.D, a.D, a.d2, a.thr, &e);
       esc += e ? 1u : 0u;
-      if (in && lane == 0) {
+      if (in && glead) {
         atomicOr(reinterpret_cast<unsigned long long*>(&a.bitmap[(int64_t)i * a.W + (j >> 6)]), 1ull << (j & 63));
         a.hasEdge[i] = 1u;
       }
     }
   }
-  if (lane == 0 && esc) {
+  if (glead && esc) {
     atomicAdd(&a.cc->n_escalate, esc);
     atomicAdd(&a.flags->n_escalate, esc);
   }
@@ -778,7 +803,7 @@ __global__ __launch_bounds__(256) void k_verify(VerifyArgs a) {
     const float* pa = a.xc + (int64_t)i * a.D;
     const float* pb = (kind == 0 ? a.xs : a.xc) + (int64_t)y * a.D;
     bool escalated = false;
-    const bool in = pair_within(pa, pb, a.D, a.d2, a.thr, &escalated);
+    const bool in = pair_within<64>(pa, pb, a.D, a.d2, a.thr, &escalated);
     if (escalated && lane == 0) {
       atomicAdd(&a.ccw->n_escalate, 1u);
       atomicAdd(&a.flags->n_escalate, 1u);
