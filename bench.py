@@ -16,7 +16,7 @@ value = near-duplicate pairs per second of the whole step, counting the
 algorithmic pairs of exhaustive greedy (each arrival against every row
 retained at its arrival).
 
-Usage: python bench.py [--steps K] [--warmup W] [--no-cpu-baseline]
+Usage: python bench.py [--steps K] [--warmup W] [--no-cpu-baseline] [--band-grid]
 Prints one JSON line.
 """
 from __future__ import annotations
@@ -39,6 +39,7 @@ RAW_SETS = 4
 BAND_R = 4          # band width and quantizer step (eps = rel * sigma, sigma = 1 / sqrt(D))
 BAND_REL = 0.2      # of the banded candidate index, the operating point for tau = 0.95
 BAND_REPS = 5
+BAND_PREFIX = 4096  # arrivals of the grid's trial run per setting
 
 
 def parse():
@@ -47,6 +48,9 @@ def parse():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true", help="skip timing the CPU oracle")
+    ap.add_argument("--band-grid", action="store_true",
+                    help="instead of the step: the banded candidate index over band widths 2..32 and steps "
+                         "0.01..0.3 sigma on the subset stream (one JSON line)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after the timed steps, run a plain 1 GiB device-to-device copy three times (a "
                          "known-size reference for hardware byte counters)")
@@ -103,15 +107,16 @@ def cpu_baseline(x, pairs):
                          f"binary64 BLAS screen + exact rational ties)"}
 
 
-def banded_ingest(lam, torch, np, xd, rep_exh, pairs, ctx):
-    """The subset stream through a store with the banded candidate index next
-    to the screened store: candidate pairs against the exhaustive pair count,
-    removal and agreement with exhaustive greedy, and the time of a whole-stream
-    ingest (calls that do not wait) for both stores."""
+def banded_ingest(lam, torch, np, xd, rep_exh, pairs, ctx, r=BAND_R, rel=BAND_REL, reps=BAND_REPS,
+                  screened=True):
+    """The subset stream through a store with the banded candidate index
+    (band width r, step eps = rel / sqrt(D)) next to the screened store:
+    candidate pairs against the exhaustive pair count, removal and agreement
+    with exhaustive greedy, and the time of a whole-stream ingest (calls that
+    do not wait) for both stores."""
     n = xd.shape[0]
-    eps = BAND_REL / D ** 0.5
-    band = lam.Store(D, TAU, n, ctx=ctx, eps_band=eps, band_width=BAND_R)
-    plain = lam.Store(D, TAU, n, ctx=ctx)
+    eps = rel / D ** 0.5
+    band = lam.Store(D, TAU, n, ctx=ctx, eps_band=eps, band_width=r)
     outs = [torch.empty(min(BATCH, n - b0), dtype=torch.int64, device=xd.device) for b0 in range(0, n, BATCH)]
 
     def stream(s, sync):
@@ -123,20 +128,65 @@ def banded_ingest(lam, torch, np, xd, rep_exh, pairs, ctx):
     stats = stream(band, True)
     brep = torch.cat(outs).cpu().numpy()
     cand = sum(st["n_ambiguous_pairs"] for st in stats)
+    stores = [("banded", band)] + ([("screened", lam.Store(D, TAU, n, ctx=ctx))] if screened else [])
     times = {}
-    for name, s in (("banded", band), ("screened", plain)):
+    for name, s in stores:
         stream(s, False)
         torch.cuda.synchronize()
         t0 = time.perf_counter()
-        for _ in range(BAND_REPS):
+        for _ in range(reps):
             stream(s, False)
         torch.cuda.synchronize()
-        times[name] = (time.perf_counter() - t0) * 1e3 / BAND_REPS
+        times[name] = (time.perf_counter() - t0) * 1e3 / reps
     kept = int(np.count_nonzero(brep < 0))
-    return {"band_width": BAND_R, "eps_band": eps, "rel": BAND_REL,
-            "candidate_pairs": int(cand), "exhaustive_pairs": int(pairs), "candidate_frac": cand / pairs,
-            "kept": kept, "removal": 1.0 - kept / n, "rep_equal_to_exhaustive": bool(np.array_equal(brep, rep_exh)),
-            "ms_per_stream": times["banded"], "screened_ms_per_stream": times["screened"]}
+    dropped_exh = int(np.count_nonzero(rep_exh >= 0))
+    out = {"band_width": r, "eps_band": eps, "rel": rel,
+           "candidate_pairs": int(cand), "exhaustive_pairs": int(pairs), "candidate_frac": cand / pairs,
+           "kept": kept, "removal": 1.0 - kept / n, "removal_recall": (n - kept) / max(dropped_exh, 1),
+           "rep_agreement": float(np.mean(brep == rep_exh)),
+           "rep_equal_to_exhaustive": bool(np.array_equal(brep, rep_exh)), "ms_per_stream": times["banded"]}
+    if screened:
+        out["screened_ms_per_stream"] = times["screened"]
+    del band
+    return out
+
+
+def band_grid(lam, torch, np, synth, ctx):
+    """Band width x quantizer step grid (Appendix "Band width and quantizer
+    step") on the subset stream: per setting the candidate share of the
+    exhaustive pairs, removal recall against exhaustive greedy and the
+    stream's ingest time."""
+    cfg = synth.subset_ingest()
+    xfull = torch.from_numpy(cfg["x"]).cuda()
+
+    def exhaustive(xd):
+        n = xd.shape[0]
+        plain = lam.Store(D, TAU, n, ctx=ctx)
+        rep = torch.cat([plain.ingest(xd[b0:b0 + BATCH])[0] for b0 in range(0, n, BATCH)]).cpu().numpy()
+        return rep, int(np.concatenate([[0], np.cumsum(rep < 0)[:-1]]).sum())
+
+    # Settings whose candidates exceed a fifth of the exhaustive pairs on the
+    # stream's first 4,096 arrivals are reported on that prefix only: there
+    # most arrivals overflow the per-arrival candidate set.
+    xpre = xfull[:BAND_PREFIX]
+    rep_full, pairs_full = exhaustive(xfull)
+    rep_pre, pairs_pre = exhaustive(xpre)
+    pairs = pairs_full
+    grid = []
+    for r in (2, 4, 8, 16, 32):
+        for rel in (0.01, 0.05, 0.1, 0.2, 0.3):
+            pt = banded_ingest(lam, torch, np, xpre, rep_pre, pairs_pre, ctx, r=r, rel=rel, reps=1, screened=False)
+            pt["arrivals"] = BAND_PREFIX
+            if pt["candidate_frac"] <= 0.2:
+                pt = banded_ingest(lam, torch, np, xfull, rep_full, pairs_full, ctx, r=r, rel=rel, reps=2,
+                                   screened=False)
+                pt["arrivals"] = int(xfull.shape[0])
+            grid.append(pt)
+            print(json.dumps({"progress": [r, rel], "ms": round(pt["ms_per_stream"], 2),
+                              "candidate_frac": round(pt["candidate_frac"], 5),
+                              "removal_recall": round(pt["removal_recall"], 4)}), file=sys.stderr, flush=True)
+    return {"workload": cfg["name"], "tau": TAU, "sigma": 1.0 / D ** 0.5, "exhaustive_pairs": pairs,
+            "exhaustive_removal": float(np.mean(rep_full >= 0)), "grid": grid}
 
 
 def main():
@@ -156,6 +206,9 @@ def main():
         sys.exit(2)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.band_grid:
+        print(json.dumps(band_grid(lam, torch, np, synth, lam.default_context())), flush=True)
+        return
 
     # ------------------------------------------------------------ inputs (resident in HBM)
     raw = synth.raw_qeps(log2n=RAW_LOG2N)["x"]
