@@ -407,7 +407,12 @@ __global__ __launch_bounds__(C::kThreads, C::kMinWaves) void k_screen(ScreenArgs
   }
 }
 
-using ScreenTile = Tile<2, 2, 2, 2>;   // 128 x 128, four waves of 64 x 64
+// 128 x 128, eight waves of 64 x 32 held to 128 registers, so that LDS (two
+// 37 KB stages) and registers both allow two workgroups (four waves per SIMD)
+// per CU: the short reductions (D = 768) are latency-bound, and this
+// occupancy took the subset stream's screen from 1.16 to 1.01 ms against
+// four waves of 64 x 64 at two waves per SIMD.
+using ScreenTile = Tile<2, 4, 2, 1, 4>;
 
 // ------------------------------------------------------------------ merge predicate of one pair
 // sum_d (a_d - b_d)^2 <= delta^2 for float32 rows a, b (16-byte aligned, D a

@@ -1,12 +1,12 @@
 // MFMA tile machinery shared by the similarity screen and the scoring kernel.
 //
-// A workgroup of 256 threads (4 waves of 64) computes a 128 x 128 block of
-// C = A . B^T where A and B are row-major with the reduction dimension
-// contiguous ("K-major" on both sides).  Waves sit on a 2 x 2 grid; each wave
-// owns 64 x 64 of C as 2 x 2 tiles of v_mfma_f32_32x32x16_f16 (CDNA4), i.e.
-// 64 fp32 accumulators per lane.  Operands are staged through LDS in K-slabs
-// of 64 halves per row (two stages), with rows padded by 8 halves so that the
-// 32 rows read by one fragment load fall on distinct LDS banks.
+// A workgroup of WM x WN waves computes a block of C = A . B^T where A and B
+// are row-major with the reduction dimension contiguous ("K-major" on both
+// sides); each wave owns TI x TJ tiles of v_mfma_f32_32x32x16_f16 (CDNA4),
+// i.e. 16 * TI * TJ fp32 accumulators per lane.  Operands are staged through
+// LDS in K-slabs of 64 halves per row (two stages), with rows padded by 8
+// halves so that the 32 rows read by one fragment load fall on distinct LDS
+// banks.
 //
 // Fragment layout of the 32x32x16 instruction (wave64):
 //   A operand: lane l supplies A[i = l % 32][k = 8 * (l / 32) + e], e = 0..7
@@ -97,7 +97,7 @@ __device__ __forceinline__ int acc_row(int r, int lane) { return 8 * (r >> 2) + 
 // Block shape: WM x WN waves, each owning TI x TJ tiles of 32 x 32, so a
 // workgroup computes (WM*TI*32) x (WN*TJ*32) of C = A . B^T.  Larger per-wave
 // tiles read fewer LDS bytes per MFMA: (TI + TJ) / (TI * TJ) KB.
-template <int WM_, int WN_, int TI_, int TJ_>
+template <int WM_, int WN_, int TI_, int TJ_, int MW_ = 2>
 struct Tile {
   static constexpr int WM = WM_, WN = WN_, TI = TI_, TJ = TJ_;
   static constexpr int kWaves = WM * WN;
@@ -109,8 +109,8 @@ struct Tile {
   static constexpr int kPerA = kChunksA / kThreads;
   static constexpr int kPerB = kChunksB / kThreads;
   static constexpr int kLdsHalves = 2 * (BM + BN) * kLdk;   // two K-slab stages of A and B
-  // waves per SIMD the register budget is held to (256 registers per lane)
-  static constexpr int kMinWaves = 2;
+  // waves per SIMD the register budget is held to (512 / MW registers per lane)
+  static constexpr int kMinWaves = MW_;
   static_assert(kChunksA % kThreads == 0 && kChunksB % kThreads == 0, "slab must split evenly");
 };
 
@@ -166,34 +166,18 @@ __device__ __forceinline__ bool gemm_tile(const _Float16* __restrict__ A, int ra
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.0f;
   auto compute = [&](int st) {
-    // fragments double-buffered in registers: step kk + 1's LDS reads are
-    // issued between step kk's MFMAs
-    half8 fa[2][C::TI], fb[2][C::TJ];
-#pragma unroll
-    for (int t = 0; t < C::TI; ++t) fa[0][t] = frag_load(sa(st), wm * C::TI * 32 + t * 32, 0);
-#pragma unroll
-    for (int t = 0; t < C::TJ; ++t) fb[0][t] = frag_load(sb(st), wn * C::TJ * 32 + t * 32, 0);
 #pragma unroll
     for (int kk = 0; kk < kBK / 16; ++kk) {
-      const int cb = kk & 1, nb = cb ^ 1;
-      if (kk + 1 < kBK / 16) {
+      half8 fa[C::TI], fb[C::TJ];
 #pragma unroll
-        for (int t = 0; t < C::TI; ++t) fa[nb][t] = frag_load(sa(st), wm * C::TI * 32 + t * 32, kk + 1);
+      for (int t = 0; t < C::TI; ++t) fa[t] = frag_load(sa(st), wm * C::TI * 32 + t * 32, kk);
 #pragma unroll
-        for (int t = 0; t < C::TJ; ++t) fb[nb][t] = frag_load(sb(st), wn * C::TJ * 32 + t * 32, kk + 1);
-      }
+      for (int t = 0; t < C::TJ; ++t) fb[t] = frag_load(sb(st), wn * C::TJ * 32 + t * 32, kk);
 #pragma unroll
       for (int a = 0; a < C::TI; ++a)
 #pragma unroll
         for (int b = 0; b < C::TJ; ++b)
-          acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fa[cb][a], fb[cb][b], acc[a][b], 0, 0, 0);
-      if (kk + 1 < kBK / 16) {
-#pragma unroll
-        for (int i = 0; i < C::TI + C::TJ; ++i) {
-          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one MFMA
-          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // one LDS read
-        }
-      }
+          acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fa[a], fb[b], acc[a][b], 0, 0, 0);
     }
   };
   const int S = NS > 0 ? NS : (kdim + kBK - 1) / kBK;
