@@ -1122,9 +1122,15 @@ __global__ __launch_bounds__(256) void k_append(AppendArgs a, int nB) {
     const int rr = a.rep_row[r];
     const float* b = (rr >= 0) ? a.xs + (int64_t)rr * a.D : a.xc + (int64_t)(-rr - 2) * a.D;
     double s = 0.0;
-    for (int d = lane; d < a.D; d += 64) {
-      const double t = (double)src[d] - (double)b[d];
-      s = fma(t, t, s);
+    for (int d = lane * 4; d < a.D; d += 256) {
+      const float4 u = *reinterpret_cast<const float4*>(src + d);
+      const float4 w = *reinterpret_cast<const float4*>(b + d);
+      const double t0 = (double)u.x - (double)w.x, t1 = (double)u.y - (double)w.y;
+      const double t2 = (double)u.z - (double)w.z, t3 = (double)u.w - (double)w.w;
+      s = fma(t0, t0, s);
+      s = fma(t1, t1, s);
+      s = fma(t2, t2, s);
+      s = fma(t3, t3, s);
     }
     dmax = fmax(dmax, wave_sum_f64(s));
   }

@@ -26,12 +26,14 @@ struct Big6 {
 };
 
 __host__ __device__ inline void big_zero(Big6& a) {
+#pragma unroll
   for (int i = 0; i < kExactLimbs; ++i) a.w[i] = 0u;
 }
 
 // a += b (no overflow for the magnitudes above)
 __host__ __device__ inline void big_add(Big6& a, const Big6& b) {
   uint64_t carry = 0u;
+#pragma unroll
   for (int i = 0; i < kExactLimbs; ++i) {
     const uint64_t s = a.w[i] + b.w[i];
     const uint64_t c1 = s < a.w[i] ? 1u : 0u;
@@ -45,6 +47,7 @@ __host__ __device__ inline void big_add(Big6& a, const Big6& b) {
 // a -= b, requires a >= b
 __host__ __device__ inline void big_sub(Big6& a, const Big6& b) {
   uint64_t borrow = 0u;
+#pragma unroll
   for (int i = 0; i < kExactLimbs; ++i) {
     const uint64_t d = a.w[i] - b.w[i];
     const uint64_t b1 = a.w[i] < b.w[i] ? 1u : 0u;
@@ -56,18 +59,22 @@ __host__ __device__ inline void big_sub(Big6& a, const Big6& b) {
 }
 
 __host__ __device__ inline int big_cmp(const Big6& a, const Big6& b) {
+#pragma unroll
   for (int i = kExactLimbs - 1; i >= 0; --i)
     if (a.w[i] != b.w[i]) return a.w[i] < b.w[i] ? -1 : 1;
   return 0;
 }
 
-// m * 2^s for m < 2^64, 0 <= s < 384 - 64
+// m * 2^s for m < 2^64, 0 <= s < 384 - 64.  Every limb is selected with a
+// constant index, so the limbs stay in registers (a run-time index would put
+// the array in scratch memory).
 __host__ __device__ inline Big6 big_shifted(uint64_t m, int s) {
-  Big6 r;
-  big_zero(r);
   const int limb = s >> 6, bit = s & 63;
-  if (limb < kExactLimbs) r.w[limb] = m << bit;
-  if (bit != 0 && limb + 1 < kExactLimbs) r.w[limb + 1] = m >> (64 - bit);
+  const uint64_t lo = m << bit;
+  const uint64_t hi = bit != 0 ? m >> (64 - bit) : 0u;
+  Big6 r;
+#pragma unroll
+  for (int i = 0; i < kExactLimbs; ++i) r.w[i] = (i == limb ? lo : 0u) | (i == limb + 1 ? hi : 0u);
   return r;
 }
 
@@ -106,9 +113,10 @@ __host__ __device__ inline Big6 big_sq_diff(uint32_t ua, uint32_t ub) {
   // d < 2^158 lives in limbs 0..2; the square in limbs 0..5
   Big6 r;
   big_zero(r);
+#pragma unroll
   for (int i = 0; i < 3; ++i) {
-    if (d.w[i] == 0u) continue;
     uint64_t carry = 0u;
+#pragma unroll
     for (int j = 0; j < 3; ++j) {
       const uint64_t lo = d.w[i] * d.w[j];
       const uint64_t hi = mul_hi64(d.w[i], d.w[j]);
@@ -120,7 +128,8 @@ __host__ __device__ inline Big6 big_sq_diff(uint32_t ua, uint32_t ub) {
       r.w[i + j] = t;
       carry = hi + c;   // d_i d_j + r + carry < 2^128, so this high word cannot wrap
     }
-    for (int k = i + 3; k < kExactLimbs && carry != 0u; ++k) {
+#pragma unroll
+    for (int k = i + 3; k < kExactLimbs; ++k) {   // constant indices: the limbs stay in registers
       const uint64_t s = r.w[k] + carry;
       carry = s < carry ? 1u : 0u;
       r.w[k] = s;
