@@ -16,7 +16,7 @@ value = near-duplicate pairs per second of the whole step, counting the
 algorithmic pairs of exhaustive greedy (each arrival against every row
 retained at its arrival).
 
-Usage: python bench.py [--steps K] [--warmup W] [--no-cpu-baseline] [--band-grid]
+Usage: python bench.py [--steps K] [--warmup W] [--no-cpu-baseline] [--no-extras] [--band-grid]
 Prints one JSON line.
 """
 from __future__ import annotations
@@ -51,6 +51,9 @@ def parse():
     ap.add_argument("--band-grid", action="store_true",
                     help="instead of the step: the banded candidate index over band widths 2..32 and steps "
                          "0.01..0.3 sigma on the subset stream (one JSON line)")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="skip the measurements beside the step (removal ceiling, certificate, block codec, "
+                         "banded stream), so that a profiler sees the steps only")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after the timed steps, run a plain 1 GiB device-to-device copy three times (a "
                          "known-size reference for hardware byte counters)")
@@ -149,6 +152,21 @@ def banded_ingest(lam, torch, np, xd, rep_exh, pairs, ctx, r=BAND_R, rel=BAND_RE
         out["screened_ms_per_stream"] = times["screened"]
     del band
     return out
+
+
+def beside_the_step(lam, torch, np, xd, qd, store, rep, pairs, ctx):
+    """Measurements beside the timed step (not in it): the removal ceiling of
+    the stream, the share of benchmark queries whose top-10 is certified
+    rank-invariant, the per-block codec's size on the retained store, and the
+    stream through the banded candidate index."""
+    ceil = lam.removal_ceiling(xd, TAU, batch=BATCH, ctx=ctx)
+    cert = store.score_topk_certified(qd, TOPK)[3]
+    blk = store.block_encode()
+    return {"removal_ceiling": {k: ceil[k] for k in ("kept", "kept_2delta", "removal", "ceiling",
+                                                     "frac_of_ceiling", "bits_lo", "bits_hi")},
+            "certified_top10_frac": float(cert.float().mean().item()),
+            "block_codec": {k: blk[k] for k in ("bits_per_code", "plain_bits", "codec_ratio", "composite_ratio")},
+            "banded": banded_ingest(lam, torch, np, xd, rep, pairs, ctx)}
 
 
 def band_grid(lam, torch, np, synth, ctx):
@@ -337,17 +355,9 @@ def main():
         roofline = {"kernel": dominant, "bound": "latency", "achieved": None, "peak": None, "unit": None,
                     "frac": None, "traffic": None}
 
-    # beside the timed step (not in it): the removal ceiling of the stream, the
-    # share of benchmark queries whose top-10 is certified rank-invariant, and
-    # the per-block codec's size on the retained store
-    ceil = lam.removal_ceiling(xd, TAU, batch=BATCH, ctx=ctx)
-    cert = store.score_topk_certified(qd, TOPK)[3]
-    blk = store.block_encode()
-    extras = {"removal_ceiling": {k: ceil[k] for k in ("kept", "kept_2delta", "removal", "ceiling",
-                                                         "frac_of_ceiling", "bits_lo", "bits_hi")},
-              "certified_top10_frac": float(cert.float().mean().item()),
-              "block_codec": {k: blk[k] for k in ("bits_per_code", "plain_bits", "codec_ratio", "composite_ratio")},
-              "banded": banded_ingest(lam, torch, np, xd, rep, pairs, ctx)}
+    extras = {}
+    if not args.no_extras:
+        extras = beside_the_step(lam, torch, np, xd, qd, store, rep, pairs, ctx)
 
     value = pairs / (ms / 1e3) / 1e6
     enc = kinfo.get("qeps_encode", {})
