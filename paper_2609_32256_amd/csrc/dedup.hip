@@ -228,7 +228,10 @@ __device__ __forceinline__ void push_pair(const ScreenArgs& a, int i, int kind, 
 // [nb0, nb0 + nb1), MODE 1: A = B = chunk rows, pairs ia < ib only).  The
 // A side of the error bound is the largest per-row term among the tile's own
 // A rows.
-template <class C, bool WANT_MAX>
+// NS > 0: the reduction has exactly NS slabs of 64 (D = 64 NS), fully
+// unrolled; NS = 0: any D.  Each is its own kernel, so each gets its own
+// register allocation (the unrolled ones need no scratch memory).
+template <class C, bool WANT_MAX, int NS>
 __global__ __launch_bounds__(C::kThreads, C::kMinWaves) void k_screen(ScreenArgs a) {
   static_assert(C::BM == C::BN, "the in-chunk triangle needs square tiles");
   static_assert(C::BM <= C::kThreads, "one thread per A row for the row terms");
@@ -304,15 +307,7 @@ __global__ __launch_bounds__(C::kThreads, C::kMinWaves) void k_screen(ScreenArgs
     rowsA = min(C::BM, a.meta->m - ta * C::BM);
     return rowsA > 0;
   };
-  bool ran;
-  // the common dims get a fully unrolled reduction
-  if (a.D == 768)
-    ran = gemm_tile<C, 12>(tA, rowsLim, tB, rowsB, a.D, a.D, lds, acc, go_on);
-  else if (a.D == 1024)
-    ran = gemm_tile<C, 16>(tA, rowsLim, tB, rowsB, a.D, a.D, lds, acc, go_on);
-  else
-    ran = gemm_tile<C>(tA, rowsLim, tB, rowsB, a.D, a.D, lds, acc, go_on);
-  if (!ran) return;
+  if (!gemm_tile<C, NS>(tA, rowsLim, tB, rowsB, a.D, a.D, lds, acc, go_on)) return;
   if ((int)threadIdx.x >= rowsA) eA = 0.0f;
 
   {
@@ -1507,12 +1502,16 @@ lam_status dedup_ingest(lam_ctx* ctx, lam_store* st, const float* x, int64_t n, 
       LAM_CHECK(grid < (1LL << 31), LAM_EINVAL, "screen grid too large");
       if (!lsh) {
         ProfScope ps(ctx, "dedup_screen");
+        // the common dims get a fully unrolled reduction
+        const dim3 g((unsigned)grid), b(ScreenTile::kThreads);
         if (want_max)
-          hipLaunchKernelGGL((k_screen<ScreenTile, true>), dim3((unsigned)grid), dim3(ScreenTile::kThreads), 0,
-                             ctx->stream, sa);
+          hipLaunchKernelGGL((k_screen<ScreenTile, true, 0>), g, b, 0, ctx->stream, sa);
+        else if (D == 768)
+          hipLaunchKernelGGL((k_screen<ScreenTile, false, 12>), g, b, 0, ctx->stream, sa);
+        else if (D == 1024)
+          hipLaunchKernelGGL((k_screen<ScreenTile, false, 16>), g, b, 0, ctx->stream, sa);
         else
-          hipLaunchKernelGGL((k_screen<ScreenTile, false>), dim3((unsigned)grid), dim3(ScreenTile::kThreads), 0,
-                             ctx->stream, sa);
+          hipLaunchKernelGGL((k_screen<ScreenTile, false, 0>), g, b, 0, ctx->stream, sa);
         LAM_HIP(hipGetLastError());
       }
       VerifyArgs va{pairs, status, cc, cap, xc, st->x32, D, st->d2, st->thr, firstHit, bitmap, W, hasEdge,
