@@ -839,6 +839,7 @@ struct ResolveArgs {
 };
 
 constexpr int kResolveThreads = 1024;
+static_assert(kChunk % kResolveThreads == 0, "whole rows per thread");
 constexpr int kEdgeCap = 20480;    // in-chunk candidate entries held in LDS
 
 // Fallback when the candidate lists do not fit in LDS: one wave walks the
@@ -909,22 +910,37 @@ __global__ __launch_bounds__(kResolveThreads) void k_resolve(ResolveArgs a) {
   __shared__ uint32_t n_active, n_edges, pending;
   __shared__ int wsum[kResolveThreads / 64];
   volatile uint8_t* st = st_;
-  if (skip_all(a.flags)) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // A. the first phase's loads (hits and edge flags of this thread's rows, the
+  //    status words, the store's counts) are all issued before any is used
+  constexpr int kRowsPerThread = kChunk / kResolveThreads;
+  int32_t hit_r[kRowsPerThread];
+  uint32_t edge_r[kRowsPerThread];
+#pragma unroll
+  for (int u = 0; u < kRowsPerThread; ++u) {
+    const int r = min(tid + u * kResolveThreads, a.nB - 1);
+    hit_r[u] = a.firstHit[r];
+    edge_r[u] = a.hasEdge[r];
+  }
+  const bool skip = skip_all(a.flags);
   const int m0 = a.meta->m;
   const int64_t gbase = a.meta->n_seen + a.c0;   // updated only at the end of a call
+  if (skip) return;   // (the status words do not change while this single workgroup runs)
   if (tid == 0) {
     n_active = 0u;
     n_edges = 0u;
   }
   __syncthreads();
-  for (int r = tid; r < a.nB; r += kResolveThreads) {
-    const int32_t hit = a.firstHit[r];
+#pragma unroll
+  for (int u = 0; u < kRowsPerThread; ++u) {
+    const int r = tid + u * kResolveThreads;
+    if (r >= a.nB) break;
+    const int32_t hit = hit_r[u];
     if (hit != kNone) {
       st[r] = 2;
       a.rep[r] = a.store_ids[hit];
       a.rep_row[r] = hit;
-    } else if (a.hasEdge[r] == 0u) {
+    } else if (edge_r[u] == 0u) {
       st[r] = 1;
       a.rep[r] = -1;
       a.rep_row[r] = -1;
@@ -1088,46 +1104,84 @@ struct AppendArgs {
 // and the workgroup's maximum goes to the measured bound with one atomic.
 constexpr int kAppendRows = 4;
 
+constexpr int kAppendVec = 4;   // float4 of a row per lane held in registers (D <= 1,024)
+
 __global__ __launch_bounds__(256) void k_append(AppendArgs a, int nB) {
-  const bool skip = skip_all(a.flags);
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
+  const int r = (int)blockIdx.x * kAppendRows + wave;   // one row per wave
+  const int rc = min(r, nB - 1);
+  // Every load that depends on no other is issued before any is used: the
+  // row's decision, its terms, the status words, the arrival count and (for
+  // D <= 1,024) the row itself through a buffer resource (zeros past the row).
+  const int p = a.pos[rc];
+  const int rr = a.rep_row[rc];
+  const float hn = a.hnc[rc], et = a.etc[rc];
+  const bool skip = skip_all(a.flags);
   // every workgroup reads n_seen before the last one (below) advances it
   const int64_t gbase = a.meta->n_seen + a.c0;
+  const float* src = a.xc + (int64_t)rc * a.D;
+  const bool vec = a.D <= 256 * kAppendVec;
+  float4 v[kAppendVec];
+  {
+    const __amdgpu_buffer_rsrc_t rs = f32_rsrc(src, vec ? a.D : 0);
+#pragma unroll
+    for (int u = 0; u < kAppendVec; ++u)
+      v[u] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(rs, (uint32_t)(u * 256 + lane * 4) * 4u, 0, 0));
+  }
   double dmax = 0.0;
-  for (int r = blockIdx.x * kAppendRows + wave; !skip && r < min(nB, (int)(blockIdx.x + 1) * kAppendRows);
-       r += 4) {
-    const int p = a.pos[r];
-    const float* src = a.xc + (int64_t)r * a.D;
+  if (!skip && r < nB) {
     if (p >= 0) {
       float* dst = a.xs + (int64_t)p * a.D;
-      for (int d = lane * 4; d < a.D; d += 256)
-        *reinterpret_cast<float4*>(dst + d) = *reinterpret_cast<const float4*>(src + d);
-      const _Float16* s16 = a.x16c + (int64_t)r * a.D;
       _Float16* d16 = a.x16s + (int64_t)p * a.D;
-      for (int d = lane * 8; d < a.D; d += 512)
-        *reinterpret_cast<uint4*>(d16 + d) = *reinterpret_cast<const uint4*>(s16 + d);
+      if (vec) {
+        // the fp16 operand is formed as the prep forms it, fl16(2^8 x)
+#pragma unroll
+        for (int u = 0; u < kAppendVec; ++u) {
+          const int d = u * 256 + lane * 4;
+          if (d >= a.D) break;
+          *reinterpret_cast<float4*>(dst + d) = v[u];
+          const _Float16 h[4] = {(_Float16)(v[u].x * kScale), (_Float16)(v[u].y * kScale),
+                                 (_Float16)(v[u].z * kScale), (_Float16)(v[u].w * kScale)};
+          uint2 packed;
+          __builtin_memcpy(&packed, h, 8);
+          *reinterpret_cast<uint2*>(d16 + d) = packed;
+        }
+      } else {
+        for (int d = lane * 4; d < a.D; d += 256)
+          *reinterpret_cast<float4*>(dst + d) = *reinterpret_cast<const float4*>(src + d);
+        const _Float16* s16 = a.x16c + (int64_t)r * a.D;
+        for (int d = lane * 8; d < a.D; d += 512)
+          *reinterpret_cast<uint4*>(d16 + d) = *reinterpret_cast<const uint4*>(s16 + d);
+      }
       if (lane == 0) {
-        a.hns[p] = a.hnc[r];
-        a.ets[p] = a.etc[r];
+        a.hns[p] = hn;
+        a.ets[p] = et;
         a.ids[p] = gbase + r;
       }
-      continue;
+    } else {
+      const float* b = (rr >= 0) ? a.xs + (int64_t)rr * a.D : a.xc + (int64_t)(-rr - 2) * a.D;
+      double s = 0.0;
+      auto acc4 = [&](const float4& x, const float4& y) {
+        const double t0 = (double)x.x - (double)y.x, t1 = (double)x.y - (double)y.y;
+        const double t2 = (double)x.z - (double)y.z, t3 = (double)x.w - (double)y.w;
+        s = fma(t0, t0, s);
+        s = fma(t1, t1, s);
+        s = fma(t2, t2, s);
+        s = fma(t3, t3, s);
+      };
+      if (vec) {
+        const __amdgpu_buffer_rsrc_t rb = f32_rsrc(b, a.D);
+#pragma unroll
+        for (int u = 0; u < kAppendVec; ++u)
+          acc4(v[u], __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(
+                                                    rb, (uint32_t)(u * 256 + lane * 4) * 4u, 0, 0)));
+      } else {
+        for (int d = lane * 4; d < a.D; d += 256)
+          acc4(*reinterpret_cast<const float4*>(src + d), *reinterpret_cast<const float4*>(b + d));
+      }
+      dmax = wave_sum_f64(s);
     }
-    const int rr = a.rep_row[r];
-    const float* b = (rr >= 0) ? a.xs + (int64_t)rr * a.D : a.xc + (int64_t)(-rr - 2) * a.D;
-    double s = 0.0;
-    for (int d = lane * 4; d < a.D; d += 256) {
-      const float4 u = *reinterpret_cast<const float4*>(src + d);
-      const float4 w = *reinterpret_cast<const float4*>(b + d);
-      const double t0 = (double)u.x - (double)w.x, t1 = (double)u.y - (double)w.y;
-      const double t2 = (double)u.z - (double)w.z, t3 = (double)u.w - (double)w.w;
-      s = fma(t0, t0, s);
-      s = fma(t1, t1, s);
-      s = fma(t2, t2, s);
-      s = fma(t3, t3, s);
-    }
-    dmax = fmax(dmax, wave_sum_f64(s));
   }
   __shared__ double part[4];
   if (lane == 0) part[wave] = dmax;
