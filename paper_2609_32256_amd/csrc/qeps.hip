@@ -40,6 +40,11 @@ constexpr int kThreads = 256;
 constexpr int kPerThread = 32;
 constexpr int kTile = kThreads * kPerThread;  // 8192 elements
 constexpr int kPadded = kTile + kTile / 32;    // one pad word per 32 codes
+// Cache policy of the encoder's streaming traffic: its input is read once and
+// its codes are written once, so both are marked non-temporal (the buffer
+// load's policy operand; the stores use the non-temporal builtin).  This took
+// the 2^26-value encode from 98 to 66 us; the decoder is faster without it.
+constexpr int kNonTemporal = 2;
 
 // Buffer resource over `bytes` bytes from base: loads at offsets past the
 // bound return zeros without touching memory, so a load never needs a branch
@@ -144,7 +149,7 @@ __device__ __forceinline__ void encode_tile(const float4 (&v4)[kPerThread / 4], 
   const uint64_t w0 = (uint64_t)tile * kWords;
 #pragma unroll
   for (int i = t; i < kWords; i += kThreads)
-    if (FULL || w0 + i < nwords) codes[w0 + i] = lq[i + (i >> 5)];
+    if (FULL || w0 + i < nwords) __builtin_nontemporal_store(lq[i + (i >> 5)], &codes[w0 + i]);
   if (__ballot(bad) != 0ull) {
     // classify the rare failures from the values at hand: non-finite (EINVAL)
     // vs merely above absmax (ERANGE)
@@ -188,7 +193,7 @@ __global__ __launch_bounds__(kThreads) void k_encode(const float* __restrict__ x
 #pragma unroll
       for (int j = 0; j < kPerThread / 4; ++j)
         v[j] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(
-                                              rs, (uint32_t)(j * (kThreads * 4) + t * 4) * 4u, 0, 0));
+                                              rs, (uint32_t)(j * (kThreads * 4) + t * 4) * 4u, 0, kNonTemporal));
     };
     int64_t tile = blockIdx.x;
     load_full(tile, cur);
