@@ -25,7 +25,7 @@ import numpy as np
 __all__ = [
     "unit_rows", "members", "near_dups", "cluster_sizes",
     "tiny_ingest", "subset_ingest", "raw_qeps", "corpus_retrieval",
-    "online_store", "clustered", "near_threshold_pairs", "dyadic_ties", "CONFIGS",
+    "online_store", "clustered", "near_threshold_pairs", "threshold_band_device", "dyadic_ties", "CONFIGS",
 ]
 
 
@@ -217,6 +217,32 @@ def online_store_device(seed: int = 5, device: str = "cuda", n: int = 1 << 20, n
     q = members_dev(cent[pick], uniform(0.5, 0.9, nq)).float()
     return dict(x=x, q=q, tau=0.95, eps=1e-3, k=50, batch=4096,
                 name=f"online store (device draw) n={n} D={d} dups={n_dup}")
+
+
+def threshold_band_device(seed: int = 21, device: str = "cuda", n: int = 200_000, d: int = 768,
+                          tau: float = 0.95, spread: float = 3e-3):
+    """n unit rows a_i (Gaussian; the second half heavy-tailed: coordinates
+    scaled by 2^U(-6, 2) before normalising) and one row b_i per a_i at cosine
+    tau + U(-spread, spread) to it, drawn on a device with torch's seeded
+    generator (binary64 draws, float32 at the end).  Returns (a, b) as torch
+    tensors on `device`."""
+    import torch
+    g = torch.Generator(device=device)
+    g.manual_seed(seed)
+    f64 = dict(device=device, dtype=torch.float64)
+
+    def normalize(v):
+        return v / torch.linalg.vector_norm(v, dim=1, keepdim=True)
+
+    a = torch.randn((n, d), generator=g, **f64)
+    h = n // 2
+    a[h:] *= torch.exp2(-6.0 + 8.0 * torch.rand((n - h, d), generator=g, **f64))
+    a = normalize(a)
+    c = (tau + spread * (2.0 * torch.rand(n, generator=g, **f64) - 1.0)).reshape(-1, 1)
+    gg = torch.randn((n, d), generator=g, **f64)
+    gg -= (gg * a).sum(dim=1, keepdim=True) * a
+    b = normalize(c * a + torch.sqrt(1.0 - c * c) * normalize(gg))
+    return a.float(), b.float()
 
 
 def near_threshold_pairs(rng: np.random.Generator, n_pairs: int, d: int, tau: float,
