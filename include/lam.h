@@ -186,6 +186,10 @@ typedef struct lam_ingest_stats {
                                    delta^2, decided on exact integers (device)  */
   double delta_hat_call;        /* max ||x_i - x_rep|| over this call's merges  */
   double delta_hat_run;         /* same over the store's lifetime               */
+  double min_margin_d2;         /* smallest |d^2 - delta^2| (binary64) among the
+                                   pairs the exact test decided in this call;
+                                   +inf when it decided none (every pair was
+                                   then at least the screen's bound away)       */
 } lam_ingest_stats;
 
 /* Algorithm "admit" over x_dev (n rows of dim float32, row-major, expected

@@ -54,7 +54,7 @@ class IngestStats(ctypes.Structure):
     _fields_ = [("n_in", ctypes.c_int64), ("n_kept", ctypes.c_int64), ("n_dropped", ctypes.c_int64),
                 ("store_size", ctypes.c_int64), ("n_ambiguous_pairs", ctypes.c_int64),
                 ("n_exact_escalations", ctypes.c_int64), ("delta_hat_call", ctypes.c_double),
-                ("delta_hat_run", ctypes.c_double)]
+                ("delta_hat_run", ctypes.c_double), ("min_margin_d2", ctypes.c_double)]
 
     def as_dict(self):
         return {f: getattr(self, f) for f, _ in self._fields_}

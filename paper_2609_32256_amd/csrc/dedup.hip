@@ -81,6 +81,13 @@ __device__ __forceinline__ bool skip_all(const DevFlags* f) {
   return (f->nonfinite | f->out_of_range | f->pair_overflow) != 0u;
 }
 
+// Smallest |d^2 - delta^2| among the pairs the exact test decided: kept as the
+// complement of the binary64 bits (non-negative doubles order as their bits),
+// so that the zeroed status word means "none".
+__device__ __forceinline__ void note_margin(DevFlags* f, double m) {
+  if (m < 1e300) atomicMax(&f->margin_inv, ~(unsigned long long)__double_as_longlong(m));
+}
+
 __device__ __forceinline__ float round_up_f32(double d) {
   float f = (float)d;
   if ((double)f < d) f = __uint_as_float(f >= 0.0f ? __float_as_uint(f) + 1u : __float_as_uint(f) - 1u);
@@ -415,10 +422,11 @@ using ScreenTile = Tile<2, 4, 2, 1, 4>;
 // binary64 (error below (D + 2) u64 d^2 in any order); a pair within that
 // distance of delta^2 is decided on exact integers (exact.h), so every
 // decision is the exact one.  Every lane of the group returns the decision;
-// *escalated tells whether the exact path ran.  The G lanes of a group must
-// run it together.
+// *escalated tells whether the exact path ran and *margin is |s - delta^2| for
+// the binary64 sum s.  The G lanes of a group must run it together.
 template <int G>
-__device__ bool pair_within(const float* pa, const float* pb, int D, double d2, const Big6& thr, bool* escalated) {
+__device__ bool pair_within(const float* pa, const float* pb, int D, double d2, const Big6& thr, bool* escalated,
+                            double* margin) {
   static_assert(G == 16 || G == 32 || G == 64, "a group is a power of two within one wave");
   const int gl = (int)threadIdx.x & (G - 1);
   double s = 0.0;
@@ -433,8 +441,9 @@ __device__ bool pair_within(const float* pa, const float* pb, int D, double d2, 
     s = fma(t3, t3, s);
   }
   for (int o = G / 2; o > 0; o >>= 1) s += __shfl_xor(s, o);   // every lane of the group holds the sum
-  const double margin = (double)(D + 8) * 2.5e-16 * fmax(d2, s) + 1e-300;
-  if (fabs(s - d2) > margin) {
+  const double tol = (double)(D + 8) * 2.5e-16 * fmax(d2, s) + 1e-300;
+  *margin = fabs(s - d2);
+  if (*margin > tol) {
     *escalated = false;
     return s <= d2;
   }
@@ -700,12 +709,15 @@ __global__ __launch_bounds__(kAdmitThreads) void k_lsh_admit(LshArgs a) {
   const bool glead = (tid & (kGroup - 1)) == 0;
   volatile int32_t* vh = &hit;
   uint32_t esc = 0u;
+  double mmin = 1e308;
   for (int k = grp; k < ns; k += kGroups) {
     const int y = (int)list[k];
     if (y >= *vh) continue;
     bool e = false;
-    const bool in = pair_within<kGroup>(p, a.xs + (int64_t)y * a.D, a.D, a.d2, a.thr, &e);
+    double mg;
+    const bool in = pair_within<kGroup>(p, a.xs + (int64_t)y * a.D, a.D, a.d2, a.thr, &e, &mg);
     esc += e ? 1u : 0u;
+    mmin = fmin(mmin, mg);
     if (in && glead) atomicMin(&hit, y);
   }
   __syncthreads();
@@ -717,8 +729,10 @@ __global__ __launch_bounds__(kAdmitThreads) void k_lsh_admit(LshArgs a) {
     for (int k = grp; k < nc; k += kGroups) {
       const int j = (int)cl[k];
       bool e = false;
-      const bool in = pair_within<kGroup>(p, a.xc + (int64_t)j * a.D, a.D, a.d2, a.thr, &e);
+      double mg;
+      const bool in = pair_within<kGroup>(p, a.xc + (int64_t)j * a.D, a.D, a.d2, a.thr, &e, &mg);
       esc += e ? 1u : 0u;
+      mmin = fmin(mmin, mg);
       if (in && glead) {
         atomicOr(reinterpret_cast<unsigned long long*>(&a.bitmap[(int64_t)i * a.W + (j >> 6)]), 1ull << (j & 63));
         a.hasEdge[i] = 1u;
@@ -729,6 +743,7 @@ __global__ __launch_bounds__(kAdmitThreads) void k_lsh_admit(LshArgs a) {
     atomicAdd(&a.cc->n_escalate, esc);
     atomicAdd(&a.flags->n_escalate, esc);
   }
+  if (glead) note_margin(a.flags, mmin);
 }
 
 // Kept rows of the chunk join the store's index under their store positions.
@@ -791,6 +806,7 @@ __global__ __launch_bounds__(256) void k_verify(VerifyArgs a) {
   const int lane = threadIdx.x & 63;
   const uint32_t wid = (blockIdx.x * blockDim.x + threadIdx.x) >> 6;
   const uint32_t nw = (gridDim.x * blockDim.x) >> 6;
+  double mmin = 1e308;
   for (uint32_t p = wid; p < n; p += nw) {
     const int2 e = a.pairs[p];
     const int kind = (int)((uint32_t)e.x >> 31);
@@ -803,7 +819,9 @@ __global__ __launch_bounds__(256) void k_verify(VerifyArgs a) {
     const float* pa = a.xc + (int64_t)i * a.D;
     const float* pb = (kind == 0 ? a.xs : a.xc) + (int64_t)y * a.D;
     bool escalated = false;
-    const bool in = pair_within<64>(pa, pb, a.D, a.d2, a.thr, &escalated);
+    double mg;
+    const bool in = pair_within<64>(pa, pb, a.D, a.d2, a.thr, &escalated, &mg);
+    mmin = fmin(mmin, mg);
     if (escalated && lane == 0) {
       atomicAdd(&a.ccw->n_escalate, 1u);
       atomicAdd(&a.flags->n_escalate, 1u);
@@ -819,6 +837,7 @@ __global__ __launch_bounds__(256) void k_verify(VerifyArgs a) {
     }
     a.status[p] = in ? 1u : 0u;
   }
+  if (lane == 0) note_margin(a.flags, mmin);
 }
 
 // ------------------------------------------------------------------ resolve
@@ -1377,6 +1396,7 @@ lam_status dedup_ingest(lam_ctx* ctx, lam_store* st, const float* x, int64_t n, 
     if (stats) {
       LAM_TRY(store_settle(st));
       *stats = lam_ingest_stats{};
+      stats->min_margin_d2 = HUGE_VAL;
       stats->store_size = st->size;
       stats->delta_hat_run = st->delta_hat_run;
     }
@@ -1635,6 +1655,12 @@ lam_status dedup_ingest(lam_ctx* ctx, lam_store* st, const float* x, int64_t n, 
       stats->store_size = st->size;
       stats->n_ambiguous_pairs = lsh ? (int64_t)f.n_cand : (int64_t)f.n_pairs;
       stats->n_exact_escalations = f.n_escalate;
+      double mg = HUGE_VAL;
+      if (f.margin_inv != 0ull) {
+        const unsigned long long bits = ~f.margin_inv;
+        memcpy(&mg, &bits, 8);
+      }
+      stats->min_margin_d2 = mg;
       stats->delta_hat_call = dh_call;
       stats->delta_hat_run = st->delta_hat_run;
     }

@@ -75,6 +75,7 @@ struct DevFlags {
   uint32_t pairs_needed;   // pair-list capacity that would have sufficed
   unsigned long long dhat2_bits;  // max merged d^2 (binary64 bits, non-negative)
   unsigned long long n_cand;      // candidate pairs of a banded store
+  unsigned long long margin_inv;  // ~bits of the smallest |d^2 - delta^2| the exact test saw (0: none)
 };
 
 // ------------------------------------------------------------------ profiling

@@ -79,6 +79,8 @@ def test_exact_ties_and_escalation(lam):
     assert np.array_equal(rep, ref["rep"])
     assert sum(st["n_exact_escalations"] for st in stats) > 0
     assert abs(stats[-1]["delta_hat_run"] - ref["delta_hat"]) <= 1e-12
+    # exact ties sit at delta^2 exactly: the smallest decided margin is 0
+    assert min(st["min_margin_d2"] for st in stats) == 0.0
 
 
 def test_inclusive_threshold_pair(lam):
@@ -177,6 +179,7 @@ def test_empty_batch(lam):
     s = lam.Store(64, 0.95, 10)
     rep, st = s.ingest(torch.empty((0, 64), dtype=torch.float32, device="cuda"))
     assert rep.numel() == 0 and st["n_in"] == 0 and s.size == 0
+    assert st["min_margin_d2"] == float("inf")
 
 
 # ----------------------------------------------------------------- calls that do not wait

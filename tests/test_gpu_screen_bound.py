@@ -43,11 +43,12 @@ def test_decisions_near_the_threshold(lam):
     a, b = ad.cpu().numpy(), bd.cpu().numpy()
     print(f"screen bound pin: {N} pairs at cosine {TAU} +- 3e-3, D = {D}", flush=True)
     s = lam.Store(D, TAU, 2 * N)
-    reps, amb = [], 0
+    reps, amb, margin = [], 0, float("inf")
     for b0 in range(0, 2 * N, 4096):
         rep, st = s.ingest(xd[b0:b0 + 4096])
         reps.append(rep)
         amb += st["n_ambiguous_pairs"]
+        margin = min(margin, st["min_margin_d2"])
     rep = torch.cat(reps).cpu().numpy()
     # the a rows are far apart: all kept
     assert np.all(rep[:N] == -1)
@@ -59,4 +60,6 @@ def test_decisions_near_the_threshold(lam):
     d2f = float(dedup.delta2(TAU))
     inner = int(np.count_nonzero(np.abs(d2 - d2f) <= 1e-3))
     assert inner <= amb <= N
+    # the smallest margin the exact test saw is the planted pairs' smallest
+    assert abs(margin - np.min(np.abs(d2 - d2f))) <= 1e-12
     print(f"merged {int(want.sum())} of {N}; ambiguous pairs {amb}; pairs within 1e-3 of delta^2 in d^2: {inner}")
