@@ -155,18 +155,67 @@ def banded_ingest(lam, torch, np, xd, rep_exh, pairs, ctx, r=BAND_R, rel=BAND_RE
 
 
 def beside_the_step(lam, torch, np, xd, qd, store, rep, pairs, ctx):
-    """Measurements beside the timed step (not in it): the removal ceiling of
-    the stream, the share of benchmark queries whose top-10 is certified
-    rank-invariant, the per-block codec's size on the retained store, and the
-    stream through the banded candidate index."""
+    """Measurements beside the timed step (not in it): the decision
+    statistics of the stream (ambiguous pairs, exact decisions, smallest
+    decided margin), the screen at scale, the removal ceiling of the stream,
+    the share of benchmark queries whose top-10 is certified rank-invariant,
+    the per-block codec's size on the retained store, and the stream through
+    the banded candidate index."""
     ceil = lam.removal_ceiling(xd, TAU, batch=BATCH, ctx=ctx)
     cert = store.score_topk_certified(qd, TOPK)[3]
     blk = store.block_encode()
-    return {"removal_ceiling": {k: ceil[k] for k in ("kept", "kept_2delta", "removal", "ceiling",
+    # the stream once more with calls that wait, for the decision statistics
+    n = xd.shape[0]
+    probe = lam.Store(D, TAU, n, ctx=ctx)
+    st = [probe.ingest(xd[b0:b0 + BATCH])[1] for b0 in range(0, n, BATCH)]
+    decisions = {"ambiguous_pairs": int(sum(t["n_ambiguous_pairs"] for t in st)),
+                 "exact_escalations": int(sum(t["n_exact_escalations"] for t in st)),
+                 "min_margin_d2": float(min(t["min_margin_d2"] for t in st))}
+    del probe
+    return {"decisions": decisions,
+            "screen_steady_state": screen_steady_state(lam, torch, np, ctx),
+            "removal_ceiling": {k: ceil[k] for k in ("kept", "kept_2delta", "removal", "ceiling",
                                                      "frac_of_ceiling", "bits_lo", "bits_hi")},
             "certified_top10_frac": float(cert.float().mean().item()),
             "block_codec": {k: blk[k] for k in ("bits_per_code", "plain_bits", "codec_ratio", "composite_ratio")},
             "banded": banded_ingest(lam, torch, np, xd, rep, pairs, ctx)}
+
+
+def screen_steady_state(lam, torch, np, ctx, m=262_144, batch=4096, calls=5):
+    """The screen at scale (D = 768): calls of 4,096 arrivals against the
+    store left by ingesting 262,144 rows of the online-store recipe at D = 768
+    (clusters of ~51, 20 % planted copies; drawn on the device).  Pairs are
+    the algorithmic pairs of the measured calls."""
+    import synth
+    cfg = synth.online_store_device(seed=6, n=m + calls * batch, n_clusters=m // 51, d=D, nq=16)
+    x = cfg["x"]
+    s = lam.Store(D, TAU, x.shape[0], ctx=ctx)
+    for b0 in range(0, m, batch):
+        s.ingest(x[b0:b0 + batch], sync=False)
+    sizes, pairs = [], 0
+    size0 = s.info().size
+    torch.cuda.synchronize()
+    ctx.profile_reset()
+    ctx.profile_only("dedup_screen")
+    ctx.profile(True)
+    t0 = time.perf_counter()
+    for c in range(calls):
+        b0 = m + c * batch
+        _, st = s.ingest(x[b0:b0 + batch])       # waits: one call at a time
+        sizes.append(st["store_size"])
+    t1 = time.perf_counter()
+    ctx.profile(False)
+    ctx.profile_only(None)
+    tot_ms, cnt = ctx.profile_read("dedup_screen")
+    before = [size0] + sizes[:-1]
+    pairs = sum(batch * k + batch * (batch - 1) // 2 for k in before)
+    flops = 2.0 * D * pairs
+    return {"workload": f"online-store recipe at D = {D}: {batch}-row batches against {size0} retained rows",
+            "calls": calls, "pairs": pairs, "ms_per_call": (t1 - t0) * 1e3 / calls,
+            "screen_ms_per_call": tot_ms / max(cnt, 1),
+            "M_pairs_per_s": pairs / (t1 - t0) / 1e6,
+            "screen_TFLOPs": flops / (tot_ms / 1e3) / 1e12,
+            "screen_frac_of_peak": flops / (tot_ms / 1e3) / 1e12 / MFMA_F16_PEAK_TFLOPS}
 
 
 def band_grid(lam, torch, np, synth, ctx):
@@ -303,11 +352,17 @@ def main():
     ctx.profile_only(dominant)
     ctx.profile(True)
     torch.cuda.synchronize()
+    # events between the steps on the library's stream (torch's current one)
+    # give the spread of the step time without a synchronisation per step
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     t0 = time.perf_counter()
+    evs[0].record()
     for i in range(args.steps):
         step(args.warmup + prof_steps + i)
+        evs[i + 1].record()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
+    step_ms = np.array([evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps)])
     ctx.profile(False)
     ctx.profile_only(None)
     ms = (t1 - t0) * 1e3 / args.steps
@@ -369,6 +424,8 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": ms,
+        "step_ms_p50": float(np.percentile(step_ms, 50)),
+        "step_ms_p90": float(np.percentile(step_ms, 90)),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
