@@ -130,9 +130,32 @@ __device__ __forceinline__ void list_insert(float (&ls)[KL], int (&lr)[KL], floa
   }
 }
 
+typedef _Float16 half2v __attribute__((ext_vector_type(2)));
+
 // Unpacks 32 b-bit codes starting at word w (element 0 at bit 0) to fp16.
+// Byte codes take an exact shortcut, two codes per step: the byte c + 128
+// (c XOR 0x80) becomes the low byte of the fp16 bit pattern 0x6400 | byte,
+// which is the value 1024 + c + 128 exactly; one packed fp16 subtraction of
+// 1152 leaves c.
 template <int B>
 __device__ __forceinline__ void unpack32(const uint32_t* __restrict__ w, _Float16* __restrict__ out) {
+  if constexpr (B == 8) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const uint32_t x = w[i] ^ 0x80808080u;
+      // bytes 0..3 of the selection come from x, 4..7 from the constant 0x64646464
+      const uint32_t lo = __builtin_amdgcn_perm(0x64646464u, x, 0x04010400u);
+      const uint32_t hi = __builtin_amdgcn_perm(0x64646464u, x, 0x04030402u);
+      const half2v off = {(_Float16)1152.0f, (_Float16)1152.0f};
+      const half2v a = __builtin_bit_cast(half2v, lo) - off;
+      const half2v b = __builtin_bit_cast(half2v, hi) - off;
+      out[4 * i + 0] = a.x;
+      out[4 * i + 1] = a.y;
+      out[4 * i + 2] = b.x;
+      out[4 * i + 3] = b.y;
+    }
+    return;
+  }
   uint32_t v[B + 1];
 #pragma unroll
   for (int i = 0; i < B; ++i) v[i] = w[i];
@@ -261,15 +284,21 @@ __global__ __launch_bounds__(kWG, 2) void k_score(ScoreArgs a) {
     floatx16 acc[4];
     score_tile<B>(a, rbase, rows, QH, QL, qrows, lds, acc);
 
-    float mx = -INFINITY;
+    // The scale osc is positive, so the largest score is osc times the
+    // largest accumulator; only a partial tile needs the row check.
+    float amx = -INFINITY;
+    if (rows == kTB) {
 #pragma unroll
-    for (int t = 0; t < 4; ++t)
+      for (int t = 0; t < 4; ++t)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int rl_ = t * 32 + acc_row(r, lane);
-        const float sc = acc[t][r] * osc;
-        mx = (rl_ < rows) ? fmaxf(mx, sc) : mx;
-      }
+        for (int r = 0; r < 16; ++r) amx = fmaxf(amx, acc[t][r]);
+    } else {
+#pragma unroll
+      for (int t = 0; t < 4; ++t)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) amx = (t * 32 + acc_row(r, lane) < rows) ? fmaxf(amx, acc[t][r]) : amx;
+    }
+    const float mx = amx * osc;
     if constexpr (MODE == kModeFilter) {
       const bool hot = j < a.nq && mx >= th;
       if (__ballot(hot) != 0ull && hot) {
@@ -491,8 +520,10 @@ void plan_splits(int nqt, int64_t ntiles, int* splits, int64_t* tps) {
 
 // Scoring plan.  With at most S store rows (S = k * n / 1024, at least 4,096)
 // one pass of per-lane lists gives the exact top-k.  Beyond that:
-//   1. exact top-k of the first S rows: its k-th score theta_j is a lower
-//      bound of the k-th best score over the whole store;
+//   1. the k-th best score theta_j over per-lane lists of 16 over the first S
+//      rows: a k-th best over a subset of the store's scores, hence a lower
+//      bound of the k-th best score over the whole store (16-entry lists keep
+//      this pass cheap for any k; the splits give at least 2k entries);
 //   2. a full scan appends every row scoring >= theta_j to query j's candidate
 //      buffer (about k * n / S = 1,024 entries expected; capacity 4,096);
 //   3. the k best candidates by (score desc, id asc) are the answer;
@@ -528,6 +559,12 @@ lam_status score_topk(lam_ctx* ctx, const lam_store* st, const float* q, int64_t
   int64_t tps1 = 0, tps2 = 0;
   plan_splits(nqt, stiles, &sp1, &tps1);
   plan_splits(nqt, ntiles, &sp2, &tps2);
+  constexpr int kSampleKL = 16;
+  if (two_pass && (int64_t)sp1 * 2 * kSampleKL < 2 * (int64_t)k) {
+    const int64_t want = std::min<int64_t>(stiles, (k + kSampleKL - 1) / kSampleKL);
+    tps1 = (stiles + want - 1) / want;
+    sp1 = (int)((stiles + tps1 - 1) / tps1);
+  }
   const int cands_max = std::max(sp1, sp2) * 2 * KL;
   LAM_TRY(ctx->scratch[S_PART].ensure((size_t)nq * cands_max * 8));
   float* part_s = ctx->scratch[S_PART].as<float>();
@@ -579,20 +616,16 @@ lam_status score_topk(lam_ctx* ctx, const lam_store* st, const float* q, int64_t
   uint32_t* tflag = qflag + nq;
   hipLaunchKernelGGL(k_clear_u32, dim3(64), dim3(256), 0, ctx->stream, cand_cnt, nq, tflag, (int64_t)nqt);
   LAM_HIP(hipGetLastError());
-  {  // 1. exact top-k of the sample -> thresholds
+  {  // 1. a k-th best score of the sample -> thresholds
     ProfScope ps(ctx, "score_sample");
     a.tile_begin = 0;
     a.tile_end = stiles;
     a.splits = sp1;
     a.tiles_per_split = tps1;
-    LAM_TRY(dispatch_bits<1>(b, KL, kModeLists, dim3((unsigned)(nqt * sp1)), ctx->stream, a));
-    const int nc = sp1 * 2 * KL;
-    if (KL == 16)
-      hipLaunchKernelGGL((k_topk_merge<16>), gq, dim3(256), 0, ctx->stream, nq, nc, k, part_s, part_r, qmeta, st->ids,
-                         nullptr, nullptr, nullptr, thr, nullptr);
-    else
-      hipLaunchKernelGGL((k_topk_merge<64>), gq, dim3(256), 0, ctx->stream, nq, nc, k, part_s, part_r, qmeta, st->ids,
-                         nullptr, nullptr, nullptr, thr, nullptr);
+    LAM_TRY(dispatch_bits<1>(b, kSampleKL, kModeLists, dim3((unsigned)(nqt * sp1)), ctx->stream, a));
+    const int nc = sp1 * 2 * kSampleKL;
+    hipLaunchKernelGGL((k_topk_merge<kSampleKL>), gq, dim3(256), 0, ctx->stream, nq, nc, k, part_s, part_r, qmeta,
+                       st->ids, nullptr, nullptr, nullptr, thr, nullptr);
     LAM_HIP(hipGetLastError());
   }
   a.tile_begin = 0;
