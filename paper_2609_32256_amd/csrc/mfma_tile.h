@@ -141,7 +141,7 @@ __device__ __forceinline__ void slab_store_n(_Float16* __restrict__ s, const uin
 // WN.
 //
 // Pipeline: global loads run two slabs ahead of the MFMAs in two register
-// sets; slab s is multiplied from LDS stage s % 2 while slab s + 1 is written
+// sets (three slabs ahead in three sets when NS > 0); slab s is multiplied from LDS stage s % 2 while slab s + 1 is written
 // to the other stage, so one barrier per slab suffices and the LDS writes
 // overlap the MFMAs.  Loads past the last slab are issued too (they fall
 // outside the buffer bound, read zeros and touch no memory), so that no load
@@ -180,8 +180,38 @@ __device__ __forceinline__ bool gemm_tile(const _Float16* __restrict__ A, int ra
           acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fa[a], fb[b], acc[a][b], 0, 0, 0);
     }
   };
-  const int S = NS > 0 ? NS : (kdim + kBK - 1) / kBK;
   const __amdgpu_buffer_rsrc_t rsA = tile_rsrc(A, ra, ld), rsB = tile_rsrc(B, rb, ld);
+  if constexpr (NS > 0) {
+    // Fully unrolled reduction: three register sets, so each slab's loads are
+    // issued three slabs before its LDS store (set and stage indices are
+    // compile-time constants after unrolling).
+    uint4 xa[3][C::kPerA], xb[3][C::kPerB];
+#pragma unroll
+    for (int u = 0; u < 3; ++u) {
+      slab_load_n<C::kPerA>(rsA, ra, ld, u * kBK, kdim, xa[u], C::kThreads);
+      slab_load_n<C::kPerB>(rsB, rb, ld, u * kBK, kdim, xb[u], C::kThreads);
+    }
+    if (!go_on()) return false;
+    slab_store_n<C::kPerA>(sa(0), xa[0], C::kThreads);
+    slab_store_n<C::kPerB>(sb(0), xb[0], C::kThreads);
+    slab_load_n<C::kPerA>(rsA, ra, ld, 3 * kBK, kdim, xa[0], C::kThreads);
+    slab_load_n<C::kPerB>(rsB, rb, ld, 3 * kBK, kdim, xb[0], C::kThreads);
+    __syncthreads();
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      compute(s & 1);
+      if (s + 1 < NS) {
+        const int u = (s + 1) % 3;
+        slab_store_n<C::kPerA>(sa((s + 1) & 1), xa[u], C::kThreads);
+        slab_store_n<C::kPerB>(sb((s + 1) & 1), xb[u], C::kThreads);
+        slab_load_n<C::kPerA>(rsA, ra, ld, (s + 4) * kBK, kdim, xa[u], C::kThreads);
+        slab_load_n<C::kPerB>(rsB, rb, ld, (s + 4) * kBK, kdim, xb[u], C::kThreads);
+      }
+      __syncthreads();
+    }
+    return true;
+  }
+  const int S = (kdim + kBK - 1) / kBK;
   uint4 a0[C::kPerA], b0[C::kPerB], a1[C::kPerA], b1[C::kPerB];
   slab_load_n<C::kPerA>(rsA, ra, ld, 0, kdim, a0, C::kThreads);
   slab_load_n<C::kPerB>(rsB, rb, ld, 0, kdim, b0, C::kThreads);
