@@ -83,6 +83,32 @@ def test_exact_ties_and_escalation(lam):
     assert min(st["min_margin_d2"] for st in stats) == 0.0
 
 
+@pytest.mark.parametrize("d", [32, 96, 160, 4096])
+def test_ragged_dims_parity(lam, d):
+    """Dimensions where the reduction is shorter than one slab of 64 (32),
+    ends in a partial slab (96, 160), or is the largest allowed (4,096, the
+    kernel for any length): planted near-duplicates at cosine 0.93-0.99
+    around tau = 0.95, so that merges, misses and ambiguous pairs all occur."""
+    rng = np.random.default_rng(d)
+    n_base = 500 if d < 4096 else 200
+    base = synth.unit_rows(rng, n_base, d)
+    dups = synth.members(rng, base[rng.integers(0, n_base, n_base // 2)],
+                         rng.uniform(0.93, 0.99, n_base // 2))
+    x = np.concatenate([base, dups]).astype(np.float32)
+    x = x[rng.permutation(x.shape[0])]
+    ref = dedup.greedy(x, 0.95)
+    _, rep, stats, cos = _ingest(lam, x, 0.95, 128, max_cos=True)
+    assert np.array_equal(rep, ref["rep"]), np.nonzero(rep != ref["rep"])[0][:10]
+    assert abs(stats[-1]["delta_hat_run"] - ref["delta_hat"]) <= 1e-12
+    fin = np.isfinite(ref["max_cos"])
+    assert np.array_equal(fin, np.isfinite(cos))
+    # the screen's bound for unit rows: 2 (2^-11 + 2^-22) from the fp16
+    # operands plus the fp32 accumulation's 2 D 2^-24 (1.1e-3 up to D = 1,024)
+    tol = 1.1e-3 if d <= 1024 else 2 * (2.0 ** -11 + 2.0 ** -22) + 2 * d * 2.0 ** -24 + 1e-5
+    assert np.max(np.abs(cos[fin] - ref["max_cos"][fin])) <= tol
+    assert 0 < np.count_nonzero(rep >= 0) < n_base // 2
+
+
 def test_inclusive_threshold_pair(lam):
     a = np.zeros((1, 64), np.float32)
     a[0, 0] = 0.5
