@@ -139,6 +139,38 @@ def test_clear_empties_the_index(lam):
     assert st["store_size"] == np.count_nonzero(rep < 0)
 
 
+@pytest.mark.parametrize("r,rel", [(1, 0.01), (64, 2.0)])
+def test_extreme_band_widths(lam, r, rel):
+    """One coordinate per band (64 bands of one code: many candidates) and a
+    single band of all D coordinates (candidates only for equal code
+    vectors)."""
+    x = _rows(seed=13, n=1000)
+    eps = rel / 8
+    _, rep, stats = _ingest(lam, x, 0.95, eps, r, [0, 500, 1000])
+    ref = lsh.greedy_lsh(x, 0.95, eps, r)
+    assert np.array_equal(rep, ref["rep"]) and np.count_nonzero(rep >= 0) > 0
+    assert sum(st["n_ambiguous_pairs"] for st in stats) == _expected_candidates(x, eps, r, rep, [0, 500, 1000])
+
+
+def test_invalid_input_of_a_call_that_does_not_wait(lam):
+    """A call that does not wait and holds a NaN leaves the store and its band
+    index unchanged; the next call that waits reports it once."""
+    x = _rows(seed=14, n=2000)
+    eps = 0.3 / 8
+    s = lam.Store(64, 0.95, 4000, eps_band=eps, band_width=8)
+    xd = torch.from_numpy(x).cuda()
+    s.ingest(xd[:1000], sync=False)
+    bad = xd[1000:1500].clone()
+    bad[7, 3] = float("nan")
+    s.ingest(bad, sync=False)
+    with pytest.raises(lam.LamError):
+        s.info()
+    rep2, _ = s.ingest(xd[1000:2000])
+    ref = lsh.greedy_lsh(x, 0.95, eps, 8)
+    assert np.array_equal(rep2.cpu().numpy(), ref["rep"][1000:])
+    assert s.info().size == ref["kept"].size
+
+
 def test_argument_checks(lam):
     with pytest.raises(lam.LamError):
         lam.Store(64, 0.95, 100, eps_band=0.01, band_width=5)        # does not divide dim
