@@ -4,7 +4,7 @@ Every step of the hot path runs in the HIP library; this module only turns
 torch tensors into device pointers and sizes, calls the C ABI through ctypes,
 and turns status codes into exceptions.  torch provides device memory and the
 current stream; nothing here computes on the CPU.  If the library has not been
-built (``python -m paper_2609_32256_amd.build``) importing this module fails.
+built (``python paper_2609_32256_amd/build.py``) importing this module fails.
 
     import torch, paper_2609_32256_amd as lam
     codes, p = lam.quantize(x, eps=1e-3)            # Q_eps, packed b-bit codes
@@ -13,6 +13,11 @@ built (``python -m paper_2609_32256_amd.build``) importing this module fails.
     rep, stats = s.ingest(x_batch)                 # greedy near-duplicate test
     s.quantize(eps=1e-3)
     scores, ids, bound = s.score_topk(q, k=10)
+    s.score_topk_certified(q, k=10)                # + rank-invariance flags
+    s.block_encode(); s.score_topk_blocks(q, 10)   # per-block codec of the codes
+    lam.removal_ceiling(x, tau=0.95)               # greedy at delta and at 2 delta
+    b = lam.Store(768, 0.95, 1 << 20, eps_band=0.2 / 768 ** 0.5, band_width=4)
+                                                   # banded candidates over Q_eps codes
 """
 from __future__ import annotations
 
