@@ -302,6 +302,15 @@ __global__ __launch_bounds__(kWG, 2) void k_score(ScoreArgs a) {
     if constexpr (MODE == kModeFilter) {
       const bool hot = j < a.nq && mx >= th;
       if (__ballot(hot) != 0ull && hot) {
+        // count this lane's candidates, reserve their slots with one atomic,
+        // then write them
+        uint32_t c = 0u;
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            c += (t * 32 + acc_row(r, lane) < rows && acc[t][r] * osc >= th) ? 1u : 0u;
+        uint32_t idx = atomicAdd(&a.cand_cnt[j], c);
 #pragma unroll
         for (int t = 0; t < 4; ++t)
 #pragma unroll
@@ -309,11 +318,11 @@ __global__ __launch_bounds__(kWG, 2) void k_score(ScoreArgs a) {
             const int rl_ = t * 32 + acc_row(r, lane);
             const float sc = acc[t][r] * osc;
             if (rl_ < rows && sc >= th) {
-              const uint32_t idx = atomicAdd(&a.cand_cnt[j], 1u);
               if (idx < a.cap) {
                 a.cand_s[j * a.cap + idx] = sc;
                 a.cand_r[j * a.cap + idx] = (int)(rbase + rl_);
               }
+              ++idx;
             }
           }
       }
