@@ -484,6 +484,136 @@ __global__ __launch_bounds__(256) void k_cand_select(int64_t nq, uint32_t cap, i
   wave_select<KL>(k, ls, lr, j, ids, out_s, out_i, nullptr);
 }
 
+// ------------------------------------------------------------------ radix selection (k > 16)
+constexpr int kCandCap = 4096;   // candidate buffer entries per query
+
+// The kth largest (1-based) of keys[0, n) in LDS, found one 8-bit digit at a
+// time from the top: a histogram of the digit among keys that match the
+// digits found so far, then the digit whose suffix count first reaches kth.
+// Returns the key; *ties is the number of keys equal to it and *above the
+// number of keys above it.  Called by the single wave of a workgroup.
+__device__ uint32_t wave_kth_key(const uint32_t* keys, int n, int kth, uint32_t* hist, int* ties, int* above) {
+  const int lane = threadIdx.x & 63;
+  uint32_t prefix = 0u, mask = 0u;
+  int need = kth, tie = 0;
+  for (int shift = 24; shift >= 0; shift -= 8) {
+    for (int b = lane; b < 256; b += 64) hist[b] = 0u;
+    __syncthreads();   // (a workgroup of one wave)
+    for (int i = lane; i < n; i += 64) {
+      const uint32_t key = keys[i];
+      if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
+    }
+    __syncthreads();
+    // lane L holds bins 4L .. 4L + 3; suffix sums over the lanes above
+    uint32_t h[4];
+#pragma unroll
+    for (int b = 0; b < 4; ++b) h[b] = hist[4 * lane + b];
+    const uint32_t sl = h[0] + h[1] + h[2] + h[3];
+    uint32_t incl = sl;
+    for (int o = 1; o < 64; o <<= 1) {
+      const uint32_t t = __shfl_down(incl, o);
+      if (lane + o < 64) incl += t;
+    }
+    uint32_t acc = incl - sl;   // keys in higher bins than this lane's
+    int digit = -1, rest = 0, cnt = 0;
+#pragma unroll
+    for (int b = 3; b >= 0; --b) {
+      if (digit < 0 && acc < (uint32_t)need && acc + h[b] >= (uint32_t)need) {
+        digit = 4 * lane + b;
+        rest = need - (int)acc;
+        cnt = (int)h[b];
+      }
+      acc += h[b];
+    }
+    const int src = __builtin_ctzll(__ballot(digit >= 0));   // exactly one lane found it
+    digit = __shfl(digit, src);
+    need = __shfl(rest, src);
+    tie = __shfl(cnt, src);
+    prefix |= (uint32_t)digit << shift;
+    mask |= 255u << shift;
+    __syncthreads();
+  }
+  *ties = tie;
+  *above = kth - need;
+  return prefix;
+}
+
+// One wave per query: the k best (score desc, row asc) of the candidate
+// buffer, by radix selection of the kth score (and, among the scores equal to
+// it, of the rows), then a bitonic sort of the k winners across the wave.
+__global__ __launch_bounds__(64) void k_cand_select_radix(int64_t nq, uint32_t cap, int k,
+                                                          const uint32_t* __restrict__ cnt,
+                                                          const float* __restrict__ cs, const int32_t* __restrict__ cr,
+                                                          const QMeta* __restrict__ meta,
+                                                          const int64_t* __restrict__ ids, float* __restrict__ out_s,
+                                                          int64_t* __restrict__ out_i, float* __restrict__ bound,
+                                                          uint32_t* __restrict__ qflag, uint32_t* __restrict__ tflag) {
+  __shared__ uint32_t keys[kCandCap];
+  __shared__ uint32_t hist[256];
+  __shared__ uint32_t n_win;
+  __shared__ unsigned long long win[64];
+  const int lane = threadIdx.x & 63;
+  const int64_t j = blockIdx.x;
+  if (j >= nq) return;
+  const uint32_t c = cnt[j];
+  const bool over = c > cap;
+  if (lane == 0) {
+    qflag[j] = over ? 1u : 0u;
+    if (over) atomicOr(&tflag[j / kTB], 1u);
+  }
+  if (write_bad(meta[j], j, k, out_s, out_i, bound) || over) return;
+  const float* sj = cs + j * cap;
+  const int32_t* rj = cr + j * cap;
+  const int n = (int)c;
+  // order keys of the scores (-0 counts as +0, as in the comparison)
+  for (int i = lane; i < n; i += 64) keys[i] = f2ord(sj[i] + 0.0f);
+  const int kk = min(k, n);
+  if (lane == 0) n_win = 0u;
+  win[lane] = 0ull;
+  __syncthreads();   // (a workgroup of one wave)
+  if (kk > 0) {
+    int ties = 0, above = 0;
+    const uint32_t T = wave_kth_key(keys, n, kk, hist, &ties, &above);
+    const int need_t = kk - above;    // entries equal to T to take
+    // Entries above T are all taken; of those equal to T, the need_t with the
+    // smallest rows: the keys become ~row for the ties (the larger, the
+    // smaller the row; every tie key exceeds 0) and 0 for the rest.
+    uint32_t R = 0u;
+    if (need_t < ties) {
+      for (int i = lane; i < n; i += 64) keys[i] = (keys[i] == T) ? ~(uint32_t)rj[i] : 0u;
+      __syncthreads();
+      int t2 = 0, a2 = 0;
+      R = wave_kth_key(keys, n, need_t, hist, &t2, &a2);
+    }
+    for (int i = lane; i < n; i += 64) {
+      const uint32_t ord = f2ord(sj[i] + 0.0f);
+      const uint32_t row = (uint32_t)rj[i];
+      const bool take = ord > T || (ord == T && (need_t >= ties || ~row >= R));
+      if (take) win[atomicAdd(&n_win, 1u)] = ((unsigned long long)ord << 32) | (unsigned long long)(~row);
+    }
+  }
+  __syncthreads();
+  // bitonic sort, descending, one key per lane (empty slots hold 0)
+  unsigned long long key = win[lane];
+  for (int size = 2; size <= 64; size <<= 1) {
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+      const unsigned long long other = __shfl_xor(key, stride);
+      const bool desc = (lane & size) == 0;          // the direction of this run
+      const bool lower = (lane & stride) == 0;
+      key = (desc == lower) ? (key > other ? key : other) : (key < other ? key : other);
+    }
+  }
+  if (lane < k) {
+    if (lane < kk) {
+      out_s[j * k + lane] = ord2f((uint32_t)(key >> 32));
+      out_i[j * k + lane] = ids[~(uint32_t)(key & 0xffffffffull)];
+    } else {
+      out_s[j * k + lane] = -INFINITY;
+      out_i[j * k + lane] = -1;
+    }
+  }
+}
+
 __global__ void k_clear_u32(uint32_t* a, int64_t na, uint32_t* b, int64_t nb) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t st = (int64_t)gridDim.x * blockDim.x;
@@ -615,7 +745,7 @@ lam_status score_topk(lam_ctx* ctx, const lam_store* st, const float* q, int64_t
     return LAM_OK;
   }
 
-  const uint32_t cap = 4096;
+  const uint32_t cap = kCandCap;
   LAM_TRY(ctx->scratch[S_CAND].ensure((size_t)nq * cap * 8 + (size_t)nq * 12 + (size_t)nqt * 4 + 256));
   float* cand_s = ctx->scratch[S_CAND].as<float>();
   int32_t* cand_r = reinterpret_cast<int32_t*>(cand_s + (size_t)nq * cap);
@@ -658,7 +788,7 @@ lam_status score_topk(lam_ctx* ctx, const lam_store* st, const float* q, int64_t
       hipLaunchKernelGGL((k_cand_select<16>), gq, dim3(256), 0, ctx->stream, nq, cap, k, cand_cnt, cand_s, cand_r,
                          qmeta, st->ids, scores, ids, bound, qflag, tflag);
     else
-      hipLaunchKernelGGL((k_cand_select<64>), gq, dim3(256), 0, ctx->stream, nq, cap, k, cand_cnt, cand_s, cand_r,
+      hipLaunchKernelGGL(k_cand_select_radix, dim3((unsigned)nq), dim3(64), 0, ctx->stream, nq, cap, k, cand_cnt, cand_s, cand_r,
                          qmeta, st->ids, scores, ids, bound, qflag, tflag);
     LAM_HIP(hipGetLastError());
   }

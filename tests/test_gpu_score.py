@@ -169,6 +169,29 @@ def test_two_pass_and_overflow_fallback(lam, k):
     _compare(gs[keep], gi[keep], c, np.arange(n), q[keep], 1e-3, k)
 
 
+@pytest.mark.parametrize("k", [17, 50, 64])
+def test_two_pass_ties_broken_by_id(lam, k):
+    """Exactly equal scores at the k-th place in the two-pass plan: 20,000
+    rows are 40 copies of 500 vectors, the copies moved by less than the code
+    step so that all copies of a vector share its codes; every query's top-k
+    cuts through a group of equal scores, which must be taken in id order."""
+    rng = np.random.default_rng(12)
+    base = synth.unit_rows(rng, 500, 64)
+    x = np.tile(base, (40, 1))
+    x[:, 0] += np.repeat(np.arange(40), 500) * 1e-6     # distinct rows, identical codes at eps = 0.02
+    x = x.astype(np.float32)
+    s = _store_from_rows(lam, x)
+    s.quantize(0.02, absmax=1.0)
+    c = qeps.codes(x, 0.02).reshape(x.shape[0], -1)
+    assert np.array_equal(c[:500], c[500:1000])
+    q = synth.unit_rows(rng, 24, 64).astype(np.float32)
+    gs, gi, _ = s.score_topk(_dev(q), k)
+    S = score.scores(q, c, 0.02)
+    ts, ti = score.topk(S, np.arange(x.shape[0]), k)
+    assert np.array_equal(gi.cpu().numpy(), ti)
+    assert np.all(np.abs(gs.cpu().numpy().astype(np.float64) - ts) <= TOL)
+
+
 def test_rank_invariance_certificate(lam):
     """Certified queries have an exact margin above 2 (beta + ||q|| delta_hat)
     (soundness); queries whose exact margin clears that by more than the
