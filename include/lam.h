@@ -15,6 +15,12 @@
  *   3. Retrieval scoring of queries against the quantized retained store,
  *      dequantized on the fly, with top-k and the per-query bound
  *      eps * ||q||_1 on |q.x - q.x_hat| (Appendix "Rank invariance, in full").
+ * and, around them, the paper's further mechanisms: candidates from a band
+ * index over Q_eps codes (lam_store_create_banded), the removal ceiling and
+ * entropy bracket from greedy at delta and 2 delta (lam_removal_ceiling), the
+ * rank-invariance certificate (lam_score_topk_certified) and a per-block
+ * fixed-length codec of the store's codes (lam_store_block_*,
+ * lam_score_topk_blocks).
  *
  * Conventions for every call:
  *   - Pointers named *_dev are device pointers on the context's device; the
