@@ -492,6 +492,15 @@ static_assert(kSetMax + kAdmitThreads < kSetSlots, "the set always keeps an empt
 struct LshArgs {
   const float* xc;            // chunk rows (float32)
   const float* xs;            // store rows (float32)
+  // the screen's operands: fp16 rows x 2^8 and the per-row terms ||x||^2 / 2
+  // and error term, of the chunk and of the store
+  const _Float16* xc16;
+  const float* hnc;
+  const float* etc;
+  const _Float16* xs16;
+  const float* hns;
+  const float* ets;
+  double half_d2;             // delta^2 / 2
   int nB;
   int D;
   int r, nb;                  // band width, bands per row
@@ -613,6 +622,34 @@ __device__ __forceinline__ void band_rows(const LshArgs& a, int i, int b, int m,
 }
 
 __device__ __forceinline__ uint32_t set_hash(uint32_t v) { return (v * 0x9e3779b1u) >> (32 - 12); }
+
+// Decision of one candidate pair by a group of G lanes: the fp16 screen's dot
+// (exact products, float32 sums in any order) against the same error bound as
+// the MFMA screen, with the binary64 and exact test (pair_within) only for a
+// pair the bound leaves ambiguous.  a = the arrival (chunk row i), b = the
+// candidate.  *tested tells whether pair_within ran.
+template <int G>
+__device__ bool screened_within(const LshArgs& a, int i, const float* pb32, const _Float16* pb16, float hn_b,
+                                float et_b, bool* escalated, double* margin, bool* tested) {
+  const int gl = (int)threadIdx.x & (G - 1);
+  const _Float16* pa16 = a.xc16 + (int64_t)i * a.D;
+  float acc = 0.0f;
+  for (int d = gl * 8; d < a.D; d += 8 * G) {
+    const half8 u = *reinterpret_cast<const half8*>(pa16 + d);
+    const half8 v = *reinterpret_cast<const half8*>(pb16 + d);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc = fmaf((float)u[e], (float)v[e], acc);
+  }
+  for (int o = G / 2; o > 0; o >>= 1) acc += __shfl_xor(acc, o);
+  const float v = acc * kInvScale2 - hn_b;
+  const double base = (double)a.hnc[i] - a.half_d2;
+  const double e = (double)a.etc[i] + (double)et_b;
+  *tested = false;
+  if (v >= round_up_f32(base + e)) return true;
+  if (v < round_down_f32(base - e)) return false;
+  *tested = true;
+  return pair_within<G>(a.xc + (int64_t)i * a.D, pb32, a.D, a.d2, a.thr, escalated, margin);
+}
 static_assert(kSetSlots == 1 << 12, "set_hash yields 12 bits");
 
 __global__ __launch_bounds__(kAdmitThreads) void k_lsh_admit(LshArgs a) {
@@ -713,11 +750,12 @@ __global__ __launch_bounds__(kAdmitThreads) void k_lsh_admit(LshArgs a) {
   for (int k = grp; k < ns; k += kGroups) {
     const int y = (int)list[k];
     if (y >= *vh) continue;
-    bool e = false;
-    double mg;
-    const bool in = pair_within<kGroup>(p, a.xs + (int64_t)y * a.D, a.D, a.d2, a.thr, &e, &mg);
+    bool e = false, tested = false;
+    double mg = 1e308;
+    const bool in = screened_within<kGroup>(a, i, a.xs + (int64_t)y * a.D, a.xs16 + (int64_t)y * a.D, a.hns[y],
+                                            a.ets[y], &e, &mg, &tested);
     esc += e ? 1u : 0u;
-    mmin = fmin(mmin, mg);
+    if (tested) mmin = fmin(mmin, mg);
     if (in && glead) atomicMin(&hit, y);
   }
   __syncthreads();
@@ -728,11 +766,12 @@ __global__ __launch_bounds__(kAdmitThreads) void k_lsh_admit(LshArgs a) {
     const uint32_t* cl = list + kSetMax + kAdmitThreads - nc;
     for (int k = grp; k < nc; k += kGroups) {
       const int j = (int)cl[k];
-      bool e = false;
-      double mg;
-      const bool in = pair_within<kGroup>(p, a.xc + (int64_t)j * a.D, a.D, a.d2, a.thr, &e, &mg);
+      bool e = false, tested = false;
+      double mg = 1e308;
+      const bool in = screened_within<kGroup>(a, i, a.xc + (int64_t)j * a.D, a.xc16 + (int64_t)j * a.D, a.hnc[j],
+                                              a.etc[j], &e, &mg, &tested);
       esc += e ? 1u : 0u;
-      mmin = fmin(mmin, mg);
+      if (tested) mmin = fmin(mmin, mg);
       if (in && glead) {
         atomicOr(reinterpret_cast<unsigned long long*>(&a.bitmap[(int64_t)i * a.W + (j >> 6)]), 1ull << (j & 63));
         a.hasEdge[i] = 1u;
@@ -1465,6 +1504,10 @@ lam_status dedup_ingest(lam_ctx* ctx, lam_store* st, const float* x, int64_t n, 
     la.bslots = bslots;
     la.bmask = bslots - 1;
     la.xs = st->x32;
+    la.xs16 = st->x16;
+    la.hns = st->hn;
+    la.ets = st->et;
+    la.half_d2 = 0.5 * st->d2;
     la.D = D;
     la.r = st->lsh_r;
     la.nb = nb;
@@ -1522,6 +1565,9 @@ lam_status dedup_ingest(lam_ctx* ctx, lam_store* st, const float* x, int64_t n, 
 
       if (lsh) {
         la.xc = xc;
+        la.xc16 = x16;
+        la.hnc = hnc + c0;
+        la.etc = etc + c0;
         la.nB = nB;
         la.m_exact = (!async && c0 == 0) ? (int)m_before : -1;
         la.pairs = pairs;
