@@ -252,16 +252,24 @@ __global__ __launch_bounds__(C::kThreads, C::kMinWaves) void k_screen(ScreenArgs
   const int MODE = bid < nb0 ? 0 : 1;
   int ta, tb;
   if (MODE == 0) {
-    // Grouped order: within an XCD's contiguous range, consecutive workgroups
-    // sweep a group of kGroupA store tiles against each chunk tile in turn, so
-    // the tiles in flight on one XCD (kGroupA store tiles plus a few chunk
-    // tiles) stay inside its L2 and each store tile leaves HBM once.
-    const int logical = xcd_remap32(bid, nb0);
+    // Grouped order: a group is gA store tiles against every chunk tile,
+    // swept store tile fastest, and one XCD takes a whole group, so the tiles
+    // in flight on one XCD (two per CU, 64 in all: 8 store tiles and 8 chunk
+    // tiles either way -- one group of gA = 8, or eight groups of one store
+    // tile when the chunk has at most 8 tiles) stay inside its L2 and each
+    // store tile leaves HBM once.  With the store size known the grid is
+    // exact and each XCD takes a contiguous range of groups; when the grid
+    // covers an upper bound of the size, groups go round-robin to the XCDs so
+    // that the empty tiles at its end are shared out instead of idling the
+    // last XCDs.
+    const bool exact = a.m_exact >= 0;
+    const int gA = (exact || a.ntB > 8) ? kGroupA : 1;
+    const int per_group = gA * a.ntB;
+    const int logical = exact ? xcd_remap32(bid, nb0) : group_interleave(bid, nb0, per_group);
     const int ntA = nb0 / a.ntB;
-    const int per_group = kGroupA * a.ntB;
     const int g = logical / per_group, l = logical - g * per_group;
-    const int ta0 = g * kGroupA;
-    const int gsize = min(kGroupA, ntA - ta0);
+    const int ta0 = g * gA;
+    const int gsize = min(gA, ntA - ta0);
     ta = ta0 + l % gsize;
     tb = l / gsize;
   } else {

@@ -262,6 +262,24 @@ __device__ __forceinline__ int xcd_remap32(int bid, int nblocks) {
   return x * q + (x < rem ? x : rem) + (bid >> 3);
 }
 
+// Workgroup index -> logical tile for a grid made of groups of P consecutive
+// logical tiles that share operand rows: XCD x = bid % 8 takes whole groups,
+// x, x + 8, x + 16, ..., each group's tiles in order, so a group stays in one
+// L2 while the groups are dealt round-robin over the XCDs (tiles at the end of
+// the logical order, e.g. tiles that turn out to be empty, are spread over all
+// XCDs rather than all falling to the last).  The grid's tail of fewer than 8
+// whole groups is split into contiguous ranges as by xcd_remap32.  A bijection
+// of [0, nblocks).
+__device__ __forceinline__ int group_interleave(int bid, int nblocks, int P) {
+  const int span = 8 * P;
+  const int full = nblocks / span;
+  if (bid < full * span) {
+    const int i = bid >> 3;
+    return (i / P) * span + (bid & 7) * P + i % P;
+  }
+  return full * span + xcd_remap32(bid - full * span, nblocks - full * span);
+}
+
 // Order-preserving map of float to uint32 for atomicMax.
 __device__ __forceinline__ uint32_t f2ord(float f) {
   const uint32_t u = __float_as_uint(f);
