@@ -412,10 +412,13 @@ __device__ __forceinline__ bool write_bad(const QMeta& m, int64_t j, int k, floa
   return true;
 }
 
-// One wave per query: the k best of the per-lane lists (segments of KL sorted
-// entries, of which only the first k can matter).  With qflag set, only
-// flagged queries are processed (the fallback after a candidate overflow).
-template <int KL>
+// One wave per query: the k best of the per-lane lists (segments of SEG sorted
+// entries, of which only the first k can matter), each lane folding its share
+// into a register list of KL.  With KL >= k and the shares' lists complete this
+// is the exact k best; otherwise the k picks are still k distinct entries.
+// With qflag set, only flagged queries are processed (the fallback after a
+// candidate overflow).
+template <int KL, int SEG = KL>
 __global__ __launch_bounds__(256) void k_topk_merge(int64_t nq, int cands, int k, const float* __restrict__ ps,
                                                     const int32_t* __restrict__ pr, const QMeta* __restrict__ meta,
                                                     const int64_t* __restrict__ ids, float* __restrict__ out_s,
@@ -439,7 +442,7 @@ __global__ __launch_bounds__(256) void k_topk_merge(int64_t nq, int cands, int k
     lr[p] = kNoRow;
   }
   for (int c = lane; c < cands; c += 64) {
-    if ((c % KL) >= k) continue;              // below rank k of its own sorted segment
+    if ((c % SEG) >= k) continue;             // below rank k of its own sorted segment
     const int cr = r[c];
     if (cr == kNoRow) continue;
     const float cs = s[c];
@@ -631,7 +634,13 @@ void launch_mode(int mode, dim3 grid, hipStream_t st, const ScoreArgs& a) {
 template <int B>
 lam_status dispatch_bits(int b, int kl, int mode, dim3 grid, hipStream_t st, const ScoreArgs& a) {
   if (b == B) {
-    if (kl == 16) launch_mode<B, 16>(mode, grid, st, a);
+    if (kl == 4) {   // the sample pass's short lists
+      if (mode != kModeLists) {
+        set_error("internal: lists of 4 serve the sample pass only");
+        return LAM_EINVAL;
+      }
+      hipLaunchKernelGGL((k_score<B, 4, kModeLists>), grid, dim3(kWG), 0, st, a);
+    } else if (kl == 16) launch_mode<B, 16>(mode, grid, st, a);
     else launch_mode<B, 64>(mode, grid, st, a);
     return LAM_OK;
   }
@@ -659,10 +668,12 @@ void plan_splits(int nqt, int64_t ntiles, int* splits, int64_t* tps) {
 
 // Scoring plan.  With at most S store rows (S = k * n / 1024, at least 4,096)
 // one pass of per-lane lists gives the exact top-k.  Beyond that:
-//   1. the k-th best score theta_j over per-lane lists of 16 over the first S
-//      rows: a k-th best over a subset of the store's scores, hence a lower
-//      bound of the k-th best score over the whole store (16-entry lists keep
-//      this pass cheap for any k; the splits give at least 2k entries);
+//   1. theta_j, the k-th best entry of per-lane lists of the 4 best scores
+//      over the first S rows: the least of k distinct rows' scores, hence a
+//      lower bound of the k-th best score over the whole store (short lists
+//      keep this pass cheap -- the insertions, not the MFMAs, dominate it --
+//      at the price of a slightly lower theta_j when one lane holds more than
+//      4 of the sample's best k; the splits give at least 2k entries);
 //   2. a full scan appends every row scoring >= theta_j to query j's candidate
 //      buffer (about k * n / S = 1,024 entries expected; capacity 4,096);
 //   3. the k best candidates by (score desc, id asc) are the answer;
@@ -698,7 +709,7 @@ lam_status score_topk(lam_ctx* ctx, const lam_store* st, const float* q, int64_t
   int64_t tps1 = 0, tps2 = 0;
   plan_splits(nqt, stiles, &sp1, &tps1);
   plan_splits(nqt, ntiles, &sp2, &tps2);
-  constexpr int kSampleKL = 16;
+  constexpr int kSampleKL = 4;
   if (two_pass && (int64_t)sp1 * 2 * kSampleKL < 2 * (int64_t)k) {
     const int64_t want = std::min<int64_t>(stiles, (k + kSampleKL - 1) / kSampleKL);
     tps1 = (stiles + want - 1) / want;
@@ -763,7 +774,7 @@ lam_status score_topk(lam_ctx* ctx, const lam_store* st, const float* q, int64_t
     a.tiles_per_split = tps1;
     LAM_TRY(dispatch_bits<1>(b, kSampleKL, kModeLists, dim3((unsigned)(nqt * sp1)), ctx->stream, a));
     const int nc = sp1 * 2 * kSampleKL;
-    hipLaunchKernelGGL((k_topk_merge<kSampleKL>), gq, dim3(256), 0, ctx->stream, nq, nc, k, part_s, part_r, qmeta,
+    hipLaunchKernelGGL((k_topk_merge<16, kSampleKL>), gq, dim3(256), 0, ctx->stream, nq, nc, k, part_s, part_r, qmeta,
                        st->ids, nullptr, nullptr, nullptr, thr, nullptr);
     LAM_HIP(hipGetLastError());
   }
