@@ -68,7 +68,10 @@ lam_status prof_begin(lam_ctx* ctx, const char* name, size_t* slot) {
       *ev = ctx->event_pool.back();
       ctx->event_pool.pop_back();
     } else {
-      LAM_HIP(hipEventCreate(ev));
+      // timing events only: no system-scope fence (nothing on the host
+      // reads device memory through them), which would flush the L2 at each
+      // record and hold up the next kernel
+      LAM_HIP(hipEventCreateWithFlags(ev, hipEventDisableSystemFence));
     }
   }
   LAM_HIP(hipEventRecord(r.a, ctx->stream));

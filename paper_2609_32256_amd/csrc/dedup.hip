@@ -1341,7 +1341,10 @@ lam_status store_alloc(lam_store* st) {
     LAM_HIP(hipMemset(st->lsh_key, 0, slots * 8));
     LAM_HIP(hipMemset(st->lsh_head, 0xff, slots * 4));   // -1: empty list
   }
-  LAM_HIP(hipEventCreateWithFlags(&st->done, hipEventDisableTiming));
+  // Marks the end of the store's last call that did not wait.  Settling reads
+  // the device-side bookkeeping with a device copy after it, so the event
+  // needs no system-scope fence (which would flush the L2 between calls).
+  LAM_HIP(hipEventCreateWithFlags(&st->done, hipEventDisableTiming | hipEventDisableSystemFence));
   LAM_HIP(hipDeviceSynchronize());
   st->thr = exact_threshold(st->tau);
   return LAM_OK;
