@@ -80,6 +80,29 @@ lam_status prof_begin(lam_ctx* ctx, const char* name, size_t* slot) {
   return LAM_OK;
 }
 
+// Timing of one launch by the launch itself: the two events go to
+// hipExtLaunchKernel, which stamps them at the kernel's start and end, so no
+// marker packets sit between this kernel and its neighbours.  Both stay null
+// unless this kernel is being profiled.
+lam_status prof_launch_events(lam_ctx* ctx, const char* name, hipEvent_t* start, hipEvent_t* stop) {
+  *start = *stop = nullptr;
+  if (!ctx->profiling) return LAM_OK;
+  if (!ctx->prof_only.empty() && ctx->prof_only != name) return LAM_OK;
+  ProfRec r{name, nullptr, nullptr};
+  for (hipEvent_t* ev : {&r.a, &r.b}) {
+    if (!ctx->event_pool.empty()) {
+      *ev = ctx->event_pool.back();
+      ctx->event_pool.pop_back();
+    } else {
+      LAM_HIP(hipEventCreateWithFlags(ev, hipEventDisableSystemFence));
+    }
+  }
+  ctx->prof.push_back(r);
+  *start = r.a;
+  *stop = r.b;
+  return LAM_OK;
+}
+
 lam_status prof_end(lam_ctx* ctx, size_t slot) {
   if (slot >= ctx->prof.size()) return LAM_OK;
   LAM_HIP(hipEventRecord(ctx->prof[slot].b, ctx->stream));

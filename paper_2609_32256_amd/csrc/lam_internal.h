@@ -152,6 +152,8 @@ namespace lam {
 // profiling helpers (no-ops unless ctx->profiling)
 lam_status prof_begin(lam_ctx* ctx, const char* name, size_t* slot);
 lam_status prof_end(lam_ctx* ctx, size_t slot);
+// events for hipExtLaunchKernel (null unless this kernel is profiled)
+lam_status prof_launch_events(lam_ctx* ctx, const char* name, hipEvent_t* start, hipEvent_t* stop);
 
 struct ProfScope {
   lam_ctx* ctx;
