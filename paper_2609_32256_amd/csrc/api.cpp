@@ -417,6 +417,7 @@ lam_status lam_store_quantize(lam_ctx* ctx, lam_store* st, double eps, float abs
   }
   st->q = p;
   st->coded_rows = st->size;
+  LAM_TRY(store_norm_max(ctx, st));
   if (out) *out = p;
   return LAM_OK;
 }

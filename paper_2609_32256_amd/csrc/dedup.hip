@@ -1330,6 +1330,7 @@ lam_status store_alloc(lam_store* st) {
   LAM_HIP(hipMalloc(&st->et, cap * 4));
   LAM_HIP(hipMalloc(&st->ids, cap * 8));
   LAM_HIP(hipMalloc(&st->stat_dev, sizeof(StoreMeta)));
+  LAM_HIP(hipMalloc(&st->hn_max, 4));
   LAM_HIP(hipMemset(st->stat_dev, 0, sizeof(StoreMeta)));
   if (st->lsh_r > 0) {
     const uint64_t entries = (uint64_t)cap * (uint64_t)st->lsh_nb;
@@ -1370,7 +1371,7 @@ lam_status lsh_reset(lam_ctx* ctx, lam_store* st, int64_t keep_rows) {
 
 void store_free(lam_store* st) {
   for (void* p : {(void*)st->x32, (void*)st->x16, (void*)st->hn, (void*)st->et, (void*)st->ids,
-                  (void*)st->stat_dev, (void*)st->codes})
+                  (void*)st->stat_dev, (void*)st->codes, (void*)st->hn_max})
     if (p) (void)hipFree(p);
   for (void* p : {(void*)st->blk_w, (void*)st->blk_row_off, (void*)st->blk_data, (void*)st->lsh_key,
                   (void*)st->lsh_head, (void*)st->lsh_next, (void*)st->lsh_rowkey})
@@ -1389,6 +1390,7 @@ void store_free(lam_store* st) {
   st->hn = st->et = st->stat_dev = nullptr;
   st->ids = nullptr;
   st->codes = nullptr;
+  st->hn_max = nullptr;
 }
 
 // ------------------------------------------------------------------ host orchestration

@@ -133,6 +133,7 @@ struct lam_store {
   float* et = nullptr;        // per-row term of the screen's error bound (float32, rounded up)
   int64_t* ids = nullptr;     // global ids
   float* stat_dev = nullptr;  // device bookkeeping block (retained-row count)
+  uint32_t* hn_max = nullptr; // max of hn over the coded rows (float bits), set with the codes
   // codes
   uint32_t* codes = nullptr;
   uint64_t codes_cap = 0;
@@ -200,5 +201,8 @@ lam_status lsh_reset(lam_ctx* ctx, lam_store* st, int64_t keep_rows);
 // Waits for ingest calls that did not wait, copies the device bookkeeping into
 // the host fields and reports (once) invalid input those calls met.
 lam_status store_settle(lam_store* st);
+// Largest ||x||^2 / 2 over the store's rows, for the scoring error bound
+// (score.hip); enqueued by lam_store_quantize.
+lam_status store_norm_max(lam_ctx* ctx, lam_store* st);
 
 }  // namespace lam

@@ -18,6 +18,11 @@
 // of its best KL (score, row) pairs in registers, touched only when a score
 // reaches the list's current threshold.  A merge kernel then picks the k best
 // per query from all lists by (score desc, id asc).
+//
+// Stores beyond the sample size take a threshold plan (score_topk) whose
+// sample and filter passes multiply the hi part alone -- half the MFMAs --
+// with thresholds lowered by twice a per-query bound on the hi part's error;
+// the few candidates near the k-th are then rescored exactly.
 #include <cmath>
 #include <cstring>
 
@@ -35,7 +40,7 @@ struct QMeta {
   float osc;     // float32(s * 2^-e): multiplies the raw accumulator
   float bound;   // eps * ||q||_1 rounded up, or NaN for an invalid query
   int bad;       // query holds NaN/Inf
-  int pad;
+  float err;     // >= |hi-only score - rescored score| for every store row (rounded up)
 };
 
 __device__ __forceinline__ float ru32(double d) {
@@ -44,15 +49,34 @@ __device__ __forceinline__ float ru32(double d) {
   return f;
 }
 
+__device__ __forceinline__ float rd32(double d) {
+  float f = (float)d;
+  if ((double)f > d) f = nextafterf(f, -INFINITY);
+  return f;
+}
+
+// Per query: the hi/lo split and the meta block.  err bounds the difference
+// between a score from the hi part alone (H) and the rescored one (S), both
+// against T = s sum_d q_d code_d, in score units, with R >= ||x_hat_y|| for
+// every row y (R from the largest ||x||^2 / 2 of the store plus eps sqrt(D))
+// and h = hi 2^-e the query's hi part in its own units:
+//   hi part:   |s sum_d (q_d - h_d) code_d| <= ||q - h||_2 R (Cauchy-Schwarz;
+//              ||q - h||_2 is computed here in binary64);
+//   fp32 sum:  g = 2 (D + 64) 2^-24 of s sum |h_d code_d| <= (||q|| + ||q - h||) R
+//              (two roundings per addition, in any order);
+//   scalings:  osc and the final product, 2^-24 each;
+//   S:         the rescoring sums in binary64 and rounds once to float32.
+// |H - S| <= |H - T| + |T - S| <= ||q - h|| R + (g + 2^-21)(||q|| + ||q - h||) R.
 __global__ __launch_bounds__(256) void k_score_prep(const float* __restrict__ q, int64_t nq, int D, double s,
-                                                    double eps, _Float16* __restrict__ qhi,
+                                                    double eps, const uint32_t* __restrict__ hn_max,
+                                                    _Float16* __restrict__ qhi,
                                                     _Float16* __restrict__ qlo, QMeta* __restrict__ meta) {
   const int lane = threadIdx.x & 63;
   const int64_t j = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (j >= nq) return;
   const float* p = q + j * D;
   float mx = 0.0f;
-  double l1 = 0.0;
+  double l1 = 0.0, l2 = 0.0;
   bool bad = false;
   for (int d = lane; d < D; d += 64) {
     const float v = p[d];
@@ -60,28 +84,41 @@ __global__ __launch_bounds__(256) void k_score_prep(const float* __restrict__ q,
     bad |= !(a <= 3.402823466e38f);
     mx = fmaxf(mx, a);
     l1 += (double)a;
+    l2 = fma((double)v, (double)v, l2);
   }
   for (int o = 32; o > 0; o >>= 1) {
     mx = fmaxf(mx, __shfl_xor(mx, o));
     l1 += __shfl_xor(l1, o);
+    l2 += __shfl_xor(l2, o);
   }
   bad = __ballot(bad) != 0ull;
   int e = 0;
   if (!bad && mx > 0.0f) e = 14 - ilogbf(mx);   // max |q| 2^e in [2^14, 2^15)
   const float sc = ldexpf(1.0f, e);
+  const double isc = ldexp(1.0, -e);
+  double dh2 = 0.0;   // ||q - h||^2
   for (int d = lane; d < D; d += 64) {
     const float v = bad ? 0.0f : p[d] * sc;     // exact power-of-two scaling
     const _Float16 h = (_Float16)v;
     const _Float16 l = (_Float16)(v - (float)h);
     qhi[j * D + d] = h;
     qlo[j * D + d] = l;
+    const double r = bad ? 0.0 : (double)p[d] - (double)(float)h * isc;   // exact in binary64
+    dh2 = fma(r, r, dh2);
   }
+  for (int o = 32; o > 0; o >>= 1) dh2 += __shfl_xor(dh2, o);
   if (lane == 0) {
     QMeta m;
     m.osc = (float)ldexp(s, -e);
     m.bound = bad ? __builtin_nanf("") : ru32(eps * l1 * (1.0 + 0x1p-50));
     m.bad = bad ? 1 : 0;
-    m.pad = 0;
+    const double R = sqrt(2.0 * (double)__uint_as_float(*hn_max) * (1.0 + 0x1p-22)) * (1.0 + 0x1p-50) +
+                     eps * sqrt((double)D) * (1.0 + 0x1p-50);
+    const double g = 2.0 * (double)(D + 64) * 0x1p-24;
+    const double qn = sqrt(l2) * (1.0 + 0x1p-50);
+    const double dh = sqrt(dh2) * (1.0 + 0x1p-50);
+    const double E = dh * R + (g + 0x1p-21) * (qn + dh) * R;
+    m.err = bad ? 0.0f : ru32(E * (1.0 + 0x1p-20));
     meta[j] = m;
   }
 }
@@ -173,15 +210,16 @@ __device__ __forceinline__ void unpack32(const uint32_t* __restrict__ w, _Float1
 // acc[t] (t = 0..3) <- the 128 x 128 tile of raw scores: store rows
 // [rbase, rbase + rows) against the workgroup's 128 queries (wave w holds
 // queries [32w, 32w + 32), lane j % 32, store rows t*32 + acc_row(r, lane)).
-// Codes are unpacked straight into an fp16 LDS slab; queries enter as hi/lo.
+// Codes are unpacked straight into an fp16 LDS slab; queries enter as hi/lo
+// (LO), or as the hi part alone.
 //
-// One LDS stage (codes, hi, lo: 3 x 128 rows of kLdk halves) is refilled
+// One LDS stage (codes, hi[, lo]: 2 or 3 x 128 rows of kLdk halves) is refilled
 // between two barriers while the next slab's loads are in flight in
 // registers; loads go through buffer resources (zeros past the tile) so none
 // sits behind a branch.  With one slab in flight, the wait at the top of each
 // step is for all outstanding loads, which is exactly the slab being stored.
 // Ends with a barrier, so the caller may reuse the LDS.
-template <int B>
+template <int B, bool LO>
 __device__ __forceinline__ void score_tile(const ScoreArgs& a, int64_t rbase, int rows, const _Float16* QH,
                                            const _Float16* QL, int qrows, _Float16* lds, floatx16 (&acc)[4]) {
   _Float16* sc = lds;
@@ -203,20 +241,22 @@ __device__ __forceinline__ void score_tile(const ScoreArgs& a, int64_t rbase, in
     for (int i = 0; i < B; ++i)
       cw[i] = (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(rsC, ok ? (w0 + i) * 4u : kOffOOB, 0, 0);
     slab_load_n<4>(rsH, qrows, a.D, k0, a.D, rh, kWG);
-    slab_load_n<4>(rsL, qrows, a.D, k0, a.D, rl, kWG);
+    if (LO) slab_load_n<4>(rsL, qrows, a.D, k0, a.D, rl, kWG);
   };
   auto compute = [&]() {
 #pragma unroll
     for (int kk = 0; kk < kBK / 16; ++kk) {
       const half8 bh = frag_load(sh, wave * 32, kk);
-      const half8 bl = frag_load(sl, wave * 32, kk);
       half8 fa[4];
 #pragma unroll
       for (int t = 0; t < 4; ++t) fa[t] = frag_load(sc, t * 32, kk);
 #pragma unroll
       for (int t = 0; t < 4; ++t) acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fa[t], bh, acc[t], 0, 0, 0);
+      if (LO) {
+        const half8 bl = frag_load(sl, wave * 32, kk);
 #pragma unroll
-      for (int t = 0; t < 4; ++t) acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fa[t], bl, acc[t], 0, 0, 0);
+        for (int t = 0; t < 4; ++t) acc[t] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fa[t], bl, acc[t], 0, 0, 0);
+      }
     }
   };
   const int S = (a.D + kBK - 1) / kBK;
@@ -233,7 +273,7 @@ __device__ __forceinline__ void score_tile(const ScoreArgs& a, int64_t rbase, in
       for (int i = 0; i < 32; i += 8) *reinterpret_cast<uint4*>(dst + i) = *reinterpret_cast<const uint4*>(h + i);
     }
     slab_store_n<4>(sh, rh, kWG);
-    slab_store_n<4>(sl, rl, kWG);
+    if (LO) slab_store_n<4>(sl, rl, kWG);
     __syncthreads();
     load_slab((s + 1) * kBK, cw, rh, rl);   // past the last slab: zeros, no memory touched
     __builtin_amdgcn_sched_barrier(0);      // issue the loads before the MFMAs
@@ -247,11 +287,16 @@ enum { kModeLists = 0, kModeFilter = 1, kModeFallback = 2 };
 // MODE kModeLists / kModeFallback: each lane keeps a sorted private list of its
 // best KL (score, row) pairs; the lists go to part_s/part_r.  kModeFallback
 // only runs query tiles flagged in tflag.  MODE kModeFilter: every score at or
-// above the query's threshold is appended to its candidate buffer.
-template <int B, int KL, int MODE>
+// above the query's threshold is appended to its candidate buffer.  LO: the
+// scores include the query's lo part; without it they are the hi-only scores
+// H of the sample and filter passes (within QMeta::err of the rescored ones).
+template <int B, int KL, int MODE, bool LO>
 __global__ __launch_bounds__(kWG, 2) void k_score(ScoreArgs a) {
-  // one slab stage (3 x 128 rows) or the list epilogue's 4 x 64 x 64 scores
-  constexpr int kLdsHalves = (3 * kTB * kLdk > 2 * 4 * 64 * 64) ? 3 * kTB * kLdk : 2 * 4 * 64 * 64;
+  // one slab stage (codes, hi[, lo]: 128 rows each) or the list epilogue's
+  // 4 x 64 x 64 scores
+  constexpr int kSlab = (LO ? 3 : 2) * kTB * kLdk;
+  constexpr int kLists = MODE == kModeFilter ? 0 : 2 * 4 * 64 * 64;
+  constexpr int kLdsHalves = kSlab > kLists ? kSlab : kLists;
   __shared__ __attribute__((aligned(16))) _Float16 lds[kLdsHalves];
   const int qt = blockIdx.x % a.nqt;
   const int split = blockIdx.x / a.nqt;
@@ -282,7 +327,7 @@ __global__ __launch_bounds__(kWG, 2) void k_score(ScoreArgs a) {
     const int64_t rbase = tile * kTB;
     const int rows = (int)min<int64_t>(kTB, a.n - rbase);
     floatx16 acc[4];
-    score_tile<B>(a, rbase, rows, QH, QL, qrows, lds, acc);
+    score_tile<B, LO>(a, rbase, rows, QH, QL, qrows, lds, acc);
 
     // The scale osc is positive, so the largest score is osc times the
     // largest accumulator; only a partial tile needs the row check.
@@ -370,7 +415,8 @@ __global__ __launch_bounds__(kWG, 2) void k_score(ScoreArgs a) {
 template <int KL>
 __device__ __forceinline__ void wave_select(int k, float (&ls)[KL], int (&lr)[KL], int64_t j,
                                             const int64_t* __restrict__ ids, float* __restrict__ out_s,
-                                            int64_t* __restrict__ out_i, float* __restrict__ kth) {
+                                            int64_t* __restrict__ out_i, float* __restrict__ kth,
+                                            float kth_drop = 0.0f) {
   const int lane = threadIdx.x & 63;
   for (int t = 0; t < k; ++t) {
     float bs = ls[0];
@@ -394,7 +440,7 @@ __device__ __forceinline__ void wave_select(int k, float (&ls)[KL], int (&lr)[KL
         out_s[j * k + t] = (br == kNoRow) ? -INFINITY : bs;
         out_i[j * k + t] = (br == kNoRow) ? -1 : ids[br];
       }
-      if (kth && t == k - 1) kth[j] = (br == kNoRow) ? -INFINITY : bs;
+      if (kth && t == k - 1) kth[j] = (br == kNoRow) ? -INFINITY : rd32((double)bs - (double)kth_drop);
     }
   }
 }
@@ -449,7 +495,9 @@ __global__ __launch_bounds__(256) void k_topk_merge(int64_t nq, int cands, int k
     if (!better(cs, cr, ls[KL - 1], lr[KL - 1])) continue;
     list_insert<KL>(ls, lr, cs, cr);
   }
-  wave_select<KL>(k, ls, lr, j, ids, out_s, out_i, kth);
+  // the sample's k-th hi-only score, lowered by 2 err: a threshold no row of
+  // the final top-k falls below in hi-only terms
+  wave_select<KL>(k, ls, lr, j, ids, out_s, out_i, kth, kth ? 2.0f * meta[j].err : 0.0f);
 }
 
 // One wave per query: the k best of the query's candidate buffer.  A buffer
@@ -617,6 +665,110 @@ __global__ __launch_bounds__(64) void k_cand_select_radix(int64_t nq, uint32_t c
   }
 }
 
+// ------------------------------------------------------------------ rescoring
+constexpr int kRescoreCap = 256;     // candidates near the k-th score rescored per query
+constexpr int kRescoreThreads = 256;
+constexpr int kRescoreLanes = 16;    // lanes per rescored row
+
+// One workgroup per query, after the selection of the k best hi-only scores H
+// among the candidates.  With h_k the k-th of them, every row of the final
+// top-k has H >= h_k - 2 err (k rows have S >= h_k - err, and |H - S| <= err),
+// so those candidates are rescored from the codes and the float32 query,
+// summed in binary64 and rounded once to float32, and the k best by (S desc,
+// row asc) replace the selection's output.  More than kRescoreCap such
+// candidates (many near-equal scores) flag the query for the exact fallback
+// pass.  Queries already flagged, or invalid, are left as the selection wrote
+// them.  Sixteen lanes share a row (16 rows in flight per workgroup); a lane
+// takes whole groups of 32 codes (B words), unpacked as the scoring kernel
+// unpacks them (exactly, to fp16).
+template <int B>
+__global__ __launch_bounds__(kRescoreThreads) void k_rescore(
+    int64_t nq, uint32_t cap, int k, const uint32_t* __restrict__ cnt, const float* __restrict__ cs,
+    const int32_t* __restrict__ cr, const QMeta* __restrict__ meta, const int64_t* __restrict__ ids,
+    const float* __restrict__ q, double step, const uint32_t* __restrict__ codes, int64_t row_words, int D,
+    float* __restrict__ out_s, int64_t* __restrict__ out_i, uint32_t* __restrict__ qflag,
+    uint32_t* __restrict__ tflag) {
+  __shared__ int32_t rows[kRescoreCap];
+  __shared__ unsigned long long keys[kRescoreCap];
+  __shared__ uint32_t m_sh;
+  const int tid = threadIdx.x;
+  const int64_t j = blockIdx.x;
+  if (j >= nq) return;
+  const QMeta mj = meta[j];
+  if (qflag[j] != 0u || mj.bad) return;
+  const uint32_t c = cnt[j];
+  const int kk = (int)min((uint32_t)k, c);
+  if (kk == 0) return;
+  const float thr = rd32((double)out_s[j * k + kk - 1] - 2.0 * (double)mj.err);
+  if (tid == 0) m_sh = 0u;
+  __syncthreads();
+  for (uint32_t i = tid; i < c; i += kRescoreThreads) {
+    if (cs[j * cap + i] >= thr) {
+      const uint32_t p = atomicAdd(&m_sh, 1u);
+      if (p < (uint32_t)kRescoreCap) rows[p] = cr[j * cap + i];
+    }
+  }
+  __syncthreads();
+  const uint32_t m = m_sh;
+  if (m > (uint32_t)kRescoreCap) {
+    if (tid == 0) {
+      qflag[j] = 1u;
+      atomicOr(&tflag[j / kTB], 1u);
+    }
+    return;
+  }
+  const float* qj = q + j * D;
+  const int slot = tid / kRescoreLanes, sl = tid % kRescoreLanes;
+  const int ngroups = D / 32;
+  for (uint32_t t0 = 0; t0 < m; t0 += kRescoreThreads / kRescoreLanes) {
+    const uint32_t t = t0 + (uint32_t)slot;
+    double acc = 0.0;
+    if (t < m) {
+      const uint32_t* w = codes + (int64_t)rows[t] * row_words;
+      for (int g = sl; g < ngroups; g += kRescoreLanes) {
+        uint32_t cw[B];
+#pragma unroll
+        for (int i = 0; i < B; ++i) cw[i] = w[g * B + i];
+        float qv[32];
+#pragma unroll
+        for (int e = 0; e < 32; ++e) qv[e] = qj[g * 32 + e];
+        _Float16 h[32];
+        unpack32<B>(cw, h);
+#pragma unroll
+        for (int e = 0; e < 32; ++e) acc = fma((double)qv[e], (double)(float)h[e], acc);
+      }
+    }
+    for (int o = kRescoreLanes / 2; o > 0; o >>= 1) acc += __shfl_xor(acc, o);   // within the row's lanes
+    if (t < m && sl == 0)
+      keys[t] = ((unsigned long long)f2ord((float)(acc * step) + 0.0f) << 32) | (unsigned long long)(~(uint32_t)rows[t]);
+  }
+  // bitonic sort of the m keys, descending (score, then ~row); padding keys 0
+  uint32_t P = 1u;
+  while (P < m) P <<= 1;
+  for (uint32_t i = m + tid; i < P; i += kRescoreThreads) keys[i] = 0ull;
+  __syncthreads();
+  for (uint32_t size = 2; size <= P; size <<= 1) {
+    for (uint32_t stride = size >> 1; stride > 0; stride >>= 1) {
+      for (uint32_t i = tid; i < P; i += kRescoreThreads) {
+        const uint32_t l = i ^ stride;
+        if (l > i) {
+          const unsigned long long x = keys[i], y = keys[l];
+          const bool desc = (i & size) == 0;
+          if (desc ? (x < y) : (x > y)) {
+            keys[i] = y;
+            keys[l] = x;
+          }
+        }
+      }
+      __syncthreads();
+    }
+  }
+  for (int t = tid; t < kk; t += kRescoreThreads) {
+    out_s[j * k + t] = ord2f((uint32_t)(keys[t] >> 32));
+    out_i[j * k + t] = ids[~(uint32_t)(keys[t] & 0xffffffffull)];
+  }
+}
+
 __global__ void k_clear_u32(uint32_t* a, int64_t na, uint32_t* b, int64_t nb) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t st = (int64_t)gridDim.x * blockDim.x;
@@ -624,27 +776,58 @@ __global__ void k_clear_u32(uint32_t* a, int64_t na, uint32_t* b, int64_t nb) {
   for (int64_t t = i; t < nb; t += st) b[t] = 0u;
 }
 
+// Largest value of hn[0, n) as float bits (non-negative floats order as
+// their bits); *out must hold 0 before.
+__global__ __launch_bounds__(256) void k_hn_max(const float* __restrict__ hn, int64_t n, uint32_t* __restrict__ out) {
+  uint32_t mx = 0u;
+  const int64_t st = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += st)
+    mx = max(mx, __float_as_uint(hn[i]));
+  for (int o = 32; o > 0; o >>= 1) mx = max(mx, (uint32_t)__shfl_xor((int)mx, o));
+  if ((threadIdx.x & 63) == 0 && mx != 0u) atomicMax(out, mx);
+}
+
+// Lists and fallback give final scores (hi and lo); the filter pass works on
+// hi-only scores.
 template <int B, int KL>
 void launch_mode(int mode, dim3 grid, hipStream_t st, const ScoreArgs& a) {
-  if (mode == kModeLists) hipLaunchKernelGGL((k_score<B, KL, kModeLists>), grid, dim3(kWG), 0, st, a);
-  else if (mode == kModeFilter) hipLaunchKernelGGL((k_score<B, KL, kModeFilter>), grid, dim3(kWG), 0, st, a);
-  else hipLaunchKernelGGL((k_score<B, KL, kModeFallback>), grid, dim3(kWG), 0, st, a);
+  if (mode == kModeLists) hipLaunchKernelGGL((k_score<B, KL, kModeLists, true>), grid, dim3(kWG), 0, st, a);
+  else if (mode == kModeFilter) hipLaunchKernelGGL((k_score<B, KL, kModeFilter, false>), grid, dim3(kWG), 0, st, a);
+  else hipLaunchKernelGGL((k_score<B, KL, kModeFallback, true>), grid, dim3(kWG), 0, st, a);
 }
 
 template <int B>
 lam_status dispatch_bits(int b, int kl, int mode, dim3 grid, hipStream_t st, const ScoreArgs& a) {
   if (b == B) {
-    if (kl == 4) {   // the sample pass's short lists
+    if (kl == 4) {   // the sample pass: short lists of hi-only scores
       if (mode != kModeLists) {
         set_error("internal: lists of 4 serve the sample pass only");
         return LAM_EINVAL;
       }
-      hipLaunchKernelGGL((k_score<B, 4, kModeLists>), grid, dim3(kWG), 0, st, a);
+      hipLaunchKernelGGL((k_score<B, 4, kModeLists, false>), grid, dim3(kWG), 0, st, a);
     } else if (kl == 16) launch_mode<B, 16>(mode, grid, st, a);
     else launch_mode<B, 64>(mode, grid, st, a);
     return LAM_OK;
   }
   if constexpr (B < 12) return dispatch_bits<B + 1>(b, kl, mode, grid, st, a);
+  set_error("scoring supports codes of at most 12 bits (got %d)", b);
+  return LAM_ESTATE;
+}
+
+template <int B>
+lam_status launch_rescore(int b, dim3 grid, hipStream_t st, int64_t nq, uint32_t cap, int k, const uint32_t* cnt,
+                          const float* cs, const int32_t* cr, const QMeta* meta, const int64_t* ids, const float* q,
+                          double step, const uint32_t* codes, int64_t row_words, int D, float* out_s,
+                          int64_t* out_i, uint32_t* qflag, uint32_t* tflag) {
+  if (b == B) {
+    hipLaunchKernelGGL((k_rescore<B>), grid, dim3(kRescoreThreads), 0, st, nq, cap, k, cnt, cs, cr, meta, ids, q,
+                       step, codes, row_words, D, out_s, out_i, qflag, tflag);
+    LAM_HIP(hipGetLastError());
+    return LAM_OK;
+  }
+  if constexpr (B < 12)
+    return launch_rescore<B + 1>(b, grid, st, nq, cap, k, cnt, cs, cr, meta, ids, q, step, codes, row_words, D, out_s,
+                                 out_i, qflag, tflag);
   set_error("scoring supports codes of at most 12 bits (got %d)", b);
   return LAM_ESTATE;
 }
@@ -667,19 +850,24 @@ void plan_splits(int nqt, int64_t ntiles, int* splits, int64_t* tps) {
 }  // namespace
 
 // Scoring plan.  With at most S store rows (S = k * n / 1024, at least 4,096)
-// one pass of per-lane lists gives the exact top-k.  Beyond that:
-//   1. theta_j, the k-th best entry of per-lane lists of the 4 best scores
-//      over the first S rows: the least of k distinct rows' scores, hence a
-//      lower bound of the k-th best score over the whole store (short lists
-//      keep this pass cheap -- the insertions, not the MFMAs, dominate it --
-//      at the price of a slightly lower theta_j when one lane holds more than
-//      4 of the sample's best k; the splits give at least 2k entries);
-//   2. a full scan appends every row scoring >= theta_j to query j's candidate
-//      buffer (about k * n / S = 1,024 entries expected; capacity 4,096);
-//   3. the k best candidates by (score desc, id asc) are the answer;
-//   4. a query whose buffer overflowed (many equal scores, say) is redone with
-//      per-lane lists over the whole store; launched always, it returns at once
-//      when nothing overflowed, so the call stays asynchronous.
+// one pass of per-lane lists gives the exact top-k.  Beyond that (H: scores
+// of the hi part alone, within err of the rescored scores S):
+//   1. theta_j, the k-th best H of per-lane lists of the 4 best H over the
+//      first S rows, minus 2 err_j: k distinct rows have S >= theta_j + err_j,
+//      so every row of the final top-k has H >= theta_j (short lists keep
+//      this pass cheap -- the insertions, not the MFMAs, dominate it -- at
+//      the price of a slightly lower theta_j when one lane holds more than 4
+//      of the sample's best k; the splits give at least 2k entries);
+//   2. a full scan of H appends every row with H >= theta_j to query j's
+//      candidate buffer (about k * n / S = 1,024 entries expected; capacity
+//      4,096);
+//   3. the k best candidates by H; the candidates within 2 err_j of the k-th
+//      of them are rescored exactly and their k best by (S desc, id asc) are
+//      the answer (k_rescore);
+//   4. a query whose buffer overflowed, or with more than 256 candidates to
+//      rescore (many equal scores, say), is redone with exact per-lane lists
+//      over the whole store; launched always, it returns at once when nothing
+//      was flagged, so the call stays asynchronous.
 lam_status score_topk(lam_ctx* ctx, const lam_store* st, const float* q, int64_t nq, int32_t k, float* scores,
                       int64_t* ids, float* bound, const uint32_t* codes) {
   if (nq == 0) return LAM_OK;
@@ -696,7 +884,8 @@ lam_status score_topk(lam_ctx* ctx, const lam_store* st, const float* q, int64_t
   {
     ProfScope ps(ctx, "score_prep");
     hipLaunchKernelGGL(k_score_prep, dim3((unsigned)((nq + 3) / 4)), dim3(256), 0, ctx->stream, q, nq, D, st->q.step,
-                       st->q.eps, ctx->scratch[S_QHI].as<_Float16>(), ctx->scratch[S_QLO].as<_Float16>(), qmeta);
+                       st->q.eps, st->hn_max, ctx->scratch[S_QHI].as<_Float16>(), ctx->scratch[S_QLO].as<_Float16>(),
+                       qmeta);
     LAM_HIP(hipGetLastError());
   }
   const int nqt = (int)((nq + kTB - 1) / kTB);
@@ -802,6 +991,8 @@ lam_status score_topk(lam_ctx* ctx, const lam_store* st, const float* q, int64_t
       hipLaunchKernelGGL(k_cand_select_radix, dim3((unsigned)nq), dim3(64), 0, ctx->stream, nq, cap, k, cand_cnt, cand_s, cand_r,
                          qmeta, st->ids, scores, ids, bound, qflag, tflag);
     LAM_HIP(hipGetLastError());
+    LAM_TRY(launch_rescore<1>(b, dim3((unsigned)nq), ctx->stream, nq, cap, k, cand_cnt, cand_s, cand_r, qmeta,
+                              st->ids, q, st->q.step, a.codes, a.row_words, D, scores, ids, qflag, tflag));
   }
   {
     ProfScope ps(ctx, "score_fallback");
@@ -870,6 +1061,16 @@ __global__ __launch_bounds__(256) void k_certify(int64_t nq, int k, const float*
 
 }  // namespace
 
+lam_status store_norm_max(lam_ctx* ctx, lam_store* st) {
+  hipLaunchKernelGGL(k_clear_u32, dim3(1), dim3(64), 0, ctx->stream, st->hn_max, (int64_t)1, nullptr, (int64_t)0);
+  const int64_t n = st->size;
+  if (n > 0)
+    hipLaunchKernelGGL(k_hn_max, dim3((unsigned)std::min<int64_t>(256, (n + 255) / 256)), dim3(256), 0, ctx->stream,
+                       st->hn, n, st->hn_max);
+  LAM_HIP(hipGetLastError());
+  return LAM_OK;
+}
+
 lam_status score_certify(lam_ctx* ctx, const lam_store* st, const float* q, int64_t nq, int32_t k, float* scores,
                          int64_t* ids, float* bound, uint8_t* certified, float* margin) {
   if (nq == 0) return LAM_OK;
@@ -884,6 +1085,8 @@ lam_status score_certify(lam_ctx* ctx, const lam_store* st, const float* q, int6
   // error bound of the float32 score per unit of ||q||_1: kappa (A + eps)
   const double u = std::ldexp(1.0, -24);
   const double g2d = 2.0 * st->dim * u / (1.0 - 2.0 * st->dim * u);
+  // (the split residual, the sums, the two scalings; a rescored score is
+  // within 2^-24 relative of its binary64 sum, far inside this)
   const double kappa = 1.01 * (std::ldexp(1.0, -22) + g2d + std::ldexp(1.0, -23));
   const double err_per_l1 = kappa * ((double)st->q.absmax + st->q.eps);
   hipLaunchKernelGGL(k_certify, dim3((unsigned)((nq + 3) / 4)), dim3(256), 0, ctx->stream, nq, k, s1, i1, b1, q,

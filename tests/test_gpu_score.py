@@ -244,3 +244,68 @@ def test_certificate_small_store_and_invalid_rows(lam):
     for k in (0, 64):
         with pytest.raises(lam.LamError):
             s.score_topk_certified(_dev(q), k)
+
+
+def _flip_store(n=6000, d=64, group=0):
+    """Rows whose hi-only scores order differently from their exact scores:
+    with eps = 2^-11 (code step 2^-10) row 100 has codes 1000 on coordinates
+    0-3 and row 200 codes 1000, 1000, 1000, 1001 on coordinates 4-7.  The query
+    is 1 + 2^-11 on coordinates 0-3 and 1 on 4-7: scaled by 2^14 its first four
+    entries are 2^14 + 8, which the fp16 hi part rounds to 2^14 (a tie, to
+    even).  Exactly, row 100 scores 4000 (1 + 2^-11) 2^-10 > 4001 2^-10 (row
+    200); from the hi part alone row 200 is ahead.  The other rows are random
+    unit rows on coordinates 8 and up (score 0); `group` more rows carry row
+    200's codes exactly (scores tied with it)."""
+    rng = np.random.default_rng(31)
+    x = np.zeros((n, d), np.float64)
+    x[:, 8:] = synth.unit_rows(rng, n, d - 8)
+    x[100] = 0.0
+    x[100, 0:4] = 1000 * 2.0 ** -10
+    r2 = np.zeros(d)
+    r2[4:8] = np.array([1000, 1000, 1000, 1001]) * 2.0 ** -10
+    x[200] = r2
+    for i in range(group):                       # distinct rows, same codes: moved on a coordinate
+        x[300 + i] = r2                          # the query ignores, by less than half a step
+        x[300 + i, 8] = (i + 1) * 1e-7
+    q = np.zeros((3, d))
+    q[:, 0:4] = 1.0 + 2.0 ** -11
+    q[:, 4:8] = 1.0
+    q[1] = 0.0
+    q[1, 8:] = synth.unit_rows(rng, 1, d - 8)[0]
+    q[2, 0:4] = 1.0                              # no rounding in the hi part
+    return x.astype(np.float32), q.astype(np.float32)
+
+
+@pytest.mark.parametrize("k", [1, 2, 10])
+def test_rescoring_restores_the_exact_order(lam, k):
+    """The two-pass plan filters and selects on hi-only scores, then rescores
+    the candidates near the k-th: the exact order must come back (row 100
+    before row 200), the scores within tolerance of the oracle."""
+    x, q = _flip_store()
+    s = _store_from_rows(lam, x)
+    eps = 2.0 ** -11
+    p = s.quantize(eps)
+    c = qeps.codes(x, eps).reshape(x.shape[0], -1)
+    assert c[100, 0] == 1000 and c[200, 7] == 1001 and p.bits <= 12
+    gs, gi, _ = s.score_topk(_dev(q), k)
+    gs, gi = gs.cpu().numpy(), gi.cpu().numpy()
+    assert gi[0, 0] == 100 and (k == 1 or gi[0, 1] == 200)
+    assert gi[2, 0] == 200                       # 4000 < 4001 when nothing is lost to rounding
+    _compare(gs, gi, c, np.arange(x.shape[0]), q, eps, k)
+
+
+def test_rescoring_cap_falls_back_exactly(lam):
+    """600 rows tied with row 200 (identical codes) sit within the rescoring
+    band of query 2 (row 200's codes win it): more than the rescoring cap, so
+    the query is redone by the exact pass; the k best are the tied rows in id
+    order."""
+    x, q = _flip_store(group=600)
+    s = _store_from_rows(lam, x)
+    eps = 2.0 ** -11
+    s.quantize(eps)
+    c = qeps.codes(x, eps).reshape(x.shape[0], -1)
+    assert all(np.array_equal(c[200], c[300 + i]) for i in (0, 299, 599))
+    gs, gi, _ = s.score_topk(_dev(q), 10)
+    gi = gi.cpu().numpy()
+    assert np.array_equal(gi[2], np.concatenate([[200], np.arange(300, 309)]))
+    _compare(gs.cpu().numpy(), gi, c, np.arange(x.shape[0]), q, eps, 10)
