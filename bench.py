@@ -61,8 +61,8 @@ def parse():
 
 
 KERNELS = ("qeps_encode", "qeps_decode", "dedup_prep", "dedup_screen", "dedup_verify", "dedup_resolve",
-           "dedup_append", "store_absmax", "store_encode", "store_decode", "score_prep", "score_mfma",
-           "score_merge")
+           "dedup_append", "store_absmax", "store_encode", "store_decode", "score_prep", "score_sample",
+           "score_mfma", "score_merge", "score_fallback")
 HERE = os.path.dirname(os.path.abspath(__file__))
 TRAFFIC_FILE = os.path.join(HERE, "profiles", "traffic.json")
 
@@ -441,9 +441,9 @@ def main():
             "raw_code_bits": int(p_raw.bits),
         },
         "qeps_encode_GBps": enc.get("achieved", 0.0) * 1.0 if enc else None,
-        "queries_per_s": (qd.shape[0] / (sum(kinfo[k]["ms_per_step"] for k in ("score_prep", "score_mfma",
-                                                                                "score_merge") if k in kinfo)
-                                          / 1e3)),
+        # every scoring launch: prep, sample, filter, select and rescore, fallback
+        "queries_per_s": (qd.shape[0] / (sum(kinfo[k]["ms_per_step"] for k in KERNELS
+                                             if k.startswith("score_") and k in kinfo) / 1e3)),
         "roofline": roofline,
         **extras,
         "kernels": kinfo,
