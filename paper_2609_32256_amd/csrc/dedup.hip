@@ -131,12 +131,26 @@ __device__ __forceinline__ void init_chunk_row(const ChunkState& c, int64_t r, i
   }
 }
 
+constexpr int kPrepVec = 4;   // float4 of a row per lane held in registers (D <= 1,024)
+
 __global__ __launch_bounds__(256) void k_prep(const float* __restrict__ x, int64_t n, int D,
                                               _Float16* __restrict__ x16, float* __restrict__ hn,
                                               float* __restrict__ eterm, double K1, double K2, double K3h,
                                               DevFlags* __restrict__ flags, ChunkState cs) {
   const int lane = threadIdx.x & 63;
   const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const float* p = x + row * D;
+  // For D <= 1,024 the row's loads are issued first, through a buffer resource
+  // (no memory touched past the row, nor for a row past n), so their latency
+  // overlaps the chunk-state stores below.
+  const bool vec = D <= 256 * kPrepVec;
+  float4 v4[kPrepVec];
+  {
+    const __amdgpu_buffer_rsrc_t rs = f32_rsrc(p, (vec && row < n) ? D : 0);
+#pragma unroll
+    for (int u = 0; u < kPrepVec; ++u)
+      v4[u] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(rs, (uint32_t)(u * 256 + lane * 4) * 4u, 0, 0));
+  }
   if (blockIdx.x == 0 && threadIdx.x == 0) {
     cs.cc->npairs = 0u;
     cs.cc->n_escalate = 0u;
@@ -145,12 +159,10 @@ __global__ __launch_bounds__(256) void k_prep(const float* __restrict__ x, int64
   }
   if (row < cs.nB) init_chunk_row(cs, row, lane);
   if (row >= n) return;
-  const float* p = x + row * D;
   _Float16* q = x16 + row * D;
   double na = 0.0, l1 = 0.0;
   bool nf = false, rng = false;
-  for (int d = lane * 4; d < D; d += 256) {
-    const float4 v = *reinterpret_cast<const float4*>(p + d);
+  auto take = [&](const float4& v, int d) {
     const float c[4] = {v.x, v.y, v.z, v.w};
     _Float16 h[4];
 #pragma unroll
@@ -165,6 +177,16 @@ __global__ __launch_bounds__(256) void k_prep(const float* __restrict__ x, int64
     uint2 packed;
     __builtin_memcpy(&packed, h, 8);
     *reinterpret_cast<uint2*>(q + d) = packed;
+  };
+  if (vec) {
+#pragma unroll
+    for (int u = 0; u < kPrepVec; ++u) {
+      const int d = u * 256 + lane * 4;
+      if (d >= D) break;
+      take(v4[u], d);
+    }
+  } else {
+    for (int d = lane * 4; d < D; d += 256) take(*reinterpret_cast<const float4*>(p + d), d);
   }
   na = wave_sum_f64(na);
   l1 = wave_sum_f64(l1);
