@@ -244,8 +244,10 @@ lam_status lam_store_export(lam_ctx* ctx, const lam_store* store, int64_t* ids_d
 
 /* Score nq float32 queries (row-major, dim each) against the quantized store:
  * score(j, y) = step * sum_d q_j,d * code_y,d, i.e. q_j . x_hat_y with the
- * exact dequantized row, accumulated in float32 (|error| <= 1e-5 for unit
- * rows).  Per query the k best by (score desc, id asc) go to scores_dev and
+ * exact dequantized row (|error| <= 1e-5 for unit rows: float32 accumulation
+ * of the query's fp16 hi and lo parts, or, for the rows of a large store that
+ * reach a query's top-k, a binary64 sum rounded once; the ranking is the one
+ * these scores give).  Per query the k best by (score desc, id asc) go to scores_dev and
  * ids_dev (nq x k, row-major), padded with (-inf, -1) past the store size.
  * bound_dev (optional): eps * ||q_j||_1 rounded up to float32.
  * 1 <= k <= 64.  ESTATE if the store is not quantized (or has rows added
