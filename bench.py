@@ -159,8 +159,8 @@ def beside_the_step(lam, torch, np, xd, qd, store, rep, pairs, ctx):
     statistics of the stream (ambiguous pairs, exact decisions, smallest
     decided margin), the screen at scale, the removal ceiling of the stream,
     the share of benchmark queries whose top-10 is certified rank-invariant,
-    the per-block codec's size on the retained store, and the stream through
-    the banded candidate index."""
+    the per-block codec's size on the retained store, scoring at the corpus
+    size, and the stream through the banded candidate index."""
     ceil = lam.removal_ceiling(xd, TAU, batch=BATCH, ctx=ctx)
     cert = store.score_topk_certified(qd, TOPK)[3]
     blk = store.block_encode()
@@ -174,11 +174,40 @@ def beside_the_step(lam, torch, np, xd, qd, store, rep, pairs, ctx):
     del probe
     return {"decisions": decisions,
             "screen_steady_state": screen_steady_state(lam, torch, np, ctx),
+            "corpus_scoring": corpus_scoring(lam, torch, np, ctx),
             "removal_ceiling": {k: ceil[k] for k in ("kept", "kept_2delta", "removal", "ceiling",
                                                      "frac_of_ceiling", "bits_lo", "bits_hi")},
             "certified_top10_frac": float(cert.float().mean().item()),
             "block_codec": {k: blk[k] for k in ("bits_per_code", "plain_bits", "codec_ratio", "composite_ratio")},
             "banded": banded_ingest(lam, torch, np, xd, rep, pairs, ctx)}
+
+
+def corpus_scoring(lam, torch, np, ctx, calls=5):
+    """Scoring at the corpus size: 4,096 queries top-10 against all 361,802
+    records of the corpus recipe at D = 768 (every record in the store,
+    quantized at eps = 1e-3).  Work is 2 D flop per (query, row)."""
+    import synth
+    cfg = synth.corpus_retrieval()
+    xd = torch.from_numpy(cfg["x"]).cuda()
+    qd = torch.from_numpy(cfg["q"]).cuda()
+    n, nq = xd.shape[0], qd.shape[0]
+    s = lam.Store(D, 1.0, n, ctx=ctx)
+    for b0 in range(0, n, 16384):
+        s.ingest(xd[b0:b0 + 16384], sync=False)
+    p = s.quantize(cfg["eps"])
+    out = s.score_topk(qd, cfg["k"])
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(calls):
+        s.score_topk(qd, cfg["k"], out=out)
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / calls
+    flops = 2.0 * D * nq * s.size
+    del s, xd
+    return {"workload": f"corpus recipe: {nq} queries top-{cfg['k']} against {n} rows, D = {D}, "
+                        f"{p.bits}-bit codes", "ms_per_call": ms, "queries_per_s": nq / (ms / 1e3),
+            "TFLOPs_algorithmic": flops / (ms / 1e3) / 1e12,
+            "frac_of_peak": flops / (ms / 1e3) / 1e12 / MFMA_F16_PEAK_TFLOPS}
 
 
 def screen_steady_state(lam, torch, np, ctx, m=262_144, batch=4096, calls=5):
