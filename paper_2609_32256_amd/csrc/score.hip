@@ -207,6 +207,35 @@ __device__ __forceinline__ void unpack32(const uint32_t* __restrict__ w, _Float1
   }
 }
 
+// One group of 32 b-bit codes (B consecutive words starting at word w0 of the
+// buffer, or zeros when !ok): the widest loads the group's alignment allows
+// (a group starts at a multiple of B words), so a lane asks for its bytes in
+// one or two pieces rather than B.
+template <int B>
+__device__ __forceinline__ void load_group(__amdgpu_buffer_rsrc_t rs, bool ok, uint32_t w0, uint32_t (&cw)[B]) {
+  if constexpr (B % 4 == 0) {
+#pragma unroll
+    for (int i = 0; i < B; i += 4) {
+      const uint4 v = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rs, ok ? (w0 + i) * 4u : kOffOOB, 0, 0));
+      cw[i] = v.x;
+      cw[i + 1] = v.y;
+      cw[i + 2] = v.z;
+      cw[i + 3] = v.w;
+    }
+  } else if constexpr (B % 2 == 0) {
+#pragma unroll
+    for (int i = 0; i < B; i += 2) {
+      const uint2 v = __builtin_bit_cast(uint2, __builtin_amdgcn_raw_buffer_load_b64(rs, ok ? (w0 + i) * 4u : kOffOOB, 0, 0));
+      cw[i] = v.x;
+      cw[i + 1] = v.y;
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < B; ++i)
+      cw[i] = (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(rs, ok ? (w0 + i) * 4u : kOffOOB, 0, 0);
+  }
+}
+
 // acc[t] (t = 0..3) <- the 128 x 128 tile of raw scores: store rows
 // [rbase, rbase + rows) against the workgroup's 128 queries (wave w holds
 // queries [32w, 32w + 32), lane j % 32, store rows t*32 + acc_row(r, lane)).
@@ -237,9 +266,7 @@ __device__ __forceinline__ void score_tile(const ScoreArgs& a, int64_t rbase, in
   auto load_slab = [&](int k0, uint32_t (&cw)[B], uint4 (&rh)[4], uint4 (&rl)[4]) {
     const bool ok = urow < rows && k0 + 32 * uhalf < a.D;
     const uint32_t w0 = (uint32_t)(urow * a.row_words + (int64_t)(k0 / 32 + uhalf) * B);
-#pragma unroll
-    for (int i = 0; i < B; ++i)
-      cw[i] = (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(rsC, ok ? (w0 + i) * 4u : kOffOOB, 0, 0);
+    load_group<B>(rsC, ok, w0, cw);
     slab_load_n<4>(rsH, qrows, a.D, k0, a.D, rh, kWG);
     if (LO) slab_load_n<4>(rsL, qrows, a.D, k0, a.D, rl, kWG);
   };
@@ -665,6 +692,154 @@ __global__ __launch_bounds__(64) void k_cand_select_radix(int64_t nq, uint32_t c
   }
 }
 
+// ------------------------------------------------------------------ filter pass on the screen's pipeline
+using FilterTile = Tile<2, 4, 2, 1, 4>;
+constexpr int kFilterGroupQ = 8;   // query tiles per group in the tile order
+
+// The threshold plan's filter pass (hi-only scores H) for D = 64 NS: one
+// 128 x 128 tile (store rows x queries) per workgroup of 8 waves, each wave
+// 64 rows x 32 queries (2 x 1 tiles of v_mfma_f32_32x32x16_f16); K-slabs of 64
+// through two LDS stages with every load issued three slabs before its LDS
+// store, one barrier per slab.  Threads 0-255 load one group of 32 codes (B
+// words) per slab and unpack it straight to fp16 (exact for B <= 12); every
+// thread loads two 16-byte pieces of the queries' hi part.  Tile order:
+// groups of 8 query tiles against every store tile, query tile fastest, each
+// XCD a contiguous range, so an XCD holds its 8 query tiles in L2 while the
+// codes stream past.  Every row with H >= the query's threshold is appended to
+// its candidate buffer, as in k_score's filter mode.
+template <int B, int NS>
+__global__ __launch_bounds__(FilterTile::kThreads, FilterTile::kMinWaves) void k_filter(ScoreArgs a) {
+  using C = FilterTile;
+  __shared__ _Float16 lds[C::kLdsHalves];
+  const int64_t nt = (a.n + kTB - 1) / kTB;
+  const int64_t logical = xcd_remap((int64_t)blockIdx.x, (int64_t)a.nqt * nt);
+  const int64_t per = (int64_t)kFilterGroupQ * nt;
+  const int g = (int)(logical / per);
+  const int64_t l = logical - (int64_t)g * per;
+  const int gsize = min(kFilterGroupQ, a.nqt - g * kFilterGroupQ);
+  const int qt = g * kFilterGroupQ + (int)(l % gsize);
+  const int64_t rbase = (l / gsize) * kTB;
+  const int rows = (int)min<int64_t>(kTB, a.n - rbase);
+  const int64_t qbase = (int64_t)qt * kTB;
+  const int qrows = (int)min<int64_t>(kTB, a.nq - qbase);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / C::WN, wn = wave % C::WN;
+  // this lane's query and its threshold, loaded before the GEMM
+  const int64_t j = qbase + wn * 32 + (lane & 31);
+  const bool jv = j < a.nq;
+  const float th = jv ? a.thr[j] : 0.0f;
+  const float osc = jv ? a.meta[j].osc : 0.0f;
+
+  auto sa = [&](int i) -> _Float16* { return lds + i * ((C::BM + C::BN) * kLdk); };
+  auto sb = [&](int i) -> _Float16* { return lds + i * ((C::BM + C::BN) * kLdk) + C::BM * kLdk; };
+  floatx16 acc[C::TI][C::TJ];
+#pragma unroll
+  for (int x = 0; x < C::TI; ++x)
+#pragma unroll
+    for (int y = 0; y < C::TJ; ++y)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[x][y][r] = 0.0f;
+  const __amdgpu_buffer_rsrc_t rsC = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint32_t*>(a.codes + rbase * a.row_words), (short)0, (int)(rows * a.row_words * 4), 0x00020000);
+  const __amdgpu_buffer_rsrc_t rsQ = tile_rsrc(a.qhi + qbase * a.D, qrows, a.D);
+  const int urow = tid >> 1, uhalf = tid & 1;   // code groups: two per row, threads 0-255
+  const bool unpacker = tid < 2 * kTB;
+  auto load = [&](int s, uint32_t (&cw)[B], uint4 (&qv)[C::kPerB]) {
+    const int k0 = s * kBK;
+    const bool ok = unpacker && urow < rows && k0 < a.D;
+    const uint32_t w0 = (uint32_t)(urow * a.row_words + (int64_t)(k0 / 32 + uhalf) * B);
+    load_group<B>(rsC, ok, w0, cw);
+    slab_load_n<C::kPerB>(rsQ, qrows, a.D, k0, a.D, qv, C::kThreads);
+  };
+  auto store = [&](int st, const uint32_t (&cw)[B], const uint4 (&qv)[C::kPerB]) {
+    if (unpacker) {
+      _Float16 h[32];
+      unpack32<B>(cw, h);
+      _Float16* dst = sa(st) + urow * kLdk + uhalf * 32;
+#pragma unroll
+      for (int i = 0; i < 32; i += 8) *reinterpret_cast<uint4*>(dst + i) = *reinterpret_cast<const uint4*>(h + i);
+    }
+    slab_store_n<C::kPerB>(sb(st), qv, C::kThreads);
+  };
+  auto compute = [&](int st) {
+#pragma unroll
+    for (int kk = 0; kk < kBK / 16; ++kk) {
+      half8 fa[C::TI], fb[C::TJ];
+#pragma unroll
+      for (int t = 0; t < C::TI; ++t) fa[t] = frag_load(sa(st), wm * C::TI * 32 + t * 32, kk);
+#pragma unroll
+      for (int t = 0; t < C::TJ; ++t) fb[t] = frag_load(sb(st), wn * C::TJ * 32 + t * 32, kk);
+#pragma unroll
+      for (int x = 0; x < C::TI; ++x)
+#pragma unroll
+        for (int y = 0; y < C::TJ; ++y)
+          acc[x][y] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fa[x], fb[y], acc[x][y], 0, 0, 0);
+    }
+  };
+  {
+    uint32_t cw[3][B];
+    uint4 qv[3][C::kPerB];
+#pragma unroll
+    for (int u = 0; u < 3; ++u) load(u, cw[u], qv[u]);
+    store(0, cw[0], qv[0]);
+    load(3, cw[0], qv[0]);
+    __syncthreads();
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      compute(s & 1);
+      if (s + 1 < NS) {
+        const int u = (s + 1) % 3;
+        store((s + 1) & 1, cw[u], qv[u]);
+        load(s + 4, cw[u], qv[u]);   // past the last slab: zeros, no memory touched
+      }
+      __syncthreads();
+    }
+  }
+  // epilogue: the tile's largest raw accumulator first (osc > 0)
+  float amx = -INFINITY;
+#pragma unroll
+  for (int x = 0; x < C::TI; ++x)
+#pragma unroll
+    for (int r = 0; r < 16; ++r)
+      amx = (wm * 64 + x * 32 + acc_row(r, lane) < rows) ? fmaxf(amx, acc[x][0][r]) : amx;
+  const bool hot = jv && amx * osc >= th;
+  if (__ballot(hot) == 0ull || !hot) return;
+  uint32_t c = 0u;
+#pragma unroll
+  for (int x = 0; x < C::TI; ++x)
+#pragma unroll
+    for (int r = 0; r < 16; ++r)
+      c += (wm * 64 + x * 32 + acc_row(r, lane) < rows && acc[x][0][r] * osc >= th) ? 1u : 0u;
+  uint32_t idx = atomicAdd(&a.cand_cnt[j], c);
+#pragma unroll
+  for (int x = 0; x < C::TI; ++x)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int rl_ = wm * 64 + x * 32 + acc_row(r, lane);
+      const float sc = acc[x][0][r] * osc;
+      if (rl_ < rows && sc >= th) {
+        if (idx < a.cap) {
+          a.cand_s[j * a.cap + idx] = sc;
+          a.cand_r[j * a.cap + idx] = (int)(rbase + rl_);
+        }
+        ++idx;
+      }
+    }
+}
+
+template <int B>
+lam_status launch_filter(int b, int D, dim3 grid, hipStream_t st, const ScoreArgs& a) {
+  if (b == B) {
+    if (D == 768) hipLaunchKernelGGL((k_filter<B, 12>), grid, dim3(FilterTile::kThreads), 0, st, a);
+    else hipLaunchKernelGGL((k_filter<B, 16>), grid, dim3(FilterTile::kThreads), 0, st, a);
+    LAM_HIP(hipGetLastError());
+    return LAM_OK;
+  }
+  if constexpr (B < 12) return launch_filter<B + 1>(b, D, grid, st, a);
+  set_error("scoring supports codes of at most 12 bits (got %d)", b);
+  return LAM_ESTATE;
+}
+
 // ------------------------------------------------------------------ rescoring
 constexpr int kRescoreCap = 256;     // candidates near the k-th score rescored per query
 constexpr int kRescoreThreads = 256;
@@ -979,8 +1154,15 @@ lam_status score_topk(lam_ctx* ctx, const lam_store* st, const float* q, int64_t
   a.tflag = tflag;
   {  // 2. full scan with the thresholds
     ProfScope ps(ctx, "score_mfma");
-    LAM_TRY(dispatch_bits<1>(b, KL, kModeFilter, dim3((unsigned)(nqt * sp2)), ctx->stream, a));
-    LAM_HIP(hipGetLastError());
+    if (D == 768 || D == 1024) {
+      // one 128 x 128 tile per workgroup on the screen's pipeline
+      const int64_t grid = (int64_t)nqt * ntiles;
+      LAM_CHECK(grid < (1LL << 31), LAM_EINVAL, "scoring grid too large");
+      LAM_TRY(launch_filter<1>(b, D, dim3((unsigned)grid), ctx->stream, a));
+    } else {
+      LAM_TRY(dispatch_bits<1>(b, KL, kModeFilter, dim3((unsigned)(nqt * sp2)), ctx->stream, a));
+      LAM_HIP(hipGetLastError());
+    }
   }
   {  // 3. select; 4. exact fallback for overflowed buffers (returns at once otherwise)
     ProfScope ps(ctx, "score_merge");

@@ -148,17 +148,18 @@ def test_corpus_sampled(lam):
     print(f"corpus: max |score - oracle| = {worst:.3g}")
 
 
-@pytest.mark.parametrize("k", [10, 50])
-def test_two_pass_and_overflow_fallback(lam, k):
-    """A store beyond the sample size takes the threshold/candidate plan; an
-    all-zero query ties every row at score 0, overflows its candidate buffer
-    and must come back exact from the fallback (the k lowest ids)."""
+@pytest.mark.parametrize("k,d", [(10, 64), (50, 64), (10, 768), (50, 768)])
+def test_two_pass_and_overflow_fallback(lam, k, d):
+    """A store beyond the sample size takes the threshold/candidate plan (at
+    D = 768 its filter pass runs on the screen's pipeline); an all-zero query
+    ties every row at score 0, overflows its candidate buffer and must come
+    back exact from the fallback (the k lowest ids)."""
     rng = np.random.default_rng(11)
     n = 20000
-    x = synth.unit_rows(rng, n, 64).astype(np.float32)
+    x = synth.unit_rows(rng, n, d).astype(np.float32)
     s = _store_from_rows(lam, x)
     s.quantize(1e-3)
-    q = synth.unit_rows(rng, 40, 64).astype(np.float32)
+    q = synth.unit_rows(rng, 40, d).astype(np.float32)
     q[[3, 17]] = 0.0
     gs, gi, gb = s.score_topk(_dev(q), k)
     gs, gi = gs.cpu().numpy(), gi.cpu().numpy()
@@ -169,14 +170,14 @@ def test_two_pass_and_overflow_fallback(lam, k):
     _compare(gs[keep], gi[keep], c, np.arange(n), q[keep], 1e-3, k)
 
 
-@pytest.mark.parametrize("k", [17, 50, 64])
-def test_two_pass_ties_broken_by_id(lam, k):
+@pytest.mark.parametrize("k,d", [(17, 64), (50, 64), (64, 64), (50, 768)])
+def test_two_pass_ties_broken_by_id(lam, k, d):
     """Exactly equal scores at the k-th place in the two-pass plan: 20,000
     rows are 40 copies of 500 vectors, the copies moved by less than the code
     step so that all copies of a vector share its codes; every query's top-k
     cuts through a group of equal scores, which must be taken in id order."""
     rng = np.random.default_rng(12)
-    base = synth.unit_rows(rng, 500, 64)
+    base = synth.unit_rows(rng, 500, d)
     x = np.tile(base, (40, 1))
     x[:, 0] += np.repeat(np.arange(40), 500) * 1e-6     # distinct rows, identical codes at eps = 0.02
     x = x.astype(np.float32)
@@ -184,7 +185,7 @@ def test_two_pass_ties_broken_by_id(lam, k):
     s.quantize(0.02, absmax=1.0)
     c = qeps.codes(x, 0.02).reshape(x.shape[0], -1)
     assert np.array_equal(c[:500], c[500:1000])
-    q = synth.unit_rows(rng, 24, 64).astype(np.float32)
+    q = synth.unit_rows(rng, 24, d).astype(np.float32)
     gs, gi, _ = s.score_topk(_dev(q), k)
     S = score.scores(q, c, 0.02)
     ts, ti = score.topk(S, np.arange(x.shape[0]), k)
@@ -276,12 +277,12 @@ def _flip_store(n=6000, d=64, group=0):
     return x.astype(np.float32), q.astype(np.float32)
 
 
-@pytest.mark.parametrize("k", [1, 2, 10])
-def test_rescoring_restores_the_exact_order(lam, k):
+@pytest.mark.parametrize("k,d", [(1, 64), (2, 64), (10, 64), (1, 768), (2, 768)])
+def test_rescoring_restores_the_exact_order(lam, k, d):
     """The two-pass plan filters and selects on hi-only scores, then rescores
     the candidates near the k-th: the exact order must come back (row 100
     before row 200), the scores within tolerance of the oracle."""
-    x, q = _flip_store()
+    x, q = _flip_store(d=d)
     s = _store_from_rows(lam, x)
     eps = 2.0 ** -11
     p = s.quantize(eps)
@@ -294,12 +295,13 @@ def test_rescoring_restores_the_exact_order(lam, k):
     _compare(gs, gi, c, np.arange(x.shape[0]), q, eps, k)
 
 
-def test_rescoring_cap_falls_back_exactly(lam):
+@pytest.mark.parametrize("d", [64, 768])
+def test_rescoring_cap_falls_back_exactly(lam, d):
     """600 rows tied with row 200 (identical codes) sit within the rescoring
     band of query 2 (row 200's codes win it): more than the rescoring cap, so
     the query is redone by the exact pass; the k best are the tied rows in id
     order."""
-    x, q = _flip_store(group=600)
+    x, q = _flip_store(d=d, group=600)
     s = _store_from_rows(lam, x)
     eps = 2.0 ** -11
     s.quantize(eps)
