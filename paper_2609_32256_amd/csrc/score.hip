@@ -22,7 +22,9 @@
 // Stores beyond the sample size take a threshold plan (score_topk) whose
 // sample and filter passes multiply the hi part alone -- half the MFMAs --
 // with thresholds lowered by twice a per-query bound on the hi part's error;
-// the few candidates near the k-th are then rescored exactly.
+// the few candidates near the k-th are then rescored exactly.  At D = 768 and
+// 1,024 the filter pass is k_filter: one 128 x 128 tile per workgroup on the
+// similarity screen's pipeline (two LDS stages, loads three slabs ahead).
 #include <cmath>
 #include <cstring>
 
