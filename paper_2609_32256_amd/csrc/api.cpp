@@ -403,12 +403,16 @@ lam_status lam_store_quantize(lam_ctx* ctx, lam_store* st, double eps, float abs
                               lam_qparams* out) {
   LAM_CHECK(ctx != nullptr && st != nullptr, LAM_EINVAL, "ctx or store is NULL");
   DeviceGuard g(ctx->device);
-  LAM_TRY(store_settle(st));
+  // the store's max |x| and max ||x||^2 / 2 are kept by the appends, so
+  // neither needs a pass over the rows here
+  LAM_TRY(store_maxima(st));
   const int64_t n = st->size * (int64_t)st->dim;
   DevBuf holder{st->codes, st->codes_cap};
   lam_qparams p{};
   st->blk_rows = -1;   // any block encoding describes the previous codes
-  lam_status s = quantize_impl(ctx, st->x32, n, eps, absmax, mode, nullptr, 0, &p, &holder, true);
+  float a = absmax;
+  if (!(absmax > 0.0f) && st->absmax_bits != 0u) memcpy(&a, &st->absmax_bits, 4);   // the exact maximum
+  lam_status s = quantize_impl(ctx, st->x32, n, eps, a, mode, nullptr, 0, &p, &holder, true);
   st->codes = holder.as<uint32_t>();
   st->codes_cap = holder.bytes;
   if (s != LAM_OK) {
@@ -417,7 +421,7 @@ lam_status lam_store_quantize(lam_ctx* ctx, lam_store* st, double eps, float abs
   }
   st->q = p;
   st->coded_rows = st->size;
-  LAM_TRY(store_norm_max(ctx, st));
+  st->hn_max = st->hnmax_bits;
   if (out) *out = p;
   return LAM_OK;
 }
@@ -434,6 +438,7 @@ lam_status lam_store_clear(lam_ctx* ctx, lam_store* st) {
   st->size_ub = 0;
   st->size = 0;
   st->n_seen = 0;
+  st->maxima_known = false;
   st->delta_hat_run = 0.0;
   st->coded_rows = -1;
   st->q = lam_qparams{};

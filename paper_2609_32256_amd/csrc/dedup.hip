@@ -68,6 +68,9 @@ struct StoreMeta {
   int64_t n_seen;                  // arrivals taken so far (global id of the next arrival)
   unsigned long long dhat2_bits;   // max merged squared distance of the run (binary64 bits)
   uint32_t err_bits;               // bit 0: non-finite input, bit 1: a coordinate with |x| >= 256
+  uint32_t absmax_bits;            // max |x| over the retained rows (float32 bits; non-negative
+                                   // floats order as their bits), the store codec's width input
+  uint32_t hnmax_bits;             // max ||x||^2 / 2 over the retained rows (float32 bits)
   uint32_t pad;
 };
 
@@ -1210,6 +1213,7 @@ __global__ __launch_bounds__(256) void k_append(AppendArgs a, int nB) {
   const bool skip = skip_all(a.flags);
   // every workgroup reads n_seen before the last one (below) advances it
   const int64_t gbase = a.meta->n_seen + a.c0;
+  const uint32_t am0 = a.meta->absmax_bits, hm0 = a.meta->hnmax_bits;   // the store's maxima so far
   const float* src = a.xc + (int64_t)rc * a.D;
   const bool vec = a.D <= 256 * kAppendVec;
   float4 v[kAppendVec];
@@ -1220,16 +1224,23 @@ __global__ __launch_bounds__(256) void k_append(AppendArgs a, int nB) {
       v[u] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(rs, (uint32_t)(u * 256 + lane * 4) * 4u, 0, 0));
   }
   double dmax = 0.0;
+  uint32_t amax = 0u, hmax = 0u;   // |x| and hn of a kept row (float bits, non-negative)
   if (!skip && r < nB) {
     if (p >= 0) {
       float* dst = a.xs + (int64_t)p * a.D;
       _Float16* d16 = a.x16s + (int64_t)p * a.D;
+      hmax = __float_as_uint(hn);
+      auto absbits = [](const float4& x) {
+        return max(max(__float_as_uint(x.x) & 0x7fffffffu, __float_as_uint(x.y) & 0x7fffffffu),
+                   max(__float_as_uint(x.z) & 0x7fffffffu, __float_as_uint(x.w) & 0x7fffffffu));
+      };
       if (vec) {
         // the fp16 operand is formed as the prep forms it, fl16(2^8 x)
 #pragma unroll
         for (int u = 0; u < kAppendVec; ++u) {
           const int d = u * 256 + lane * 4;
           if (d >= a.D) break;
+          amax = max(amax, absbits(v[u]));
           *reinterpret_cast<float4*>(dst + d) = v[u];
           const _Float16 h[4] = {(_Float16)(v[u].x * kScale), (_Float16)(v[u].y * kScale),
                                  (_Float16)(v[u].z * kScale), (_Float16)(v[u].w * kScale)};
@@ -1238,8 +1249,11 @@ __global__ __launch_bounds__(256) void k_append(AppendArgs a, int nB) {
           *reinterpret_cast<uint2*>(d16 + d) = packed;
         }
       } else {
-        for (int d = lane * 4; d < a.D; d += 256)
-          *reinterpret_cast<float4*>(dst + d) = *reinterpret_cast<const float4*>(src + d);
+        for (int d = lane * 4; d < a.D; d += 256) {
+          const float4 x = *reinterpret_cast<const float4*>(src + d);
+          amax = max(amax, absbits(x));
+          *reinterpret_cast<float4*>(dst + d) = x;
+        }
         const _Float16* s16 = a.x16c + (int64_t)r * a.D;
         for (int d = lane * 8; d < a.D; d += 512)
           *reinterpret_cast<uint4*>(d16 + d) = *reinterpret_cast<const uint4*>(s16 + d);
@@ -1273,14 +1287,26 @@ __global__ __launch_bounds__(256) void k_append(AppendArgs a, int nB) {
       dmax = wave_sum_f64(s);
     }
   }
+  for (int o = 32; o > 0; o >>= 1) amax = max(amax, (uint32_t)__shfl_xor((int)amax, o));
   __shared__ double part[4];
-  if (lane == 0) part[wave] = dmax;
+  __shared__ uint32_t apart[4], hpart[4];
+  if (lane == 0) {
+    part[wave] = dmax;
+    apart[wave] = amax;
+    hpart[wave] = hmax;
+  }
   __syncthreads();
   if (threadIdx.x == 0) {
     const double m = fmax(fmax(part[0], part[1]), fmax(part[2], part[3]));
     if (m > 0.0)
       atomicMax(reinterpret_cast<unsigned long long*>(&a.flags->dhat2_bits),
                 (unsigned long long)__double_as_longlong(m));
+    // the store's maxima: rows are appended only by calls that go through
+    // (skip is uniform over the call), so an invalid call leaves them as they were
+    const uint32_t am = max(max(apart[0], apart[1]), max(apart[2], apart[3]));
+    const uint32_t hm = max(max(hpart[0], hpart[1]), max(hpart[2], hpart[3]));
+    if (am > am0) atomicMax(&a.meta->absmax_bits, am);
+    if (hm > hm0) atomicMax(&a.meta->hnmax_bits, hm);
   }
   if (!a.last_chunk) return;
   // The last workgroup to finish folds the call into the store's bookkeeping
@@ -1352,7 +1378,6 @@ lam_status store_alloc(lam_store* st) {
   LAM_HIP(hipMalloc(&st->et, cap * 4));
   LAM_HIP(hipMalloc(&st->ids, cap * 8));
   LAM_HIP(hipMalloc(&st->stat_dev, sizeof(StoreMeta)));
-  LAM_HIP(hipMalloc(&st->hn_max, 4));
   LAM_HIP(hipMemset(st->stat_dev, 0, sizeof(StoreMeta)));
   if (st->lsh_r > 0) {
     const uint64_t entries = (uint64_t)cap * (uint64_t)st->lsh_nb;
@@ -1393,7 +1418,7 @@ lam_status lsh_reset(lam_ctx* ctx, lam_store* st, int64_t keep_rows) {
 
 void store_free(lam_store* st) {
   for (void* p : {(void*)st->x32, (void*)st->x16, (void*)st->hn, (void*)st->et, (void*)st->ids,
-                  (void*)st->stat_dev, (void*)st->codes, (void*)st->hn_max})
+                  (void*)st->stat_dev, (void*)st->codes})
     if (p) (void)hipFree(p);
   for (void* p : {(void*)st->blk_w, (void*)st->blk_row_off, (void*)st->blk_data, (void*)st->lsh_key,
                   (void*)st->lsh_head, (void*)st->lsh_next, (void*)st->lsh_rowkey})
@@ -1412,7 +1437,6 @@ void store_free(lam_store* st) {
   st->hn = st->et = st->stat_dev = nullptr;
   st->ids = nullptr;
   st->codes = nullptr;
-  st->hn_max = nullptr;
 }
 
 // ------------------------------------------------------------------ host orchestration
@@ -1448,6 +1472,9 @@ lam_status store_settle(lam_store* st) {
   st->size = m.m;
   st->size_ub = m.m;
   st->n_seen = m.n_seen;
+  st->absmax_bits = m.absmax_bits;
+  st->hnmax_bits = m.hnmax_bits;
+  st->maxima_known = true;
   double dh2 = 0.0;
   memcpy(&dh2, &m.dhat2_bits, 8);
   st->delta_hat_run = std::sqrt(dh2);
@@ -1465,6 +1492,17 @@ lam_status store_settle(lam_store* st) {
   return LAM_OK;
 }
 
+lam_status store_maxima(lam_store* st) {
+  LAM_TRY(store_settle(st));
+  if (st->maxima_known) return LAM_OK;
+  StoreMeta m{};
+  LAM_HIP(hipMemcpy(&m, st->stat_dev, sizeof m, hipMemcpyDeviceToHost));
+  st->absmax_bits = m.absmax_bits;
+  st->hnmax_bits = m.hnmax_bits;
+  st->maxima_known = true;
+  return LAM_OK;
+}
+
 lam_status dedup_ingest(lam_ctx* ctx, lam_store* st, const float* x, int64_t n, int64_t* rep, float* max_cos,
                         lam_ingest_stats* stats) {
   const int D = st->dim;
@@ -1478,6 +1516,7 @@ lam_status dedup_ingest(lam_ctx* ctx, lam_store* st, const float* x, int64_t n, 
     }
     return LAM_OK;
   }
+  st->maxima_known = false;   // appended rows may raise them
   const int CH = (int)std::min<int64_t>(n, kChunk);
   const int W = (CH + 63) / 64;
   const bool lsh = st->lsh_r > 0;

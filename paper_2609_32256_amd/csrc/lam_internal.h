@@ -133,7 +133,11 @@ struct lam_store {
   float* et = nullptr;        // per-row term of the screen's error bound (float32, rounded up)
   int64_t* ids = nullptr;     // global ids
   float* stat_dev = nullptr;  // device bookkeeping block (retained-row count)
-  uint32_t* hn_max = nullptr; // max of hn over the coded rows (float bits), set with the codes
+  uint32_t hn_max = 0;        // max of hn over the coded rows (float bits), set with the codes
+  // the device bookkeeping's maxima over the retained rows, as last read by the host
+  bool maxima_known = false;  // false until read again after calls that may have changed them
+  uint32_t absmax_bits = 0;   // max |x| (float bits)
+  uint32_t hnmax_bits = 0;    // max ||x||^2 / 2 (float bits)
   // codes
   uint32_t* codes = nullptr;
   uint64_t codes_cap = 0;
@@ -182,6 +186,7 @@ lam_status dedup_ingest(lam_ctx* ctx, lam_store* st, const float* x, int64_t n, 
                         float* max_cos, lam_ingest_stats* stats);
 lam_status store_alloc(lam_store* st);
 size_t store_meta_bytes();   // device bookkeeping block of a store (cleared by lam_store_clear)
+lam_status store_maxima(lam_store* st);   // settles the store and makes absmax_bits / hnmax_bits current
 void store_free(lam_store* st);
 
 // ------------------------------------------------------------------ scoring (score.hip)
@@ -203,6 +208,5 @@ lam_status lsh_reset(lam_ctx* ctx, lam_store* st, int64_t keep_rows);
 lam_status store_settle(lam_store* st);
 // Largest ||x||^2 / 2 over the store's rows, for the scoring error bound
 // (score.hip); enqueued by lam_store_quantize.
-lam_status store_norm_max(lam_ctx* ctx, lam_store* st);
 
 }  // namespace lam

@@ -70,7 +70,7 @@ __device__ __forceinline__ float rd32(double d) {
 //   S:         the rescoring sums in binary64 and rounds once to float32.
 // |H - S| <= |H - T| + |T - S| <= ||q - h|| R + (g + 2^-21)(||q|| + ||q - h||) R.
 __global__ __launch_bounds__(256) void k_score_prep(const float* __restrict__ q, int64_t nq, int D, double s,
-                                                    double eps, const uint32_t* __restrict__ hn_max,
+                                                    double eps, uint32_t hn_max,
                                                     _Float16* __restrict__ qhi,
                                                     _Float16* __restrict__ qlo, QMeta* __restrict__ meta) {
   const int lane = threadIdx.x & 63;
@@ -114,7 +114,7 @@ __global__ __launch_bounds__(256) void k_score_prep(const float* __restrict__ q,
     m.osc = (float)ldexp(s, -e);
     m.bound = bad ? __builtin_nanf("") : ru32(eps * l1 * (1.0 + 0x1p-50));
     m.bad = bad ? 1 : 0;
-    const double R = sqrt(2.0 * (double)__uint_as_float(*hn_max) * (1.0 + 0x1p-22)) * (1.0 + 0x1p-50) +
+    const double R = sqrt(2.0 * (double)__uint_as_float(hn_max) * (1.0 + 0x1p-22)) * (1.0 + 0x1p-50) +
                      eps * sqrt((double)D) * (1.0 + 0x1p-50);
     const double g = 2.0 * (double)(D + 64) * 0x1p-24;
     const double qn = sqrt(l2) * (1.0 + 0x1p-50);
@@ -953,17 +953,6 @@ __global__ void k_clear_u32(uint32_t* a, int64_t na, uint32_t* b, int64_t nb) {
   for (int64_t t = i; t < nb; t += st) b[t] = 0u;
 }
 
-// Largest value of hn[0, n) as float bits (non-negative floats order as
-// their bits); *out must hold 0 before.
-__global__ __launch_bounds__(256) void k_hn_max(const float* __restrict__ hn, int64_t n, uint32_t* __restrict__ out) {
-  uint32_t mx = 0u;
-  const int64_t st = (int64_t)gridDim.x * blockDim.x;
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += st)
-    mx = max(mx, __float_as_uint(hn[i]));
-  for (int o = 32; o > 0; o >>= 1) mx = max(mx, (uint32_t)__shfl_xor((int)mx, o));
-  if ((threadIdx.x & 63) == 0 && mx != 0u) atomicMax(out, mx);
-}
-
 // Lists and fallback give final scores (hi and lo); the filter pass works on
 // hi-only scores.
 template <int B, int KL>
@@ -1244,16 +1233,6 @@ __global__ __launch_bounds__(256) void k_certify(int64_t nq, int k, const float*
 }
 
 }  // namespace
-
-lam_status store_norm_max(lam_ctx* ctx, lam_store* st) {
-  hipLaunchKernelGGL(k_clear_u32, dim3(1), dim3(64), 0, ctx->stream, st->hn_max, (int64_t)1, nullptr, (int64_t)0);
-  const int64_t n = st->size;
-  if (n > 0)
-    hipLaunchKernelGGL(k_hn_max, dim3((unsigned)std::min<int64_t>(256, (n + 255) / 256)), dim3(256), 0, ctx->stream,
-                       st->hn, n, st->hn_max);
-  LAM_HIP(hipGetLastError());
-  return LAM_OK;
-}
 
 lam_status score_certify(lam_ctx* ctx, const lam_store* st, const float* q, int64_t nq, int32_t k, float* scores,
                          int64_t* ids, float* bound, uint8_t* certified, float* margin) {

@@ -7,7 +7,7 @@ import pytest
 import torch
 
 import synth
-from oracle import dedup, invariants
+from oracle import dedup, invariants, qeps, score
 
 pytestmark = pytest.mark.gpu
 
@@ -276,6 +276,65 @@ def test_async_invalid_input_reported_later(lam):
     assert info.n_seen == 600 and info.size == int(np.count_nonzero(ref["rep"] < 0))
     assert np.array_equal(torch.cat([r1, r3]).cpu().numpy(), ref["rep"])
     assert (rb.cpu().numpy() == -7).all()
+
+
+def _small_rows(rng, n, d):
+    """Unit rows whose coordinates all lie near 1/sqrt(d) in magnitude."""
+    v = np.sign(rng.standard_normal((n, d))) + 0.1 * rng.standard_normal((n, d))
+    return (v / np.linalg.norm(v, axis=1, keepdims=True)).astype(np.float32)
+
+
+def test_store_codec_width_follows_retained_rows(lam):
+    """The store codec's measured absmax is max |x| over the retained rows
+    only: a dropped near-duplicate with a larger coordinate, an invalid call
+    that did not wait and a cleared store's old rows must not count.  The
+    magnitudes make each of those mistakes change the code width."""
+    rng = np.random.default_rng(11)
+    d, tau, eps = 64, 0.95, 1e-3
+    u = _small_rows(rng, 1, d - 1)[0]
+    def planted(c0):
+        r = np.zeros(d, np.float64)
+        r[0] = c0
+        r[1:] = np.sqrt(1.0 - c0 * c0) * u
+        return r.astype(np.float32)
+    keep_big, drop_bigger = planted(0.5), planted(0.6)       # cos 0.993: the second is dropped
+    x = np.concatenate([_small_rows(rng, 300, d), keep_big[None], _small_rows(rng, 200, d),
+                        drop_bigger[None], _small_rows(rng, 100, d)])
+    bad = _small_rows(rng, 50, d)
+    bad[3] = planted(0.9)
+    bad[7, 5] = np.nan
+    s = lam.Store(d, tau, 2000)
+    s.ingest(_dev(x[:250]), sync=False)
+    s.ingest(_dev(bad), sync=False)
+    with pytest.raises(lam.LamError):
+        s.info()                                  # the invalid call is reported once
+    s.ingest(_dev(x[250:500]), sync=False)
+    s.ingest(_dev(x[500:]))                       # a call that waits
+    ref = dedup.greedy(x, tau)
+    kept = ref["kept"]
+    assert ref["rep"][501] == 300                 # the planted pair merged
+    p = s.quantize(eps)
+    a = np.abs(x[kept]).max()
+    assert p.absmax == a == np.float32(0.5)
+    assert p.bits == qeps.plan(eps, float(a))["bits"] == 9
+    assert np.array_equal(s.codes().cpu().numpy().view(np.uint32), qeps.pack(qeps.codes(x[kept], eps), p.bits))
+    q = _small_rows(rng, 8, d)
+    gs, gi, _ = s.score_topk(_dev(q), 5)
+    S = score.scores(q, qeps.codes(x[kept], eps).reshape(kept.size, -1), eps)
+    want_s, want_i = score.topk(S, kept, 5)
+    assert np.array_equal(gi.cpu().numpy(), want_i)
+    assert np.all(np.abs(gs.cpu().numpy() - want_s) <= 1e-5)
+
+    s.clear()
+    y = _small_rows(rng, 400, d)
+    s.ingest(_dev(y), sync=False)
+    refy = dedup.greedy(y, tau)
+    p = s.quantize(eps)
+    a = np.abs(y[refy["kept"]]).max()
+    assert p.absmax == a and a < 0.2
+    assert p.bits == qeps.plan(eps, float(a))["bits"] == 8
+    assert np.array_equal(s.codes().cpu().numpy().view(np.uint32),
+                          qeps.pack(qeps.codes(y[refy["kept"]], eps), p.bits))
 
 
 @pytest.mark.parametrize("tau", [0.95, 0.99])
