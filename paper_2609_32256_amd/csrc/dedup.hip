@@ -1307,22 +1307,26 @@ __global__ __launch_bounds__(256) void k_append(AppendArgs a, int nB) {
     const uint32_t hm = max(max(hpart[0], hpart[1]), max(hpart[2], hpart[3]));
     if (am > am0) atomicMax(&a.meta->absmax_bits, am);
     if (hm > hm0) atomicMax(&a.meta->hnmax_bits, hm);
+    // This workgroup is counted below only once its maximum has been
+    // performed: the wait covers the atomics issued above.  Device-scope
+    // atomics are performed where every XCD sees them, so the last workgroup,
+    // which reads the status words with device-scope atomic loads, needs no
+    // cache write-back or invalidation (fences here cost 1.7 us per call).
+    __builtin_amdgcn_s_waitcnt(0);
   }
   if (!a.last_chunk) return;
   // The last workgroup to finish folds the call into the store's bookkeeping
   // (arrival count and delta_hat if the call went through, an error count if
   // its input was invalid), copies the status words to host memory when asked,
-  // and clears them for the next call.  Every other workgroup's updates are
-  // ordered before its count by the fence.
+  // and clears them for the next call.  The only words of this launch it reads
+  // are the status words' maxima, updated by atomics that each workgroup has
+  // waited for before its count (above); everything else it reads was written
+  // by earlier launches.
   __shared__ bool last;
   __syncthreads();
-  if (threadIdx.x == 0) {
-    __threadfence();
-    last = atomicAdd(&a.cc->blocks_done, 1u) == gridDim.x - 1;
-  }
+  if (threadIdx.x == 0) last = atomicAdd(&a.cc->blocks_done, 1u) == gridDim.x - 1;
   __syncthreads();
   if (!last) return;
-  __threadfence();
   constexpr int kWords = (int)(sizeof(DevFlags) / 4);
   uint32_t* f = reinterpret_cast<uint32_t*>(a.flags);
   if (threadIdx.x == 0) {
