@@ -875,8 +875,11 @@ struct VerifyArgs {
 
 // One wave per listed pair, decided by the merge predicate (pair_within).
 __global__ __launch_bounds__(256) void k_verify(VerifyArgs a) {
-  if (skip_all(a.flags)) return;
-  const uint32_t n = min(a.cc->npairs, a.pair_cap);
+  // the pair count is loaded with the status words (both decide the exit), so
+  // the two do not take dependent round trips
+  const uint32_t np = a.cc->npairs;
+  if ((np == 0u) | skip_all(a.flags)) return;
+  const uint32_t n = min(np, a.pair_cap);
   const int lane = threadIdx.x & 63;
   const uint32_t wid = (blockIdx.x * blockDim.x + threadIdx.x) >> 6;
   const uint32_t nw = (gridDim.x * blockDim.x) >> 6;
