@@ -80,13 +80,37 @@ __global__ __launch_bounds__(256) void k_score_prep(const float* __restrict__ q,
   float mx = 0.0f;
   double l1 = 0.0, l2 = 0.0;
   bool bad = false;
-  for (int d = lane; d < D; d += 64) {
-    const float v = p[d];
+  // D <= 1,024: the row is loaded once as float4 pieces held in registers (all
+  // loads in flight together; the resource ends at the row, so pieces past it
+  // read as zero), and both passes below work from them
+  constexpr int kVec = 4;
+  const bool vec = D <= 256 * kVec;
+  float4 v4[kVec];
+  {
+    const __amdgpu_buffer_rsrc_t rs =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(p), (short)0, vec ? D * 4 : 0, 0x00020000);
+#pragma unroll
+    for (int u = 0; u < kVec; ++u)
+      v4[u] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(rs, (uint32_t)(u * 256 + lane * 4) * 4u, 0, 0));
+  }
+  auto take1 = [&](float v) {
     const float a = fabsf(v);
     bad |= !(a <= 3.402823466e38f);
     mx = fmaxf(mx, a);
     l1 += (double)a;
     l2 = fma((double)v, (double)v, l2);
+  };
+  if (vec) {
+#pragma unroll
+    for (int u = 0; u < kVec; ++u) {
+      if (u * 256 + lane * 4 >= D) break;
+      take1(v4[u].x);
+      take1(v4[u].y);
+      take1(v4[u].z);
+      take1(v4[u].w);
+    }
+  } else {
+    for (int d = lane; d < D; d += 64) take1(p[d]);
   }
   for (int o = 32; o > 0; o >>= 1) {
     mx = fmaxf(mx, __shfl_xor(mx, o));
@@ -99,14 +123,35 @@ __global__ __launch_bounds__(256) void k_score_prep(const float* __restrict__ q,
   const float sc = ldexpf(1.0f, e);
   const double isc = ldexp(1.0, -e);
   double dh2 = 0.0;   // ||q - h||^2
-  for (int d = lane; d < D; d += 64) {
-    const float v = bad ? 0.0f : p[d] * sc;     // exact power-of-two scaling
-    const _Float16 h = (_Float16)v;
-    const _Float16 l = (_Float16)(v - (float)h);
-    qhi[j * D + d] = h;
-    qlo[j * D + d] = l;
-    const double r = bad ? 0.0 : (double)p[d] - (double)(float)h * isc;   // exact in binary64
+  auto split = [&](float x, _Float16& h, _Float16& l) {
+    const float v = bad ? 0.0f : x * sc;     // exact power-of-two scaling
+    h = (_Float16)v;
+    l = (_Float16)(v - (float)h);
+    const double r = bad ? 0.0 : (double)x - (double)(float)h * isc;   // exact in binary64
     dh2 = fma(r, r, dh2);
+  };
+  if (vec) {
+#pragma unroll
+    for (int u = 0; u < kVec; ++u) {
+      const int d = u * 256 + lane * 4;
+      if (d >= D) break;
+      const float c[4] = {v4[u].x, v4[u].y, v4[u].z, v4[u].w};
+      _Float16 h[4], l[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) split(c[e], h[e], l[e]);
+      uint2 ph, pl;
+      __builtin_memcpy(&ph, h, 8);
+      __builtin_memcpy(&pl, l, 8);
+      *reinterpret_cast<uint2*>(qhi + j * D + d) = ph;
+      *reinterpret_cast<uint2*>(qlo + j * D + d) = pl;
+    }
+  } else {
+    for (int d = lane; d < D; d += 64) {
+      _Float16 h, l;
+      split(p[d], h, l);
+      qhi[j * D + d] = h;
+      qlo[j * D + d] = l;
+    }
   }
   for (int o = 32; o > 0; o >>= 1) dh2 += __shfl_xor(dh2, o);
   if (lane == 0) {
