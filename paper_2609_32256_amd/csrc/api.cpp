@@ -138,7 +138,8 @@ lam_status quantize_impl(lam_ctx* ctx, const float* x, int64_t n, double eps, fl
   // argument checks that do not depend on the data
   LAM_TRY(qeps_plan_host(eps, 0.0f, mode, n, &p));
   LAM_CHECK(std::isfinite(absmax), LAM_EINVAL, "absmax must be finite");
-  LAM_TRY(clear_flags(ctx));
+  if (!ctx->flags_zero) LAM_TRY(clear_flags(ctx));   // (already zero after an ingest or a clean quantize)
+  ctx->flags_zero = false;
   float a = absmax;
   if (!(absmax > 0.0f)) {
     LAM_TRY(launch_absmax(ctx, x, n, &ctx->flags_dev->absmax_bits, store_path ? "store_absmax" : "qeps_absmax"));
@@ -162,6 +163,11 @@ lam_status quantize_impl(lam_ctx* ctx, const float* x, int64_t n, double eps, fl
             ctx->flags_host->nonfinite);
   LAM_CHECK(ctx->flags_host->out_of_range == 0, LAM_ERANGE, "%u elements exceed the declared absmax %g",
             ctx->flags_host->out_of_range, (double)a);
+  // a declared absmax and valid input leave every status word at zero, which
+  // the next call need not clear again (the host copy is exact: the stream was
+  // synchronised after the encode)
+  static const DevFlags kZero{};
+  ctx->flags_zero = memcmp(ctx->flags_host, &kZero, sizeof(DevFlags)) == 0;
   if (out) *out = p;
   return LAM_OK;
 }
