@@ -210,11 +210,16 @@ def decide_one(x, i: int, kept_before, tau: float):
         return -1
     xi = x[i].astype(np.float64)
     rows = x[kb].astype(np.float64)
-    d2row = np.einsum("ij,ij->i", rows, rows) + xi @ xi - 2.0 * (rows @ xi)
+    rn = np.einsum("ij,ij->i", rows, rows)
+    d2row = rn + xi @ xi - 2.0 * (rows @ xi)
     d2f = float(delta2(tau))
-    for c in np.nonzero(d2row <= d2f + 1e-11 * max(1.0, 2 * float(xi @ xi)))[0].tolist():
-        if d2row[c] < d2f - 1e-11 * max(1.0, float(xi @ xi + rows[c] @ rows[c])) \
-                or within(x[i], x[kb[c]], tau):
+    # the binary64 distance is within 1e-11 (||x_i||^2 + ||y||^2) of the exact
+    # one (far more than its rounding error at any dim this library takes);
+    # the same margin decides which rows are candidates and which are
+    # definitely inside, the rest take the exact test
+    tol = 1e-11 * np.maximum(1.0, xi @ xi + rn)
+    for c in np.nonzero(d2row <= d2f + tol)[0].tolist():
+        if d2row[c] < d2f - tol[c] or within(x[i], x[kb[c]], tau):
             return int(kb[c])
     return -1
 
@@ -245,10 +250,9 @@ def decide_many(x, samples, kept, tau: float, block: int = 1 << 16):
         d2 = rn[:, None] + sn[None, cols] - 2.0 * (rows @ xs[cols].T)
         for c, sidx in enumerate(cols):
             i = int(samples[sidx])
-            tol = 1e-11 * max(1.0, 2.0 * float(sn[sidx]))
+            tol = 1e-11 * np.maximum(1.0, sn[sidx] + rn)   # as in decide_one, per row
             for r in np.nonzero((ids < i) & (d2[:, c] <= d2f + tol))[0].tolist():
-                if d2[r, c] < d2f - 1e-11 * max(1.0, float(sn[sidx] + rn[r])) \
-                        or within(x[i], x[ids[r]], tau):
+                if d2[r, c] < d2f - tol[r] or within(x[i], x[ids[r]], tau):
                     best[sidx] = int(ids[r])
                     break
     return best

@@ -116,8 +116,7 @@ def test_exact_path_is_exercised(seed):
 
 
 def test_planted_mistake_is_caught():
-    # A representative that is not the lowest index fails lowest_index; a rep
-    # outside delta fails cover.
+    # A representative that is not the lowest index fails lowest_index.
     x = _mixed(3, 128)
     r = dedup.greedy(x, 0.95)
     rep = r["rep"].copy()
@@ -125,6 +124,69 @@ def test_planted_mistake_is_caught():
     bad = rep.copy()
     bad[i] = int(np.nonzero(rep[:i] < 0)[0][-1]) if rep[i] != np.nonzero(rep[:i] < 0)[0][-1] else -1
     assert invariants.lowest_index(x, bad, 0.95, sample=[i]) == [i]
+
+
+def test_planted_cover_mistakes_are_caught():
+    """Proposition "greedy is a cover and a packing", cover part: a dropped
+    arrival whose representative lies outside delta, arrived later, or was
+    itself dropped is reported, and only that arrival."""
+    x = _mixed(4, 160)
+    tau = 0.95
+    rep = dedup.greedy(x, tau)["rep"]
+    assert invariants.cover(x, rep, tau) == []
+    dropped = np.nonzero(rep >= 0)[0]
+    kept = np.nonzero(rep < 0)[0]
+    i = int(dropped[-1])
+    far = [int(k) for k in kept if k < i and not dedup.within(x[i], x[k], tau)][0]
+    for wrong in (far,                                       # retained and earlier, but outside delta
+                  int(kept[kept > i][0]) if np.any(kept > i) else i,   # not earlier
+                  int(dropped[0])):                          # not retained
+        bad = rep.copy()
+        bad[i] = wrong
+        assert invariants.cover(x, bad, tau) == [i]
+
+
+def test_planted_packing_mistake_is_caught():
+    """Packing part: marking a dropped arrival as retained puts two retained
+    rows within delta of each other, and the pair is reported."""
+    x = _mixed(5, 160)
+    tau = 0.95
+    rep = dedup.greedy(x, tau)["rep"]
+    assert invariants.packing(x, rep, tau) == []
+    i = int(np.nonzero(rep >= 0)[0][0])
+    bad = rep.copy()
+    bad[i] = -1
+    found = invariants.packing(x, bad, tau)
+    assert (int(rep[i]), i) in found
+    assert all(i in pr for pr in found)
+
+
+def test_planted_score_deficit_mistake_is_caught():
+    """Theorem "Score deficit": on the tight example the deficit equals
+    delta_hat, so a claimed bound just below it is reported, and a retained
+    set that loses the best record for some query shows a deficit the bound
+    does not cover."""
+    a = np.array([1.0, 0.0], np.float32)
+    b = np.array([0.96, 0.28], np.float32)
+    x = np.stack([b, a])
+    rep = np.array([-1, 0])
+    dh = float(np.linalg.norm(a.astype(np.float64) - b))
+    q = ((a.astype(np.float64) - b) / dh)[None, :]
+    assert invariants.score_deficit(x, rep, q, dh, tol=1e-12) == []
+    assert invariants.score_deficit(x, rep, q, dh * (1 - 1e-9), tol=0.0) == [0]
+    # on the tiny workload, queries along retained rows pass with the run's
+    # delta_hat; dropping one of those rows (a representative far away) leaves
+    # its query a deficit near 1, far above the bound, and only that query fails
+    t = synth.tiny_ingest()
+    x = t["x"][:600]
+    r = dedup.greedy(x, t["tau"])
+    kept = np.nonzero(r["rep"] < 0)[0]
+    qq = x[kept[5:25]].astype(np.float64)
+    qq /= np.linalg.norm(qq, axis=1, keepdims=True)
+    assert invariants.score_deficit(x, r["rep"], qq, r["delta_hat"]) == []
+    bad = r["rep"].copy()
+    bad[kept[7]] = kept[0]
+    assert invariants.score_deficit(x, bad, qq, r["delta_hat"]) == [2]
 
 
 @pytest.fixture(scope="module")
@@ -230,6 +292,34 @@ def test_decide_many_matches_decide_one():
     got = dedup.decide_many(x, samples, kept, tau, block=17)
     one = [dedup.decide_one(x, int(i), kept[kept < i], tau) for i in samples]
     assert got.tolist() == one == ref["rep"].tolist()
+
+
+def test_decide_on_rows_that_are_not_unit():
+    """decide_one and decide_many on rows of norm 1/2 to 64 with pairs planted
+    exactly on the threshold and one float32 ulp either side (the library
+    takes such rows as given): both equal the pure-Python brute force on exact
+    integers, so their candidate margins scale with the rows' norms."""
+    rng = np.random.default_rng(12)
+    rows = []
+    for scale in (0.5, 4.0, 64.0):
+        a, b, b_in, b_out, tau = synth.dyadic_ties(rng, 12, 64)
+        # a * scale stays on a power-of-two grid; b keeps b - a = (e_i - e_j)/4
+        a_s = (a.astype(np.float64) * scale).astype(np.float32)
+        for bb in (b, b_in, b_out):
+            d = bb.astype(np.float64) - a.astype(np.float64)
+            rows.append((a_s.astype(np.float64) + d).astype(np.float32))
+        rows.append(a_s)
+        rows.append((synth.unit_rows(rng, 20, 64) * scale).astype(np.float32))
+    x = np.concatenate(rows)
+    x = x[rng.permutation(x.shape[0])]
+    ref = dedup.greedy_naive(x, tau)
+    assert np.count_nonzero(ref["rep"] >= 0) > 20          # the planted pairs merge
+    kept = np.nonzero(ref["rep"] < 0)[0]
+    samples = np.arange(x.shape[0])
+    one = [dedup.decide_one(x, int(i), kept[kept < i], tau) for i in samples]
+    assert one == ref["rep"].tolist()
+    assert dedup.decide_many(x, samples, kept, tau, block=13).tolist() == ref["rep"].tolist()
+    assert np.array_equal(dedup.greedy(x, tau, block=7)["rep"], ref["rep"])
 
 
 def test_removal_ceiling_closed_forms():
