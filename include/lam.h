@@ -219,7 +219,9 @@ typedef struct lam_ingest_stats {
  * next call on the store that waits: lam_store_get_info, lam_store_quantize,
  * lam_store_dequantize, lam_store_export, lam_score_topk or an ingest with
  * stats; later calls are decided as if it had not happened.
- * EINVAL: n < 0, NaN/Inf or |x| >= 256 in a coordinate (store unchanged).
+ * EINVAL: n < 0, NaN/Inf or |x| >= 255.9375 (= 2^8 - 2^-4, above which the
+ * screen's float16 operand 2^8 x would overflow) in a coordinate (store
+ * unchanged).
  * ECAPACITY: size + n > capacity (checked before any work; a call that does
  * not wait checks an upper bound of the size and waits if that bound is over). */
 lam_status lam_dedup_ingest(lam_ctx* ctx, lam_store* store, const float* x_dev, int64_t n,

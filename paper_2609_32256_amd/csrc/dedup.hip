@@ -20,11 +20,15 @@
 //                the pair list.
 //   verify    -- each ambiguous pair is re-decided in binary64 (one wave per
 //                pair); a pair within rounding distance of delta^2 is decided
-//                on exact integers on the host (a second, "careful", pass).
-//   resolve   -- one wave walks the chunk in arrival order: a row with a store
-//                hit is dropped; a row with no in-chunk edge is kept; any other
-//                row takes its lowest earlier in-chunk neighbour that was kept,
-//                using a 4096-bit kept mask held in the wave's registers.
+//                by the same wave on exact integers (exact.h: six 64-bit limbs
+//                hold the squared distance scaled to an integer).
+//   resolve   -- one workgroup of 1,024 threads: a row with a store hit is
+//                dropped, a row with no in-chunk edge is kept; the others copy
+//                their earlier in-chunk neighbours into LDS lists and decide in
+//                rounds (a row decides once every earlier neighbour has: it
+//                takes the lowest kept one, or is kept when none is).  When
+//                the lists overflow LDS, one wave walks the chunk in arrival
+//                order with the kept mask in its registers instead.
 //   append    -- kept rows join the store; for dropped rows ||x - rep||^2 in
 //                binary64 feeds the measured bound delta_hat.
 //
@@ -55,6 +59,10 @@ constexpr int kChunk = 4096;           // rows per resolve (64 lanes x 64 bits)
 constexpr int kNone = 0x7fffffff;       // "no store hit"
 constexpr int kGroupA = 8;              // store tiles per group in the screen's tile order
 constexpr float kScale = 256.0f;        // fp16 operands hold x * 2^8
+// Largest accepted |x| (exclusive): 2^8 x rounds to a finite float16 exactly
+// when 2^8 |x| < 65520 (the midpoint between the largest finite value 65504
+// and 2^16), i.e. |x| < 2^8 - 2^-4.
+constexpr float kXLimit = 255.9375f;
 constexpr float kInvScale2 = 1.0f / 65536.0f;
 
 enum Scratch { S_X16 = 0, S_ROWF, S_CHUNK, S_BITMAP, S_PAIRS, S_STATUS, S_G };
@@ -67,7 +75,7 @@ struct StoreMeta {
   uint32_t err_calls;              // calls since the host last looked that had invalid input
   int64_t n_seen;                  // arrivals taken so far (global id of the next arrival)
   unsigned long long dhat2_bits;   // max merged squared distance of the run (binary64 bits)
-  uint32_t err_bits;               // bit 0: non-finite input, bit 1: a coordinate with |x| >= 256
+  uint32_t err_bits;               // bit 0: non-finite input, bit 1: a coordinate with |x| >= kXLimit
   uint32_t absmax_bits;            // max |x| over the retained rows (float32 bits; non-negative
                                    // floats order as their bits), the store codec's width input
   uint32_t hnmax_bits;             // max ||x||^2 / 2 over the retained rows (float32 bits)
@@ -172,7 +180,7 @@ __global__ __launch_bounds__(256) void k_prep(const float* __restrict__ x, int64
     for (int r = 0; r < 4; ++r) {
       const float a = fabsf(c[r]);
       nf |= !(a <= 3.402823466e38f);
-      rng |= !(a < 256.0f);
+      rng |= !(a < kXLimit);
       na = fma((double)c[r], (double)c[r], na);
       l1 += (double)a;
       h[r] = (_Float16)(c[r] * kScale);
@@ -1493,7 +1501,7 @@ lam_status store_settle(lam_store* st) {
     set_error("%u earlier ingest call(s) that did not wait for the device had %s; they left the store "
               "unchanged and wrote no outputs", calls,
               (bits & 4u) ? "too many ambiguous pairs (internal)"
-                          : (bits & 1u) ? "NaN or Inf in the input" : "coordinates with |x| >= 256");
+                          : (bits & 1u) ? "NaN or Inf in the input" : "coordinates with |x| >= 255.9375");
     return LAM_EINVAL;
   }
   return LAM_OK;
@@ -1767,7 +1775,7 @@ lam_status dedup_ingest(lam_ctx* ctx, lam_store* st, const float* x, int64_t n, 
     LAM_HIP(hipStreamSynchronize(ctx->stream));
     const DevFlags f = *ctx->flags_host;
     LAM_CHECK(f.nonfinite == 0, LAM_EINVAL, "input holds NaN or Inf (%u rows)", f.nonfinite);
-    LAM_CHECK(f.out_of_range == 0, LAM_EINVAL, "input has coordinates with |x| >= 256 (%u rows)", f.out_of_range);
+    LAM_CHECK(f.out_of_range == 0, LAM_EINVAL, "input has coordinates with |x| >= 255.9375 (%u rows)", f.out_of_range);
     if (f.pair_overflow & 1u) {
       ctx->pair_cap = std::max<uint32_t>(ctx->pair_cap * 2u, f.pairs_needed + (f.pairs_needed >> 2));
       continue;

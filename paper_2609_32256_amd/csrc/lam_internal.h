@@ -66,7 +66,7 @@ struct DevBuf {
 // synchronous call.  Pinned host mirror for the readback.
 struct DevFlags {
   uint32_t nonfinite;      // NaN/Inf seen in an input
-  uint32_t out_of_range;   // |x| > declared absmax, or |x| >= 256 for the screen
+  uint32_t out_of_range;   // |x| > declared absmax, or |x| >= 255.9375 for the screen
   uint32_t absmax_bits;    // max |x| as float bits (measured absmax)
   uint32_t pair_overflow;  // bit 0: ambiguous-pair list overflowed
   uint32_t n_pairs;        // ambiguous pairs found

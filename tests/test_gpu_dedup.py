@@ -186,11 +186,12 @@ def test_errors_leave_store_unchanged(lam):
     with pytest.raises(lam.LamError) as e:
         s.ingest(_dev(bad))
     assert e.value.name == "LAM_EINVAL" and s.size == size and s.info().n_seen == 100
-    big = x[100:200].copy()
-    big[7, 0] = 300.0
-    with pytest.raises(lam.LamError) as e:
-        s.ingest(_dev(big))
-    assert e.value.name == "LAM_EINVAL" and s.size == size
+    for v in (300.0, 255.9375, -255.95):   # 2^8 x would overflow the screen's float16 operand
+        big = x[100:200].copy()
+        big[7, 0] = v
+        with pytest.raises(lam.LamError) as e:
+            s.ingest(_dev(big))
+        assert e.value.name == "LAM_EINVAL" and s.size == size
     with pytest.raises(lam.LamError) as e:
         s.ingest(_dev(synth.unit_rows(rng, 301, 64).astype(np.float32)))
     assert e.value.name == "LAM_ECAPACITY" and s.size == size
@@ -359,3 +360,25 @@ def test_removal_ceiling_errors(lam):
         assert e.value.name == "LAM_EINVAL"
     r = lam.removal_ceiling(x, 0.6, batch=3)
     assert (r["kept"], r["kept_2delta"]) == (10, 1)
+
+
+def test_largest_accepted_coordinates(lam):
+    """Coordinates just below the accepted limit (|x| < 255.9375, where 2^8 x
+    is still a finite float16) are screened with a finite operand: a near
+    copy of such a row merges, a sign-flipped one and the unit rows do not,
+    exactly as the oracle decides."""
+    rng = np.random.default_rng(8)
+    u = synth.unit_rows(rng, 40, 64).astype(np.float32)
+    big = u[:4].copy()
+    big[:, 0] = np.float32(255.93)
+    near = big.copy()
+    near[:, 1] += np.float32(0.05)
+    flip = big.copy()
+    flip[:, 0] = -flip[:, 0]
+    x = np.concatenate([u[4:20], big, near, flip, u[20:]])
+    ref = dedup.greedy(x, 0.95)
+    s = lam.Store(64, 0.95, x.shape[0])
+    rep, st = s.ingest(_dev(x))
+    assert np.array_equal(rep.cpu().numpy(), ref["rep"])
+    assert np.all(ref["rep"][20:24] == np.arange(16, 20))   # the near copies merge into the big rows
+    assert abs(st["delta_hat_run"] - ref["delta_hat"]) <= 1e-12
