@@ -1531,7 +1531,6 @@ lam_status dedup_ingest(lam_ctx* ctx, lam_store* st, const float* x, int64_t n, 
     }
     return LAM_OK;
   }
-  st->maxima_known = false;   // appended rows may raise them
   const int CH = (int)std::min<int64_t>(n, kChunk);
   const int W = (CH + 63) / 64;
   const bool lsh = st->lsh_r > 0;
@@ -1553,6 +1552,9 @@ lam_status dedup_ingest(lam_ctx* ctx, lam_store* st, const float* x, int64_t n, 
     // grow geometrically: every growth reallocates, which waits for the device
     ctx->pair_cap = (uint32_t)std::min<uint64_t>(kAsyncPairLimit, std::max<uint64_t>(worst, 2ull * ctx->pair_cap));
   }
+  // the rows this call appends may raise the store's maxima (after the
+  // settling above, which reads the maxima of the earlier calls)
+  st->maxima_known = false;
   const int64_t m_before = async ? m_ub : st->size;   // exact when waiting, an upper bound otherwise
   const Consts K = screen_consts(D);
   StoreMeta* meta = reinterpret_cast<StoreMeta*>(st->stat_dev);

@@ -382,3 +382,23 @@ def test_largest_accepted_coordinates(lam):
     assert np.array_equal(rep.cpu().numpy(), ref["rep"])
     assert np.all(ref["rep"][20:24] == np.arange(16, 20))   # the near copies merge into the big rows
     assert abs(st["delta_hat_run"] - ref["delta_hat"]) <= 1e-12
+
+
+def test_store_maxima_after_calls_that_wait_and_calls_that_do_not(lam):
+    """The store's max |x| and max ||x||^2 / 2, kept by the appends, cover
+    every retained row when calls that do not wait are followed by one that
+    waits (it settles the earlier calls first, then appends its own rows): the
+    store's codec then takes the exact maximum as its absmax."""
+    rng = np.random.default_rng(21)
+    x = synth.unit_rows(rng, 3000, 128).astype(np.float32)
+    x[2900, 5] = np.float32(0.9)      # the largest coordinate arrives in the last call
+    s = lam.Store(128, 0.95, x.shape[0])
+    xd = _dev(x)
+    s.ingest(xd[:1000], sync=False)
+    s.ingest(xd[1000:2000], sync=False)
+    rep, _ = s.ingest(xd[2000:])      # waits
+    p = s.quantize(1e-3)              # absmax measured: the appends' maximum
+    ref = dedup.greedy(x, 0.95)
+    kept = ref["kept"]
+    assert p.absmax == float(np.abs(x[kept]).max()) == np.float32(0.9)
+    assert np.array_equal(rep.cpu().numpy(), ref["rep"][2000:])
