@@ -258,6 +258,21 @@ lam_status lam_store_export(lam_ctx* ctx, const lam_store* store, int64_t* ids_d
 lam_status lam_score_topk(lam_ctx* ctx, const lam_store* store, const float* q_dev, int64_t nq,
                           int32_t k, float* scores_dev, int64_t* ids_dev, float* bound_dev);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation):
+ * lam_score_topk with every scratch buffer taken from a fixed 32 MiB array
+ * that each device holds from the library's load until the process ends (set
+ * up by lam_ctx_create); the call itself allocates nothing.  Results equal
+ * lam_score_topk's.  Limits: nq <= 256 (EINVAL beyond).  The store must be
+ * quantized and settled: ESTATE while ingest calls that did not wait are in
+ * flight (lam_store_get_info settles them) -- settling can need the host.
+ * Every call on one device shares that device's array: calls that overlap on
+ * one device (through any contexts or streams) race and give undefined
+ * results; calls in one stream's order are safe.  No profiling events are
+ * recorded.  Asynchronous. */
+lam_status lam_score_topk_noalloc(lam_ctx* ctx, const lam_store* store, const float* q_dev, int64_t nq,
+                                  int32_t k, float* scores_dev, int64_t* ids_dev, float* bound_dev);
+
 /* Top-k with the rank-invariance certificate (Appendix "Rank invariance, in
  * full"): as lam_score_topk (1 <= k <= 63), plus per query certified_dev[j] = 1
  * when the float32 margin m_j = s_k - s_{k+1} between ranks k and k+1 exceeds

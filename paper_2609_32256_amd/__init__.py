@@ -127,6 +127,7 @@ _SIGS = {
     "lam_removal_ceiling": ([_P, _P, _I64, ctypes.c_int32, ctypes.c_double, _I64, ctypes.POINTER(CeilingStats)],
                             ctypes.c_int),
     "lam_score_topk": ([_P, _P, _P, _I64, ctypes.c_int32, _P, _P, _P], ctypes.c_int),
+    "lam_score_topk_noalloc": ([_P, _P, _P, _I64, ctypes.c_int32, _P, _P, _P], ctypes.c_int),
 }
 for _name, (_args, _res) in _SIGS.items():
     _fn = getattr(_lib, _name)
@@ -201,6 +202,19 @@ class Context:
         ms, n = ctypes.c_double(), _I64()
         _check(_lib.lam_ctx_profile_read(self._h, kernel.encode(), ctypes.byref(ms), ctypes.byref(n)))
         return ms.value, n.value
+
+    def score_topk_noalloc(self, q: torch.Tensor, k: int, out):
+        """score_topk through the allocation-free entry point (lam_score_topk_noalloc):
+        the library takes its scratch from a fixed per-device array; the caller
+        passes every output, out = (scores float32[nq, k], ids int64[nq, k],
+        bound float32[nq]).  nq <= 256; the store must be settled (info())."""
+        q = _dev_tensor(q, torch.float32, "q")
+        if q.dim() != 2 or q.shape[1] != self.dim:
+            raise ValueError(f"q must be (nq, {self.dim})")
+        s, i, b = out
+        _check(_lib.lam_score_topk_noalloc(self.ctx.handle, self._h, _ptr(q), q.shape[0], int(k), _ptr(s), _ptr(i),
+                                           _ptr(b)))
+        return s, i, b
 
     def close(self):
         if getattr(self, "_h", None):
@@ -416,6 +430,19 @@ class Store:
                    torch.empty(nq, dtype=torch.float32, device=q.device))
         s, i, b = out
         _check(_lib.lam_score_topk(self.ctx.handle, self._h, _ptr(q), nq, int(k), _ptr(s), _ptr(i), _ptr(b)))
+        return s, i, b
+
+    def score_topk_noalloc(self, q: torch.Tensor, k: int, out):
+        """score_topk through the allocation-free entry point (lam_score_topk_noalloc):
+        the library takes its scratch from a fixed per-device array; the caller
+        passes every output, out = (scores float32[nq, k], ids int64[nq, k],
+        bound float32[nq]).  nq <= 256; the store must be settled (info())."""
+        q = _dev_tensor(q, torch.float32, "q")
+        if q.dim() != 2 or q.shape[1] != self.dim:
+            raise ValueError(f"q must be (nq, {self.dim})")
+        s, i, b = out
+        _check(_lib.lam_score_topk_noalloc(self.ctx.handle, self._h, _ptr(q), q.shape[0], int(k), _ptr(s), _ptr(i),
+                                           _ptr(b)))
         return s, i, b
 
     def close(self):

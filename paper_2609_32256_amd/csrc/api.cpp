@@ -217,6 +217,12 @@ lam_status lam_ctx_create(int device, void* hip_stream, lam_ctx** out) {
     return LAM_ENOMEM;
   }
   memset(c->flags_host, 0, sizeof(DevFlags));
+  // the allocation-free scoring call's workspace on this device (once per device)
+  const lam_status ns = noalloc_setup(device);
+  if (ns != LAM_OK) {
+    lam_ctx_destroy(c);
+    return ns;
+  }
   *out = c;
   return LAM_OK;
 }
@@ -496,6 +502,22 @@ lam_status lam_score_topk(lam_ctx* ctx, const lam_store* st, const float* q_dev,
             "store must be quantized (lam_store_quantize) after its last ingest");
   DeviceGuard g(ctx->device);
   return score_topk(ctx, st, q_dev, nq, k, scores_dev, ids_dev, bound_dev);
+}
+
+lam_status lam_score_topk_noalloc(lam_ctx* ctx, const lam_store* st, const float* q_dev, int64_t nq, int32_t k,
+                                  float* scores_dev, int64_t* ids_dev, float* bound_dev) {
+  LAM_CHECK(ctx != nullptr && st != nullptr, LAM_EINVAL, "ctx or store is NULL");
+  LAM_CHECK(nq >= 0, LAM_EINVAL, "nq must be >= 0");
+  LAM_CHECK(k >= 1 && k <= 64, LAM_EINVAL, "k must be in [1, 64]");
+  LAM_CHECK((q_dev != nullptr && scores_dev != nullptr && ids_dev != nullptr) || nq == 0, LAM_EINVAL,
+            "NULL buffer");
+  LAM_CHECK(((uintptr_t)q_dev & 15u) == 0, LAM_EINVAL, "q must be 16-byte aligned");
+  LAM_CHECK(!st->pending, LAM_ESTATE,
+            "ingest calls that did not wait are still in flight: settle the store first (lam_store_get_info)");
+  LAM_CHECK(st->codes != nullptr && st->coded_rows == st->size, LAM_ESTATE,
+            "store must be quantized (lam_store_quantize) after its last ingest");
+  DeviceGuard g(ctx->device);
+  return score_topk_noalloc(ctx, st, q_dev, nq, k, scores_dev, ids_dev, bound_dev);
 }
 
 lam_status lam_store_block_encode(lam_ctx* ctx, lam_store* st, lam_block_stats* out) {

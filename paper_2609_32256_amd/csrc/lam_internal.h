@@ -164,7 +164,9 @@ struct ProfScope {
   lam_ctx* ctx;
   size_t slot = (size_t)-1;
   lam_status st = LAM_OK;
-  ProfScope(lam_ctx* c, const char* name) : ctx(c) { st = prof_begin(ctx, name, &slot); }
+  ProfScope(lam_ctx* c, const char* name, bool on = true) : ctx(c) {
+    if (on) st = prof_begin(ctx, name, &slot);
+  }
   ~ProfScope() { if (slot != (size_t)-1) prof_end(ctx, slot); }
 };
 
@@ -193,6 +195,12 @@ void store_free(lam_store* st);
 // codes: the b-bit code stream to score (NULL: the store's own)
 lam_status score_topk(lam_ctx* ctx, const lam_store* st, const float* q, int64_t nq, int32_t k,
                       float* scores, int64_t* ids, float* bound, const uint32_t* codes = nullptr);
+// score_topk with every scratch buffer carved from the file-scope device
+// array of score.hip (no allocation); noalloc_setup must have run on the
+// device (lam_ctx_create does).
+lam_status score_topk_noalloc(lam_ctx* ctx, const lam_store* st, const float* q, int64_t nq, int32_t k,
+                              float* scores, int64_t* ids, float* bound);
+lam_status noalloc_setup(int device);
 lam_status score_certify(lam_ctx* ctx, const lam_store* st, const float* q, int64_t nq, int32_t k, float* scores,
                          int64_t* ids, float* bound, uint8_t* certified, float* margin);
 lam_status block_encode(lam_ctx* ctx, lam_store* st, lam_block_stats* out);

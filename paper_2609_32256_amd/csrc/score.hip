@@ -27,6 +27,7 @@
 // similarity screen's pipeline (two LDS stages, loads three slabs ahead).
 #include <cmath>
 #include <cstring>
+#include <mutex>
 
 #include "lam_internal.h"
 #include "mfma_tile.h"
@@ -611,6 +612,7 @@ __global__ __launch_bounds__(256) void k_cand_select(int64_t nq, uint32_t cap, i
 
 // ------------------------------------------------------------------ radix selection (k > 16)
 constexpr int kCandCap = 4096;   // candidate buffer entries per query
+constexpr int kNoAllocMaxQ = 256;   // queries of one allocation-free scoring call
 
 // The kth largest (1-based) of keys[0, n) in LDS, found one 8-bit digit at a
 // time from the top: a histogram of the digit among keys that match the
@@ -1045,13 +1047,13 @@ lam_status launch_rescore(int b, dim3 grid, hipStream_t st, int64_t nq, uint32_t
 
 // Split a tile range over query tiles so that the grid holds about 1024
 // workgroups; returns (splits, tiles per split).
-void plan_splits(int nqt, int64_t ntiles, int* splits, int64_t* tps) {
+void plan_splits(int nqt, int64_t ntiles, int* splits, int64_t* tps, int max_splits) {
   if (ntiles <= 0) {
     *splits = 1;
     *tps = 0;
     return;
   }
-  const int64_t want = std::max<int64_t>(1, (1024 + nqt - 1) / nqt);
+  const int64_t want = std::min<int64_t>(max_splits, std::max<int64_t>(1, (1024 + nqt - 1) / nqt));
   int64_t s = std::min<int64_t>(want, ntiles);
   const int64_t t = (ntiles + s - 1) / s;
   *tps = t;
@@ -1079,8 +1081,37 @@ void plan_splits(int nqt, int64_t ntiles, int* splits, int64_t* tps) {
 //      rescore (many equal scores, say), is redone with exact per-lane lists
 //      over the whole store; launched always, it returns at once when nothing
 //      was flagged, so the call stays asynchronous.
-lam_status score_topk(lam_ctx* ctx, const lam_store* st, const float* q, int64_t nq, int32_t k, float* scores,
-                      int64_t* ids, float* bound, const uint32_t* codes) {
+namespace {
+
+// Scratch of one scoring call: the context's arena (grown on demand), or a
+// fixed region carved in order (the allocation-free entry point).
+struct ScoreWork {
+  char* base = nullptr;   // fixed region; nullptr: the context arena
+  size_t bytes = 0;
+  size_t used = 0;
+  template <class T>
+  lam_status take(lam_ctx* ctx, int slot, size_t need, T** out) {
+    if (!base) {
+      LAM_TRY(ctx->scratch[slot].ensure(need));
+      *out = ctx->scratch[slot].as<T>();
+      return LAM_OK;
+    }
+    const size_t at = (used + 255) & ~(size_t)255;
+    LAM_CHECK(at + need <= bytes, LAM_ECAPACITY,
+              "scoring needs more than the %zu bytes of the fixed workspace", bytes);
+    *out = reinterpret_cast<T*>(base + at);
+    used = at + need;
+    return LAM_OK;
+  }
+};
+
+// score_topk on the workspace w.  Every buffer is taken before the first
+// launch, so a workspace that is too small fails with nothing enqueued.
+// max_splits caps the store ranges per query tile of the list passes (their
+// candidate lists grow with it); no profiling events are recorded unless prof.
+lam_status score_topk_impl(lam_ctx* ctx, const lam_store* st, const float* q, int64_t nq, int32_t k, float* scores,
+                           int64_t* ids, float* bound, const uint32_t* codes, ScoreWork& w, int max_splits,
+                           bool prof) {
   if (nq == 0) return LAM_OK;
   const int D = st->dim;
   const int b = st->q.bits;
@@ -1088,17 +1119,6 @@ lam_status score_topk(lam_ctx* ctx, const lam_store* st, const float* q, int64_t
             "scoring supports codes of at most 12 bits (store codes have %d); quantize with a larger eps", b);
   const int KL = (k <= 16) ? 16 : 64;
   const int64_t n = st->size;
-  LAM_TRY(ctx->scratch[S_QHI].ensure((size_t)nq * D * 2));
-  LAM_TRY(ctx->scratch[S_QLO].ensure((size_t)nq * D * 2));
-  LAM_TRY(ctx->scratch[S_QMETA].ensure((size_t)nq * sizeof(QMeta)));
-  QMeta* qmeta = ctx->scratch[S_QMETA].as<QMeta>();
-  {
-    ProfScope ps(ctx, "score_prep");
-    hipLaunchKernelGGL(k_score_prep, dim3((unsigned)((nq + 3) / 4)), dim3(256), 0, ctx->stream, q, nq, D, st->q.step,
-                       st->q.eps, st->hn_max, ctx->scratch[S_QHI].as<_Float16>(), ctx->scratch[S_QLO].as<_Float16>(),
-                       qmeta);
-    LAM_HIP(hipGetLastError());
-  }
   const int nqt = (int)((nq + kTB - 1) / kTB);
   const int64_t ntiles = (n + kTB - 1) / kTB;
   const int64_t sample_rows = std::max<int64_t>(4096, ((int64_t)k * n + 1023) / 1024);
@@ -1107,8 +1127,8 @@ lam_status score_topk(lam_ctx* ctx, const lam_store* st, const float* q, int64_t
 
   int sp1 = 1, sp2 = 1;
   int64_t tps1 = 0, tps2 = 0;
-  plan_splits(nqt, stiles, &sp1, &tps1);
-  plan_splits(nqt, ntiles, &sp2, &tps2);
+  plan_splits(nqt, stiles, &sp1, &tps1, max_splits);
+  plan_splits(nqt, ntiles, &sp2, &tps2, max_splits);
   constexpr int kSampleKL = 4;
   if (two_pass && (int64_t)sp1 * 2 * kSampleKL < 2 * (int64_t)k) {
     const int64_t want = std::min<int64_t>(stiles, (k + kSampleKL - 1) / kSampleKL);
@@ -1116,17 +1136,34 @@ lam_status score_topk(lam_ctx* ctx, const lam_store* st, const float* q, int64_t
     sp1 = (int)((stiles + tps1 - 1) / tps1);
   }
   const int cands_max = std::max(sp1, sp2) * 2 * KL;
-  LAM_TRY(ctx->scratch[S_PART].ensure((size_t)nq * cands_max * 8));
-  float* part_s = ctx->scratch[S_PART].as<float>();
+  const uint32_t cap = kCandCap;
+
+  // every buffer first
+  _Float16 *qhi = nullptr, *qlo = nullptr;
+  QMeta* qmeta = nullptr;
+  float* part_s = nullptr;
+  float* cand_s = nullptr;
+  LAM_TRY(w.take(ctx, S_QHI, (size_t)nq * D * 2, &qhi));
+  LAM_TRY(w.take(ctx, S_QLO, (size_t)nq * D * 2, &qlo));
+  LAM_TRY(w.take(ctx, S_QMETA, (size_t)nq * sizeof(QMeta), &qmeta));
+  LAM_TRY(w.take(ctx, S_PART, (size_t)nq * cands_max * 8, &part_s));
+  if (two_pass) LAM_TRY(w.take(ctx, S_CAND, (size_t)nq * cap * 8 + (size_t)nq * 12 + (size_t)nqt * 4 + 256, &cand_s));
   int32_t* part_r = reinterpret_cast<int32_t*>(part_s + (size_t)nq * cands_max);
+
+  {
+    ProfScope ps(ctx, "score_prep", prof);
+    hipLaunchKernelGGL(k_score_prep, dim3((unsigned)((nq + 3) / 4)), dim3(256), 0, ctx->stream, q, nq, D, st->q.step,
+                       st->q.eps, st->hn_max, qhi, qlo, qmeta);
+    LAM_HIP(hipGetLastError());
+  }
 
   ScoreArgs a{};
   a.codes = codes ? codes : st->codes;
   a.n = n;
   a.D = D;
   a.row_words = (int64_t)D * b / 32;
-  a.qhi = ctx->scratch[S_QHI].as<_Float16>();
-  a.qlo = ctx->scratch[S_QLO].as<_Float16>();
+  a.qhi = qhi;
+  a.qlo = qlo;
   a.meta = qmeta;
   a.nq = nq;
   a.nqt = nqt;
@@ -1140,11 +1177,11 @@ lam_status score_topk(lam_ctx* ctx, const lam_store* st, const float* q, int64_t
       a.tile_end = ntiles;
       a.splits = sp2;
       a.tiles_per_split = tps2;
-      ProfScope ps(ctx, "score_mfma");
+      ProfScope ps(ctx, "score_mfma", prof);
       LAM_TRY(dispatch_bits<1>(b, KL, kModeLists, dim3((unsigned)(nqt * sp2)), ctx->stream, a));
       LAM_HIP(hipGetLastError());
     }
-    ProfScope ps(ctx, "score_merge");
+    ProfScope ps(ctx, "score_merge", prof);
     const int nc = ntiles > 0 ? sp2 * 2 * KL : 0;
     if (KL == 16)
       hipLaunchKernelGGL((k_topk_merge<16>), gq, dim3(256), 0, ctx->stream, nq, nc, k, part_s, part_r, qmeta, st->ids,
@@ -1156,18 +1193,17 @@ lam_status score_topk(lam_ctx* ctx, const lam_store* st, const float* q, int64_t
     return LAM_OK;
   }
 
-  const uint32_t cap = kCandCap;
-  LAM_TRY(ctx->scratch[S_CAND].ensure((size_t)nq * cap * 8 + (size_t)nq * 12 + (size_t)nqt * 4 + 256));
-  float* cand_s = ctx->scratch[S_CAND].as<float>();
   int32_t* cand_r = reinterpret_cast<int32_t*>(cand_s + (size_t)nq * cap);
   uint32_t* cand_cnt = reinterpret_cast<uint32_t*>(cand_r + (size_t)nq * cap);
   float* thr = reinterpret_cast<float*>(cand_cnt + nq);
   uint32_t* qflag = reinterpret_cast<uint32_t*>(thr + nq);
   uint32_t* tflag = qflag + nq;
+  // the candidate counts and tile flags start at zero (cleared by a kernel:
+  // the buffer may hold anything from an earlier call)
   hipLaunchKernelGGL(k_clear_u32, dim3(64), dim3(256), 0, ctx->stream, cand_cnt, nq, tflag, (int64_t)nqt);
   LAM_HIP(hipGetLastError());
   {  // 1. a k-th best score of the sample -> thresholds
-    ProfScope ps(ctx, "score_sample");
+    ProfScope ps(ctx, "score_sample", prof);
     a.tile_begin = 0;
     a.tile_end = stiles;
     a.splits = sp1;
@@ -1189,7 +1225,7 @@ lam_status score_topk(lam_ctx* ctx, const lam_store* st, const float* q, int64_t
   a.cap = cap;
   a.tflag = tflag;
   {  // 2. full scan with the thresholds
-    ProfScope ps(ctx, "score_mfma");
+    ProfScope ps(ctx, "score_mfma", prof);
     if (D == 768 || D == 1024) {
       // one 128 x 128 tile per workgroup on the screen's pipeline
       const int64_t grid = (int64_t)nqt * ntiles;
@@ -1201,7 +1237,7 @@ lam_status score_topk(lam_ctx* ctx, const lam_store* st, const float* q, int64_t
     }
   }
   {  // 3. select; 4. exact fallback for overflowed buffers (returns at once otherwise)
-    ProfScope ps(ctx, "score_merge");
+    ProfScope ps(ctx, "score_merge", prof);
     if (KL == 16)
       hipLaunchKernelGGL((k_cand_select<16>), gq, dim3(256), 0, ctx->stream, nq, cap, k, cand_cnt, cand_s, cand_r,
                          qmeta, st->ids, scores, ids, bound, qflag, tflag);
@@ -1213,7 +1249,7 @@ lam_status score_topk(lam_ctx* ctx, const lam_store* st, const float* q, int64_t
                               st->ids, q, st->q.step, a.codes, a.row_words, D, scores, ids, qflag, tflag));
   }
   {
-    ProfScope ps(ctx, "score_fallback");
+    ProfScope ps(ctx, "score_fallback", prof);
     LAM_TRY(dispatch_bits<1>(b, KL, kModeFallback, dim3((unsigned)(nqt * sp2)), ctx->stream, a));
     const int nc = sp2 * 2 * KL;
     if (KL == 16)
@@ -1225,6 +1261,62 @@ lam_status score_topk(lam_ctx* ctx, const lam_store* st, const float* q, int64_t
     LAM_HIP(hipGetLastError());
   }
   return LAM_OK;
+}
+
+// ------------------------------------------------------------------ allocation-free scoring
+// Its scratch memory: one array per device, allocated with the code object,
+// held until the process ends.  Sized for kNoAllocMaxQ queries of up to 4,096
+// dimensions with at most kNoAllocSplits store ranges per query tile:
+// fp16 hi and lo query parts (4 D bytes per query), the query meta block, the
+// list passes' candidates (2 x 64 entries of 8 bytes per range) and the
+// threshold plan's candidate buffer (kCandCap entries of 8 bytes, 12 bytes
+// of counts and flags) -- 112 KB per query, 28 MB at the limits.
+constexpr int kNoAllocSplits = 64;
+constexpr size_t kNoAllocBytes = (size_t)32 << 20;
+static_assert((size_t)kNoAllocMaxQ * (4 * 4096 + 16 + (size_t)kNoAllocSplits * 2 * 64 * 8 + (size_t)kCandCap * 8 + 12) +
+                      6 * 256 + 256 <= kNoAllocBytes,
+              "the workspace holds a call at the limits");
+
+}  // namespace
+
+static __device__ __align__(256) unsigned char scratch[kNoAllocBytes];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_noalloc_mu;
+void* g_noalloc_ptr[kMaxDevices];   // device address of `scratch` on each device (host code must not use its name)
+}  // namespace
+
+lam_status noalloc_setup(int device) {
+  LAM_CHECK(device >= 0 && device < kMaxDevices, LAM_EINVAL, "device %d beyond the supported %d", device, kMaxDevices);
+  std::lock_guard<std::mutex> lk(g_noalloc_mu);
+  if (g_noalloc_ptr[device]) return LAM_OK;
+  void* p = nullptr;
+  LAM_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));   // the current device is `device`
+  g_noalloc_ptr[device] = p;
+  return LAM_OK;
+}
+
+lam_status score_topk(lam_ctx* ctx, const lam_store* st, const float* q, int64_t nq, int32_t k, float* scores,
+                      int64_t* ids, float* bound, const uint32_t* codes) {
+  ScoreWork w;
+  return score_topk_impl(ctx, st, q, nq, k, scores, ids, bound, codes, w, 1 << 30, true);
+}
+
+lam_status score_topk_noalloc(lam_ctx* ctx, const lam_store* st, const float* q, int64_t nq, int32_t k, float* scores,
+                              int64_t* ids, float* bound) {
+  LAM_CHECK(nq <= kNoAllocMaxQ, LAM_EINVAL, "the allocation-free call takes at most %d queries (asked %lld)",
+            kNoAllocMaxQ, (long long)nq);
+  void* p = nullptr;
+  {
+    std::lock_guard<std::mutex> lk(g_noalloc_mu);
+    p = ctx->device < kMaxDevices ? g_noalloc_ptr[ctx->device] : nullptr;
+  }
+  LAM_CHECK(p != nullptr, LAM_ESTATE, "the fixed workspace of device %d was not set up", ctx->device);
+  ScoreWork w;
+  w.base = static_cast<char*>(p);
+  w.bytes = kNoAllocBytes;
+  return score_topk_impl(ctx, st, q, nq, k, scores, ids, bound, nullptr, w, kNoAllocSplits, false);
 }
 
 // ------------------------------------------------------------------ certificate
