@@ -14,7 +14,9 @@ the paper's workloads:
   4. top-10 scoring of 1,024 queries against the quantized store.
 value = near-duplicate pairs per second of the whole step, counting the
 algorithmic pairs of exhaustive greedy (each arrival against every row
-retained at its arrival).
+retained at its arrival: config.pairs_per_step).  The screen's roofline counts
+the pairs its launches screen (each chunk against the rows retained before the
+chunk, plus the chunk's own lower triangle: config.screened_pairs_per_step).
 
 Usage: python bench.py [--steps K] [--warmup W] [--no-cpu-baseline] [--no-extras] [--band-grid]
 Prints one JSON line.
@@ -40,6 +42,8 @@ BAND_R = 4          # band width and quantizer step (eps = rel * sigma, sigma = 
 BAND_REL = 0.2      # of the banded candidate index, the operating point for tau = 0.95
 BAND_REPS = 5
 BAND_PREFIX = 4096  # arrivals of the grid's trial run per setting
+QEPS_WIDTH_EPS = (1e-2, 1e-3, 1e-4)   # 7-, 10- and 14-bit codes of the raw workload
+TRIAD_N = 1 << 27                     # floats per triad array (3 x 512 MB)
 
 
 def parse():
@@ -92,10 +96,13 @@ def measured_traffic(kernel):
         return None
 
 
-def cpu_baseline(x, pairs):
-    """The oracle, as it stands, on the same subset stream (dedup only)."""
-    import numpy as np  # noqa: F401
-    from oracle import dedup
+def cpu_baseline(x, pairs, raw, q):
+    """The oracle, as it stands, on the host's cores: the whole subset stream
+    through the dedup oracle (the headline figure), and beside it Q_eps encode
+    on a 2^24-value prefix of the raw workload and top-10 scoring of 256
+    queries against the stream's retained rows coded by the oracle."""
+    import numpy as np
+    from oracle import dedup, qeps, score
     try:
         from threadpoolctl import threadpool_info
         threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
@@ -104,10 +111,29 @@ def cpu_baseline(x, pairs):
     t0 = time.perf_counter()
     r = dedup.greedy(x, TAU, block=512)
     dt = time.perf_counter() - t0
-    return r, {"value": pairs / dt / 1e6, "unit": "M pairs/s", "cores": int(threads), "kind": "oracle",
-               "seconds": dt,
-               "sample": f"exhaustive greedy over the whole {x.shape[0]}-row subset stream (ingest only; "
-                         f"binary64 BLAS screen + exact rational ties)"}
+    out = {"value": pairs / dt / 1e6, "unit": "M pairs/s", "cores": int(threads), "kind": "oracle",
+           "seconds": dt,
+           "sample": f"exhaustive greedy over the whole {x.shape[0]}-row subset stream (ingest only; "
+                     f"binary64 BLAS screen + exact rational ties)"}
+    xs = raw[:1 << 24]
+    t0 = time.perf_counter()
+    _, _, plan = qeps.encode(xs, EPS, absmax=1.0)
+    dq = time.perf_counter() - t0
+    nbytes = (4 + plan["bits"] / 8) * xs.size
+    out["qeps_encode"] = {"value": nbytes / dq / 1e9, "unit": "GB/s", "cores": 1, "kind": "oracle", "seconds": dq,
+                          "sample": f"2^24 values of the raw workload at eps={EPS} ({plan['bits']}-bit codes; "
+                                    f"binary64 NumPy + exact rational near-ties, one thread)"}
+    store_ids = r["kept"]
+    store_codes = qeps.codes(x[store_ids], EPS).reshape(store_ids.size, -1)   # not timed
+    qs = q[:256]
+    t0 = time.perf_counter()
+    score.score_topk(qs, store_codes, store_ids, EPS, TOPK)
+    dsc = time.perf_counter() - t0
+    out["scoring"] = {"value": qs.shape[0] / dsc, "unit": "queries/s", "cores": int(threads), "kind": "oracle",
+                      "seconds": dsc,
+                      "sample": f"{qs.shape[0]} queries top-{TOPK} against the {store_codes.shape[0]}-row quantized "
+                                f"store of the stream (binary64 BLAS scores + sort)"}
+    return r, out
 
 
 def banded_ingest(lam, torch, np, xd, rep_exh, pairs, ctx, r=BAND_R, rel=BAND_REL, reps=BAND_REPS,
@@ -154,16 +180,20 @@ def banded_ingest(lam, torch, np, xd, rep_exh, pairs, ctx, r=BAND_R, rel=BAND_RE
     return out
 
 
-def beside_the_step(lam, torch, np, xd, qd, store, rep, pairs, ctx):
+def beside_the_step(lam, torch, np, xd, qd, store, rep, pairs, ctx, raw_sets, raw_out):
     """Measurements beside the timed step (not in it): the decision
     statistics of the stream (ambiguous pairs, exact decisions, smallest
-    decided margin), the screen at scale, the removal ceiling of the stream,
-    the share of benchmark queries whose top-10 is certified rank-invariant,
-    the per-block codec's size on the retained store, scoring at the corpus
-    size, and the stream through the banded candidate index."""
+    decided margin), the triad bandwidth anchor, raw Q_eps at three widths,
+    the screen at scale, the large online store at full size, the tiny
+    workload's per-call latency, the removal ceiling of the stream, the share
+    of benchmark queries whose top-10 is certified rank-invariant, the
+    per-block codec (size and speed) on the retained store, scoring at the
+    corpus size, and the stream through the banded candidate index."""
     ceil = lam.removal_ceiling(xd, TAU, batch=BATCH, ctx=ctx)
     cert = store.score_topk_certified(qd, TOPK)[3]
+    blk_t = block_codec_timing(lam, torch, store, ctx)
     blk = store.block_encode()
+    triad = triad_anchor(lam, torch, ctx)
     # the stream once more with calls that wait, for the decision statistics
     n = xd.shape[0]
     probe = lam.Store(D, TAU, n, ctx=ctx)
@@ -173,12 +203,17 @@ def beside_the_step(lam, torch, np, xd, qd, store, rep, pairs, ctx):
                  "min_margin_d2": float(min(t["min_margin_d2"] for t in st))}
     del probe
     return {"decisions": decisions,
+            "triad": triad,
+            "qeps_widths": qeps_widths(lam, torch, raw_sets, raw_out, ctx, triad["GBps"]),
             "screen_steady_state": screen_steady_state(lam, torch, np, ctx),
+            "online_store": online_store_run(lam, torch, np, ctx),
+            "tiny_latency": tiny_latency(lam, torch, ctx),
             "corpus_scoring": corpus_scoring(lam, torch, np, ctx),
             "removal_ceiling": {k: ceil[k] for k in ("kept", "kept_2delta", "removal", "ceiling",
                                                      "frac_of_ceiling", "bits_lo", "bits_hi")},
             "certified_top10_frac": float(cert.float().mean().item()),
-            "block_codec": {k: blk[k] for k in ("bits_per_code", "plain_bits", "codec_ratio", "composite_ratio")},
+            "block_codec": {**{k: blk[k] for k in ("bits_per_code", "plain_bits", "codec_ratio", "composite_ratio")},
+                            **{k: v for k, v in blk_t.items() if k.startswith("store_block")}},
             "banded": banded_ingest(lam, torch, np, xd, rep, pairs, ctx)}
 
 
@@ -245,6 +280,195 @@ def screen_steady_state(lam, torch, np, ctx, m=262_144, batch=4096, calls=5):
             "M_pairs_per_s": pairs / (t1 - t0) / 1e6,
             "screen_TFLOPs": flops / (tot_ms / 1e3) / 1e12,
             "screen_frac_of_peak": flops / (tot_ms / 1e3) / 1e12 / MFMA_F16_PEAK_TFLOPS}
+
+
+def triad_anchor(lam, torch, ctx, reps=20):
+    """The bandwidth anchor: triad c = a + s b over 3 x 512 MB float32
+    (lam_triad), timed by its launches; 12 bytes per element."""
+    a = torch.ones(TRIAD_N, dtype=torch.float32, device="cuda")
+    b = torch.full((TRIAD_N,), 2.0, dtype=torch.float32, device="cuda")
+    c = torch.empty_like(a)
+    lam.triad(a, b, c, 3.0, ctx=ctx)
+    torch.cuda.synchronize()
+    ctx.profile_reset()
+    ctx.profile_only("triad")
+    ctx.profile(True)
+    for _ in range(reps):
+        lam.triad(a, b, c, 3.0, ctx=ctx)
+    torch.cuda.synchronize()
+    ctx.profile(False)
+    ctx.profile_only(None)
+    tot, cnt = ctx.profile_read("triad")
+    ok = bool(torch.all(c == 7.0).item())
+    del a, b, c
+    gbs = 12.0 * TRIAD_N / (tot / cnt / 1e3) / 1e9
+    return {"workload": "triad c = a + 3 b, 3 x 512 MB float32", "GBps": gbs, "frac_of_spec": gbs / HBM_PEAK_GBS,
+            "us_per_launch": tot / cnt * 1e3, "result_checked": ok}
+
+
+def qeps_widths(lam, torch, raw_sets, raw_out, ctx, triad_gbs, reps=20):
+    """Raw Q_eps (2^26 values) at eps = 1e-2, 1e-3 and 1e-4 (7-, 10- and
+    14-bit codes, absmax 1 declared): encode and decode GB/s from events the
+    launches stamp themselves, four input sets rotating; (4 + b/8) bytes per
+    element, against the spec and the measured triad."""
+    n = raw_sets[0].numel()
+    out = {}
+    for eps in QEPS_WIDTH_EPS:
+        p = lam.qeps_plan(eps, 1.0, "bits", n)
+        codes = [torch.empty(p.code_bytes // 4, dtype=torch.int32, device="cuda") for _ in raw_sets]
+        for k in range(len(raw_sets)):   # warm-up
+            lam.quantize(raw_sets[k], eps, absmax=1.0, out=codes[k], ctx=ctx)
+            lam.dequantize(codes[k], p, out=raw_out[k], ctx=ctx)
+        torch.cuda.synchronize()
+        ctx.profile_reset()
+        ctx.profile_only("qeps_encode,qeps_decode")
+        ctx.profile(True)
+        for i in range(reps):
+            k = i % len(raw_sets)
+            lam.quantize(raw_sets[k], eps, absmax=1.0, out=codes[k], ctx=ctx)
+            lam.dequantize(codes[k], p, out=raw_out[k], ctx=ctx)
+        torch.cuda.synchronize()
+        ctx.profile(False)
+        ctx.profile_only(None)
+        nbytes = (4 + p.bits / 8) * n
+        row = {"bits": int(p.bits)}
+        for name in ("qeps_encode", "qeps_decode"):
+            tot, cnt = ctx.profile_read(name)
+            gbs = nbytes / (tot / cnt / 1e3) / 1e9
+            row[name] = {"us_per_launch": tot / cnt * 1e3, "GBps": gbs, "frac_of_spec": gbs / HBM_PEAK_GBS,
+                         "frac_of_triad": gbs / triad_gbs if triad_gbs else None}
+        out[f"eps={eps:g}"] = row
+        del codes
+    return out
+
+
+def online_store_run(lam, torch, np, ctx, calls=2):
+    """The large online store at its full size: 1,048,576 rows of D = 1,024
+    (16,384 clusters, 20 % planted copies; drawn on the device) ingested in
+    batches of 4,096 with calls that do not wait, tau = 0.95; the store coded
+    at eps = 1e-3; then 16,384 queries top-50.  The screen is timed by its own
+    launches; pairs are the algorithmic (retained at arrival) and the screened
+    ones."""
+    import synth
+    cfg = synth.online_store_device(device="cuda")
+    x, q = cfg["x"], cfg["q"]
+    n, d = x.shape
+    batch, k, eps = cfg["batch"], cfg["k"], cfg["eps"]
+    s = lam.Store(d, cfg["tau"], n, ctx=ctx)
+    reps = [torch.empty(min(batch, n - b0), dtype=torch.int64, device="cuda") for b0 in range(0, n, batch)]
+    ingest_s = []
+    for c in range(calls):
+        s.clear()
+        torch.cuda.synchronize()
+        if c == calls - 1:
+            ctx.profile_reset()
+            ctx.profile_only("dedup_screen")
+            ctx.profile(True)
+        t0 = time.perf_counter()
+        for bi, b0 in enumerate(range(0, n, batch)):
+            s.ingest(x[b0:b0 + batch], rep=reps[bi], sync=False)
+        info = s.info()   # waits for every call
+        ingest_s.append(time.perf_counter() - t0)
+    ctx.profile(False)
+    ctx.profile_only(None)
+    scr_ms, scr_n = ctx.profile_read("dedup_screen")
+    rep = torch.cat(reps)
+    kept = (rep < 0).to(torch.int64)
+    kept_before = torch.cumsum(kept, 0) - kept
+    pairs = int(kept_before.sum().item())
+    starts = torch.arange(0, n, batch, device="cuda")
+    nb = torch.clamp(n - starts, max=batch)
+    screened = int((nb * kept_before[starts]).sum().item() + (nb * (nb - 1) // 2).sum().item())
+    t0 = time.perf_counter()
+    p = s.quantize(eps)
+    q_ms = (time.perf_counter() - t0) * 1e3
+    res = s.score_topk(q, k)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(3):
+        s.score_topk(q, k, out=res)
+    torch.cuda.synchronize()
+    sc_ms = (time.perf_counter() - t0) * 1e3 / 3
+    t_ing = min(ingest_s)
+    flops = 2.0 * d * screened
+    out = {"workload": f"online store: {n} x {d} in batches of {batch}, tau={cfg['tau']}, eps={eps}, "
+                       f"{q.shape[0]} queries top-{k}",
+           "kept": int(info.size), "ingest_s": t_ing, "M_pairs_per_s": pairs / t_ing / 1e6, "pairs": pairs,
+           "screened_pairs": screened, "screen_ms": scr_ms, "screen_launches": scr_n,
+           "screen_TFLOPs": flops / (scr_ms / 1e3) / 1e12,
+           "screen_frac_of_peak": flops / (scr_ms / 1e3) / 1e12 / MFMA_F16_PEAK_TFLOPS,
+           "store_quantize_ms": q_ms, "store_code_bits": int(p.bits),
+           "scoring_ms": sc_ms, "queries_per_s": q.shape[0] / (sc_ms / 1e3),
+           "scoring_TFLOPs_algorithmic": 2.0 * d * q.shape[0] * info.size / (sc_ms / 1e3) / 1e12}
+    del s, x, q, reps, rep
+    return out
+
+
+def tiny_latency(lam, torch, ctx, calls=20):
+    """The tiny workload as a latency test: 4,096 rows of D = 768 ingested as
+    four calls of 1,024 that each wait (median ms per call, host to host),
+    the store coded, and 64 queries top-10 (median ms per scoring call that
+    waits)."""
+    import synth
+    t = synth.tiny_ingest()
+    x = torch.from_numpy(t["x"]).cuda()
+    q = torch.from_numpy(t["q"]).cuda()
+    s = lam.Store(x.shape[1], t["tau"], x.shape[0], ctx=ctx)
+    per_call = []
+    for c in range(calls // 4 + 1):
+        s.clear()
+        torch.cuda.synchronize()
+        for b0 in range(0, x.shape[0], 1024):
+            t0 = time.perf_counter()
+            s.ingest(x[b0:b0 + 1024])   # waits
+            per_call.append((time.perf_counter() - t0) * 1e3)
+    s.quantize(t["eps"])
+    out = s.score_topk(q, 10)
+    sc = []
+    for _ in range(calls):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        s.score_topk(q, 10, out=out)
+        torch.cuda.synchronize()
+        sc.append((time.perf_counter() - t0) * 1e3)
+    per_call = sorted(per_call[4:])   # the first pass warms up
+    sc.sort()
+    return {"workload": "tiny ingest: 4096 x 768 in calls of 1024 that wait; 64 queries top-10",
+            "ingest_ms_per_call_p50": per_call[len(per_call) // 2], "ingest_ms_per_call_p90": per_call[int(0.9 * len(per_call))],
+            "scoring_ms_p50": sc[len(sc) // 2], "scoring_ms_p90": sc[int(0.9 * len(sc))], "kept": int(s.size)}
+
+
+def block_codec_timing(lam, torch, store, ctx, reps=10):
+    """The per-block codec on the benchmark's store: encode (widths, then bit
+    planes), decode to float32 and expansion back to the fixed-width stream
+    for scoring, each as GB/s of the bytes it must move (fixed-width codes,
+    encoded blocks, float32 rows) against the HBM peak."""
+    ctx.profile_reset()
+    ctx.profile_only("store_block_encode,store_block_pack,store_block_decode,store_block_expand")
+    ctx.profile(True)
+    xhat = torch.empty((store.size, D), dtype=torch.float32, device="cuda")
+    for _ in range(reps):
+        st = store.block_encode()
+        store.block_decode(out=xhat)
+    q = torch.zeros((1, D), dtype=torch.float32, device="cuda")
+    for _ in range(reps):
+        store.score_topk_blocks(q, 1)
+    torch.cuda.synchronize()
+    ctx.profile(False)
+    ctx.profile_only(None)
+    n = store.size * D
+    fixed = n * st["plain_bits"] / 8
+    enc = st["total_bytes"]
+    res = {"bits_per_code": st["bits_per_code"], "plain_bits": st["plain_bits"]}
+    moved = {"store_block_encode": fixed, "store_block_pack": fixed + enc, "store_block_decode": enc + 4 * n,
+             "store_block_expand": enc + fixed}
+    for name, b in moved.items():
+        tot, cnt = ctx.profile_read(name)
+        if cnt:
+            gbs = b / (tot / cnt / 1e3) / 1e9
+            res[name] = {"us_per_launch": tot / cnt * 1e3, "GBps": gbs, "frac_of_spec": gbs / HBM_PEAK_GBS}
+    del xhat
+    return res
 
 
 def band_grid(lam, torch, np, synth, ctx):
@@ -376,9 +600,10 @@ def main():
                            "avg_launch_ms": tot / cnt}
     dominant = max(kinfo, key=lambda k: kinfo[k]["ms_per_step"])
 
-    # 2. timed pass: events on the dominant kernel's launches only
+    # 2. timed pass: events carried by the launches of the dominant kernel and
+    #    of the raw Q_eps encode / decode (no marker packets between launches)
     ctx.profile_reset()
-    ctx.profile_only(dominant)
+    ctx.profile_only(f"{dominant},qeps_encode,qeps_decode")
     ctx.profile(True)
     torch.cuda.synchronize()
     # events between the steps on the library's stream (torch's current one)
@@ -396,6 +621,7 @@ def main():
     ctx.profile_only(None)
     ms = (t1 - t0) * 1e3 / args.steps
     dom_tot, dom_cnt = ctx.profile_read(dominant)
+    timed_qeps = {name: ctx.profile_read(name) for name in ("qeps_encode", "qeps_decode")}
 
     if args.copy_calibration:
         src = torch.ones(1 << 28, dtype=torch.float32, device=dev)
@@ -422,6 +648,12 @@ def main():
         if name in kinfo:
             rate = amt / (kinfo[name]["ms_per_step"] / 1e3)
             kinfo[name].update({"achieved": rate, "unit": unit + "/s", "peak": peak, "frac": rate / peak})
+    # the raw Q_eps kernels as timed by their own launches in the timed steps
+    qeps_timed = {}
+    for name, (tot, cnt) in timed_qeps.items():
+        if cnt:
+            gbs = work[name][0] / (tot / cnt / 1e3)
+            qeps_timed[name] = {"us_per_launch": tot / cnt * 1e3, "GBps": gbs, "frac_of_spec": gbs / HBM_PEAK_GBS}
     dom_work = work.get(dominant)
     if dom_work and dom_cnt:
         launches = dom_cnt / args.steps
@@ -434,17 +666,22 @@ def main():
                     "avg_launch_us": avg_s * 1e6, "launches_per_step": launches,
                     "algorithmic_per_launch": per_launch * (1e3 if dom_work[1] == "GB" else 1.0),
                     "algorithmic_unit": "MB" if dom_work[1] == "GB" else "TFLOP",
-                    "algorithmic_bytes_per_launch": (dom_work[4] / launches if dom_work[4] else None)}
+                    "algorithmic_bytes_per_launch": (dom_work[4] / launches if dom_work[4] else None),
+                    "counts": ("screened pairs: each call's rows against the rows retained before it, plus the "
+                               "call's lower triangle, 2 D flop each" if dominant == "dedup_screen" else
+                               "algorithmic units of the kernel")}
     else:
         roofline = {"kernel": dominant, "bound": "latency", "achieved": None, "peak": None, "unit": None,
                     "frac": None, "traffic": None}
 
     extras = {}
     if not args.no_extras:
-        extras = beside_the_step(lam, torch, np, xd, qd, store, rep, pairs, ctx)
+        extras = beside_the_step(lam, torch, np, xd, qd, store, rep, pairs, ctx, raw_sets, raw_out)
+        tgbs = extras["triad"]["GBps"]
+        for v in qeps_timed.values():
+            v["frac_of_triad"] = v["GBps"] / tgbs
 
     value = pairs / (ms / 1e3) / 1e6
-    enc = kinfo.get("qeps_encode", {})
     out = {
         "metric": "Q_eps encode GB/s; near-dup M pairs/s at D=768; queries/s; % of roofline",
         "value": value,
@@ -465,11 +702,13 @@ def main():
                          f"tau={TAU}; store Q_eps eps={EPS} + decode; {qd.shape[0]} queries top-{TOPK}; "
                          f"plus raw Q_eps encode+decode of 2^{RAW_LOG2N} float32 at eps={EPS}"),
             "pairs_per_step": pairs,
+            "screened_pairs_per_step": screen_store_pairs + screen_chunk_pairs,
             "retained": n_store,
             "store_code_bits": int(info.q.bits),
             "raw_code_bits": int(p_raw.bits),
         },
-        "qeps_encode_GBps": enc.get("achieved", 0.0) * 1.0 if enc else None,
+        "qeps_encode_GBps": qeps_timed.get("qeps_encode", {}).get("GBps"),
+        "qeps_timed": qeps_timed,
         # every scoring launch: prep, sample, filter, select and rescore, fallback
         "queries_per_s": (qd.shape[0] / (sum(kinfo[k]["ms_per_step"] for k in KERNELS
                                              if k.startswith("score_") and k in kinfo) / 1e3)),
@@ -480,7 +719,7 @@ def main():
                          f"launch; the timed steps carry events on the dominant kernel only"),
     }
     if not args.no_cpu_baseline:
-        ref, cb = cpu_baseline(x, pairs)
+        ref, cb = cpu_baseline(x, pairs, raw, cfg["q"])
         if not np.array_equal(ref["rep"], rep):
             raise SystemExit("GPU decisions differ from the oracle on the benchmark stream")
         out["cpu_baseline"] = cb

@@ -82,9 +82,9 @@ lam_status lam_ctx_synchronize(lam_ctx* ctx);
  * returns the summed elapsed milliseconds and launch count of one kernel name
  * (0 / 0 if never launched).  For benchmarks; off by default. */
 lam_status lam_ctx_profile(lam_ctx* ctx, int enable);
-/* Restricts the timing to the launches of one kernel name (NULL or "": every
- * kernel), so that a timed run carries only that kernel's events.  The name is
- * copied. */
+/* Restricts the timing to the launches of the kernel names in a
+ * comma-separated list (NULL or "": every kernel), so that a timed run carries
+ * only those kernels' events.  The list is copied. */
 lam_status lam_ctx_profile_only(lam_ctx* ctx, const char* kernel);
 lam_status lam_ctx_profile_reset(lam_ctx* ctx);
 lam_status lam_ctx_profile_read(lam_ctx* ctx, const char* kernel, double* total_ms, int64_t* launches);
@@ -356,6 +356,17 @@ typedef struct lam_ceiling_stats {
  * (as lam_dedup_ingest); ENOMEM if the two stores do not fit. */
 lam_status lam_removal_ceiling(lam_ctx* ctx, const float* x_dev, int64_t n, int32_t dim, double tau,
                                int64_t batch, lam_ceiling_stats* out);
+
+/* ------------------------------------------------------------------ bandwidth anchor */
+
+/* The triad c = a + s * b over n float32 values (a_dev, b_dev, c_dev
+ * 16-byte aligned device arrays; 12 bytes moved per element): the streaming
+ * bandwidth the paper measures on its platform so that every bandwidth figure
+ * is stated against a measured ceiling as well as the published one
+ * (Appendix "Measured hardware constants", Table "anchors", 3 x 512 MB).
+ * Timed under the kernel name "triad" when profiling.  EINVAL: n < 0, NULL or
+ * misaligned arrays.  Asynchronous. */
+lam_status lam_triad(lam_ctx* ctx, const float* a_dev, const float* b_dev, float* c_dev, int64_t n, float s);
 
 #ifdef __cplusplus
 }

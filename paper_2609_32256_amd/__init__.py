@@ -128,6 +128,7 @@ _SIGS = {
                             ctypes.c_int),
     "lam_score_topk": ([_P, _P, _P, _I64, ctypes.c_int32, _P, _P, _P], ctypes.c_int),
     "lam_score_topk_noalloc": ([_P, _P, _P, _I64, ctypes.c_int32, _P, _P, _P], ctypes.c_int),
+    "lam_triad": ([_P, _P, _P, _P, _I64, ctypes.c_float], ctypes.c_int),
 }
 for _name, (_args, _res) in _SIGS.items():
     _fn = getattr(_lib, _name)
@@ -192,7 +193,8 @@ class Context:
         _check(_lib.lam_ctx_profile(self._h, 1 if enable else 0))
 
     def profile_only(self, kernel: str | None):
-        """Time only the launches of one kernel name (None: every kernel)."""
+        """Time only the launches of the kernel names in a comma-separated list
+        (None: every kernel)."""
         _check(_lib.lam_ctx_profile_only(self._h, (kernel or "").encode()))
 
     def profile_reset(self):
@@ -202,19 +204,6 @@ class Context:
         ms, n = ctypes.c_double(), _I64()
         _check(_lib.lam_ctx_profile_read(self._h, kernel.encode(), ctypes.byref(ms), ctypes.byref(n)))
         return ms.value, n.value
-
-    def score_topk_noalloc(self, q: torch.Tensor, k: int, out):
-        """score_topk through the allocation-free entry point (lam_score_topk_noalloc):
-        the library takes its scratch from a fixed per-device array; the caller
-        passes every output, out = (scores float32[nq, k], ids int64[nq, k],
-        bound float32[nq]).  nq <= 256; the store must be settled (info())."""
-        q = _dev_tensor(q, torch.float32, "q")
-        if q.dim() != 2 or q.shape[1] != self.dim:
-            raise ValueError(f"q must be (nq, {self.dim})")
-        s, i, b = out
-        _check(_lib.lam_score_topk_noalloc(self.ctx.handle, self._h, _ptr(q), q.shape[0], int(k), _ptr(s), _ptr(i),
-                                           _ptr(b)))
-        return s, i, b
 
     def close(self):
         if getattr(self, "_h", None):
@@ -282,6 +271,19 @@ def dequantize(codes: torch.Tensor, p: QParams, out: torch.Tensor | None = None,
         out = torch.empty(p.n, dtype=torch.float32, device=codes.device)
     _check(_lib.lam_dequantize(ctx.handle, _ptr(codes), ctypes.byref(p), _ptr(out)))
     return out
+
+
+def triad(a: torch.Tensor, b: torch.Tensor, c: torch.Tensor, s: float = 3.0, ctx: Context | None = None):
+    """The bandwidth anchor c = a + s * b over float32 device tensors of equal
+    size (lam_triad; 12 bytes moved per element)."""
+    ctx = ctx or default_context()
+    a = _dev_tensor(a, torch.float32, "a")
+    b = _dev_tensor(b, torch.float32, "b")
+    c = _dev_tensor(c, torch.float32, "c")
+    if not (a.numel() == b.numel() == c.numel()):
+        raise ValueError("a, b and c must have the same size")
+    _check(_lib.lam_triad(ctx.handle, _ptr(a), _ptr(b), _ptr(c), a.numel(), float(s)))
+    return c
 
 
 # ---------------------------------------------------------------- store
@@ -458,4 +460,4 @@ class Store:
 
 
 __all__ = ["LamError", "QParams", "IngestStats", "StoreInfo", "Context", "default_context", "quantize",
-           "dequantize", "Store", "qeps_plan", "removal_ceiling", "CeilingStats", "abi_version", "EXPORTED", "LIB_PATH"]
+           "dequantize", "triad", "Store", "qeps_plan", "removal_ceiling", "CeilingStats", "abi_version", "EXPORTED", "LIB_PATH"]

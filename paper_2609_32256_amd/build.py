@@ -22,7 +22,7 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 OUT = os.path.join(HERE, "liblam.so")
 OBJDIR = os.path.join(ROOT, "_build", "lam")
-SOURCES = ["api.cpp", "qeps.hip", "dedup.hip", "score.hip", "exact.cpp", "ceiling.cpp", "blockcodec.hip"]
+SOURCES = ["api.cpp", "qeps.hip", "dedup.hip", "score.hip", "exact.cpp", "ceiling.cpp", "blockcodec.hip", "triad.hip"]
 ARCH = os.environ.get("LAM_OFFLOAD_ARCH", "gfx950")
 
 

@@ -58,10 +58,25 @@ struct DeviceGuard {
   }
 };
 
+// Whether launches of kernel `name` are timed: every kernel, or those named in
+// the comma-separated list of lam_ctx_profile_only.
+static bool prof_selected(const lam_ctx* ctx, const char* name) {
+  if (!ctx->profiling) return false;
+  if (ctx->prof_only.empty()) return true;
+  const std::string& l = ctx->prof_only;
+  const size_t n = strlen(name);
+  for (size_t p = 0; p <= l.size();) {
+    size_t e = l.find(',', p);
+    if (e == std::string::npos) e = l.size();
+    if (e - p == n && l.compare(p, n, name) == 0) return true;
+    p = e + 1;
+  }
+  return false;
+}
+
 lam_status prof_begin(lam_ctx* ctx, const char* name, size_t* slot) {
   *slot = (size_t)-1;
-  if (!ctx->profiling) return LAM_OK;
-  if (!ctx->prof_only.empty() && ctx->prof_only != name) return LAM_OK;
+  if (!prof_selected(ctx, name)) return LAM_OK;
   ProfRec r{name, nullptr, nullptr};
   for (hipEvent_t* ev : {&r.a, &r.b}) {
     if (!ctx->event_pool.empty()) {
@@ -86,8 +101,7 @@ lam_status prof_begin(lam_ctx* ctx, const char* name, size_t* slot) {
 // unless this kernel is being profiled.
 lam_status prof_launch_events(lam_ctx* ctx, const char* name, hipEvent_t* start, hipEvent_t* stop) {
   *start = *stop = nullptr;
-  if (!ctx->profiling) return LAM_OK;
-  if (!ctx->prof_only.empty() && ctx->prof_only != name) return LAM_OK;
+  if (!prof_selected(ctx, name)) return LAM_OK;
   ProfRec r{name, nullptr, nullptr};
   for (hipEvent_t* ev : {&r.a, &r.b}) {
     if (!ctx->event_pool.empty()) {
@@ -518,6 +532,16 @@ lam_status lam_score_topk_noalloc(lam_ctx* ctx, const lam_store* st, const float
             "store must be quantized (lam_store_quantize) after its last ingest");
   DeviceGuard g(ctx->device);
   return score_topk_noalloc(ctx, st, q_dev, nq, k, scores_dev, ids_dev, bound_dev);
+}
+
+lam_status lam_triad(lam_ctx* ctx, const float* a_dev, const float* b_dev, float* c_dev, int64_t n, float s) {
+  LAM_CHECK(ctx != nullptr, LAM_EINVAL, "ctx is NULL");
+  LAM_CHECK(n >= 0, LAM_EINVAL, "n must be >= 0");
+  LAM_CHECK(n == 0 || (a_dev && b_dev && c_dev), LAM_EINVAL, "NULL buffer");
+  LAM_CHECK((((uintptr_t)a_dev | (uintptr_t)b_dev | (uintptr_t)c_dev) & 15u) == 0, LAM_EINVAL,
+            "arrays must be 16-byte aligned");
+  DeviceGuard g(ctx->device);
+  return launch_triad(ctx, a_dev, b_dev, c_dev, n, s);
 }
 
 lam_status lam_store_block_encode(lam_ctx* ctx, lam_store* st, lam_block_stats* out) {

@@ -201,6 +201,9 @@ lam_status score_topk(lam_ctx* ctx, const lam_store* st, const float* q, int64_t
 lam_status score_topk_noalloc(lam_ctx* ctx, const lam_store* st, const float* q, int64_t nq, int32_t k,
                               float* scores, int64_t* ids, float* bound);
 lam_status noalloc_setup(int device);
+
+// ------------------------------------------------------------------ bandwidth anchor (triad.hip)
+lam_status launch_triad(lam_ctx* ctx, const float* a, const float* b, float* c, int64_t n, float s);
 lam_status score_certify(lam_ctx* ctx, const lam_store* st, const float* q, int64_t nq, int32_t k, float* scores,
                          int64_t* ids, float* bound, uint8_t* certified, float* margin);
 lam_status block_encode(lam_ctx* ctx, lam_store* st, lam_block_stats* out);
