@@ -23,14 +23,16 @@ import numpy as np
 
 
 def scores(q, codes_rows, eps: float) -> np.ndarray:
-    """(nq x N) binary64 scores s * Q . C^T."""
+    """(nq x N) binary64 scores s * Q . C^T.  Codes may be given as integers or
+    as binary64 values already holding them (exact below 2^53)."""
     q64 = np.asarray(q, dtype=np.float32).astype(np.float64)
-    c64 = np.asarray(codes_rows, dtype=np.int64).astype(np.float64)
+    c = np.asarray(codes_rows)
+    c64 = c if c.dtype == np.float64 else c.astype(np.int64).astype(np.float64)
     return (2.0 * float(eps)) * (q64 @ c64.T)
 
 
-def topk(s, ids, k: int):
-    """Per row, the k best by (score desc, id asc)."""
+def topk_sorted(s, ids, k: int):
+    """Per row, the k best by (score desc, id asc): the whole row sorted."""
     s = np.asarray(s, dtype=np.float64)
     ids = np.asarray(ids, dtype=np.int64)
     nq, n = s.shape
@@ -41,6 +43,26 @@ def topk(s, ids, k: int):
         order = np.lexsort((ids, -s[j]))[:kk]
         out_s[j, :kk] = s[j, order]
         out_i[j, :kk] = ids[order]
+    return out_s, out_i
+
+
+def topk(s, ids, k: int):
+    """Per row, the k best by (score desc, id asc) -- topk_sorted's result,
+    found by sorting only the entries at or above the row's k-th largest score
+    (every entry tied with it included), which is all the order can take."""
+    s = np.asarray(s, dtype=np.float64)
+    ids = np.asarray(ids, dtype=np.int64)
+    nq, n = s.shape
+    if n <= 4 * k:
+        return topk_sorted(s, ids, k)
+    out_s = np.full((nq, k), -np.inf)
+    out_i = np.full((nq, k), -1, dtype=np.int64)
+    for j in range(nq):
+        kth = np.partition(s[j], n - k)[n - k]          # the k-th largest score
+        cand = np.nonzero(s[j] >= kth)[0]
+        order = cand[np.lexsort((ids[cand], -s[j, cand]))][:k]
+        out_s[j] = s[j, order]
+        out_i[j] = ids[order]
     return out_s, out_i
 
 

@@ -7,6 +7,7 @@ import pytest
 import torch
 
 import synth
+from test_gpu_score import _compare
 from oracle import blockcodec, dedup, qeps
 
 pytestmark = pytest.mark.gpu
@@ -25,12 +26,26 @@ def _store(lam, x, tau, eps, batch=1024, spare=0):
     return s, p
 
 
+@pytest.fixture(scope="module")
+def subset():
+    cfg = synth.subset_ingest()
+    return cfg, dedup.greedy(cfg["x"], 0.95)
+
+
 @pytest.mark.parametrize("eps", [1e-2, 1e-3, 1e-4])
-def test_subset_store_blocks_bit_exact(lam, eps):
-    x = synth.subset_ingest()["x"][:9000]
+def test_subset_store_blocks_bit_exact(lam, subset, eps):
+    """The whole 27,986-row subset stream at tau = 0.95, its store coded at
+    each eps: the fixed-width codes and the block encoding equal the oracle's
+    bit for bit, and top-10 scores of the stream's 1,024 queries match the
+    oracle's."""
+    cfg, ref = subset
+    x = cfg["x"]
     s, p = _store(lam, x, 0.95, eps)
     kept = s.ids().cpu().numpy()
+    assert np.array_equal(kept, ref["kept"])
     codes = qeps.codes(x[kept], eps).reshape(kept.size, -1)
+    assert p.bits == qeps.plan(eps, float(np.abs(x[kept]).max()))["bits"]
+    assert np.array_equal(s.codes().cpu().numpy().view(np.uint32), qeps.pack(codes, p.bits))
     ref = blockcodec.encode(codes)
     st = s.block_encode()
     w, ro, d = s.block_export()
@@ -44,6 +59,10 @@ def test_subset_store_blocks_bit_exact(lam, eps):
     assert st["composite_ratio"] == pytest.approx(x.shape[0] * x.shape[1] * 4 / sz["total_bytes"], rel=1e-12)
     # lossless: the decode is the store's Q_eps decode, bit for bit
     assert torch.equal(s.block_decode(), s.dequantize())
+    q = cfg["q"]
+    gs, gi, _ = s.score_topk(torch.from_numpy(q).cuda(), 10)
+    worst = _compare(gs.cpu().numpy(), gi.cpu().numpy(), codes, kept, q, eps, 10)
+    assert worst <= 1e-5
     print(f"eps={eps}: b={p.bits}, {st['bits_per_code']:.3f} bits/code, codec x{st['codec_ratio']:.2f}, "
           f"composite x{st['composite_ratio']:.2f}")
 

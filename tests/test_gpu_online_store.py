@@ -56,16 +56,20 @@ def test_store_bookkeeping(run):
 
 
 def test_sampled_decisions(run):
-    """Decisions of sampled arrivals recomputed by the oracle against the
-    retained set at their arrival."""
+    """Decisions of 1,024 arrivals, four from each of the 256 batches, and of
+    64 more dropped ones, recomputed by the oracle against the retained set at
+    their arrival."""
     x, rep, tau = run["x"], run["rep"], run["tau"]
     rng = np.random.default_rng(2)
     n = rep.size
-    samples = np.unique(np.concatenate([rng.integers(0, n, 40), rng.integers(n - n // 8, n, 8),
-                                        rng.choice(np.nonzero(rep >= 0)[0], 16)]))
+    batch = 4096
+    per_batch = np.concatenate([b0 + rng.choice(min(batch, n - b0), 4, replace=False) for b0 in range(0, n, batch)])
+    samples = np.unique(np.concatenate([per_batch, rng.choice(np.nonzero(rep >= 0)[0], 64, replace=False)]))
+    assert samples.size >= 1024
     kept = np.nonzero(rep < 0)[0]
     want = dedup.decide_many(x, samples, kept, tau)
     assert np.array_equal(rep[samples], want), samples[rep[samples] != want]
+    print(f"{samples.size} sampled decisions equal the oracle's ({np.count_nonzero(want >= 0)} dropped)")
 
 
 def test_cover_on_dropped_sample(run):
@@ -101,11 +105,12 @@ def test_store_codes_sampled_rows(run):
 
 
 def test_sampled_queries_topk(run):
-    """Top-50 of sampled queries against the oracle over every retained row."""
+    """Top-50 of 256 sampled queries against the oracle over every retained
+    row."""
     x, q, ids, eps, k = run["x"], run["q"], run["ids"], run["eps"], run["k"]
     gs, gi, gb = run["gs"], run["gi"], run["gb"]
     rng = np.random.default_rng(5)
-    qs = np.sort(rng.choice(q.shape[0], 24, replace=False))
+    qs = np.sort(rng.choice(q.shape[0], 256, replace=False))
     ts, ti, beta = score.score_topk_blocked(q[qs], x[ids], ids, eps, k)
     xs = set(ids.tolist())
     for n_, j in enumerate(qs):

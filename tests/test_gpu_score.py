@@ -131,21 +131,27 @@ def test_state_errors(lam):
     assert e.value.name == "LAM_EINVAL"
 
 
-def test_corpus_sampled(lam):
+def test_corpus_all_queries(lam):
     """361,802 clustered rows quantized at eps = 1e-3, 4,096 queries, top-10:
-    the benchmark's launch configuration; oracle scores on a sample of 64
-    queries against the whole store."""
+    the benchmark's launch configuration; every query against the oracle's
+    scores of the whole store (in blocks of 256 queries)."""
     cfg = synth.corpus_retrieval()
     x, q, eps, k = cfg["x"], cfg["q"], cfg["eps"], cfg["k"]
     s = _store_from_rows(lam, x)
     p = s.quantize(eps)
-    gs, gi, _ = s.score_topk(_dev(q), k)
-    gs, gi = gs.cpu().numpy(), gi.cpu().numpy()
-    c = qeps.codes(x, eps).reshape(x.shape[0], -1)
+    gs, gi, gb = s.score_topk(_dev(q), k)
+    gs, gi, gb = gs.cpu().numpy(), gi.cpu().numpy(), gb.cpu().numpy()
+    c = qeps.codes(x, eps).reshape(x.shape[0], -1).astype(np.float64)
     assert p.bits == qeps.plan(eps, float(np.abs(x).max()))["bits"]
-    sample = np.random.default_rng(0).choice(q.shape[0], 64, replace=False)
-    worst = _compare(gs[sample], gi[sample], c, np.arange(x.shape[0]), q[sample], eps, k)
-    print(f"corpus: max |score - oracle| = {worst:.3g}")
+    ids = np.arange(x.shape[0])
+    worst = 0.0
+    for j0 in range(0, q.shape[0], 256):
+        sl = slice(j0, j0 + 256)
+        worst = max(worst, _compare(gs[sl], gi[sl], c, ids, q[sl], eps, k))
+    beta = score.bound(q, eps)
+    gbn = gb.astype(np.float64)
+    assert np.all(gbn >= beta) and np.all(gbn - beta <= np.spacing(gbn.astype(np.float32)))
+    print(f"corpus, {q.shape[0]} queries: max |score - oracle| = {worst:.3g}")
 
 
 @pytest.mark.parametrize("k,d", [(10, 64), (50, 64), (10, 768), (50, 768)])

@@ -133,3 +133,16 @@ def test_certify_closed_forms():
     assert not f[0] and m[0] == 0.0
     f, m, _ = score.certify(q, c[:3], ids[:3], eps, 3, 10.0)
     assert f[0] and m[0] == np.inf
+
+
+def test_topk_selection_equals_the_sorted_definition():
+    """topk (partition, then sort of the entries at or above the k-th score)
+    gives topk_sorted's result (every row sorted by score desc, id asc), with
+    ties planted at the k-th score, ids out of order and k near the row size."""
+    rng = np.random.default_rng(31)
+    for n, k in ((50, 10), (400, 10), (400, 64), (3000, 50), (41, 10)):
+        s = np.round(rng.standard_normal((23, n)), 1)   # many exact ties
+        ids = rng.permutation(10 * n)[:n]
+        a = score.topk(s, ids, k)
+        b = score.topk_sorted(s, ids, k)
+        assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
