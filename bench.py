@@ -64,8 +64,8 @@ def parse():
     return ap.parse_args()
 
 
-KERNELS = ("qeps_encode", "qeps_decode", "dedup_prep", "dedup_screen", "dedup_verify", "dedup_resolve",
-           "dedup_append", "store_encode", "store_decode", "score_prep", "score_sample",
+KERNELS = ("qeps_encode", "qeps_decode", "dedup_prep", "dedup_screen", "dedup_verify", "dedup_resolve_append",
+           "dedup_resolve", "dedup_append", "store_encode", "store_decode", "score_prep", "score_sample",
            "score_mfma", "score_merge", "score_fallback")
 HERE = os.path.dirname(os.path.abspath(__file__))
 TRAFFIC_FILE = os.path.join(HERE, "profiles", "traffic.json")

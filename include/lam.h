@@ -253,8 +253,10 @@ lam_status lam_store_export(lam_ctx* ctx, const lam_store* store, int64_t* ids_d
  * ids_dev (nq x k, row-major), padded with (-inf, -1) past the store size.
  * bound_dev (optional): eps * ||q_j||_1 rounded up to float32.
  * 1 <= k <= 64.  ESTATE if the store is not quantized (or has rows added
- * since).  A query row holding NaN/Inf gets (NaN, -1) in all k slots and a
- * NaN bound instead of an error status.  Asynchronous. */
+ * since), or if its codes are wider than 12 bits (the scorer multiplies codes
+ * as exact float16 values; quantize with a larger eps, e.g. 12 bits hold
+ * absmax / (2 eps) < 2,047.5).  A query row holding NaN/Inf gets (NaN, -1) in
+ * all k slots and a NaN bound instead of an error status.  Asynchronous. */
 lam_status lam_score_topk(lam_ctx* ctx, const lam_store* store, const float* q_dev, int64_t nq,
                           int32_t k, float* scores_dev, int64_t* ids_dev, float* bound_dev);
 

@@ -87,7 +87,7 @@ struct ChunkCounters {
   uint32_t npairs;        // ambiguous pairs appended in this chunk
   uint32_t n_escalate;
   uint32_t blocks_done;   // append workgroups finished (last one exports the status words)
-  uint32_t pad;
+  uint32_t kept;          // rows of the chunk kept, summed by the workgroups of k_resolve_append
 };
 
 __device__ __forceinline__ bool skip_all(const DevFlags* f) {
@@ -166,6 +166,7 @@ __global__ __launch_bounds__(256) void k_prep(const float* __restrict__ x, int64
     cs.cc->npairs = 0u;
     cs.cc->n_escalate = 0u;
     cs.cc->blocks_done = 0u;
+    cs.cc->kept = 0u;
     if (cs.m_first >= 0) cs.meta->m = cs.m_first;   // a retried call starts from the store as it was
   }
   if (row < cs.nB) init_chunk_row(cs, row, lane);
@@ -222,6 +223,7 @@ __global__ void k_chunk_init(ChunkState cs) {
     cs.cc->npairs = 0u;
     cs.cc->n_escalate = 0u;
     cs.cc->blocks_done = 0u;
+    cs.cc->kept = 0u;
   }
 }
 
@@ -946,22 +948,38 @@ constexpr int kResolveThreads = 1024;
 static_assert(kChunk % kResolveThreads == 0, "whole rows per thread");
 constexpr int kEdgeCap = 20480;    // in-chunk candidate entries held in LDS
 
+// LDS of the in-chunk resolve.  rrow: the decision of each row as rep_row
+// encodes it; posv: the store position of each kept row (-1 if dropped).
+struct ResolveLds {
+  uint8_t st[kChunk];        // 0 undecided, 1 kept, 2 dropped
+  uint16_t edges[kEdgeCap];
+  uint32_t eoff[kChunk];
+  uint16_t elen[kChunk];
+  uint16_t ecur[kChunk];
+  uint16_t active[kChunk];
+  int32_t rrow[kChunk];
+  int32_t posv[kChunk];
+  uint32_t n_active, n_edges, pending, total;
+  int wsum[kResolveThreads / 64];
+};
+
 // Fallback when the candidate lists do not fit in LDS: one wave walks the
 // undecided rows in arrival order; lane L keeps bits [64L, 64L + 64) of the
 // kept mask in a register, and a row takes the lowest kept candidate of its
 // bitmap row.
-__device__ void resolve_sequential(const ResolveArgs& a, volatile uint8_t* st, int64_t gbase) {
+__device__ void resolve_sequential(const ResolveArgs& a, ResolveLds& L, int n) {
+  volatile uint8_t* st = L.st;
   const int lane = threadIdx.x & 63;
-  const int nblk = (a.nB + 63) >> 6;
+  const int nblk = (n + 63) >> 6;
   uint64_t kept = 0ull;
   for (int w = 0; w < nblk; ++w) {
     const int r = w * 64 + lane;
-    const uint64_t b = __ballot(r < a.nB && st[r] == 1);
+    const uint64_t b = __ballot(r < n && st[r] == 1);
     if (lane == w) kept = b;
   }
   for (int blk = 0; blk < nblk; ++blk) {
     const int r = blk * 64 + lane;
-    uint64_t act = __ballot(r < a.nB && st[r] == 0);
+    uint64_t act = __ballot(r < n && st[r] == 0);
     while (act) {
       const int b = __builtin_ctzll(act);
       act &= act - 1ull;
@@ -976,22 +994,21 @@ __device__ void resolve_sequential(const ResolveArgs& a, volatile uint8_t* st, i
         const int j = F * 64 + __builtin_ctzll(uf);
         if (lane == 0) {
           st[i] = 2;
-          a.rep[i] = gbase + j;
-          a.rep_row[i] = -(j + 2);
+          L.rrow[i] = -(j + 2);
         }
       } else {
         if (lane == blk) kept |= 1ull << b;
         if (lane == 0) {
           st[i] = 1;
-          a.rep[i] = -1;
-          a.rep_row[i] = -1;
+          L.rrow[i] = -1;
         }
       }
     }
   }
 }
 
-// In-order resolve of one chunk by one workgroup.
+// In-order resolve of the first n rows of a chunk by one workgroup of T
+// threads, into L (the decision of a row depends only on rows before it).
 //  A. Rows with a store hit are dropped (their representative is the lowest
 //     store row); rows with no in-chunk edge are kept.  Neither depends on any
 //     other row of the chunk.  The rest are "active".
@@ -1003,71 +1020,52 @@ __device__ void resolve_sequential(const ResolveArgs& a, volatile uint8_t* st, i
 //     list keeps the row.  A decision is taken only once every earlier
 //     candidate is decided, so it is the one the sequential walk takes, and
 //     the lowest undecided row can always decide, so the rounds end.
-//  D. Kept rows get consecutive store positions in arrival order.
-__global__ __launch_bounds__(kResolveThreads) void k_resolve(ResolveArgs a) {
-  __shared__ uint8_t st_[kChunk];        // 0 undecided, 1 kept, 2 dropped
-  __shared__ uint16_t edges[kEdgeCap];
-  __shared__ uint32_t eoff[kChunk];
-  __shared__ uint16_t elen[kChunk];
-  __shared__ uint16_t ecur[kChunk];
-  __shared__ uint16_t active[kChunk];
-  __shared__ uint32_t n_active, n_edges, pending;
-  __shared__ int wsum[kResolveThreads / 64];
-  volatile uint8_t* st = st_;
+//  D. Kept rows get consecutive store positions from m0, in arrival order;
+//     L.total is the number kept among the n rows.
+// The first phase's loads (hits and edge flags) are issued by the caller
+// with the others that open its kernel; hit_r / edge_r hold rows
+// tid + u T.  Returns with every thread past a barrier.
+template <int T>
+__device__ void resolve_core(const ResolveArgs& a, ResolveLds& L, int n, int m0, const int32_t (&hit_r)[kChunk / T],
+                             const uint32_t (&edge_r)[kChunk / T]) {
+  volatile uint8_t* st = L.st;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  // A. the first phase's loads (hits and edge flags of this thread's rows, the
-  //    status words, the store's counts) are all issued before any is used
-  constexpr int kRowsPerThread = kChunk / kResolveThreads;
-  int32_t hit_r[kRowsPerThread];
-  uint32_t edge_r[kRowsPerThread];
-#pragma unroll
-  for (int u = 0; u < kRowsPerThread; ++u) {
-    const int r = min(tid + u * kResolveThreads, a.nB - 1);
-    hit_r[u] = a.firstHit[r];
-    edge_r[u] = a.hasEdge[r];
-  }
-  const bool skip = skip_all(a.flags);
-  const int m0 = a.meta->m;
-  const int64_t gbase = a.meta->n_seen + a.c0;   // updated only at the end of a call
-  if (skip) return;   // (the status words do not change while this single workgroup runs)
   if (tid == 0) {
-    n_active = 0u;
-    n_edges = 0u;
+    L.n_active = 0u;
+    L.n_edges = 0u;
   }
   __syncthreads();
 #pragma unroll
-  for (int u = 0; u < kRowsPerThread; ++u) {
-    const int r = tid + u * kResolveThreads;
-    if (r >= a.nB) break;
+  for (int u = 0; u < kChunk / T; ++u) {
+    const int r = tid + u * T;
+    if (r >= n) break;
     const int32_t hit = hit_r[u];
     if (hit != kNone) {
       st[r] = 2;
-      a.rep[r] = a.store_ids[hit];
-      a.rep_row[r] = hit;
+      L.rrow[r] = hit;
     } else if (edge_r[u] == 0u) {
       st[r] = 1;
-      a.rep[r] = -1;
-      a.rep_row[r] = -1;
+      L.rrow[r] = -1;
     } else {
       st[r] = 0;
-      active[atomicAdd(&n_active, 1u)] = (uint16_t)r;
+      L.active[atomicAdd(&L.n_active, 1u)] = (uint16_t)r;
     }
   }
   __syncthreads();
-  const int na = (int)n_active;
+  const int na = (int)L.n_active;
   // B. A row's bitmap words (bits j < i) are read by G lanes, G = W rounded up
   //    to a power of two, so a wave covers 64 / G rows at once; four such sets
   //    are loaded before any is used, which keeps several loads in flight.
   const int G = a.W <= 1 ? 1 : 1 << (32 - __clz(a.W - 1));
   const int sub = lane / G, wl = lane % G;
-  const int rstep = (kResolveThreads / 64) * (64 / G);
+  const int rstep = (T / 64) * (64 / G);
   for (int kb = wave * (64 / G); kb < na; kb += 4 * rstep) {
     uint64_t e[4];
     int ir[4];
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
       const int k = kb + u * rstep + sub;
-      ir[u] = k < na ? (int)active[k] : -1;
+      ir[u] = k < na ? (int)L.active[k] : -1;
       const int nw = (ir[u] + 63) >> 6;
       e[u] = (ir[u] >= 0 && wl < nw) ? a.bitmap[(int64_t)ir[u] * a.W + wl] : 0ull;
     }
@@ -1082,70 +1080,68 @@ __global__ __launch_bounds__(kResolveThreads) void k_resolve(ResolveArgs a) {
       }
       const int tot = __shfl(incl, sub * G + G - 1);
       uint32_t base = 0u;
-      if (wl == 0 && ir[u] >= 0) base = atomicAdd(&n_edges, (uint32_t)tot);
+      if (wl == 0 && ir[u] >= 0) base = atomicAdd(&L.n_edges, (uint32_t)tot);
       base = __shfl(base, sub * G);
       if (ir[u] >= 0) {
         if (base + (uint32_t)tot <= (uint32_t)kEdgeCap) {
           uint32_t p = base + (uint32_t)(incl - c);
           while (eu) {
-            edges[p++] = (uint16_t)(wl * 64 + __builtin_ctzll(eu));
+            L.edges[p++] = (uint16_t)(wl * 64 + __builtin_ctzll(eu));
             eu &= eu - 1ull;
           }
         }
         if (wl == 0) {
-          eoff[ir[u]] = base;
-          elen[ir[u]] = (uint16_t)tot;
-          ecur[ir[u]] = 0;
+          L.eoff[ir[u]] = base;
+          L.elen[ir[u]] = (uint16_t)tot;
+          L.ecur[ir[u]] = 0;
         }
       }
     }
   }
   __syncthreads();
-  if (n_edges > (uint32_t)kEdgeCap) {
-    if (wave == 0) resolve_sequential(a, st, gbase);
+  if (L.n_edges > (uint32_t)kEdgeCap) {
+    if (wave == 0) resolve_sequential(a, L, n);
   } else {
     for (;;) {
-      if (tid == 0) pending = 0u;
+      if (tid == 0) L.pending = 0u;
       __syncthreads();
-      for (int k = tid; k < na; k += kResolveThreads) {
-        const int i = active[k];
+      for (int k = tid; k < na; k += T) {
+        const int i = L.active[k];
         if (st[i] != 0) continue;
-        const int L = elen[i];
-        const uint32_t b0 = eoff[i];
-        int p = ecur[i];
+        const int len = L.elen[i];
+        const uint32_t b0 = L.eoff[i];
+        int p = L.ecur[i];
         int dec = -1;   // -1 wait, 0 keep, 1 drop
         int j = -1;
-        for (; p < L; ++p) {
-          j = edges[b0 + p];
+        for (; p < len; ++p) {
+          j = L.edges[b0 + p];
           const uint8_t s = st[j];
           if (s == 2) continue;
           dec = (s == 1) ? 1 : -1;
           break;
         }
-        if (p == L) dec = 0;
-        ecur[i] = (uint16_t)p;
+        if (p == len) dec = 0;
+        L.ecur[i] = (uint16_t)p;
         if (dec == 1) {
           st[i] = 2;
-          a.rep[i] = gbase + j;
-          a.rep_row[i] = -(j + 2);
+          L.rrow[i] = -(j + 2);
         } else if (dec == 0) {
           st[i] = 1;
-          a.rep[i] = -1;
-          a.rep_row[i] = -1;
+          L.rrow[i] = -1;
         } else {
-          pending = 1u;
+          L.pending = 1u;
         }
       }
       __syncthreads();
-      const bool done = pending == 0u;
+      const bool done = L.pending == 0u;
       __syncthreads();
       if (done) break;
     }
   }
   __syncthreads();
-  // D. store positions: exclusive scan of kept flags, 4 rows per thread
-  const int per = (a.nB + kResolveThreads - 1) / kResolveThreads;
-  const int r0 = tid * per, r1 = min(a.nB, r0 + per);
+  // D. store positions: exclusive scan of kept flags, whole rows per thread
+  const int per = (n + T - 1) / T;
+  const int r0 = tid * per, r1 = min(n, r0 + per);
   int c = 0;
   for (int r = r0; r < r1; ++r) c += (st[r] == 1) ? 1 : 0;
   int x = c;
@@ -1153,29 +1149,58 @@ __global__ __launch_bounds__(kResolveThreads) void k_resolve(ResolveArgs a) {
     const int t = __shfl_up(x, o);
     if (lane >= o) x += t;
   }
-  if (lane == 63) wsum[wave] = x;
+  if (lane == 63) L.wsum[wave] = x;
   __syncthreads();
   if (tid == 0) {
     int acc = 0;
-    for (int w = 0; w < kResolveThreads / 64; ++w) {
-      const int t = wsum[w];
-      wsum[w] = acc;
+    for (int w = 0; w < T / 64; ++w) {
+      const int t = L.wsum[w];
+      L.wsum[w] = acc;
       acc += t;
     }
-    n_active = (uint32_t)acc;   // reused: kept rows of the chunk
+    L.total = (uint32_t)acc;
   }
   __syncthreads();
-  int pos = m0 + wsum[wave] + x - c;
-  for (int r = r0; r < r1; ++r) a.pos[r] = (st[r] == 1) ? pos++ : -1;
+  int pos = m0 + L.wsum[wave] + x - c;
+  for (int r = r0; r < r1; ++r) L.posv[r] = (st[r] == 1) ? pos++ : -1;
+  __syncthreads();
+}
+
+// The resolve as a kernel of its own (one workgroup): decisions to rep, pos,
+// rep_row and the kept mask in global memory, the store size advanced.
+__global__ __launch_bounds__(kResolveThreads) void k_resolve(ResolveArgs a) {
+  __shared__ ResolveLds L;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // the first phase's loads (hits and edge flags of this thread's rows, the
+  // status words, the store's counts) are all issued before any is used
+  constexpr int kRowsPerThread = kChunk / kResolveThreads;
+  int32_t hit_r[kRowsPerThread];
+  uint32_t edge_r[kRowsPerThread];
+#pragma unroll
+  for (int u = 0; u < kRowsPerThread; ++u) {
+    const int r = min(tid + u * kResolveThreads, a.nB - 1);
+    hit_r[u] = a.firstHit[r];
+    edge_r[u] = a.hasEdge[r];
+  }
+  const bool skip = skip_all(a.flags);
+  const int m0 = a.meta->m;
+  const int64_t gbase = a.meta->n_seen + a.c0;   // updated only at the end of a call
+  if (skip) return;   // (the status words do not change while this single workgroup runs)
+  resolve_core<kResolveThreads>(a, L, a.nB, m0, hit_r, edge_r);
+  for (int r = tid; r < a.nB; r += kResolveThreads) {
+    const int32_t rr = L.rrow[r];
+    a.rep[r] = rr >= 0 ? a.store_ids[rr] : (rr == -1 ? -1 : gbase + (-rr - 2));
+    a.rep_row[r] = rr;
+    a.pos[r] = L.posv[r];
+  }
   for (int w = wave; w < 64; w += kResolveThreads / 64) {
     const int r = w * 64 + lane;
-    const uint64_t b = __ballot(r < a.nB && st[r] == 1);
+    const uint64_t b = __ballot(r < a.nB && L.st[r] == 1);
     if (lane == 0) a.kept_words[w] = b;
   }
   if (tid == 0) {
-    const int total = (int)n_active;
-    a.meta->m = m0 + total;
-    atomicAdd(&a.flags->n_kept, (uint32_t)total);
+    a.meta->m = m0 + (int)L.total;
+    atomicAdd(&a.flags->n_kept, L.total);
   }
 }
 
@@ -1203,104 +1228,103 @@ struct AppendArgs {
   DevFlags* flags_out;      // host-mapped copy of the status words, or NULL
 };
 
-// One wave per row, four rows per workgroup.  Kept rows are copied into the
-// store; for dropped rows ||x - x_rep||^2 is formed in binary64 (fixed order)
-// and the workgroup's maximum goes to the measured bound with one atomic.
-constexpr int kAppendRows = 4;
-
+constexpr int kAppendRows = 4;  // rows per workgroup of k_append (one wave each)
 constexpr int kAppendVec = 4;   // float4 of a row per lane held in registers (D <= 1,024)
 
-__global__ __launch_bounds__(256) void k_append(AppendArgs a, int nB) {
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
-  const int r = (int)blockIdx.x * kAppendRows + wave;   // one row per wave
-  const int rc = min(r, nB - 1);
-  // Every load that depends on no other is issued before any is used: the
-  // row's decision, its terms, the status words, the arrival count and (for
-  // D <= 1,024) the row itself through a buffer resource (zeros past the row).
-  const int p = a.pos[rc];
-  const int rr = a.rep_row[rc];
-  const float hn = a.hnc[rc], et = a.etc[rc];
-  const bool skip = skip_all(a.flags);
-  // every workgroup reads n_seen before the last one (below) advances it
-  const int64_t gbase = a.meta->n_seen + a.c0;
-  const uint32_t am0 = a.meta->absmax_bits, hm0 = a.meta->hnmax_bits;   // the store's maxima so far
-  const float* src = a.xc + (int64_t)rc * a.D;
+// Loads row r of the chunk into registers (D <= 1,024: the whole row, zeros
+// past it, through a buffer resource; otherwise nothing, and append_row reads
+// the row itself).
+__device__ __forceinline__ void append_load(const AppendArgs& a, int r, float4 (&v)[kAppendVec]) {
   const bool vec = a.D <= 256 * kAppendVec;
-  float4 v[kAppendVec];
-  {
-    const __amdgpu_buffer_rsrc_t rs = f32_rsrc(src, vec ? a.D : 0);
+  const int lane = threadIdx.x & 63;
+  const __amdgpu_buffer_rsrc_t rs = f32_rsrc(a.xc + (int64_t)r * a.D, vec ? a.D : 0);
 #pragma unroll
-    for (int u = 0; u < kAppendVec; ++u)
-      v[u] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(rs, (uint32_t)(u * 256 + lane * 4) * 4u, 0, 0));
-  }
-  double dmax = 0.0;
-  uint32_t amax = 0u, hmax = 0u;   // |x| and hn of a kept row (float bits, non-negative)
-  if (!skip && r < nB) {
-    if (p >= 0) {
-      float* dst = a.xs + (int64_t)p * a.D;
-      _Float16* d16 = a.x16s + (int64_t)p * a.D;
-      hmax = __float_as_uint(hn);
-      auto absbits = [](const float4& x) {
-        return max(max(__float_as_uint(x.x) & 0x7fffffffu, __float_as_uint(x.y) & 0x7fffffffu),
-                   max(__float_as_uint(x.z) & 0x7fffffffu, __float_as_uint(x.w) & 0x7fffffffu));
-      };
-      if (vec) {
-        // the fp16 operand is formed as the prep forms it, fl16(2^8 x)
+  for (int u = 0; u < kAppendVec; ++u)
+    v[u] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(rs, (uint32_t)(u * 256 + lane * 4) * 4u, 0, 0));
+}
+
+// One wave's work for chunk row r (its data in v, from append_load): a kept
+// row (store position p >= 0) is copied into the store, with its terms and
+// global id, and raises amax / hmax (|x| and ||x||^2 / 2 as float bits); for a
+// dropped row ||x - x_rep||^2 (rr: the representative as rep_row encodes it)
+// is summed in binary64 in a fixed order into dmax (every lane).
+__device__ __forceinline__ void append_row(const AppendArgs& a, int r, int p, int rr, float hn, float et,
+                                           int64_t gbase, const float4 (&v)[kAppendVec], double& dmax,
+                                           uint32_t& amax, uint32_t& hmax) {
+  const int lane = threadIdx.x & 63;
+  const bool vec = a.D <= 256 * kAppendVec;
+  const float* src = a.xc + (int64_t)r * a.D;
+  if (p >= 0) {
+    float* dst = a.xs + (int64_t)p * a.D;
+    _Float16* d16 = a.x16s + (int64_t)p * a.D;
+    hmax = max(hmax, __float_as_uint(hn));
+    auto absbits = [](const float4& x) {
+      return max(max(__float_as_uint(x.x) & 0x7fffffffu, __float_as_uint(x.y) & 0x7fffffffu),
+                 max(__float_as_uint(x.z) & 0x7fffffffu, __float_as_uint(x.w) & 0x7fffffffu));
+    };
+    if (vec) {
+      // the fp16 operand is formed as the prep forms it, fl16(2^8 x)
 #pragma unroll
-        for (int u = 0; u < kAppendVec; ++u) {
-          const int d = u * 256 + lane * 4;
-          if (d >= a.D) break;
-          amax = max(amax, absbits(v[u]));
-          *reinterpret_cast<float4*>(dst + d) = v[u];
-          const _Float16 h[4] = {(_Float16)(v[u].x * kScale), (_Float16)(v[u].y * kScale),
-                                 (_Float16)(v[u].z * kScale), (_Float16)(v[u].w * kScale)};
-          uint2 packed;
-          __builtin_memcpy(&packed, h, 8);
-          *reinterpret_cast<uint2*>(d16 + d) = packed;
-        }
-      } else {
-        for (int d = lane * 4; d < a.D; d += 256) {
-          const float4 x = *reinterpret_cast<const float4*>(src + d);
-          amax = max(amax, absbits(x));
-          *reinterpret_cast<float4*>(dst + d) = x;
-        }
-        const _Float16* s16 = a.x16c + (int64_t)r * a.D;
-        for (int d = lane * 8; d < a.D; d += 512)
-          *reinterpret_cast<uint4*>(d16 + d) = *reinterpret_cast<const uint4*>(s16 + d);
-      }
-      if (lane == 0) {
-        a.hns[p] = hn;
-        a.ets[p] = et;
-        a.ids[p] = gbase + r;
+      for (int u = 0; u < kAppendVec; ++u) {
+        const int d = u * 256 + lane * 4;
+        if (d >= a.D) break;
+        amax = max(amax, absbits(v[u]));
+        *reinterpret_cast<float4*>(dst + d) = v[u];
+        const _Float16 h[4] = {(_Float16)(v[u].x * kScale), (_Float16)(v[u].y * kScale),
+                               (_Float16)(v[u].z * kScale), (_Float16)(v[u].w * kScale)};
+        uint2 packed;
+        __builtin_memcpy(&packed, h, 8);
+        *reinterpret_cast<uint2*>(d16 + d) = packed;
       }
     } else {
-      const float* b = (rr >= 0) ? a.xs + (int64_t)rr * a.D : a.xc + (int64_t)(-rr - 2) * a.D;
-      double s = 0.0;
-      auto acc4 = [&](const float4& x, const float4& y) {
-        const double t0 = (double)x.x - (double)y.x, t1 = (double)x.y - (double)y.y;
-        const double t2 = (double)x.z - (double)y.z, t3 = (double)x.w - (double)y.w;
-        s = fma(t0, t0, s);
-        s = fma(t1, t1, s);
-        s = fma(t2, t2, s);
-        s = fma(t3, t3, s);
-      };
-      if (vec) {
-        const __amdgpu_buffer_rsrc_t rb = f32_rsrc(b, a.D);
-#pragma unroll
-        for (int u = 0; u < kAppendVec; ++u)
-          acc4(v[u], __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(
-                                                    rb, (uint32_t)(u * 256 + lane * 4) * 4u, 0, 0)));
-      } else {
-        for (int d = lane * 4; d < a.D; d += 256)
-          acc4(*reinterpret_cast<const float4*>(src + d), *reinterpret_cast<const float4*>(b + d));
+      for (int d = lane * 4; d < a.D; d += 256) {
+        const float4 x = *reinterpret_cast<const float4*>(src + d);
+        amax = max(amax, absbits(x));
+        *reinterpret_cast<float4*>(dst + d) = x;
       }
-      dmax = wave_sum_f64(s);
+      const _Float16* s16 = a.x16c + (int64_t)r * a.D;
+      for (int d = lane * 8; d < a.D; d += 512)
+        *reinterpret_cast<uint4*>(d16 + d) = *reinterpret_cast<const uint4*>(s16 + d);
     }
+    if (lane == 0) {
+      a.hns[p] = hn;
+      a.ets[p] = et;
+      a.ids[p] = gbase + r;
+    }
+  } else {
+    const float* b = (rr >= 0) ? a.xs + (int64_t)rr * a.D : a.xc + (int64_t)(-rr - 2) * a.D;
+    double s = 0.0;
+    auto acc4 = [&](const float4& x, const float4& y) {
+      const double t0 = (double)x.x - (double)y.x, t1 = (double)x.y - (double)y.y;
+      const double t2 = (double)x.z - (double)y.z, t3 = (double)x.w - (double)y.w;
+      s = fma(t0, t0, s);
+      s = fma(t1, t1, s);
+      s = fma(t2, t2, s);
+      s = fma(t3, t3, s);
+    };
+    if (vec) {
+      const __amdgpu_buffer_rsrc_t rb = f32_rsrc(b, a.D);
+#pragma unroll
+      for (int u = 0; u < kAppendVec; ++u)
+        acc4(v[u], __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(
+                                                  rb, (uint32_t)(u * 256 + lane * 4) * 4u, 0, 0)));
+    } else {
+      for (int d = lane * 4; d < a.D; d += 256)
+        acc4(*reinterpret_cast<const float4*>(src + d), *reinterpret_cast<const float4*>(b + d));
+    }
+    dmax = fmax(dmax, wave_sum_f64(s));
   }
+}
+
+// A workgroup's maxima go to the status words and the store's bookkeeping
+// (one atomic each, only when they rise); am0 / hm0: the store's maxima as the
+// workgroup read them at its start.  parts: 3 x kWaves words of LDS.
+template <int kWaves>
+__device__ __forceinline__ void append_maxima(const AppendArgs& a, double dmax, uint32_t amax, uint32_t hmax,
+                                              uint32_t am0, uint32_t hm0, double* part, uint32_t* apart,
+                                              uint32_t* hpart) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   for (int o = 32; o > 0; o >>= 1) amax = max(amax, (uint32_t)__shfl_xor((int)amax, o));
-  __shared__ double part[4];
-  __shared__ uint32_t apart[4], hpart[4];
   if (lane == 0) {
     part[wave] = dmax;
     apart[wave] = amax;
@@ -1308,36 +1332,53 @@ __global__ __launch_bounds__(256) void k_append(AppendArgs a, int nB) {
   }
   __syncthreads();
   if (threadIdx.x == 0) {
-    const double m = fmax(fmax(part[0], part[1]), fmax(part[2], part[3]));
+    double m = part[0];
+    uint32_t am = apart[0], hm = hpart[0];
+    for (int w = 1; w < kWaves; ++w) {
+      m = fmax(m, part[w]);
+      am = max(am, apart[w]);
+      hm = max(hm, hpart[w]);
+    }
     if (m > 0.0)
       atomicMax(reinterpret_cast<unsigned long long*>(&a.flags->dhat2_bits),
                 (unsigned long long)__double_as_longlong(m));
     // the store's maxima: rows are appended only by calls that go through
     // (skip is uniform over the call), so an invalid call leaves them as they were
-    const uint32_t am = max(max(apart[0], apart[1]), max(apart[2], apart[3]));
-    const uint32_t hm = max(max(hpart[0], hpart[1]), max(hpart[2], hpart[3]));
     if (am > am0) atomicMax(&a.meta->absmax_bits, am);
     if (hm > hm0) atomicMax(&a.meta->hnmax_bits, hm);
-    // This workgroup is counted below only once its maximum has been
+    // This workgroup is counted (append_finish) only once its maxima have been
     // performed: the wait covers the atomics issued above.  Device-scope
     // atomics are performed where every XCD sees them, so the last workgroup,
     // which reads the status words with device-scope atomic loads, needs no
     // cache write-back or invalidation (fences here cost 1.7 us per call).
     __builtin_amdgcn_s_waitcnt(0);
   }
-  if (!a.last_chunk) return;
-  // The last workgroup to finish folds the call into the store's bookkeeping
-  // (arrival count and delta_hat if the call went through, an error count if
-  // its input was invalid), copies the status words to host memory when asked,
-  // and clears them for the next call.  The only words of this launch it reads
-  // are the status words' maxima, updated by atomics that each workgroup has
-  // waited for before its count (above); everything else it reads was written
-  // by earlier launches.
+}
+
+// The last workgroup to finish (counted in cc->blocks_done) runs `last_work`
+// (thread 0), and on the call's last chunk folds the call into the store's
+// bookkeeping (arrival count and delta_hat if the call went through, an error
+// count if its input was invalid), copies the status words to host memory
+// when asked, and clears them for the next call.  The only words of this
+// launch it reads are the status words' maxima, updated by atomics that each
+// workgroup has waited for before its count; everything else it reads was
+// written by earlier launches.  Called by every thread of every workgroup.
+template <class F>
+__device__ __forceinline__ void append_finish(const AppendArgs& a, bool count_every_chunk, F&& last_work) {
+  if (!a.last_chunk && !count_every_chunk) return;
   __shared__ bool last;
   __syncthreads();
   if (threadIdx.x == 0) last = atomicAdd(&a.cc->blocks_done, 1u) == gridDim.x - 1;
   __syncthreads();
   if (!last) return;
+  if (threadIdx.x == 0) {
+    last_work();
+    __builtin_amdgcn_s_waitcnt(0);   // its atomics are performed before the words are read below
+  }
+  if (!a.last_chunk) {
+    if (threadIdx.x == 0) a.cc->blocks_done = 0u;
+    return;
+  }
   constexpr int kWords = (int)(sizeof(DevFlags) / 4);
   uint32_t* f = reinterpret_cast<uint32_t*>(a.flags);
   if (threadIdx.x == 0) {
@@ -1355,6 +1396,7 @@ __global__ __launch_bounds__(256) void k_append(AppendArgs a, int nB) {
       if (d2 > a.meta->dhat2_bits) a.meta->dhat2_bits = d2;   // non-negative doubles order as their bits
     }
   }
+  __syncthreads();
   if ((int)threadIdx.x < kWords) {
     const uint32_t v = __hip_atomic_load(f + threadIdx.x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     if (a.flags_out) reinterpret_cast<uint32_t*>(a.flags_out)[threadIdx.x] = v;
@@ -1362,6 +1404,111 @@ __global__ __launch_bounds__(256) void k_append(AppendArgs a, int nB) {
   __syncthreads();
   if ((int)threadIdx.x < kWords) f[threadIdx.x] = 0u;
   if (threadIdx.x == 0) a.cc->blocks_done = 0u;
+}
+
+// One wave per row, four rows per workgroup, decisions from k_resolve.  Kept
+// rows are copied into the store; for dropped rows ||x - x_rep||^2 is formed
+// in binary64 (fixed order) and the workgroup's maximum goes to the measured
+// bound with one atomic.
+__global__ __launch_bounds__(256) void k_append(AppendArgs a, int nB) {
+  const int wave = threadIdx.x >> 6;
+  const int r = (int)blockIdx.x * kAppendRows + wave;   // one row per wave
+  const int rc = min(r, nB - 1);
+  // Every load that depends on no other is issued before any is used: the
+  // row's decision, its terms, the status words, the arrival count and (for
+  // D <= 1,024) the row itself through a buffer resource (zeros past the row).
+  const int p = a.pos[rc];
+  const int rr = a.rep_row[rc];
+  const float hn = a.hnc[rc], et = a.etc[rc];
+  const bool skip = skip_all(a.flags);
+  // every workgroup reads n_seen before the last one (below) advances it
+  const int64_t gbase = a.meta->n_seen + a.c0;
+  const uint32_t am0 = a.meta->absmax_bits, hm0 = a.meta->hnmax_bits;   // the store's maxima so far
+  float4 v[kAppendVec];
+  append_load(a, rc, v);
+  double dmax = 0.0;
+  uint32_t amax = 0u, hmax = 0u;
+  if (!skip && r < nB) append_row(a, r, p, rr, hn, et, gbase, v, dmax, amax, hmax);
+  __shared__ double part[4];
+  __shared__ uint32_t apart[4], hpart[4];
+  append_maxima<4>(a, dmax, amax, hmax, am0, hm0, part, apart, hpart);
+  append_finish(a, false, [] {});
+}
+
+// The in-chunk resolve and the append in one launch.  Workgroup b appends
+// rows [16 b, 16 b + 16) of the chunk, one wave per row; it first resolves,
+// in its own LDS, every row up to its last one (a decision depends only on
+// earlier rows: those with a store hit or without in-chunk candidates are
+// immediate, the rest take a few rounds).  This saves a launch and the
+// decisions' round trip through global memory.  Every workgroup reads the
+// store size at its start and adds its own kept count to the chunk's; the
+// last one to finish advances the store size.
+constexpr int kAppendGroupThreads = kResolveThreads;
+constexpr int kAppendGroupRows = kAppendGroupThreads / 64;
+
+__global__ __launch_bounds__(kAppendGroupThreads) void k_resolve_append(ResolveArgs ra, AppendArgs a, int nB,
+                                                                         float* max_cos,
+                                                                         const uint32_t* maxcos_store,
+                                                                         const float* G) {
+  __shared__ ResolveLds L;
+  constexpr int T = kAppendGroupThreads;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int r = (int)blockIdx.x * kAppendGroupRows + wave;   // this wave's row
+  const int rc = min(r, nB - 1);
+  const int nres = min(nB, ((int)blockIdx.x + 1) * kAppendGroupRows);   // rows this workgroup resolves
+  // every load that depends on no other first: hits and edge flags of the
+  // rows resolved here, the status words, the store's counts, and this
+  // wave's row with its terms
+  constexpr int kRowsPerThread = kChunk / T;
+  int32_t hit_r[kRowsPerThread];
+  uint32_t edge_r[kRowsPerThread];
+#pragma unroll
+  for (int u = 0; u < kRowsPerThread; ++u) {
+    const int q = tid + u * T;
+    hit_r[u] = q < nres ? ra.firstHit[q] : kNone;
+    edge_r[u] = q < nres ? ra.hasEdge[q] : 0u;
+  }
+  const bool skip = skip_all(a.flags);
+  const int m0 = a.meta->m;
+  const int64_t gbase = a.meta->n_seen + a.c0;
+  const uint32_t am0 = a.meta->absmax_bits, hm0 = a.meta->hnmax_bits;
+  const float hn = a.hnc[rc], et = a.etc[rc];
+  float4 v[kAppendVec];
+  append_load(a, rc, v);
+  double dmax = 0.0;
+  uint32_t amax = 0u, hmax = 0u;
+  uint32_t kept_here = 0u;
+  if (!skip) {   // (uniform: the status words do not change during this launch)
+    resolve_core<T>(ra, L, nres, m0, hit_r, edge_r);
+    if (r < nB) {
+      const int rr = L.rrow[r];
+      if (lane == 0) ra.rep[r] = rr >= 0 ? ra.store_ids[rr] : (rr == -1 ? -1 : gbase + (-rr - 2));
+      append_row(a, r, L.posv[r], rr, hn, et, gbase, v, dmax, amax, hmax);
+      if (max_cos) {
+        // the largest cosine over the store (from the screen) and over the
+        // kept chunk rows before this one
+        float mc = ord2f(maxcos_store[r]);
+        for (int j = lane; j < r; j += 64)
+          if (L.st[j] == 1) mc = fmaxf(mc, G[(int64_t)r * nB + j]);
+        for (int o = 32; o > 0; o >>= 1) mc = fmaxf(mc, __shfl_xor(mc, o));
+        if (lane == 0) max_cos[r] = mc;
+      }
+    }
+    // kept rows among this workgroup's own
+    const int first = (int)blockIdx.x * kAppendGroupRows;
+    const uint64_t k = __ballot(lane < nres - first && L.st[first + lane] == 1);
+    kept_here = (uint32_t)__popcll(k);
+  }
+  if (tid == 0 && kept_here) atomicAdd(&a.cc->kept, kept_here);   // waited for in append_maxima
+  __shared__ double part[T / 64];
+  __shared__ uint32_t apart[T / 64], hpart[T / 64];
+  append_maxima<T / 64>(a, dmax, amax, hmax, am0, hm0, part, apart, hpart);
+  append_finish(a, true, [&] {
+    if (skip) return;
+    const uint32_t total = __hip_atomic_load(&a.cc->kept, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    a.meta->m = m0 + (int)total;
+    atomicAdd(&a.flags->n_kept, total);
+  });
 }
 
 // ------------------------------------------------------------------ max cos
@@ -1738,6 +1885,18 @@ lam_status dedup_ingest(lam_ctx* ctx, lam_store* st, const float* x, int64_t n, 
       }
       ResolveArgs ra{nB, W, firstHit, hasEdge, bitmap, st->ids, meta, c0, rep + c0, pos, rep_row, kept_words,
                      ctx->flags_dev};
+      AppendArgs aa{xc, x16, hnc + c0, etc + c0, pos, rep_row, c0, D, st->x32, st->x16, st->hn, st->et, st->ids,
+                    ctx->flags_dev, cc, meta, n, last_chunk ? 1 : 0, async ? 1 : 0,
+                    (last_chunk && !async) ? ctx->flags_host_dev : nullptr};
+      if (!lsh) {
+        // resolve, largest cosines and append in one launch
+        ProfScope ps(ctx, "dedup_resolve_append");
+        hipLaunchKernelGGL(k_resolve_append, dim3((unsigned)((nB + kAppendGroupRows - 1) / kAppendGroupRows)),
+                           dim3(kAppendGroupThreads), 0, ctx->stream, ra, aa, nB, want_max ? max_cos + c0 : nullptr,
+                           maxcos, G);
+        LAM_HIP(hipGetLastError());
+        continue;
+      }
       {
         ProfScope ps(ctx, "dedup_resolve");
         hipLaunchKernelGGL(k_resolve, dim3(1), dim3(kResolveThreads), 0, ctx->stream, ra);
@@ -1756,9 +1915,6 @@ lam_status dedup_ingest(lam_ctx* ctx, lam_store* st, const float* x, int64_t n, 
                            ctx->stream, la, pos, st->lsh_key, st->lsh_head, st->lsh_next, st->lsh_rowkey);
         LAM_HIP(hipGetLastError());
       }
-      AppendArgs aa{xc, x16, hnc + c0, etc + c0, pos, rep_row, c0, D, st->x32, st->x16, st->hn, st->et, st->ids,
-                    ctx->flags_dev, cc, meta, n, last_chunk ? 1 : 0, async ? 1 : 0,
-                    (last_chunk && !async) ? ctx->flags_host_dev : nullptr};
       {
         ProfScope ps(ctx, "dedup_append");
         hipLaunchKernelGGL(k_append, dim3((unsigned)((nB + kAppendRows - 1) / kAppendRows)), dim3(256), 0,
