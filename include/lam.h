@@ -252,11 +252,16 @@ lam_status lam_store_export(lam_ctx* ctx, const lam_store* store, int64_t* ids_d
  * these scores give).  Per query the k best by (score desc, id asc) go to scores_dev and
  * ids_dev (nq x k, row-major), padded with (-inf, -1) past the store size.
  * bound_dev (optional): eps * ||q_j||_1 rounded up to float32.
- * 1 <= k <= 64.  ESTATE if the store is not quantized (or has rows added
- * since), or if its codes are wider than 12 bits (the scorer multiplies codes
- * as exact float16 values; quantize with a larger eps, e.g. 12 bits hold
- * absmax / (2 eps) < 2,047.5).  A query row holding NaN/Inf gets (NaN, -1) in
- * all k slots and a NaN bound instead of an error status.  Asynchronous. */
+ * 1 <= k <= 64.  Codes of up to 12 bits are multiplied as exact float16
+ * values; codes of 13 to 22 bits are scored in a split form, each code c as
+ * the two 12-bit parts c >> 11 and c & 2047 against the query scaled by 2^11
+ * and the query itself (the same scores; twice the matrix work, 3 dim bytes
+ * per stored row and 8 dim bytes per query of context scratch; a query with
+ * |q| * 2^11 beyond float32 range counts as holding Inf).  ESTATE if the
+ * store is not quantized (or has rows added since), or if its codes are wider
+ * than 22 bits (quantize with a larger eps: 22 bits hold absmax / (2 eps) <
+ * 2,097,151.5).  A query row holding NaN/Inf gets (NaN, -1) in all k slots
+ * and a NaN bound instead of an error status.  Asynchronous. */
 lam_status lam_score_topk(lam_ctx* ctx, const lam_store* store, const float* q_dev, int64_t nq,
                           int32_t k, float* scores_dev, int64_t* ids_dev, float* bound_dev);
 
@@ -265,7 +270,9 @@ lam_status lam_score_topk(lam_ctx* ctx, const lam_store* store, const float* q_d
  * lam_score_topk with every scratch buffer taken from a fixed 32 MiB array
  * that each device holds from the library's load until the process ends (set
  * up by lam_ctx_create); the call itself allocates nothing.  Results equal
- * lam_score_topk's.  Limits: nq <= 256 (EINVAL beyond).  The store must be
+ * lam_score_topk's.  Limits: nq <= 256 (EINVAL beyond); codes of at most 12
+ * bits (ESTATE for wider ones, whose split form needs scratch in proportion
+ * to the store).  The store must be
  * quantized and settled: ESTATE while ingest calls that did not wait are in
  * flight (lam_store_get_info settles them) -- settling can need the host.
  * Every call on one device shares that device's array: calls that overlap on

@@ -52,7 +52,9 @@ constexpr int kScratchCertify = 13;      // top-(k+1) lists of the certified sco
 constexpr int kScratchBlocks = 14;       // block codec: row word counts and scan sums
 constexpr int kScratchExpand = 15;       // block codec: codes expanded back to the b-bit stream for scoring
 constexpr int kScratchLsh = 16;          // banded candidates: chunk keys and the chunk's own index
-constexpr int kScratchSlots = 17;
+constexpr int kScratchWideCodes = 17;    // scoring: wide codes in their split 12-bit form
+constexpr int kScratchWideQueries = 18;  // scoring: queries in the split form [2^11 q, q]
+constexpr int kScratchSlots = 19;
 
 struct DevBuf {
   void* p = nullptr;

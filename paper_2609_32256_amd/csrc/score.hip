@@ -4,6 +4,9 @@
 //
 // score(j, y) = s * sum_d q_j,d * code_y,d  (s = 2 eps), i.e. q_j . x_hat_y with
 // the exact dequantized row.  Codes of at most 12 bits are exact in fp16.
+// Codes of 13 to 22 bits are scored as a 12-bit store of 2D columns, each
+// code c split as 2^11 (c >> 11) + (c & 2047), against queries [2^11 q, q]:
+// the same score term by term (see widen).
 // Each query is scaled by a power of two 2^e_j (max |q| into [2^14, 2^15)) and
 // split into fp16 hi + lo parts, q 2^e = hi + lo + r with |r| <= 2^-22 |q 2^e|;
 // hi*code and lo*code are exact in fp32 and the MFMA accumulates in fp32.  The
@@ -60,9 +63,10 @@ __device__ __forceinline__ float rd32(double d) {
 
 // Per query: the hi/lo split and the meta block.  err bounds the difference
 // between a score from the hi part alone (H) and the rescored one (S), both
-// against T = s sum_d q_d code_d, in score units, with R >= ||x_hat_y|| for
-// every row y (R from the largest ||x||^2 / 2 of the store plus eps sqrt(D))
-// and h = hi 2^-e the query's hi part in its own units:
+// against T = s sum_d q_d code_d, in score units, with R >= s ||code_y|| for
+// every row y (row_norm_bound) and h = hi 2^-e the query's hi part in its own
+// units; the reported bound is eps times the l1 norm of columns [l1_from, D)
+// (all of them, except for the split form of wide codes):
 //   hi part:   |s sum_d (q_d - h_d) code_d| <= ||q - h||_2 R (Cauchy-Schwarz;
 //              ||q - h||_2 is computed here in binary64);
 //   fp32 sum:  g = 2 (D + 64) 2^-24 of s sum |h_d code_d| <= (||q|| + ||q - h||) R
@@ -71,7 +75,7 @@ __device__ __forceinline__ float rd32(double d) {
 //   S:         the rescoring sums in binary64 and rounds once to float32.
 // |H - S| <= |H - T| + |T - S| <= ||q - h|| R + (g + 2^-21)(||q|| + ||q - h||) R.
 __global__ __launch_bounds__(256) void k_score_prep(const float* __restrict__ q, int64_t nq, int D, double s,
-                                                    double eps, uint32_t hn_max,
+                                                    double eps, double R, int l1_from,
                                                     _Float16* __restrict__ qhi,
                                                     _Float16* __restrict__ qlo, QMeta* __restrict__ meta) {
   const int lane = threadIdx.x & 63;
@@ -94,24 +98,26 @@ __global__ __launch_bounds__(256) void k_score_prep(const float* __restrict__ q,
     for (int u = 0; u < kVec; ++u)
       v4[u] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(rs, (uint32_t)(u * 256 + lane * 4) * 4u, 0, 0));
   }
-  auto take1 = [&](float v) {
+  auto take1 = [&](float v, bool in_l1) {
     const float a = fabsf(v);
     bad |= !(a <= 3.402823466e38f);
     mx = fmaxf(mx, a);
-    l1 += (double)a;
+    l1 += in_l1 ? (double)a : 0.0;
     l2 = fma((double)v, (double)v, l2);
   };
   if (vec) {
 #pragma unroll
     for (int u = 0; u < kVec; ++u) {
-      if (u * 256 + lane * 4 >= D) break;
-      take1(v4[u].x);
-      take1(v4[u].y);
-      take1(v4[u].z);
-      take1(v4[u].w);
+      const int d = u * 256 + lane * 4;
+      if (d >= D) break;
+      const bool in = d >= l1_from;   // (l1_from is a multiple of 32)
+      take1(v4[u].x, in);
+      take1(v4[u].y, in);
+      take1(v4[u].z, in);
+      take1(v4[u].w, in);
     }
   } else {
-    for (int d = lane; d < D; d += 64) take1(p[d]);
+    for (int d = lane; d < D; d += 64) take1(p[d], d >= l1_from);
   }
   for (int o = 32; o > 0; o >>= 1) {
     mx = fmaxf(mx, __shfl_xor(mx, o));
@@ -160,8 +166,6 @@ __global__ __launch_bounds__(256) void k_score_prep(const float* __restrict__ q,
     m.osc = (float)ldexp(s, -e);
     m.bound = bad ? __builtin_nanf("") : ru32(eps * l1 * (1.0 + 0x1p-50));
     m.bad = bad ? 1 : 0;
-    const double R = sqrt(2.0 * (double)__uint_as_float(hn_max) * (1.0 + 0x1p-22)) * (1.0 + 0x1p-50) +
-                     eps * sqrt((double)D) * (1.0 + 0x1p-50);
     const double g = 2.0 * (double)(D + 64) * 0x1p-24;
     const double qn = sqrt(l2) * (1.0 + 0x1p-50);
     const double dh = sqrt(dh2) * (1.0 + 0x1p-50);
@@ -1060,6 +1064,130 @@ void plan_splits(int nqt, int64_t ntiles, int* splits, int64_t* tps, int max_spl
   *splits = (int)((ntiles + t - 1) / t);
 }
 
+// ---- codes of 13 to 22 bits
+// A code c of b bits is 2^11 (c >> 11) + (c & 2047) with |c >> 11| <= 2^(b-12)
+// <= 1,024 and 0 <= c & 2047 <= 2,047: both parts are 12-bit codes, exact in
+// fp16.  The split store has 2D columns, column d holding c_d >> 11 and column
+// D + d holding c_d & 2047; a query q becomes [2^11 q, q] (exact scalings), so
+// that s sum_d' q'_d' code'_d' = s sum_d q_d code_d term by term.
+constexpr int kWideMaxBits = 22;
+constexpr int kWideShift = 11;
+
+// One thread per 32 columns of a split row (12 words of 12-bit codes).
+__global__ __launch_bounds__(256) void k_wide_codes(const uint32_t* __restrict__ src, int64_t n, int D, int b,
+                                                    uint32_t* __restrict__ dst) {
+  const int G = 2 * D / 32;   // groups of 32 split columns per row
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (t >= n * G) return;
+  const int64_t row = t / G;
+  const int g = (int)(t - row * G);
+  const bool low = g >= D / 32;
+  const int d0 = (low ? g - D / 32 : g) * 32;
+  const uint32_t* w = src + row * ((int64_t)D * b / 32);
+  uint32_t o[12];
+#pragma unroll
+  for (int i = 0; i < 12; ++i) o[i] = 0u;
+#pragma unroll
+  for (int e = 0; e < 32; ++e) {
+    const int64_t bit = (int64_t)(d0 + e) * b;
+    const int wi = (int)(bit >> 5), off = (int)(bit & 31);
+    uint32_t u = w[wi] >> off;
+    if (off + b > 32) u |= w[wi + 1] << (32 - off);   // the code's bits lie inside the row
+    const int32_t c = (int32_t)(u << (32 - b)) >> (32 - b);
+    const uint32_t v = (uint32_t)(low ? (c & ((1 << kWideShift) - 1)) : (c >> kWideShift)) & 0xfffu;
+    const int ob = e * 12, ow = ob >> 5, oo = ob & 31;
+    o[ow] |= v << oo;
+    if (oo + 12 > 32) o[ow + 1] |= v >> (32 - oo);
+  }
+  uint32_t* out = dst + row * ((int64_t)2 * D * 12 / 32) + (int64_t)g * 12;
+#pragma unroll
+  for (int i = 0; i < 12; ++i) out[i] = o[i];
+}
+
+// q' = [2^11 q, q], one thread per element.
+__global__ __launch_bounds__(256) void k_wide_queries(const float* __restrict__ q, int64_t nq, int D,
+                                                      float* __restrict__ qw) {
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (t >= nq * 2 * D) return;
+  const int64_t j = t / (2 * D);
+  const int d = (int)(t - j * 2 * D);
+  qw[t] = d < D ? q[j * D + d] * (float)(1 << kWideShift) : q[j * D + d - D];
+}
+
+}  // namespace
+
+// What the scoring passes read of a store: its coded rows (D columns of b-bit
+// codes, step s = 2 eps), their ids, R >= s ||code_y|| for every row y, and
+// the first column counted in the reported bound.
+struct ScoreView {
+  int D;
+  int b;
+  int64_t n;
+  double step;
+  double eps;
+  double R;
+  int l1_from;
+  const uint32_t* codes;
+  const int64_t* ids;
+};
+
+namespace {
+
+// R >= ||x_hat_y||: ||x|| from the largest ||x||^2 / 2 of the coded rows
+// (float32, rounded up by one part in 2^22) plus ||x_hat - x|| <= eps sqrt(D).
+double row_norm_bound(uint32_t hn_max_bits, double eps, int D) {
+  float hn;
+  std::memcpy(&hn, &hn_max_bits, 4);
+  return std::sqrt(2.0 * (double)hn * (1.0 + 0x1p-22)) * (1.0 + 0x1p-50) +
+         eps * std::sqrt((double)D) * (1.0 + 0x1p-50);
+}
+
+ScoreView store_view(const lam_store* st, const uint32_t* codes) {
+  ScoreView v;
+  v.D = st->dim;
+  v.b = st->q.bits;
+  v.n = st->size;
+  v.step = st->q.step;
+  v.eps = st->q.eps;
+  v.R = row_norm_bound(st->hn_max, st->q.eps, st->dim);
+  v.l1_from = 0;
+  v.codes = codes ? codes : st->codes;
+  v.ids = st->ids;
+  return v;
+}
+
+// The split form of a store with wide codes and of the queries, in the
+// context's arena.  With |c >> 11| <= ||c|| / 2^11 + 1 per column and
+// c & 2047 <= 2,047, s ||code'|| <= R / 2^11 + 2^12 eps sqrt(D).
+lam_status widen(lam_ctx* ctx, ScoreView& v, const float*& q, int64_t nq) {
+  LAM_CHECK(v.b <= kWideMaxBits, LAM_ESTATE,
+            "scoring supports codes of at most %d bits (store codes have %d); quantize with a larger eps",
+            kWideMaxBits, v.b);
+  const int D = v.D;
+  LAM_TRY(ctx->scratch[kScratchWideCodes].ensure(std::max<size_t>((size_t)v.n * 2 * D * 12 / 8, 4)));
+  LAM_TRY(ctx->scratch[kScratchWideQueries].ensure(std::max<size_t>((size_t)nq * 2 * D * 4, 4)));
+  uint32_t* wc = ctx->scratch[kScratchWideCodes].as<uint32_t>();
+  float* wq = ctx->scratch[kScratchWideQueries].as<float>();
+  const int64_t ng = v.n * (2 * D / 32);
+  if (ng > 0) {
+    hipLaunchKernelGGL(k_wide_codes, dim3((unsigned)((ng + 255) / 256)), dim3(256), 0, ctx->stream, v.codes, v.n, D,
+                       v.b, wc);
+    LAM_HIP(hipGetLastError());
+  }
+  const int64_t ne = nq * 2 * D;
+  if (ne > 0) {
+    hipLaunchKernelGGL(k_wide_queries, dim3((unsigned)((ne + 255) / 256)), dim3(256), 0, ctx->stream, q, nq, D, wq);
+    LAM_HIP(hipGetLastError());
+  }
+  v.R = (v.R * 0x1p-11 + 4096.0 * v.eps * std::sqrt((double)D) * (1.0 + 0x1p-50)) * (1.0 + 0x1p-50);
+  v.D = 2 * D;
+  v.b = 12;
+  v.l1_from = D;
+  v.codes = wc;
+  q = wq;
+  return LAM_OK;
+}
+
 }  // namespace
 
 // Scoring plan.  With at most S store rows (S = k * n / 1024, at least 4,096)
@@ -1109,16 +1237,14 @@ struct ScoreWork {
 // launch, so a workspace that is too small fails with nothing enqueued.
 // max_splits caps the store ranges per query tile of the list passes (their
 // candidate lists grow with it); no profiling events are recorded unless prof.
-lam_status score_topk_impl(lam_ctx* ctx, const lam_store* st, const float* q, int64_t nq, int32_t k, float* scores,
-                           int64_t* ids, float* bound, const uint32_t* codes, ScoreWork& w, int max_splits,
-                           bool prof) {
+lam_status score_topk_impl(lam_ctx* ctx, const ScoreView& st, const float* q, int64_t nq, int32_t k, float* scores,
+                           int64_t* ids, float* bound, ScoreWork& w, int max_splits, bool prof) {
   if (nq == 0) return LAM_OK;
-  const int D = st->dim;
-  const int b = st->q.bits;
-  LAM_CHECK(b >= 1 && b <= 12, LAM_ESTATE,
-            "scoring supports codes of at most 12 bits (store codes have %d); quantize with a larger eps", b);
+  const int D = st.D;
+  const int b = st.b;
+  LAM_CHECK(b >= 1 && b <= 12, LAM_ESTATE, "internal: the scoring passes take codes of 1 to 12 bits (got %d)", b);
   const int KL = (k <= 16) ? 16 : 64;
-  const int64_t n = st->size;
+  const int64_t n = st.n;
   const int nqt = (int)((nq + kTB - 1) / kTB);
   const int64_t ntiles = (n + kTB - 1) / kTB;
   const int64_t sample_rows = std::max<int64_t>(4096, ((int64_t)k * n + 1023) / 1024);
@@ -1152,13 +1278,13 @@ lam_status score_topk_impl(lam_ctx* ctx, const lam_store* st, const float* q, in
 
   {
     ProfScope ps(ctx, "score_prep", prof);
-    hipLaunchKernelGGL(k_score_prep, dim3((unsigned)((nq + 3) / 4)), dim3(256), 0, ctx->stream, q, nq, D, st->q.step,
-                       st->q.eps, st->hn_max, qhi, qlo, qmeta);
+    hipLaunchKernelGGL(k_score_prep, dim3((unsigned)((nq + 3) / 4)), dim3(256), 0, ctx->stream, q, nq, D, st.step,
+                       st.eps, st.R, st.l1_from, qhi, qlo, qmeta);
     LAM_HIP(hipGetLastError());
   }
 
   ScoreArgs a{};
-  a.codes = codes ? codes : st->codes;
+  a.codes = st.codes;
   a.n = n;
   a.D = D;
   a.row_words = (int64_t)D * b / 32;
@@ -1184,10 +1310,10 @@ lam_status score_topk_impl(lam_ctx* ctx, const lam_store* st, const float* q, in
     ProfScope ps(ctx, "score_merge", prof);
     const int nc = ntiles > 0 ? sp2 * 2 * KL : 0;
     if (KL == 16)
-      hipLaunchKernelGGL((k_topk_merge<16>), gq, dim3(256), 0, ctx->stream, nq, nc, k, part_s, part_r, qmeta, st->ids,
+      hipLaunchKernelGGL((k_topk_merge<16>), gq, dim3(256), 0, ctx->stream, nq, nc, k, part_s, part_r, qmeta, st.ids,
                          scores, ids, bound, nullptr, nullptr);
     else
-      hipLaunchKernelGGL((k_topk_merge<64>), gq, dim3(256), 0, ctx->stream, nq, nc, k, part_s, part_r, qmeta, st->ids,
+      hipLaunchKernelGGL((k_topk_merge<64>), gq, dim3(256), 0, ctx->stream, nq, nc, k, part_s, part_r, qmeta, st.ids,
                          scores, ids, bound, nullptr, nullptr);
     LAM_HIP(hipGetLastError());
     return LAM_OK;
@@ -1211,7 +1337,7 @@ lam_status score_topk_impl(lam_ctx* ctx, const lam_store* st, const float* q, in
     LAM_TRY(dispatch_bits<1>(b, kSampleKL, kModeLists, dim3((unsigned)(nqt * sp1)), ctx->stream, a));
     const int nc = sp1 * 2 * kSampleKL;
     hipLaunchKernelGGL((k_topk_merge<16, kSampleKL>), gq, dim3(256), 0, ctx->stream, nq, nc, k, part_s, part_r, qmeta,
-                       st->ids, nullptr, nullptr, nullptr, thr, nullptr);
+                       st.ids, nullptr, nullptr, nullptr, thr, nullptr);
     LAM_HIP(hipGetLastError());
   }
   a.tile_begin = 0;
@@ -1240,23 +1366,23 @@ lam_status score_topk_impl(lam_ctx* ctx, const lam_store* st, const float* q, in
     ProfScope ps(ctx, "score_merge", prof);
     if (KL == 16)
       hipLaunchKernelGGL((k_cand_select<16>), gq, dim3(256), 0, ctx->stream, nq, cap, k, cand_cnt, cand_s, cand_r,
-                         qmeta, st->ids, scores, ids, bound, qflag, tflag);
+                         qmeta, st.ids, scores, ids, bound, qflag, tflag);
     else
       hipLaunchKernelGGL(k_cand_select_radix, dim3((unsigned)nq), dim3(64), 0, ctx->stream, nq, cap, k, cand_cnt, cand_s, cand_r,
-                         qmeta, st->ids, scores, ids, bound, qflag, tflag);
+                         qmeta, st.ids, scores, ids, bound, qflag, tflag);
     LAM_HIP(hipGetLastError());
     LAM_TRY(launch_rescore<1>(b, dim3((unsigned)nq), ctx->stream, nq, cap, k, cand_cnt, cand_s, cand_r, qmeta,
-                              st->ids, q, st->q.step, a.codes, a.row_words, D, scores, ids, qflag, tflag));
+                              st.ids, q, st.step, a.codes, a.row_words, D, scores, ids, qflag, tflag));
   }
   {
     ProfScope ps(ctx, "score_fallback", prof);
     LAM_TRY(dispatch_bits<1>(b, KL, kModeFallback, dim3((unsigned)(nqt * sp2)), ctx->stream, a));
     const int nc = sp2 * 2 * KL;
     if (KL == 16)
-      hipLaunchKernelGGL((k_topk_merge<16>), gq, dim3(256), 0, ctx->stream, nq, nc, k, part_s, part_r, qmeta, st->ids,
+      hipLaunchKernelGGL((k_topk_merge<16>), gq, dim3(256), 0, ctx->stream, nq, nc, k, part_s, part_r, qmeta, st.ids,
                          scores, ids, bound, nullptr, qflag);
     else
-      hipLaunchKernelGGL((k_topk_merge<64>), gq, dim3(256), 0, ctx->stream, nq, nc, k, part_s, part_r, qmeta, st->ids,
+      hipLaunchKernelGGL((k_topk_merge<64>), gq, dim3(256), 0, ctx->stream, nq, nc, k, part_s, part_r, qmeta, st.ids,
                          scores, ids, bound, nullptr, qflag);
     LAM_HIP(hipGetLastError());
   }
@@ -1299,8 +1425,11 @@ lam_status noalloc_setup(int device) {
 
 lam_status score_topk(lam_ctx* ctx, const lam_store* st, const float* q, int64_t nq, int32_t k, float* scores,
                       int64_t* ids, float* bound, const uint32_t* codes) {
+  if (nq == 0) return LAM_OK;
   ScoreWork w;
-  return score_topk_impl(ctx, st, q, nq, k, scores, ids, bound, codes, w, 1 << 30, true);
+  ScoreView v = store_view(st, codes);
+  if (v.b > 12) LAM_TRY(widen(ctx, v, q, nq));
+  return score_topk_impl(ctx, v, q, nq, k, scores, ids, bound, w, 1 << 30, true);
 }
 
 lam_status score_topk_noalloc(lam_ctx* ctx, const lam_store* st, const float* q, int64_t nq, int32_t k, float* scores,
@@ -1313,10 +1442,12 @@ lam_status score_topk_noalloc(lam_ctx* ctx, const lam_store* st, const float* q,
     p = ctx->device < kMaxDevices ? g_noalloc_ptr[ctx->device] : nullptr;
   }
   LAM_CHECK(p != nullptr, LAM_ESTATE, "the fixed workspace of device %d was not set up", ctx->device);
+  LAM_CHECK(st->q.bits <= 12, LAM_ESTATE,
+            "the allocation-free call scores codes of at most 12 bits (store codes have %d)", st->q.bits);
   ScoreWork w;
   w.base = static_cast<char*>(p);
   w.bytes = kNoAllocBytes;
-  return score_topk_impl(ctx, st, q, nq, k, scores, ids, bound, nullptr, w, kNoAllocSplits, false);
+  return score_topk_impl(ctx, store_view(st, nullptr), q, nq, k, scores, ids, bound, w, kNoAllocSplits, false);
 }
 
 // ------------------------------------------------------------------ certificate
@@ -1382,13 +1513,19 @@ lam_status score_certify(lam_ctx* ctx, const lam_store* st, const float* q, int6
   float* s1 = reinterpret_cast<float*>(base + (size_t)nq * K1 * 8);
   float* b1 = s1 + (size_t)nq * K1;
   LAM_TRY(score_topk(ctx, st, q, nq, K1, s1, i1, b1));
-  // error bound of the float32 score per unit of ||q||_1: kappa (A + eps)
+  // error bound of the float32 score per unit of ||q||_1: kappa (A + eps).
+  // Wide codes are scored in their split form (2 D columns): twice the terms,
+  // and sum |q'_d' x_hat'_d'| <= ||q||_1 (A + eps + 2^12 s) since
+  // 2^11 |c >> 11| <= |c| + 2^11 and c & 2047 < 2^11.
+  const bool wide = st->q.bits > 12;
+  const double Dt = (wide ? 2.0 : 1.0) * st->dim;
   const double u = std::ldexp(1.0, -24);
-  const double g2d = 2.0 * st->dim * u / (1.0 - 2.0 * st->dim * u);
+  const double g2d = 2.0 * Dt * u / (1.0 - 2.0 * Dt * u);
   // (the split residual, the sums, the two scalings; a rescored score is
   // within 2^-24 relative of its binary64 sum, far inside this)
   const double kappa = 1.01 * (std::ldexp(1.0, -22) + g2d + std::ldexp(1.0, -23));
-  const double err_per_l1 = kappa * ((double)st->q.absmax + st->q.eps);
+  const double mag = (double)st->q.absmax + st->q.eps + (wide ? 4096.0 * st->q.step : 0.0);
+  const double err_per_l1 = kappa * mag;
   hipLaunchKernelGGL(k_certify, dim3((unsigned)((nq + 3) / 4)), dim3(256), 0, ctx->stream, nq, k, s1, i1, b1, q,
                      st->dim, st->q.eps, st->delta_hat_run, err_per_l1, scores, ids, bound, certified, margin);
   LAM_HIP(hipGetLastError());
