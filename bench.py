@@ -183,7 +183,7 @@ def banded_ingest(lam, torch, np, xd, rep_exh, pairs, ctx, r=BAND_R, rel=BAND_RE
 def beside_the_step(lam, torch, np, xd, qd, store, rep, pairs, ctx, raw_sets, raw_out):
     """Measurements beside the timed step (not in it): the decision
     statistics of the stream (ambiguous pairs, exact decisions, smallest
-    decided margin), the triad bandwidth anchor, raw Q_eps at three widths,
+    decided margin), the triad and matrix-unit anchors, raw Q_eps at three widths,
     the screen at scale, the large online store at full size, the tiny
     workload's per-call latency, the removal ceiling of the stream, the share
     of benchmark queries whose top-10 is certified rank-invariant, the
@@ -194,6 +194,7 @@ def beside_the_step(lam, torch, np, xd, qd, store, rep, pairs, ctx, raw_sets, ra
     blk_t = block_codec_timing(lam, torch, store, ctx)
     blk = store.block_encode()
     triad = triad_anchor(lam, torch, ctx)
+    matmul = matmul_anchor(torch)
     # the stream once more with calls that wait, for the decision statistics
     n = xd.shape[0]
     probe = lam.Store(D, TAU, n, ctx=ctx)
@@ -202,10 +203,13 @@ def beside_the_step(lam, torch, np, xd, qd, store, rep, pairs, ctx, raw_sets, ra
                  "exact_escalations": int(sum(t["n_exact_escalations"] for t in st)),
                  "min_margin_d2": float(min(t["min_margin_d2"] for t in st))}
     del probe
+    steady = screen_steady_state(lam, torch, np, ctx)
+    steady["screen_frac_of_matmul_anchor"] = steady["screen_TFLOPs"] / matmul["TFLOPs"]
     return {"decisions": decisions,
             "triad": triad,
+            "matmul_anchor": matmul,
             "qeps_widths": qeps_widths(lam, torch, raw_sets, raw_out, ctx, triad["GBps"]),
-            "screen_steady_state": screen_steady_state(lam, torch, np, ctx),
+            "screen_steady_state": steady,
             "online_store": online_store_run(lam, torch, np, ctx),
             "tiny_latency": tiny_latency(lam, torch, ctx),
             "corpus_scoring": corpus_scoring(lam, torch, np, ctx),
@@ -304,6 +308,30 @@ def triad_anchor(lam, torch, ctx, reps=20):
     gbs = 12.0 * TRIAD_N / (tot / cnt / 1e3) / 1e9
     return {"workload": "triad c = a + 3 b, 3 x 512 MB float32", "GBps": gbs, "frac_of_spec": gbs / HBM_PEAK_GBS,
             "us_per_launch": tot / cnt * 1e3, "result_checked": ok}
+
+
+def matmul_anchor(torch, n=8192, reps=10):
+    """The matrix-unit anchor: an n^3 fp16 GEMM with float32 accumulation
+    through the vendor BLAS (torch.matmul) on N(0, 1) operands, the fp16
+    matmul row of the paper's anchors (App. "Measured hardware constants",
+    Table "anchors": an 8192^3 GEMM).  A measurement, not a step of the path."""
+    g = torch.Generator(device="cuda").manual_seed(5)
+    a = torch.randn(n, n, device="cuda", dtype=torch.float16, generator=g)
+    b = torch.randn(n, n, device="cuda", dtype=torch.float16, generator=g)
+    for _ in range(3):
+        c = torch.matmul(a, b)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        c = torch.matmul(a, b)
+    e1.record()
+    e1.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    del a, b, c
+    tf = 2.0 * n ** 3 / (ms / 1e3) / 1e12
+    return {"workload": f"fp16 GEMM {n}^3 (torch.matmul), N(0, 1) operands", "ms": ms, "TFLOPs": tf,
+            "frac_of_spec": tf / MFMA_F16_PEAK_TFLOPS}
 
 
 def qeps_widths(lam, torch, raw_sets, raw_out, ctx, triad_gbs, reps=20):
@@ -680,6 +708,8 @@ def main():
         tgbs = extras["triad"]["GBps"]
         for v in qeps_timed.values():
             v["frac_of_triad"] = v["GBps"] / tgbs
+        if roofline.get("bound") == "mfma" and roofline.get("achieved"):
+            roofline["frac_of_matmul_anchor"] = roofline["achieved"] / extras["matmul_anchor"]["TFLOPs"]
 
     value = pairs / (ms / 1e3) / 1e6
     out = {

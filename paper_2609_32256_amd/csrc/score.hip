@@ -77,10 +77,17 @@ __device__ __forceinline__ float rd32(double d) {
 __global__ __launch_bounds__(256) void k_score_prep(const float* __restrict__ q, int64_t nq, int D, double s,
                                                     double eps, double R, int l1_from,
                                                     _Float16* __restrict__ qhi,
-                                                    _Float16* __restrict__ qlo, QMeta* __restrict__ meta) {
+                                                    _Float16* __restrict__ qlo, QMeta* __restrict__ meta,
+                                                    uint32_t* __restrict__ cand_cnt, uint32_t* __restrict__ tflag) {
   const int lane = threadIdx.x & 63;
   const int64_t j = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (j >= nq) return;
+  // the threshold plan's candidate count of this query and flag of its query
+  // tile start at zero (the buffers may hold anything from an earlier call)
+  if (cand_cnt && lane == 0) {
+    cand_cnt[j] = 0u;
+    if (j % kTB == 0) tflag[j / kTB] = 0u;
+  }
   const float* p = q + j * D;
   float mx = 0.0f;
   double l1 = 0.0, l2 = 0.0;
@@ -748,6 +755,7 @@ __global__ __launch_bounds__(64) void k_cand_select_radix(int64_t nq, uint32_t c
 // ------------------------------------------------------------------ filter pass on the screen's pipeline
 using FilterTile = Tile<2, 4, 2, 1, 4>;
 constexpr int kFilterGroupQ = 8;   // query tiles per group in the tile order
+constexpr int kSampleEntries = 4;  // entries per query and store tile of the sample pass on this pipeline
 
 // The threshold plan's filter pass (hi-only scores H) for D = 64 NS: one
 // 128 x 128 tile (store rows x queries) per workgroup of 8 waves, each wave
@@ -760,11 +768,17 @@ constexpr int kFilterGroupQ = 8;   // query tiles per group in the tile order
 // XCD a contiguous range, so an XCD holds its 8 query tiles in L2 while the
 // codes stream past.  Every row with H >= the query's threshold is appended to
 // its candidate buffer, as in k_score's filter mode.
-template <int B, int NS>
+// SAMPLE: the sample pass of the threshold plan over store tiles [0,
+// tile_end) instead: per query and tile, the best H of each of the four lanes
+// holding the query (disjoint sets of 32 rows) at entries [4 t, 4 t + 4) of
+// the query's partial list.  The k-th best of these entries is the H of k
+// distinct rows, so at most the sample's k-th best H: a valid base for the
+// threshold (lower only where several of the best rows share a lane).
+template <int B, int NS, bool SAMPLE>
 __global__ __launch_bounds__(FilterTile::kThreads, FilterTile::kMinWaves) void k_filter(ScoreArgs a) {
   using C = FilterTile;
   __shared__ _Float16 lds[C::kLdsHalves];
-  const int64_t nt = (a.n + kTB - 1) / kTB;
+  const int64_t nt = a.tile_end;   // store tiles of this pass (tile_begin = 0)
   const int64_t logical = xcd_remap((int64_t)blockIdx.x, (int64_t)a.nqt * nt);
   const int64_t per = (int64_t)kFilterGroupQ * nt;
   const int g = (int)(logical / per);
@@ -780,7 +794,7 @@ __global__ __launch_bounds__(FilterTile::kThreads, FilterTile::kMinWaves) void k
   // this lane's query and its threshold, loaded before the GEMM
   const int64_t j = qbase + wn * 32 + (lane & 31);
   const bool jv = j < a.nq;
-  const float th = jv ? a.thr[j] : 0.0f;
+  const float th = (jv && !SAMPLE) ? a.thr[j] : 0.0f;
   const float osc = jv ? a.meta[j].osc : 0.0f;
 
   auto sa = [&](int i) -> _Float16* { return lds + i * ((C::BM + C::BN) * kLdk); };
@@ -848,6 +862,27 @@ __global__ __launch_bounds__(FilterTile::kThreads, FilterTile::kMinWaves) void k
       __syncthreads();
     }
   }
+  if constexpr (SAMPLE) {
+    // this lane's best H over its 32 rows (the lowest row among equals)
+    float best = -INFINITY;
+    int brow = kNoRow;
+#pragma unroll
+    for (int x = 0; x < C::TI; ++x)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int rl_ = wm * 64 + x * 32 + acc_row(r, lane);   // ascending in (x, r)
+        const float sc = acc[x][0][r] * osc;
+        const bool take = rl_ < rows && sc > best;
+        best = take ? sc : best;
+        brow = take ? (int)(rbase + rl_) : brow;
+      }
+    if (jv) {
+      const int64_t o = j * (nt * kSampleEntries) + (rbase / kTB) * kSampleEntries + wm * 2 + (lane >> 5);
+      a.part_s[o] = best;
+      a.part_r[o] = brow;
+    }
+    return;
+  }
   // epilogue: the tile's largest raw accumulator first (osc > 0)
   float amx = -INFINITY;
 #pragma unroll
@@ -880,15 +915,15 @@ __global__ __launch_bounds__(FilterTile::kThreads, FilterTile::kMinWaves) void k
     }
 }
 
-template <int B>
+template <int B, bool SAMPLE>
 lam_status launch_filter(int b, int D, dim3 grid, hipStream_t st, const ScoreArgs& a) {
   if (b == B) {
-    if (D == 768) hipLaunchKernelGGL((k_filter<B, 12>), grid, dim3(FilterTile::kThreads), 0, st, a);
-    else hipLaunchKernelGGL((k_filter<B, 16>), grid, dim3(FilterTile::kThreads), 0, st, a);
+    if (D == 768) hipLaunchKernelGGL((k_filter<B, 12, SAMPLE>), grid, dim3(FilterTile::kThreads), 0, st, a);
+    else hipLaunchKernelGGL((k_filter<B, 16, SAMPLE>), grid, dim3(FilterTile::kThreads), 0, st, a);
     LAM_HIP(hipGetLastError());
     return LAM_OK;
   }
-  if constexpr (B < 12) return launch_filter<B + 1>(b, D, grid, st, a);
+  if constexpr (B < 12) return launch_filter<B + 1, SAMPLE>(b, D, grid, st, a);
   set_error("scoring supports codes of at most 12 bits (got %d)", b);
   return LAM_ESTATE;
 }
@@ -995,13 +1030,6 @@ __global__ __launch_bounds__(kRescoreThreads) void k_rescore(
     out_s[j * k + t] = ord2f((uint32_t)(keys[t] >> 32));
     out_i[j * k + t] = ids[~(uint32_t)(keys[t] & 0xffffffffull)];
   }
-}
-
-__global__ void k_clear_u32(uint32_t* a, int64_t na, uint32_t* b, int64_t nb) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int64_t st = (int64_t)gridDim.x * blockDim.x;
-  for (int64_t t = i; t < na; t += st) a[t] = 0u;
-  for (int64_t t = i; t < nb; t += st) b[t] = 0u;
 }
 
 // Lists and fallback give final scores (hi and lo); the filter pass works on
@@ -1262,6 +1290,10 @@ lam_status score_topk_impl(lam_ctx* ctx, const ScoreView& st, const float* q, in
     sp1 = (int)((stiles + tps1 - 1) / tps1);
   }
   const int cands_max = std::max(sp1, sp2) * 2 * KL;
+  // the sample pass on the filter's pipeline at D = 768 and 1,024 when its
+  // entries fit the partial lists' buffer
+  const bool filter_sample =
+      two_pass && (D == 768 || D == 1024) && stiles * kSampleEntries <= (int64_t)cands_max;
   const uint32_t cap = kCandCap;
 
   // every buffer first
@@ -1275,11 +1307,16 @@ lam_status score_topk_impl(lam_ctx* ctx, const ScoreView& st, const float* q, in
   LAM_TRY(w.take(ctx, S_PART, (size_t)nq * cands_max * 8, &part_s));
   if (two_pass) LAM_TRY(w.take(ctx, S_CAND, (size_t)nq * cap * 8 + (size_t)nq * 12 + (size_t)nqt * 4 + 256, &cand_s));
   int32_t* part_r = reinterpret_cast<int32_t*>(part_s + (size_t)nq * cands_max);
+  int32_t* cand_r = two_pass ? reinterpret_cast<int32_t*>(cand_s + (size_t)nq * cap) : nullptr;
+  uint32_t* cand_cnt = two_pass ? reinterpret_cast<uint32_t*>(cand_r + (size_t)nq * cap) : nullptr;
+  float* thr = two_pass ? reinterpret_cast<float*>(cand_cnt + nq) : nullptr;
+  uint32_t* qflag = two_pass ? reinterpret_cast<uint32_t*>(thr + nq) : nullptr;
+  uint32_t* tflag = two_pass ? qflag + nq : nullptr;
 
   {
     ProfScope ps(ctx, "score_prep", prof);
     hipLaunchKernelGGL(k_score_prep, dim3((unsigned)((nq + 3) / 4)), dim3(256), 0, ctx->stream, q, nq, D, st.step,
-                       st.eps, st.R, st.l1_from, qhi, qlo, qmeta);
+                       st.eps, st.R, st.l1_from, qhi, qlo, qmeta, cand_cnt, tflag);
     LAM_HIP(hipGetLastError());
   }
 
@@ -1319,25 +1356,23 @@ lam_status score_topk_impl(lam_ctx* ctx, const ScoreView& st, const float* q, in
     return LAM_OK;
   }
 
-  int32_t* cand_r = reinterpret_cast<int32_t*>(cand_s + (size_t)nq * cap);
-  uint32_t* cand_cnt = reinterpret_cast<uint32_t*>(cand_r + (size_t)nq * cap);
-  float* thr = reinterpret_cast<float*>(cand_cnt + nq);
-  uint32_t* qflag = reinterpret_cast<uint32_t*>(thr + nq);
-  uint32_t* tflag = qflag + nq;
-  // the candidate counts and tile flags start at zero (cleared by a kernel:
-  // the buffer may hold anything from an earlier call)
-  hipLaunchKernelGGL(k_clear_u32, dim3(64), dim3(256), 0, ctx->stream, cand_cnt, nq, tflag, (int64_t)nqt);
-  LAM_HIP(hipGetLastError());
+  // (the candidate counts and tile flags were cleared by k_score_prep)
   {  // 1. a k-th best score of the sample -> thresholds
     ProfScope ps(ctx, "score_sample", prof);
     a.tile_begin = 0;
     a.tile_end = stiles;
     a.splits = sp1;
     a.tiles_per_split = tps1;
-    LAM_TRY(dispatch_bits<1>(b, kSampleKL, kModeLists, dim3((unsigned)(nqt * sp1)), ctx->stream, a));
-    const int nc = sp1 * 2 * kSampleKL;
-    hipLaunchKernelGGL((k_topk_merge<16, kSampleKL>), gq, dim3(256), 0, ctx->stream, nq, nc, k, part_s, part_r, qmeta,
-                       st.ids, nullptr, nullptr, nullptr, thr, nullptr);
+    if (filter_sample) {
+      // one tile per workgroup on the filter's pipeline; entries unsorted (segments of 1)
+      LAM_TRY((launch_filter<1, true>(b, D, dim3((unsigned)(nqt * stiles)), ctx->stream, a)));
+      hipLaunchKernelGGL((k_topk_merge<16, 1>), gq, dim3(256), 0, ctx->stream, nq, (int)stiles * kSampleEntries, k,
+                         part_s, part_r, qmeta, st.ids, nullptr, nullptr, nullptr, thr, nullptr);
+    } else {
+      LAM_TRY(dispatch_bits<1>(b, kSampleKL, kModeLists, dim3((unsigned)(nqt * sp1)), ctx->stream, a));
+      hipLaunchKernelGGL((k_topk_merge<16, kSampleKL>), gq, dim3(256), 0, ctx->stream, nq, sp1 * 2 * kSampleKL, k,
+                         part_s, part_r, qmeta, st.ids, nullptr, nullptr, nullptr, thr, nullptr);
+    }
     LAM_HIP(hipGetLastError());
   }
   a.tile_begin = 0;
@@ -1356,7 +1391,7 @@ lam_status score_topk_impl(lam_ctx* ctx, const ScoreView& st, const float* q, in
       // one 128 x 128 tile per workgroup on the screen's pipeline
       const int64_t grid = (int64_t)nqt * ntiles;
       LAM_CHECK(grid < (1LL << 31), LAM_EINVAL, "scoring grid too large");
-      LAM_TRY(launch_filter<1>(b, D, dim3((unsigned)grid), ctx->stream, a));
+      LAM_TRY((launch_filter<1, false>(b, D, dim3((unsigned)grid), ctx->stream, a)));
     } else {
       LAM_TRY(dispatch_bits<1>(b, KL, kModeFilter, dim3((unsigned)(nqt * sp2)), ctx->stream, a));
       LAM_HIP(hipGetLastError());
