@@ -25,36 +25,74 @@ namespace {
 __device__ __forceinline__ uint32_t zigzag(int32_t q) { return ((uint32_t)q << 1) ^ (uint32_t)(q >> 31); }
 __device__ __forceinline__ int32_t unzigzag(uint32_t u) { return (int32_t)(u >> 1) ^ -(int32_t)(u & 1u); }
 
-// Code e (element index in the store's stream) of a b-bit packed stream,
-// sign-extended; the stream is padded to whole words, so word + 1 may be read
-// only when the field straddles it.
-__device__ __forceinline__ int32_t code_at(const uint32_t* __restrict__ codes, int b, int64_t e) {
-  const uint64_t bit = (uint64_t)e * (uint64_t)b;
-  const uint64_t w = bit >> 5;
-  const uint32_t off = (uint32_t)(bit & 31u);
-  uint32_t u = codes[w] >> off;
-  if (off + (uint32_t)b > 32u) u |= codes[w + 1] << (32u - off);
+// A round of a row: up to kPairs pairs of blocks, the two 32-lane halves of
+// the wave taking one block each with one code per lane (lane j of half h
+// holds code j of block k0 + 2 i + h in round slot i).  A round's loads are
+// all issued before any is used; consecutive lanes read consecutive fields,
+// so a half reads its block's b words in one or two requests.
+constexpr int kPairs = 16;
+
+// A buffer resource over the words [base, base + words): loads past the end
+// read as zero.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t words_rsrc(const uint32_t* base, uint32_t words) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint32_t*>(base), (short)0, (int)(words * 4u), 0x00020000);
+}
+
+// Code i of a row's b-bit stream (rs over the row): both words that may hold
+// the field are loaded without a branch (the second past the row's end reads
+// as zero and is shifted out), so a round's loads issue back to back.
+__device__ __forceinline__ int32_t code_rs(__amdgpu_buffer_rsrc_t rs, int b, int i) {
+  const uint32_t bit = (uint32_t)i * (uint32_t)b;
+  const uint32_t w = bit >> 5, off = bit & 31u;
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(rs, w * 4u, 0, 0);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(rs, w * 4u + 4u, 0, 0);
+  const uint32_t u = __builtin_amdgcn_alignbit(hi, lo, off);   // bits [off, off + 32) of hi:lo
   return (int32_t)(u << (32 - b)) >> (32 - b);
 }
 
-// Pass 1: one wave per row; lane l takes blocks l, l + 64, ...: block widths
-// and the row's word count.
+__device__ __forceinline__ void load_round(const uint32_t* __restrict__ codes, int b, int64_t r, int D, int nb,
+                                           int k0, uint32_t (&u)[kPairs]) {
+  const int lane = threadIdx.x & 63, half = lane >> 5, j = lane & 31;
+  const uint32_t row_words = (uint32_t)(D / 32) * (uint32_t)b;
+  const __amdgpu_buffer_rsrc_t rs = words_rsrc(codes + r * (int64_t)row_words, row_words);
+#pragma unroll
+  for (int i = 0; i < kPairs; ++i) {
+    const int kb = k0 + 2 * i + half;
+    u[i] = kb < nb ? zigzag(code_rs(rs, b, kb * 32 + j)) : 0u;
+  }
+}
+
+// Pass 1: one wave per row: block widths and the row's word count.  The bit
+// length of a block's largest zigzag code is that of the OR of its codes:
+// the highest bit t whose ballot over the half is not empty (b ballots per
+// pair of blocks, all zigzag codes being below 2^b).
 __global__ __launch_bounds__(256) void k_blk_widths(const uint32_t* __restrict__ codes, int b, int64_t rows, int D,
                                                     uint8_t* __restrict__ widths, uint32_t* __restrict__ row_words) {
-  const int lane = threadIdx.x & 63;
+  const int lane = threadIdx.x & 63, half = lane >> 5, j = lane & 31;
   const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (r >= rows) return;
   const int nb = D / 32;
   uint32_t total = 0;
-  for (int k = lane; k < nb; k += 64) {
-    uint32_t mx = 0;
-    const int64_t e0 = r * D + (int64_t)k * 32;
-    for (int j = 0; j < 32; ++j) mx = max(mx, zigzag(code_at(codes, b, e0 + j)));
-    const uint32_t w = mx ? 32u - (uint32_t)__clz(mx) : 0u;
-    widths[r * nb + k] = (uint8_t)w;
-    total += w;
+  for (int k0 = 0; k0 < nb; k0 += 2 * kPairs) {
+    uint32_t u[kPairs];
+    load_round(codes, b, r, D, nb, k0, u);
+#pragma unroll
+    for (int i = 0; i < kPairs; ++i) {
+      uint32_t w0 = 0, w1 = 0;
+      for (int t = 0; t < b; ++t) {
+        const unsigned long long m = __ballot((u[i] >> t) & 1u);
+        w0 = (uint32_t)m ? (uint32_t)t + 1u : w0;
+        w1 = (uint32_t)(m >> 32) ? (uint32_t)t + 1u : w1;
+      }
+      const uint32_t w = half ? w1 : w0;
+      const int kb = k0 + 2 * i + half;
+      if (j == 0 && kb < nb) {
+        widths[r * nb + kb] = (uint8_t)w;
+        total += w;
+      }
+    }
   }
-  for (int o = 32; o > 0; o >>= 1) total += __shfl_xor(total, o);
+  total = (uint32_t)__shfl((int)total, 0) + (uint32_t)__shfl((int)total, 32);
   if (lane == 0) row_words[r] = total;
 }
 
@@ -149,85 +187,107 @@ __device__ __forceinline__ uint32_t width_prefix(uint32_t w, uint32_t& carry) {
   return ex;
 }
 
-// Pass 2: one wave per row.  Lane l first forms the word offsets of blocks l,
-// l + 64, ...; then the two halves of the wave take a pair of blocks with one
-// code per lane, and each bit plane is a ballot.
+// The word offsets within row r of its blocks k0 + l (lane l, l < 64) and
+// their widths; carry: the words of the blocks before k0.
+__device__ __forceinline__ void row_offsets(const uint8_t* __restrict__ widths, int64_t r, int nb, int k0,
+                                            uint32_t& carry, uint32_t& wl, uint32_t& pre) {
+  const int lane = threadIdx.x & 63;
+  const int kl = k0 + lane;
+  wl = kl < nb ? widths[r * nb + kl] : 0u;
+  pre = width_prefix(wl, carry);
+}
+
+// Pass 2: one wave per row; per round of block pairs the codes are loaded
+// first, then each bit plane of a block is a ballot over its half.
 __global__ __launch_bounds__(256) void k_blk_pack(const uint32_t* __restrict__ codes, int b, int64_t rows, int D,
                                                   const uint8_t* __restrict__ widths,
                                                   const uint64_t* __restrict__ row_off, uint32_t* __restrict__ data) {
-  const int lane = threadIdx.x & 63;
+  const int lane = threadIdx.x & 63, half = lane >> 5, j = lane & 31;
   const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (r >= rows) return;
   const int nb = D / 32;
-  const int half = lane >> 5, j = lane & 31;
   const uint64_t roff = row_off[r];
-  uint32_t carry = 0;
-  for (int k0 = 0; k0 < nb; k0 += 64) {
-    const int kl = k0 + lane;
-    const uint32_t wl = kl < nb ? widths[r * nb + kl] : 0u;
-    const uint32_t pre = width_prefix(wl, carry);
-    const int kend = min(nb, k0 + 64);
-    for (int k = k0; k < kend; k += 2) {
-      const int kb = k + half;                            // this half's block
-      const bool real = kb < kend;
-      const uint32_t w = __shfl(wl, (kb - k0) & 63);
-      const uint32_t p = __shfl(pre, (kb - k0) & 63);
-      const uint32_t u = real ? zigzag(code_at(codes, b, r * D + (int64_t)kb * 32 + j)) : 0u;
-      const uint32_t wmax = max(__shfl(w, 0), __shfl(w, 32));
+  uint32_t carry = 0, wl = 0, pre = 0;
+  for (int k0 = 0; k0 < nb; k0 += 2 * kPairs) {
+    uint32_t u[kPairs];
+    load_round(codes, b, r, D, nb, k0, u);
+    if (k0 % 64 == 0) row_offsets(widths, r, nb, k0, carry, wl, pre);
+#pragma unroll
+    for (int i = 0; i < kPairs; ++i) {
+      const int kb = k0 + 2 * i + half;
+      const int src = (kb - (k0 & ~63)) & 63;
+      const uint32_t w = (uint32_t)__shfl((int)wl, src);
+      const uint32_t p = (uint32_t)__shfl((int)pre, src);
+      const uint32_t wmax = max((uint32_t)__shfl((int)w, 0), (uint32_t)__shfl((int)w, 32));
       uint32_t mine = 0;
       for (uint32_t t = 0; t < wmax; ++t) {
-        const unsigned long long m = __ballot((u >> t) & 1u);
+        const unsigned long long m = __ballot((u[i] >> t) & 1u);
         const uint32_t plane = half ? (uint32_t)(m >> 32) : (uint32_t)m;
-        if ((uint32_t)j == t) mine = plane;
+        mine = ((uint32_t)j == t) ? plane : mine;
       }
-      if (real && (uint32_t)j < w) data[roff + p + j] = mine;
+      if (kb < nb && (uint32_t)j < w) data[roff + p + j] = mine;
     }
   }
 }
 
 // One wave per row: decode every block, either to float32 x_hat =
 // float32(float64(q * s)) (xhat != NULL) or back to the b-bit stream (codes_out
-// != NULL; the block's 32 codes are exactly b words, written by lanes 0..b-1).
+// != NULL; a block's 32 codes are exactly b words).  Per round the lanes j < w
+// of each half load plane j of their block (every plane once), and a lane
+// rebuilds its code from the planes by shuffles.
 __global__ __launch_bounds__(256) void k_blk_decode(const uint8_t* __restrict__ widths,
                                                     const uint64_t* __restrict__ row_off,
                                                     const uint32_t* __restrict__ data, int64_t rows, int D, double s,
                                                     float* __restrict__ xhat, int b, uint32_t* __restrict__ codes_out) {
-  const int lane = threadIdx.x & 63;
+  const int lane = threadIdx.x & 63, half = lane >> 5, j = lane & 31;
   const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (r >= rows) return;
   const int nb = D / 32;
-  const int half = lane >> 5, j = lane & 31;
   const uint64_t roff = row_off[r];
+  const __amdgpu_buffer_rsrc_t rs = words_rsrc(data + roff, (uint32_t)(row_off[r + 1] - roff));
   const uint32_t mask = b >= 32 ? 0xffffffffu : ((1u << b) - 1u);
-  uint32_t carry = 0;
-  for (int k0 = 0; k0 < nb; k0 += 64) {
-    const int kl = k0 + lane;
-    const uint32_t wl = kl < nb ? widths[r * nb + kl] : 0u;
-    const uint32_t pre = width_prefix(wl, carry);
-    const int kend = min(nb, k0 + 64);
-    for (int k = k0; k < kend; k += 2) {
-      const int kb = k + half;
-      const bool real = kb < kend;
-      const uint32_t ws = __shfl(wl, (kb - k0) & 63);   // every lane takes part in the shuffle
-      const uint32_t w = real ? ws : 0u;
-      const uint32_t p = __shfl(pre, (kb - k0) & 63);
+  uint32_t carry = 0, wl = 0, pre = 0;
+  for (int k0 = 0; k0 < nb; k0 += 2 * kPairs) {
+    if (k0 % 64 == 0) row_offsets(widths, r, nb, k0, carry, wl, pre);
+    uint32_t w[kPairs], pl[kPairs];
+#pragma unroll
+    for (int i = 0; i < kPairs; ++i) {
+      const int kb = k0 + 2 * i + half;
+      const int src = (kb - (k0 & ~63)) & 63;
+      const uint32_t ws = (uint32_t)__shfl((int)wl, src);
+      const uint32_t p = (uint32_t)__shfl((int)pre, src);
+      w[i] = kb < nb ? ws : 0u;
+      // plane j of this half's block (lanes past the width: an offset past the row, read as zero)
+      pl[i] = (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(rs, (uint32_t)j < w[i] ? (p + j) * 4u : 0xfffffff0u, 0, 0);
+    }
+#pragma unroll
+    for (int i = 0; i < kPairs; ++i) {
+      const int kb = k0 + 2 * i + half;
+      const uint32_t wmax = max((uint32_t)__shfl((int)w[i], 0), (uint32_t)__shfl((int)w[i], 32));
       uint32_t u = 0;
-      for (uint32_t t = 0; t < w; ++t) u |= ((data[roff + p + t] >> j) & 1u) << t;
+      for (uint32_t t = 0; t < wmax; ++t) {
+        const uint32_t plane = (uint32_t)__shfl((int)pl[i], (half << 5) | (int)t);   // (zero past the width)
+        u |= ((plane >> j) & 1u) << t;
+      }
       const int32_t q = unzigzag(u);
       const int64_t e = r * D + (int64_t)kb * 32 + j;
       if (xhat) {
-        if (real) xhat[e] = (float)((double)q * s);
+        if (kb < nb) xhat[e] = (float)((double)q * s);
       } else {
-        // word t of the block's b-bit stream gathers the codes whose fields
-        // overlap bits [32t, 32t + 32)
+        // word j of the block's b-bit stream holds bits [32 j, 32 j + 32): the
+        // fields of codes c0 .. c0 + ceil(32 / b), c0 = 32 j / b (a loop of the
+        // same length on every lane, so every shuffle has all lanes)
         const uint32_t f = (uint32_t)q & mask;
+        const int c0 = (32 * j) / b;
+        const int steps = (32 + b - 1) / b + 1;
         uint32_t word = 0;
-        for (int c = 0; c < 32; ++c) {
-          const uint32_t fc = __shfl(f, (half << 5) | c);
-          const int bit = c * b - j * 32;               // field start relative to word j
-          if (bit > -b && bit < 32) word |= bit >= 0 ? (fc << bit) : (fc >> -bit);
+        for (int i2 = 0; i2 < steps; ++i2) {
+          const int c = c0 + i2;
+          const uint32_t fc = (uint32_t)__shfl((int)f, (half << 5) | (c & 31));
+          const int bit = c * b - j * 32;   // field start relative to word j
+          if (c < 32 && bit > -b && bit < 32) word |= bit >= 0 ? (fc << bit) : (fc >> -bit);
         }
-        if (real && j < b) codes_out[(r * (int64_t)D + (int64_t)kb * 32) * b / 32 + j] = word;
+        if (kb < nb && j < b) codes_out[(r * (int64_t)D + (int64_t)kb * 32) * b / 32 + j] = word;
       }
     }
   }
