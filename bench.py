@@ -339,23 +339,32 @@ def matmul_anchor(torch, n=8192, reps=10):
     through the vendor BLAS (torch.matmul) on N(0, 1) operands, the fp16
     matmul row of the paper's anchors (App. "Measured hardware constants",
     Table "anchors": an 8192^3 GEMM).  A measurement, not a step of the path."""
+    def timed(a, b):
+        for _ in range(3):
+            c = torch.matmul(a, b)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            c = torch.matmul(a, b)
+        e1.record()
+        e1.synchronize()
+        del c
+        return e0.elapsed_time(e1) / reps
+
     g = torch.Generator(device="cuda").manual_seed(5)
     a = torch.randn(n, n, device="cuda", dtype=torch.float16, generator=g)
     b = torch.randn(n, n, device="cuda", dtype=torch.float16, generator=g)
-    for _ in range(3):
-        c = torch.matmul(a, b)
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for _ in range(reps):
-        c = torch.matmul(a, b)
-    e1.record()
-    e1.synchronize()
-    ms = e0.elapsed_time(e1) / reps
-    del a, b, c
+    ms = timed(a, b)
+    # the same GEMM on all-zero operands: the matrix units' rate depends on
+    # the operand data (switching activity), so the anchor uses random data
+    a.zero_()
+    b.zero_()
+    ms0 = timed(a, b)
+    del a, b
     tf = 2.0 * n ** 3 / (ms / 1e3) / 1e12
     return {"workload": f"fp16 GEMM {n}^3 (torch.matmul), N(0, 1) operands", "ms": ms, "TFLOPs": tf,
-            "frac_of_spec": tf / MFMA_F16_PEAK_TFLOPS}
+            "frac_of_spec": tf / MFMA_F16_PEAK_TFLOPS, "TFLOPs_zero_operands": 2.0 * n ** 3 / (ms0 / 1e3) / 1e12}
 
 
 def qeps_widths(lam, torch, raw_sets, raw_out, ctx, triad_gbs, reps=20):
