@@ -22,7 +22,7 @@
 //                pair); a pair within rounding distance of delta^2 is decided
 //                by the same wave on exact integers (exact.h: six 64-bit limbs
 //                hold the squared distance scaled to an integer).
-//   resolve   -- one workgroup of 1,024 threads: a row with a store hit is
+//   resolve   -- in a workgroup of 1,024 threads: a row with a store hit is
 //                dropped, a row with no in-chunk edge is kept; the others copy
 //                their earlier in-chunk neighbours into LDS lists and decide in
 //                rounds (a row decides once every earlier neighbour has: it
@@ -31,6 +31,10 @@
 //                order with the kept mask in its registers instead.
 //   append    -- kept rows join the store; for dropped rows ||x - rep||^2 in
 //                binary64 feeds the measured bound delta_hat.
+// The resolve and the append are one launch (k_resolve_append): each
+// workgroup resolves the chunk's rows up to its own last one in its LDS and
+// appends its 16 rows.  The banded store keeps them apart (k_resolve,
+// k_lsh_insert, k_append), since its index insertion sits between them.
 //
 // Error bound of the screen (dot-product units), for rows a, b:
 //   |c16 - a.b| <= K1 (||a||^2 + ||b||^2)/2 + K2 (||a||_1 + ||b||_1) + K3
