@@ -284,7 +284,7 @@ __global__ __launch_bounds__(C::kThreads, C::kMinWaves) void k_screen(ScreenArgs
   static_assert(C::BM == C::BN, "the in-chunk triangle needs square tiles");
   static_assert(C::BM <= C::kThreads, "one thread per A row for the row terms");
   __shared__ _Float16 lds[C::kLdsHalves];
-  __shared__ float hbA[C::BM];
+  __shared__ __attribute__((aligned(16))) float hbA[C::BM];
   __shared__ float emx[C::kWaves];
   // (no early exit on the status words: the screen writes only chunk scratch,
   // and every kernel that writes caller outputs or the store checks them)
@@ -393,13 +393,22 @@ __global__ __launch_bounds__(C::kThreads, C::kMinWaves) void k_screen(ScreenArgs
     float mx = -3.0e38f, cmax = -3.0e38f;
 #pragma unroll
     for (int ti = 0; ti < C::TI; ++ti) {
+      // the row terms of this lane's 16 rows of the 32 x 32 tile: four
+      // consecutive rows per 16-byte LDS read, all read (every entry of hbA is
+      // written) before any is used, so no read waits behind a row's validity
+      const int rb = wm * C::TI * 32 + ti * 32;
+      float4 h4[4];
+#pragma unroll
+      for (int g = 0; g < 4; ++g) h4[g] = *reinterpret_cast<const float4*>(&hbA[rb + acc_row(4 * g, lane)]);
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int ial = wm * C::TI * 32 + ti * 32 + acc_row(r, lane);
+        const int ial = rb + acc_row(r, lane);
         const int ia = ta * C::BM + ial;
         const bool valid = vB && ial < rowsA && (MODE == 0 || ia < ib);
+        const float4 hg = h4[r >> 2];
+        const float hv = (r & 3) == 0 ? hg.x : (r & 3) == 1 ? hg.y : (r & 3) == 2 ? hg.z : hg.w;
         const float dot = acc[ti][tj][r] * kInvScale2;
-        const float v = dot - hbA[ial];
+        const float v = dot - hv;
         mx = valid ? fmaxf(mx, v) : mx;
         if (WANT_MAX) {
           if (MODE == 0) cmax = valid ? fmaxf(cmax, dot) : cmax;
