@@ -358,22 +358,23 @@ __global__ __launch_bounds__(C::kThreads, C::kMinWaves) void k_screen(ScreenArgs
   floatx16 acc[C::TI][C::TJ];
   const _Float16* tA = A + (int64_t)ta * C::BM * a.D;
   const _Float16* tB = a.B + (int64_t)tb * C::BN * a.D;
+  // Called by gemm_tile once the first slabs' loads are issued and before it
+  // waits for any: the store size when the host does not know it, then the
+  // A side's row terms into LDS and each wave's largest error term among the
+  // tile's rows (the error bound uses the tile's largest), all while the
+  // slabs load.  gemm_tile ends with a barrier, so the epilogue sees them.
   auto go_on = [&]() {
-    if (known) return true;
-    rowsA = min(C::BM, a.meta->m - ta * C::BM);
-    return rowsA > 0;
-  };
-  if (!gemm_tile<C, NS>(tA, rowsLim, tB, rowsB, a.D, a.D, lds, acc, go_on)) return;
-  if ((int)threadIdx.x >= rowsA) eA = 0.0f;
-
-  {
-    // A-side row terms; the error bound uses the largest term among the tile's rows
+    if (!known) {
+      rowsA = min(C::BM, a.meta->m - ta * C::BM);
+      if (rowsA <= 0) return false;
+    }
     if ((int)threadIdx.x < C::BM) hbA[threadIdx.x] = hA;
-    float e = eA;
+    float e = (int)threadIdx.x < rowsA ? eA : 0.0f;
     for (int o = 32; o > 0; o >>= 1) e = fmaxf(e, __shfl_xor(e, o));
     if (lane == 0) emx[wave] = e;
-  }
-  __syncthreads();
+    return true;
+  };
+  if (!gemm_tile<C, NS>(tA, rowsLim, tB, rowsB, a.D, a.D, lds, acc, go_on)) return;
   const int wm = wave / C::WN, wn = wave % C::WN;
   float ebA = emx[0];
 #pragma unroll
