@@ -266,6 +266,44 @@ __device__ __forceinline__ void unpack32(const uint32_t* __restrict__ w, _Float1
   }
 }
 
+// NC (16 or 32) b-bit codes from NC * B / 32 whole words (element 0 at bit 0)
+// to fp16, as unpack32 does.
+template <int B, int NC>
+__device__ __forceinline__ void unpack_codes(const uint32_t* __restrict__ w, _Float16* __restrict__ out) {
+  static_assert(NC == 16 || NC == 32, "a half or a whole group");
+  constexpr int NW = NC * B / 32;
+  if constexpr (NC == 32) {
+    unpack32<B>(w, out);
+  } else if constexpr (B == 8) {
+#pragma unroll
+    for (int i = 0; i < NW; ++i) {
+      const uint32_t x = w[i] ^ 0x80808080u;
+      const uint32_t lo = __builtin_amdgcn_perm(0x64646464u, x, 0x04010400u);
+      const uint32_t hi = __builtin_amdgcn_perm(0x64646464u, x, 0x04030402u);
+      const half2v off = {(_Float16)1152.0f, (_Float16)1152.0f};
+      const half2v a = __builtin_bit_cast(half2v, lo) - off;
+      const half2v b = __builtin_bit_cast(half2v, hi) - off;
+      out[4 * i + 0] = a.x;
+      out[4 * i + 1] = a.y;
+      out[4 * i + 2] = b.x;
+      out[4 * i + 3] = b.y;
+    }
+  } else {
+    uint32_t v[NW + 1];
+#pragma unroll
+    for (int i = 0; i < NW; ++i) v[i] = w[i];
+    v[NW] = 0u;
+#pragma unroll
+    for (int e = 0; e < NC; ++e) {
+      const int bit = e * B, wi = bit >> 5, off = bit & 31;
+      uint32_t u = v[wi] >> off;
+      if (off + B > 32) u |= v[wi + 1] << (32 - off);
+      const int32_t c = (int32_t)(u << (32 - B)) >> (32 - B);
+      out[e] = (_Float16)(float)c;
+    }
+  }
+}
+
 // One group of 32 b-bit codes (B consecutive words starting at word w0 of the
 // buffer, or zeros when !ok): the widest loads the group's alignment allows
 // (a group starts at a multiple of B words), so a lane asks for its bytes in
@@ -809,22 +847,32 @@ __global__ __launch_bounds__(FilterTile::kThreads, FilterTile::kMinWaves) void k
   const __amdgpu_buffer_rsrc_t rsC = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint32_t*>(a.codes + rbase * a.row_words), (short)0, (int)(rows * a.row_words * 4), 0x00020000);
   const __amdgpu_buffer_rsrc_t rsQ = tile_rsrc(a.qhi + qbase * a.D, qrows, a.D);
-  const int urow = tid >> 1, uhalf = tid & 1;   // code groups: two per row, threads 0-255
-  const bool unpacker = tid < 2 * kTB;
-  auto load = [&](int s, uint32_t (&cw)[B], uint4 (&qv)[C::kPerB]) {
+  // Code unpacking: for even widths every thread takes 16 codes of its row's
+  // 64-code slab (B / 2 whole words: a quarter of the row), so all eight waves
+  // share it; for odd widths threads 0-255 take 32 codes (B words) each.
+  // (With half the waves unpacking, the other half waited at every slab's
+  // barrier.)
+  constexpr bool kQuarter = (B % 2) == 0;
+  constexpr int kNW = kQuarter ? B / 2 : B;   // code words per thread and slab
+  constexpr int kNC = kQuarter ? 16 : 32;     // codes per thread and slab
+  static_assert(!kQuarter || C::kThreads == 4 * kTB, "four threads per row");
+  const int urow = kQuarter ? tid >> 2 : tid >> 1;
+  const int upart = kQuarter ? tid & 3 : tid & 1;
+  const bool unpacker = kQuarter || tid < 2 * kTB;
+  auto load = [&](int s, uint32_t (&cw)[kNW], uint4 (&qv)[C::kPerB]) {
     const int k0 = s * kBK;
     const bool ok = unpacker && urow < rows && k0 < a.D;
-    const uint32_t w0 = (uint32_t)(urow * a.row_words + (int64_t)(k0 / 32 + uhalf) * B);
-    load_group<B>(rsC, ok, w0, cw);
+    const uint32_t w0 = (uint32_t)(urow * a.row_words + (int64_t)(k0 / 32) * B + upart * kNW);
+    load_group<kNW>(rsC, ok, w0, cw);
     slab_load_n<C::kPerB>(rsQ, qrows, a.D, k0, a.D, qv, C::kThreads);
   };
-  auto store = [&](int st, const uint32_t (&cw)[B], const uint4 (&qv)[C::kPerB]) {
+  auto store = [&](int st, const uint32_t (&cw)[kNW], const uint4 (&qv)[C::kPerB]) {
     if (unpacker) {
-      _Float16 h[32];
-      unpack32<B>(cw, h);
-      _Float16* dst = sa(st) + urow * kLdk + uhalf * 32;
+      _Float16 h[kNC];
+      unpack_codes<B, kNC>(cw, h);
+      _Float16* dst = sa(st) + urow * kLdk + upart * kNC;
 #pragma unroll
-      for (int i = 0; i < 32; i += 8) *reinterpret_cast<uint4*>(dst + i) = *reinterpret_cast<const uint4*>(h + i);
+      for (int i = 0; i < kNC; i += 8) *reinterpret_cast<uint4*>(dst + i) = *reinterpret_cast<const uint4*>(h + i);
     }
     slab_store_n<C::kPerB>(sb(st), qv, C::kThreads);
   };
@@ -844,7 +892,7 @@ __global__ __launch_bounds__(FilterTile::kThreads, FilterTile::kMinWaves) void k
     }
   };
   {
-    uint32_t cw[3][B];
+    uint32_t cw[3][kNW];
     uint4 qv[3][C::kPerB];
 #pragma unroll
     for (int u = 0; u < 3; ++u) load(u, cw[u], qv[u]);
