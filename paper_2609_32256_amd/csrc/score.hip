@@ -817,13 +817,14 @@ __global__ __launch_bounds__(FilterTile::kThreads, FilterTile::kMinWaves) void k
   using C = FilterTile;
   __shared__ _Float16 lds[C::kLdsHalves];
   const int64_t nt = a.tile_end;   // store tiles of this pass (tile_begin = 0)
-  const int64_t logical = xcd_remap((int64_t)blockIdx.x, (int64_t)a.nqt * nt);
-  const int64_t per = (int64_t)kFilterGroupQ * nt;
-  const int g = (int)(logical / per);
-  const int64_t l = logical - (int64_t)g * per;
-  const int gsize = min(kFilterGroupQ, a.nqt - g * kFilterGroupQ);
-  const int qt = g * kFilterGroupQ + (int)(l % gsize);
-  const int64_t rbase = (l / gsize) * kTB;
+  // 32-bit index arithmetic: the host keeps the grid (nqt * nt) below 2^31
+  const uint32_t logical = (uint32_t)xcd_remap32((int)blockIdx.x, (int)(a.nqt * nt));
+  const uint32_t per = (uint32_t)(kFilterGroupQ * nt);
+  const uint32_t g = logical / per;
+  const uint32_t l = logical - g * per;
+  const uint32_t gsize = (uint32_t)min(kFilterGroupQ, a.nqt - (int)g * kFilterGroupQ);
+  const int qt = (int)(g * kFilterGroupQ + l % gsize);
+  const int64_t rbase = (int64_t)(l / gsize) * kTB;
   const int rows = (int)min<int64_t>(kTB, a.n - rbase);
   const int64_t qbase = (int64_t)qt * kTB;
   const int qrows = (int)min<int64_t>(kTB, a.nq - qbase);
@@ -1342,6 +1343,10 @@ lam_status score_topk_impl(lam_ctx* ctx, const ScoreView& st, const float* q, in
   // entries fit the partial lists' buffer
   const bool filter_sample =
       two_pass && (D == 768 || D == 1024) && stiles * kSampleEntries <= (int64_t)cands_max;
+  // the filter pipeline's grids (sample and filter passes) are one workgroup
+  // per (query tile, store tile), indexed in 32 bits
+  LAM_CHECK(!two_pass || !(D == 768 || D == 1024) || (int64_t)nqt * ntiles < (1LL << 31), LAM_EINVAL,
+            "scoring grid too large");
   const uint32_t cap = kCandCap;
 
   // every buffer first
