@@ -532,10 +532,44 @@ __global__ __launch_bounds__(kWG, 2) void k_score(ScoreArgs a) {
   }
 }
 
+// The largest of the wave's 64-bit keys, on every lane: data-parallel
+// primitive moves (DPP) between lanes, which do not go through LDS -- within
+// quads (swap of neighbours, then of pairs), across the quads of each half
+// row (mirror), across the halves of each row of 16 (mirror), then row 0 into
+// row 1 and row 2 into row 3 (broadcast of lane 15), and rows 0-1 into rows
+// 2-3 (broadcast of lane 31); lane 63 then holds the maximum.  A lane that a
+// move does not write keeps its own key (the max's identity).
+__device__ __forceinline__ unsigned long long wave_max_u64(unsigned long long key) {
+  uint32_t lo = (uint32_t)key, hi = (uint32_t)(key >> 32);
+  auto take = [&](uint32_t olo, uint32_t ohi) {
+    const unsigned long long o = ((unsigned long long)ohi << 32) | olo;
+    const unsigned long long c = ((unsigned long long)hi << 32) | lo;
+    if (o > c) {
+      lo = olo;
+      hi = ohi;
+    }
+  };
+#define LAM_DPP_STEP(ctrl, row_mask)                                                                     \
+  take((uint32_t)__builtin_amdgcn_update_dpp((int)lo, (int)lo, ctrl, row_mask, 0xf, false),              \
+       (uint32_t)__builtin_amdgcn_update_dpp((int)hi, (int)hi, ctrl, row_mask, 0xf, false))
+  LAM_DPP_STEP(0xb1, 0xf);    // quad_perm [1, 0, 3, 2]
+  LAM_DPP_STEP(0x4e, 0xf);    // quad_perm [2, 3, 0, 1]
+  LAM_DPP_STEP(0x141, 0xf);   // row_half_mirror
+  LAM_DPP_STEP(0x140, 0xf);   // row_mirror
+  LAM_DPP_STEP(0x142, 0xa);   // row_bcast:15 into rows 1 and 3
+  LAM_DPP_STEP(0x143, 0xc);   // row_bcast:31 into rows 2 and 3
+#undef LAM_DPP_STEP
+  const uint32_t rlo = (uint32_t)__builtin_amdgcn_readlane((int)lo, 63);
+  const uint32_t rhi = (uint32_t)__builtin_amdgcn_readlane((int)hi, 63);
+  return ((unsigned long long)rhi << 32) | rlo;
+}
+
 // Fold a lane's share of candidates into a sorted register list, then take k
 // rounds of the best list head of the wave under (score desc, row asc).  Rows
 // are distinct, so the winning head identifies its lane.  Writes the k picks
-// (ids mapped to global ids) and/or the k-th score.
+// (ids mapped to global ids) and/or the k-th score.  The head's order is that
+// of the key (order-encoded score, complement of the row): larger is better;
+// scores are taken + 0.0f so that -0 and +0 are equal, as in `better`.
 template <int KL>
 __device__ __forceinline__ void wave_select(int k, float (&ls)[KL], int (&lr)[KL], int64_t j,
                                             const int64_t* __restrict__ ids, float* __restrict__ out_s,
@@ -543,13 +577,11 @@ __device__ __forceinline__ void wave_select(int k, float (&ls)[KL], int (&lr)[KL
                                             float kth_drop = 0.0f) {
   const int lane = threadIdx.x & 63;
   for (int t = 0; t < k; ++t) {
-    float bs = ls[0];
-    int br = lr[0];
-    for (int o = 32; o > 0; o >>= 1) {
-      const float os = __shfl_xor(bs, o);
-      const int orr = __shfl_xor(br, o);
-      if (better(os, orr, bs, br)) { bs = os; br = orr; }
-    }
+    const unsigned long long key =
+        ((unsigned long long)f2ord(ls[0] + 0.0f) << 32) | (unsigned long long)(uint32_t)~(uint32_t)lr[0];
+    const unsigned long long best = wave_max_u64(key);
+    const float bs = ord2f((uint32_t)(best >> 32));
+    const int br = (int)~(uint32_t)best;
     if (br != kNoRow && lr[0] == br) {        // this lane's head won: pop it
 #pragma unroll
       for (int p = 0; p < KL - 1; ++p) {
