@@ -54,6 +54,7 @@
 #include "lam_internal.h"
 #include "mfma_tile.h"
 #include "qround.h"
+#include "wave.h"
 
 namespace lam {
 
@@ -114,11 +115,6 @@ __device__ __forceinline__ float round_down_f32(double d) {
   float f = (float)d;
   if ((double)f > d) f = __uint_as_float(f > 0.0f ? __float_as_uint(f) - 1u : (f == 0.0f ? 0x80000001u : __float_as_uint(f) + 1u));
   return f;
-}
-
-__device__ __forceinline__ double wave_sum_f64(double v) {
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-  return v;
 }
 
 // ------------------------------------------------------------------ prep
@@ -369,8 +365,7 @@ __global__ __launch_bounds__(C::kThreads, C::kMinWaves) void k_screen(ScreenArgs
       if (rowsA <= 0) return false;
     }
     if ((int)threadIdx.x < C::BM) hbA[threadIdx.x] = hA;
-    float e = (int)threadIdx.x < rowsA ? eA : 0.0f;
-    for (int o = 32; o > 0; o >>= 1) e = fmaxf(e, __shfl_xor(e, o));
+    const float e = wave_max_f32((int)threadIdx.x < rowsA ? eA : 0.0f);
     if (lane == 0) emx[wave] = e;
     return true;
   };
@@ -499,7 +494,11 @@ __device__ bool pair_within(const float* pa, const float* pb, int D, double d2, 
     s = fma(t2, t2, s);
     s = fma(t3, t3, s);
   }
-  for (int o = G / 2; o > 0; o >>= 1) s += __shfl_xor(s, o);   // every lane of the group holds the sum
+  if constexpr (G == 64) {
+    s = wave_sum_f64(s);   // a whole wave: every lane holds the sum
+  } else {
+    for (int o = G / 2; o > 0; o >>= 1) s += __shfl_xor(s, o);   // every lane of the group holds the sum
+  }
   const double tol = (double)(D + 8) * 2.5e-16 * fmax(d2, s) + 1e-300;
   *margin = fabs(s - d2);
   if (*margin > tol) {
@@ -1338,7 +1337,7 @@ __device__ __forceinline__ void append_maxima(const AppendArgs& a, double dmax, 
                                               uint32_t am0, uint32_t hm0, double* part, uint32_t* apart,
                                               uint32_t* hpart) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  for (int o = 32; o > 0; o >>= 1) amax = max(amax, (uint32_t)__shfl_xor((int)amax, o));
+  amax = wave_max_u32(amax);
   if (lane == 0) {
     part[wave] = dmax;
     apart[wave] = amax;

@@ -34,6 +34,7 @@
 
 #include "lam_internal.h"
 #include "mfma_tile.h"
+#include "wave.h"
 
 namespace lam {
 namespace {
@@ -126,11 +127,9 @@ __global__ __launch_bounds__(256) void k_score_prep(const float* __restrict__ q,
   } else {
     for (int d = lane; d < D; d += 64) take1(p[d], d >= l1_from);
   }
-  for (int o = 32; o > 0; o >>= 1) {
-    mx = fmaxf(mx, __shfl_xor(mx, o));
-    l1 += __shfl_xor(l1, o);
-    l2 += __shfl_xor(l2, o);
-  }
+  mx = wave_max_f32(mx);
+  l1 = wave_sum_f64(l1);
+  l2 = wave_sum_f64(l2);
   bad = __ballot(bad) != 0ull;
   int e = 0;
   if (!bad && mx > 0.0f) e = 14 - ilogbf(mx);   // max |q| 2^e in [2^14, 2^15)
@@ -167,15 +166,18 @@ __global__ __launch_bounds__(256) void k_score_prep(const float* __restrict__ q,
       qlo[j * D + d] = l;
     }
   }
-  for (int o = 32; o > 0; o >>= 1) dh2 += __shfl_xor(dh2, o);
+  dh2 = wave_sum_f64(dh2);
   if (lane == 0) {
     QMeta m;
     m.osc = (float)ldexp(s, -e);
-    m.bound = bad ? __builtin_nanf("") : ru32(eps * l1 * (1.0 + 0x1p-50));
+    // (a binary64 sum of D non-negative terms is below the exact one by at most
+    // (D - 1) 2^-53 relative, in any order; products and sqrt add 2^-53 each)
+    const double up = 1.0 + (double)(D + 4) * 0x1p-52;
+    m.bound = bad ? __builtin_nanf("") : ru32(eps * l1 * up);
     m.bad = bad ? 1 : 0;
     const double g = 2.0 * (double)(D + 64) * 0x1p-24;
-    const double qn = sqrt(l2) * (1.0 + 0x1p-50);
-    const double dh = sqrt(dh2) * (1.0 + 0x1p-50);
+    const double qn = sqrt(l2) * up;
+    const double dh = sqrt(dh2) * up;
     const double E = dh * R + (g + 0x1p-21) * (qn + dh) * R;
     m.err = bad ? 0.0f : ru32(E * (1.0 + 0x1p-20));
     meta[j] = m;
@@ -530,38 +532,6 @@ __global__ __launch_bounds__(kWG, 2) void k_score(ScoreArgs a) {
       a.part_r[o + p] = lr[p];
     }
   }
-}
-
-// The largest of the wave's 64-bit keys, on every lane: data-parallel
-// primitive moves (DPP) between lanes, which do not go through LDS -- within
-// quads (swap of neighbours, then of pairs), across the quads of each half
-// row (mirror), across the halves of each row of 16 (mirror), then row 0 into
-// row 1 and row 2 into row 3 (broadcast of lane 15), and rows 0-1 into rows
-// 2-3 (broadcast of lane 31); lane 63 then holds the maximum.  A lane that a
-// move does not write keeps its own key (the max's identity).
-__device__ __forceinline__ unsigned long long wave_max_u64(unsigned long long key) {
-  uint32_t lo = (uint32_t)key, hi = (uint32_t)(key >> 32);
-  auto take = [&](uint32_t olo, uint32_t ohi) {
-    const unsigned long long o = ((unsigned long long)ohi << 32) | olo;
-    const unsigned long long c = ((unsigned long long)hi << 32) | lo;
-    if (o > c) {
-      lo = olo;
-      hi = ohi;
-    }
-  };
-#define LAM_DPP_STEP(ctrl, row_mask)                                                                     \
-  take((uint32_t)__builtin_amdgcn_update_dpp((int)lo, (int)lo, ctrl, row_mask, 0xf, false),              \
-       (uint32_t)__builtin_amdgcn_update_dpp((int)hi, (int)hi, ctrl, row_mask, 0xf, false))
-  LAM_DPP_STEP(0xb1, 0xf);    // quad_perm [1, 0, 3, 2]
-  LAM_DPP_STEP(0x4e, 0xf);    // quad_perm [2, 3, 0, 1]
-  LAM_DPP_STEP(0x141, 0xf);   // row_half_mirror
-  LAM_DPP_STEP(0x140, 0xf);   // row_mirror
-  LAM_DPP_STEP(0x142, 0xa);   // row_bcast:15 into rows 1 and 3
-  LAM_DPP_STEP(0x143, 0xc);   // row_bcast:31 into rows 2 and 3
-#undef LAM_DPP_STEP
-  const uint32_t rlo = (uint32_t)__builtin_amdgcn_readlane((int)lo, 63);
-  const uint32_t rhi = (uint32_t)__builtin_amdgcn_readlane((int)hi, 63);
-  return ((unsigned long long)rhi << 32) | rlo;
 }
 
 // Fold a lane's share of candidates into a sorted register list, then take k
@@ -1614,8 +1584,10 @@ __global__ __launch_bounds__(256) void k_certify(int64_t nq, int k, const float*
   const float sk = s1[o1 + k - 1], sk1 = s1[o1 + k];
   const bool valid = !isnan(b1[j]);   // NaN bound: the query row holds NaN/Inf
   const double m = (i1[o1 + k] < 0) ? INFINITY : (double)sk - (double)sk1;
-  // (1 + 2^-50) rounds the threshold up past its own evaluation error
-  const double thr = 2.0 * (eps * l1 + sqrt(l2) * dhat + err_per_l1 * l1) * (1.0 + 0x1p-50);
+  // rounded up past its own evaluation error: the binary64 sums of D terms are
+  // within (D - 1) 2^-53 relative in any order, the few products and the
+  // square root add 2^-53 each
+  const double thr = 2.0 * (eps * l1 + sqrt(l2) * dhat + err_per_l1 * l1) * (1.0 + (double)(D + 8) * 0x1p-52);
   cert[j] = (valid && m > thr) ? 1 : 0;
   if (margin) margin[j] = valid ? (float)m : __builtin_nanf("");
 }
