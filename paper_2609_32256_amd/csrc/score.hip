@@ -626,41 +626,6 @@ __global__ __launch_bounds__(256) void k_topk_merge(int64_t nq, int cands, int k
   wave_select<KL>(k, ls, lr, j, ids, out_s, out_i, kth, kth ? 2.0f * meta[j].err : 0.0f);
 }
 
-// One wave per query: the k best of the query's candidate buffer.  A buffer
-// that overflowed is flagged (query and query tile) for the exact fallback.
-template <int KL>
-__global__ __launch_bounds__(256) void k_cand_select(int64_t nq, uint32_t cap, int k, const uint32_t* __restrict__ cnt,
-                                                     const float* __restrict__ cs, const int32_t* __restrict__ cr,
-                                                     const QMeta* __restrict__ meta, const int64_t* __restrict__ ids,
-                                                     float* __restrict__ out_s, int64_t* __restrict__ out_i,
-                                                     float* __restrict__ bound, uint32_t* __restrict__ qflag,
-                                                     uint32_t* __restrict__ tflag) {
-  const int lane = threadIdx.x & 63;
-  const int64_t j = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (j >= nq) return;
-  const uint32_t c = cnt[j];
-  const bool over = c > cap;
-  if (lane == 0) {
-    qflag[j] = over ? 1u : 0u;
-    if (over) atomicOr(&tflag[j / kTB], 1u);
-  }
-  if (write_bad(meta[j], j, k, out_s, out_i, bound) || over) return;
-  float ls[KL];
-  int lr[KL];
-#pragma unroll
-  for (int p = 0; p < KL; ++p) {
-    ls[p] = -INFINITY;
-    lr[p] = kNoRow;
-  }
-  for (uint32_t i = lane; i < c; i += 64) {
-    const int row = cr[j * cap + i];
-    const float sc = cs[j * cap + i];
-    if (!better(sc, row, ls[KL - 1], lr[KL - 1])) continue;
-    list_insert<KL>(ls, lr, sc, row);
-  }
-  wave_select<KL>(k, ls, lr, j, ids, out_s, out_i, nullptr);
-}
-
 // ------------------------------------------------------------------ radix selection (k > 16)
 constexpr int kCandCap = 4096;   // candidate buffer entries per query
 constexpr int kNoAllocMaxQ = 256;   // queries of one allocation-free scoring call
@@ -984,53 +949,16 @@ constexpr int kRescoreCap = 256;     // candidates near the k-th score rescored 
 constexpr int kRescoreThreads = 256;
 constexpr int kRescoreLanes = 16;    // lanes per rescored row
 
-// One workgroup per query, after the selection of the k best hi-only scores H
-// among the candidates.  With h_k the k-th of them, every row of the final
-// top-k has H >= h_k - 2 err (k rows have S >= h_k - err, and |H - S| <= err),
-// so those candidates are rescored from the codes and the float32 query,
-// summed in binary64 and rounded once to float32, and the k best by (S desc,
-// row asc) replace the selection's output.  More than kRescoreCap such
-// candidates (many near-equal scores) flag the query for the exact fallback
-// pass.  Queries already flagged, or invalid, are left as the selection wrote
-// them.  Sixteen lanes share a row (16 rows in flight per workgroup); a lane
-// takes whole groups of 32 codes (B words), unpacked as the scoring kernel
-// unpacks them (exactly, to fp16).
+// The rescoring of m rows (in LDS) of query j from the codes and the float32
+// query, summed in binary64 and rounded once, and a bitonic sort of the keys
+// (score desc, row asc); the kk best go to the outputs.
 template <int B>
-__global__ __launch_bounds__(kRescoreThreads) void k_rescore(
-    int64_t nq, uint32_t cap, int k, const uint32_t* __restrict__ cnt, const float* __restrict__ cs,
-    const int32_t* __restrict__ cr, const QMeta* __restrict__ meta, const int64_t* __restrict__ ids,
-    const float* __restrict__ q, double step, const uint32_t* __restrict__ codes, int64_t row_words, int D,
-    float* __restrict__ out_s, int64_t* __restrict__ out_i, uint32_t* __restrict__ qflag,
-    uint32_t* __restrict__ tflag) {
-  __shared__ int32_t rows[kRescoreCap];
-  __shared__ unsigned long long keys[kRescoreCap];
-  __shared__ uint32_t m_sh;
+__device__ __forceinline__ void rescore_sort(int64_t j, uint32_t m, int kk, int k, const int32_t* rows,
+                                             unsigned long long* keys, const int64_t* __restrict__ ids,
+                                             const float* __restrict__ q, double step,
+                                             const uint32_t* __restrict__ codes, int64_t row_words, int D,
+                                             float* __restrict__ out_s, int64_t* __restrict__ out_i) {
   const int tid = threadIdx.x;
-  const int64_t j = blockIdx.x;
-  if (j >= nq) return;
-  const QMeta mj = meta[j];
-  if (qflag[j] != 0u || mj.bad) return;
-  const uint32_t c = cnt[j];
-  const int kk = (int)min((uint32_t)k, c);
-  if (kk == 0) return;
-  const float thr = rd32((double)out_s[j * k + kk - 1] - 2.0 * (double)mj.err);
-  if (tid == 0) m_sh = 0u;
-  __syncthreads();
-  for (uint32_t i = tid; i < c; i += kRescoreThreads) {
-    if (cs[j * cap + i] >= thr) {
-      const uint32_t p = atomicAdd(&m_sh, 1u);
-      if (p < (uint32_t)kRescoreCap) rows[p] = cr[j * cap + i];
-    }
-  }
-  __syncthreads();
-  const uint32_t m = m_sh;
-  if (m > (uint32_t)kRescoreCap) {
-    if (tid == 0) {
-      qflag[j] = 1u;
-      atomicOr(&tflag[j / kTB], 1u);
-    }
-    return;
-  }
   const float* qj = q + j * D;
   const int slot = tid / kRescoreLanes, sl = tid % kRescoreLanes;
   const int ngroups = D / 32;
@@ -1083,6 +1011,156 @@ __global__ __launch_bounds__(kRescoreThreads) void k_rescore(
   }
 }
 
+// One workgroup per query, after the selection of the k best hi-only scores H
+// among the candidates.  With h_k the k-th of them, every row of the final
+// top-k has H >= h_k - 2 err (k rows have S >= h_k - err, and |H - S| <= err),
+// so those candidates are rescored from the codes and the float32 query,
+// summed in binary64 and rounded once to float32, and the k best by (S desc,
+// row asc) replace the selection's output.  More than kRescoreCap such
+// candidates (many near-equal scores) flag the query for the exact fallback
+// pass.  Queries already flagged, or invalid, are left as the selection wrote
+// them.  Sixteen lanes share a row (16 rows in flight per workgroup); a lane
+// takes whole groups of 32 codes (B words), unpacked as the scoring kernel
+// unpacks them (exactly, to fp16).
+template <int B>
+__global__ __launch_bounds__(kRescoreThreads) void k_rescore(
+    int64_t nq, uint32_t cap, int k, const uint32_t* __restrict__ cnt, const float* __restrict__ cs,
+    const int32_t* __restrict__ cr, const QMeta* __restrict__ meta, const int64_t* __restrict__ ids,
+    const float* __restrict__ q, double step, const uint32_t* __restrict__ codes, int64_t row_words, int D,
+    float* __restrict__ out_s, int64_t* __restrict__ out_i, uint32_t* __restrict__ qflag,
+    uint32_t* __restrict__ tflag) {
+  __shared__ int32_t rows[kRescoreCap];
+  __shared__ unsigned long long keys[kRescoreCap];
+  __shared__ uint32_t m_sh;
+  const int tid = threadIdx.x;
+  const int64_t j = blockIdx.x;
+  if (j >= nq) return;
+  const QMeta mj = meta[j];
+  if (qflag[j] != 0u || mj.bad) return;
+  const uint32_t c = cnt[j];
+  const int kk = (int)min((uint32_t)k, c);
+  if (kk == 0) return;
+  const float thr = rd32((double)out_s[j * k + kk - 1] - 2.0 * (double)mj.err);
+  if (tid == 0) m_sh = 0u;
+  __syncthreads();
+  for (uint32_t i = tid; i < c; i += kRescoreThreads) {
+    if (cs[j * cap + i] >= thr) {
+      const uint32_t p = atomicAdd(&m_sh, 1u);
+      if (p < (uint32_t)kRescoreCap) rows[p] = cr[j * cap + i];
+    }
+  }
+  __syncthreads();
+  const uint32_t m = m_sh;
+  if (m > (uint32_t)kRescoreCap) {
+    if (tid == 0) {
+      qflag[j] = 1u;
+      atomicOr(&tflag[j / kTB], 1u);
+    }
+    return;
+  }
+  rescore_sort<B>(j, m, kk, k, rows, keys, ids, q, step, codes, row_words, D, out_s, out_i);
+}
+
+// The selection and the rescoring in one workgroup per query (k <= 16):
+// wave 0 finds the k-th best hi-only score H among the candidates (per-lane
+// lists of 16, then k rounds of the wave's best head as in wave_select, only
+// the last one kept), and the workgroup then rescores the candidates within
+// 2 err of it as k_rescore does.  Also does the selection's other work:
+// flags an overflowed buffer, writes the bound, NaN outputs for an invalid
+// query, and (-inf, -1) past the candidates.
+template <int B>
+__global__ __launch_bounds__(kRescoreThreads) void k_select_rescore(
+    int64_t nq, uint32_t cap, int k, const uint32_t* __restrict__ cnt, const float* __restrict__ cs,
+    const int32_t* __restrict__ cr, const QMeta* __restrict__ meta, const int64_t* __restrict__ ids,
+    const float* __restrict__ q, double step, const uint32_t* __restrict__ codes, int64_t row_words, int D,
+    float* __restrict__ out_s, int64_t* __restrict__ out_i, float* __restrict__ bound, uint32_t* __restrict__ qflag,
+    uint32_t* __restrict__ tflag) {
+  constexpr int KL = 16;
+  __shared__ int32_t rows[kRescoreCap];
+  __shared__ unsigned long long keys[kRescoreCap];
+  __shared__ uint32_t m_sh;
+  __shared__ float thr_sh;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int64_t j = blockIdx.x;
+  if (j >= nq) return;
+  const uint32_t c = cnt[j];
+  const QMeta mj = meta[j];
+  const bool over = c > cap;
+  if (tid == 0) {
+    qflag[j] = over ? 1u : 0u;
+    if (over) atomicOr(&tflag[j / kTB], 1u);
+    if (bound) bound[j] = mj.bound;
+  }
+  if (mj.bad) {
+    for (int t = tid; t < k; t += kRescoreThreads) {
+      out_s[j * k + t] = __builtin_nanf("");
+      out_i[j * k + t] = -1;
+    }
+    return;
+  }
+  if (over) return;   // the exact fallback redoes the query
+  const int kk = (int)min((uint32_t)k, c);
+  for (int t = kk + tid; t < k; t += kRescoreThreads) {   // fewer candidates than k
+    out_s[j * k + t] = -INFINITY;
+    out_i[j * k + t] = -1;
+  }
+  if (kk == 0) return;
+  if (wave == 0) {
+    float ls[KL];
+    int lr[KL];
+#pragma unroll
+    for (int p = 0; p < KL; ++p) {
+      ls[p] = -INFINITY;
+      lr[p] = kNoRow;
+    }
+    for (uint32_t i = lane; i < c; i += 64) {
+      const int row = cr[j * cap + i];
+      const float sc = cs[j * cap + i];
+      if (!better(sc, row, ls[KL - 1], lr[KL - 1])) continue;
+      list_insert<KL>(ls, lr, sc, row);
+    }
+    float hk = -INFINITY;
+    for (int t = 0; t < kk; ++t) {
+      const unsigned long long key =
+          ((unsigned long long)f2ord(ls[0] + 0.0f) << 32) | (unsigned long long)(uint32_t)~(uint32_t)lr[0];
+      const unsigned long long best = wave_max_u64(key);
+      const int br = (int)~(uint32_t)best;
+      hk = ord2f((uint32_t)(best >> 32));
+      if (br != kNoRow && lr[0] == br) {
+#pragma unroll
+        for (int p = 0; p < KL - 1; ++p) {
+          ls[p] = ls[p + 1];
+          lr[p] = lr[p + 1];
+        }
+        ls[KL - 1] = -INFINITY;
+        lr[KL - 1] = kNoRow;
+      }
+    }
+    if (lane == 0) {
+      thr_sh = rd32((double)hk - 2.0 * (double)mj.err);
+      m_sh = 0u;
+    }
+  }
+  __syncthreads();
+  const float thr = thr_sh;
+  for (uint32_t i = tid; i < c; i += kRescoreThreads) {
+    if (cs[j * cap + i] >= thr) {
+      const uint32_t p = atomicAdd(&m_sh, 1u);
+      if (p < (uint32_t)kRescoreCap) rows[p] = cr[j * cap + i];
+    }
+  }
+  __syncthreads();
+  const uint32_t m = m_sh;
+  if (m > (uint32_t)kRescoreCap) {
+    if (tid == 0) {
+      qflag[j] = 1u;
+      atomicOr(&tflag[j / kTB], 1u);
+    }
+    return;
+  }
+  rescore_sort<B>(j, m, kk, k, rows, keys, ids, q, step, codes, row_words, D, out_s, out_i);
+}
+
 // Lists and fallback give final scores (hi and lo); the filter pass works on
 // hi-only scores.
 template <int B, int KL>
@@ -1110,20 +1188,26 @@ lam_status dispatch_bits(int b, int kl, int mode, dim3 grid, hipStream_t st, con
   return LAM_ESTATE;
 }
 
+// The rescoring after the radix selection (k > 16), or the fused selection
+// and rescoring (k <= 16, fused = true; bound written there too).
 template <int B>
-lam_status launch_rescore(int b, dim3 grid, hipStream_t st, int64_t nq, uint32_t cap, int k, const uint32_t* cnt,
-                          const float* cs, const int32_t* cr, const QMeta* meta, const int64_t* ids, const float* q,
-                          double step, const uint32_t* codes, int64_t row_words, int D, float* out_s,
-                          int64_t* out_i, uint32_t* qflag, uint32_t* tflag) {
+lam_status launch_rescore(int b, bool fused, dim3 grid, hipStream_t st, int64_t nq, uint32_t cap, int k,
+                          const uint32_t* cnt, const float* cs, const int32_t* cr, const QMeta* meta,
+                          const int64_t* ids, const float* q, double step, const uint32_t* codes, int64_t row_words,
+                          int D, float* out_s, int64_t* out_i, float* bound, uint32_t* qflag, uint32_t* tflag) {
   if (b == B) {
-    hipLaunchKernelGGL((k_rescore<B>), grid, dim3(kRescoreThreads), 0, st, nq, cap, k, cnt, cs, cr, meta, ids, q,
-                       step, codes, row_words, D, out_s, out_i, qflag, tflag);
+    if (fused)
+      hipLaunchKernelGGL((k_select_rescore<B>), grid, dim3(kRescoreThreads), 0, st, nq, cap, k, cnt, cs, cr, meta,
+                         ids, q, step, codes, row_words, D, out_s, out_i, bound, qflag, tflag);
+    else
+      hipLaunchKernelGGL((k_rescore<B>), grid, dim3(kRescoreThreads), 0, st, nq, cap, k, cnt, cs, cr, meta, ids, q,
+                         step, codes, row_words, D, out_s, out_i, qflag, tflag);
     LAM_HIP(hipGetLastError());
     return LAM_OK;
   }
   if constexpr (B < 12)
-    return launch_rescore<B + 1>(b, grid, st, nq, cap, k, cnt, cs, cr, meta, ids, q, step, codes, row_words, D, out_s,
-                                 out_i, qflag, tflag);
+    return launch_rescore<B + 1>(b, fused, grid, st, nq, cap, k, cnt, cs, cr, meta, ids, q, step, codes, row_words, D,
+                                 out_s, out_i, bound, qflag, tflag);
   set_error("scoring supports codes of at most 12 bits (got %d)", b);
   return LAM_ESTATE;
 }
@@ -1454,15 +1538,13 @@ lam_status score_topk_impl(lam_ctx* ctx, const ScoreView& st, const float* q, in
   }
   {  // 3. select; 4. exact fallback for overflowed buffers (returns at once otherwise)
     ProfScope ps(ctx, "score_merge", prof);
-    if (KL == 16)
-      hipLaunchKernelGGL((k_cand_select<16>), gq, dim3(256), 0, ctx->stream, nq, cap, k, cand_cnt, cand_s, cand_r,
-                         qmeta, st.ids, scores, ids, bound, qflag, tflag);
-    else
+    if (KL != 16) {
       hipLaunchKernelGGL(k_cand_select_radix, dim3((unsigned)nq), dim3(64), 0, ctx->stream, nq, cap, k, cand_cnt, cand_s, cand_r,
                          qmeta, st.ids, scores, ids, bound, qflag, tflag);
-    LAM_HIP(hipGetLastError());
-    LAM_TRY(launch_rescore<1>(b, dim3((unsigned)nq), ctx->stream, nq, cap, k, cand_cnt, cand_s, cand_r, qmeta,
-                              st.ids, q, st.step, a.codes, a.row_words, D, scores, ids, qflag, tflag));
+      LAM_HIP(hipGetLastError());
+    }
+    LAM_TRY(launch_rescore<1>(b, KL == 16, dim3((unsigned)nq), ctx->stream, nq, cap, k, cand_cnt, cand_s, cand_r,
+                              qmeta, st.ids, q, st.step, a.codes, a.row_words, D, scores, ids, bound, qflag, tflag));
   }
   {
     ProfScope ps(ctx, "score_fallback", prof);
