@@ -204,7 +204,10 @@ def beside_the_step(lam, torch, np, xd, qd, store, rep, pairs, ctx, raw_sets, ra
                  "min_margin_d2": float(min(t["min_margin_d2"] for t in st))}
     del probe
     steady = screen_steady_state(lam, torch, np, ctx)
+    small = screen_steady_state(lam, torch, np, ctx, policy="small")
+    steady["small_tile"] = {k: small[k] for k in ("tile", "screen_ms_per_call", "screen_TFLOPs", "screen_frac_of_peak")}
     steady["screen_frac_of_matmul_anchor"] = steady["screen_TFLOPs"] / matmul["TFLOPs"]
+    steady["screen_frac_of_matmul_anchor_k768"] = steady["screen_TFLOPs"] / matmul["TFLOPs_k768_nt"]
     return {"decisions": decisions,
             "triad": triad,
             "matmul_anchor": matmul,
@@ -273,14 +276,16 @@ def corpus_scoring(lam, torch, np, ctx, calls=5):
             "frac_of_peak": flops / (ms / 1e3) / 1e12 / MFMA_F16_PEAK_TFLOPS}
 
 
-def screen_steady_state(lam, torch, np, ctx, m=262_144, batch=4096, calls=5):
+def screen_steady_state(lam, torch, np, ctx, m=262_144, batch=4096, calls=5, policy="auto"):
     """The screen at scale (D = 768): calls of 4,096 arrivals against the
     store left by ingesting 262,144 rows of the online-store recipe at D = 768
     (clusters of ~51, 20 % planted copies; drawn on the device).  Pairs are
-    the algorithmic pairs of the measured calls."""
+    the algorithmic pairs of the measured calls.  policy: the screen's tile
+    (lam_ctx_set_screen_tile; "auto" takes the 256 x 256 tile at this size)."""
     import synth
     cfg = synth.online_store_device(seed=6, n=m + calls * batch, n_clusters=m // 51, d=D, nq=16)
     x = cfg["x"]
+    ctx.set_screen_tile(policy)
     s = lam.Store(D, TAU, x.shape[0], ctx=ctx)
     for b0 in range(0, m, batch):
         s.ingest(x[b0:b0 + batch], sync=False)
@@ -298,11 +303,16 @@ def screen_steady_state(lam, torch, np, ctx, m=262_144, batch=4096, calls=5):
     t1 = time.perf_counter()
     ctx.profile(False)
     ctx.profile_only(None)
+    ctx.set_screen_tile("auto")
     tot_ms, cnt = ctx.profile_read("dedup_screen")
     before = [size0] + sizes[:-1]
     pairs = sum(batch * k + batch * (batch - 1) // 2 for k in before)
     flops = 2.0 * D * pairs
+    # the automatic choice: 256 x 256 from 768 such tiles in the launch
+    large = policy == "large" or (policy == "auto" and
+                                  ((size0 + 255) // 256) * (batch // 256) + (batch // 256) * (batch // 256 + 1) // 2 >= 768)
     return {"workload": f"online-store recipe at D = {D}: {batch}-row batches against {size0} retained rows",
+            "tile": "256x256" if large else "128x128",
             "calls": calls, "pairs": pairs, "ms_per_call": (t1 - t0) * 1e3 / calls,
             "screen_ms_per_call": tot_ms / max(cnt, 1),
             "M_pairs_per_s": pairs / (t1 - t0) / 1e6,
@@ -356,6 +366,12 @@ def matmul_anchor(torch, n=8192, reps=10):
     a = torch.randn(n, n, device="cuda", dtype=torch.float16, generator=g)
     b = torch.randn(n, n, device="cuda", dtype=torch.float16, generator=g)
     ms = timed(a, b)
+    # at the screen's reduction depth, K = 768, both operands K-major (C = A B^T)
+    ak = torch.randn(32768, 768, device="cuda", dtype=torch.float16, generator=g)
+    bk = torch.randn(32768, 768, device="cuda", dtype=torch.float16, generator=g)
+    ms768 = timed(ak, bk.t())
+    del ak, bk
+    torch.cuda.empty_cache()
     # the same GEMM on all-zero operands: the matrix units' rate depends on
     # the operand data (switching activity), so the anchor uses random data
     a.zero_()
@@ -364,7 +380,9 @@ def matmul_anchor(torch, n=8192, reps=10):
     del a, b
     tf = 2.0 * n ** 3 / (ms / 1e3) / 1e12
     return {"workload": f"fp16 GEMM {n}^3 (torch.matmul), N(0, 1) operands", "ms": ms, "TFLOPs": tf,
-            "frac_of_spec": tf / MFMA_F16_PEAK_TFLOPS, "TFLOPs_zero_operands": 2.0 * n ** 3 / (ms0 / 1e3) / 1e12}
+            "frac_of_spec": tf / MFMA_F16_PEAK_TFLOPS, "TFLOPs_zero_operands": 2.0 * n ** 3 / (ms0 / 1e3) / 1e12,
+            "TFLOPs_k768_nt": 2.0 * 32768 * 32768 * 768 / (ms768 / 1e3) / 1e12,
+            "k768_workload": "fp16 GEMM 32768 x 32768 x 768, C = A B^T (both K-major), N(0, 1) operands"}
 
 
 def qeps_widths(lam, torch, raw_sets, raw_out, ctx, triad_gbs, reps=20):

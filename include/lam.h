@@ -89,6 +89,18 @@ lam_status lam_ctx_profile_only(lam_ctx* ctx, const char* kernel);
 lam_status lam_ctx_profile_reset(lam_ctx* ctx);
 lam_status lam_ctx_profile_read(lam_ctx* ctx, const char* kernel, double* total_ms, int64_t* launches);
 
+/* Tile of the similarity screen (Algorithm "admit": the store and in-chunk
+ * screens of lam_dedup_ingest on an unbanded store).  Two MFMA tilings
+ * compute the same decisions: 128 x 128 tiles (two workgroups per CU), and,
+ * at D = 768 and 1,024, 256 x 256 tiles (one workgroup per CU, half the
+ * operand loads per flop), faster for launches of many tiles and slower for
+ * small ones.  policy: LAM_SCREEN_TILE_AUTO (default: the large tile for a
+ * launch of at least 768 large tiles), LAM_SCREEN_TILE_SMALL or
+ * LAM_SCREEN_TILE_LARGE (every launch, where the dimension allows it).  A
+ * tuning and testing setting of the context; LAM_EINVAL for another value. */
+enum { LAM_SCREEN_TILE_AUTO = 0, LAM_SCREEN_TILE_SMALL = 1, LAM_SCREEN_TILE_LARGE = 2 };
+lam_status lam_ctx_set_screen_tile(lam_ctx* ctx, int policy);
+
 /* ------------------------------------------------------------------ Q_eps   */
 /* Section 2.2 (L1): Q_eps(x) = round(x / 2eps), with round half to even of the
  * exact real quotient of the float32 x by the binary64 step s = 2*eps.  Codes

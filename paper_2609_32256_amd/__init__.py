@@ -101,6 +101,7 @@ _SIGS = {
     "lam_ctx_synchronize": ([_P], ctypes.c_int),
     "lam_ctx_profile": ([_P, ctypes.c_int], ctypes.c_int),
     "lam_ctx_profile_only": ([_P, ctypes.c_char_p], ctypes.c_int),
+    "lam_ctx_set_screen_tile": ([_P, ctypes.c_int], ctypes.c_int),
     "lam_ctx_profile_reset": ([_P], ctypes.c_int),
     "lam_ctx_profile_read": ([_P, ctypes.c_char_p, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(_I64)],
                              ctypes.c_int),
@@ -199,6 +200,12 @@ class Context:
 
     def profile_reset(self):
         _check(_lib.lam_ctx_profile_reset(self._h))
+
+    def set_screen_tile(self, policy):
+        """The screen's tile: "auto" (by launch size), "small" (128 x 128) or
+        "large" (256 x 256 where D is 768 or 1,024).  Decisions are the same."""
+        code = {"auto": 0, "small": 1, "large": 2}.get(policy, policy)
+        _check(_lib.lam_ctx_set_screen_tile(self._h, int(code)))
 
     def profile_read(self, kernel: str):
         ms, n = ctypes.c_double(), _I64()

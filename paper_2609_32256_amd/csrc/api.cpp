@@ -269,6 +269,14 @@ lam_status lam_ctx_profile(lam_ctx* ctx, int enable) {
   return LAM_OK;
 }
 
+lam_status lam_ctx_set_screen_tile(lam_ctx* ctx, int policy) {
+  LAM_CHECK(ctx != nullptr, LAM_EINVAL, "ctx is NULL");
+  LAM_CHECK(policy == LAM_SCREEN_TILE_AUTO || policy == LAM_SCREEN_TILE_SMALL || policy == LAM_SCREEN_TILE_LARGE,
+            LAM_EINVAL, "screen tile policy %d is not one of 0, 1, 2", policy);
+  ctx->screen_tile = policy;
+  return LAM_OK;
+}
+
 lam_status lam_ctx_profile_only(lam_ctx* ctx, const char* kernel) {
   LAM_CHECK(ctx != nullptr, LAM_EINVAL, "ctx is NULL");
   ctx->prof_only = kernel ? kernel : "";

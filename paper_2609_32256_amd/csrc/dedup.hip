@@ -267,27 +267,13 @@ __device__ __forceinline__ void push_pair(const ScreenArgs& a, int i, int kind, 
   }
 }
 
-// One launch screens a chunk against the store (workgroups [0, nb0), MODE 0:
-// A = store rows, B = chunk rows) and against itself (workgroups
-// [nb0, nb0 + nb1), MODE 1: A = B = chunk rows, pairs ia < ib only).  The
-// A side of the error bound is the largest per-row term among the tile's own
-// A rows.
-// NS > 0: the reduction has exactly NS slabs of 64 (D = 64 NS), fully
-// unrolled; NS = 0: any D.  Each is its own kernel, so each gets its own
-// register allocation (the unrolled ones need no scratch memory).
-template <class C, bool WANT_MAX, int NS>
-__global__ __launch_bounds__(C::kThreads, C::kMinWaves) void k_screen(ScreenArgs a) {
-  static_assert(C::BM == C::BN, "the in-chunk triangle needs square tiles");
-  static_assert(C::BM <= C::kThreads, "one thread per A row for the row terms");
-  __shared__ _Float16 lds[C::kLdsHalves];
-  __shared__ __attribute__((aligned(16))) float hbA[C::BM];
-  __shared__ float emx[C::kWaves];
-  // (no early exit on the status words: the screen writes only chunk scratch,
-  // and every kernel that writes caller outputs or the store checks them)
-  const int bid = (int)blockIdx.x;
+// Tile (MODE, ta, tb) of workgroup slot bid of a screen launch: slots
+// [0, nb0) screen the chunk against the store (MODE 0: A = store rows, B =
+// chunk rows), slots [nb0, nb0 + nb1) the chunk against itself (MODE 1: A = B
+// = chunk rows, the lower triangle ta <= tb).
+__device__ __forceinline__ void screen_tile_of(const ScreenArgs& a, int bid, int& MODE, int& ta, int& tb) {
   const int nb0 = (int)a.nb0;
-  const int MODE = bid < nb0 ? 0 : 1;
-  int ta, tb;
+  MODE = bid < nb0 ? 0 : 1;
   if (MODE == 0) {
     // Grouped order: a group is gA store tiles against every chunk tile,
     // swept store tile fastest, and one XCD takes a whole group, so the tiles
@@ -318,58 +304,18 @@ __global__ __launch_bounds__(C::kThreads, C::kMinWaves) void k_screen(ScreenArgs
     tb = t;
     ta = (int)(logical - (int64_t)t * (t + 1) / 2);
   }
-  const _Float16* A = MODE == 0 ? a.As : a.B;
-  const float* hnA = MODE == 0 ? a.hnS : a.hnB;
-  const float* etA = MODE == 0 ? a.etS : a.etB;
-  const int rowsB = min(C::BN, a.nB - tb * C::BN);
-  // When the host does not know the store size, loads start against the
-  // capacity bound and the size is read while they are in flight; tiles past
-  // it stop before the main loop.  Rows between size and capacity only reach
-  // accumulators the epilogue masks out.
-  const bool known = MODE == 1 || a.m_exact >= 0;
-  const int nA0 = MODE == 1 ? a.nB : (known ? a.m_exact : a.capA);
-  const int rowsLim = min(C::BM, nA0 - ta * C::BM);
-  if (rowsLim <= 0 || rowsB <= 0) return;
-  int rowsA = rowsLim;
+}
+
+// The epilogue of one tile: thresholds from the row terms (hbA: the A side's
+// ||y||^2 / 2 in LDS; emx: each wave's largest A error term; hB, eB: this
+// lane's B columns), then the rare path that records hits and ambiguous
+// pairs.  rowsA / rowsB: valid rows of the tile.
+template <class C, bool WANT_MAX>
+__device__ __forceinline__ void screen_epilogue(const ScreenArgs& a, int MODE, int ta, int tb, int rowsA, int rowsB,
+                                                floatx16 (&acc)[C::TI][C::TJ], const float (&hB)[C::TJ],
+                                                const float (&eB)[C::TJ], const float* hbA, const float* emx) {
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
-  const int wn0 = wave % C::WN;
-
-  // Row terms of both sides: loaded before the GEMM, used after it, so their
-  // latency hides behind the first slabs.
-  const __amdgpu_buffer_rsrc_t rhA = f32_rsrc(hnA + (int64_t)ta * C::BM, rowsLim);
-  const __amdgpu_buffer_rsrc_t reA = f32_rsrc(etA + (int64_t)ta * C::BM, rowsLim);
-  const __amdgpu_buffer_rsrc_t rhB = f32_rsrc(a.hnB + (int64_t)tb * C::BN, rowsB);
-  const __amdgpu_buffer_rsrc_t reB = f32_rsrc(a.etB + (int64_t)tb * C::BN, rowsB);
-  const float hA = buf_f32(rhA, (int)threadIdx.x < rowsLim, threadIdx.x);
-  float eA = buf_f32(reA, (int)threadIdx.x < rowsLim, threadIdx.x);
-  float hB[C::TJ], eB[C::TJ];
-#pragma unroll
-  for (int tj = 0; tj < C::TJ; ++tj) {
-    const int ibl = wn0 * C::TJ * 32 + tj * 32 + (lane & 31);
-    hB[tj] = buf_f32(rhB, ibl < rowsB, ibl);
-    eB[tj] = buf_f32(reB, ibl < rowsB, ibl);
-  }
-
-  floatx16 acc[C::TI][C::TJ];
-  const _Float16* tA = A + (int64_t)ta * C::BM * a.D;
-  const _Float16* tB = a.B + (int64_t)tb * C::BN * a.D;
-  // Called by gemm_tile once the first slabs' loads are issued and before it
-  // waits for any: the store size when the host does not know it, then the
-  // A side's row terms into LDS and each wave's largest error term among the
-  // tile's rows (the error bound uses the tile's largest), all while the
-  // slabs load.  gemm_tile ends with a barrier, so the epilogue sees them.
-  auto go_on = [&]() {
-    if (!known) {
-      rowsA = min(C::BM, a.meta->m - ta * C::BM);
-      if (rowsA <= 0) return false;
-    }
-    if ((int)threadIdx.x < C::BM) hbA[threadIdx.x] = hA;
-    const float e = wave_max_f32((int)threadIdx.x < rowsA ? eA : 0.0f);
-    if (lane == 0) emx[wave] = e;
-    return true;
-  };
-  if (!gemm_tile<C, NS>(tA, rowsLim, tB, rowsB, a.D, a.D, lds, acc, go_on)) return;
   const int wm = wave / C::WN, wn = wave % C::WN;
   float ebA = emx[0];
 #pragma unroll
@@ -387,15 +333,30 @@ __global__ __launch_bounds__(C::kThreads, C::kMinWaves) void k_screen(ScreenArgs
       thrIn = round_up_f32(base + e);
     }
     float mx = -3.0e38f, cmax = -3.0e38f;
+    // A store tile with every A row valid: no element needs a validity test
+    // (a lane past rowsB has thrAmb = 3e38, which no finite mx reaches)
+    const bool full = !WANT_MAX && MODE == 0 && rowsA == C::BM;
 #pragma unroll
     for (int ti = 0; ti < C::TI; ++ti) {
       // the row terms of this lane's 16 rows of the 32 x 32 tile: four
       // consecutive rows per 16-byte LDS read, all read (every entry of hbA is
       // written) before any is used, so no read waits behind a row's validity
       const int rb = wm * C::TI * 32 + ti * 32;
+      // with four or more blocks per wave, keep each block's reads with its
+      // use (hoisted together they would not fit beside the accumulators)
+      if constexpr (C::TI * C::TJ >= 4) __builtin_amdgcn_sched_barrier(0);
       float4 h4[4];
 #pragma unroll
       for (int g = 0; g < 4; ++g) h4[g] = *reinterpret_cast<const float4*>(&hbA[rb + acc_row(4 * g, lane)]);
+      if (full) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const float4 hg = h4[r >> 2];
+          const float hv = (r & 3) == 0 ? hg.x : (r & 3) == 1 ? hg.y : (r & 3) == 2 ? hg.z : hg.w;
+          mx = fmaxf(mx, acc[ti][tj][r] * kInvScale2 - hv);
+        }
+        continue;
+      }
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int ial = rb + acc_row(r, lane);
@@ -463,12 +424,98 @@ __global__ __launch_bounds__(C::kThreads, C::kMinWaves) void k_screen(ScreenArgs
   }
 }
 
+// One launch screens a chunk against the store (workgroups [0, nb0), MODE 0:
+// A = store rows, B = chunk rows) and against itself (workgroups
+// [nb0, nb0 + nb1), MODE 1: A = B = chunk rows, pairs ia < ib only).  The
+// A side of the error bound is the largest per-row term among the tile's own
+// A rows.
+// NS > 0: the reduction has exactly NS slabs of 64 (D = 64 NS), fully
+// unrolled; NS = 0: any D.  Each is its own kernel, so each gets its own
+// register allocation (the unrolled ones need no scratch memory).
+template <class C, bool WANT_MAX, int NS, int SETS = 3>
+__global__ __launch_bounds__(C::kThreads, C::kMinWaves) void k_screen(ScreenArgs a) {
+  static_assert(C::BM == C::BN, "the in-chunk triangle needs square tiles");
+  static_assert(C::BM <= C::kThreads, "one thread per A row for the row terms");
+  __shared__ _Float16 lds[C::kLdsHalves];
+  __shared__ __attribute__((aligned(16))) float hbA[C::BM];
+  __shared__ float emx[C::kWaves];
+  // (no early exit on the status words: the screen writes only chunk scratch,
+  // and every kernel that writes caller outputs or the store checks them)
+  const int bid = (int)blockIdx.x;
+  int MODE, ta, tb;
+  screen_tile_of(a, bid, MODE, ta, tb);
+  const _Float16* A = MODE == 0 ? a.As : a.B;
+  const float* hnA = MODE == 0 ? a.hnS : a.hnB;
+  const float* etA = MODE == 0 ? a.etS : a.etB;
+  const int rowsB = min(C::BN, a.nB - tb * C::BN);
+  // When the host does not know the store size, loads start against the
+  // capacity bound and the size is read while they are in flight; tiles past
+  // it stop before the main loop.  Rows between size and capacity only reach
+  // accumulators the epilogue masks out.
+  const bool known = MODE == 1 || a.m_exact >= 0;
+  const int nA0 = MODE == 1 ? a.nB : (known ? a.m_exact : a.capA);
+  const int rowsLim = min(C::BM, nA0 - ta * C::BM);
+  if (rowsLim <= 0 || rowsB <= 0) return;
+  int rowsA = rowsLim;
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int wn0 = wave % C::WN;
+
+  // Row terms of both sides: loaded before the GEMM, used after it, so their
+  // latency hides behind the first slabs.
+  const __amdgpu_buffer_rsrc_t rhA = f32_rsrc(hnA + (int64_t)ta * C::BM, rowsLim);
+  const __amdgpu_buffer_rsrc_t reA = f32_rsrc(etA + (int64_t)ta * C::BM, rowsLim);
+  const __amdgpu_buffer_rsrc_t rhB = f32_rsrc(a.hnB + (int64_t)tb * C::BN, rowsB);
+  const __amdgpu_buffer_rsrc_t reB = f32_rsrc(a.etB + (int64_t)tb * C::BN, rowsB);
+  const float hA = buf_f32(rhA, (int)threadIdx.x < rowsLim, threadIdx.x);
+  float eA = buf_f32(reA, (int)threadIdx.x < rowsLim, threadIdx.x);
+  float hB[C::TJ], eB[C::TJ];
+#pragma unroll
+  for (int tj = 0; tj < C::TJ; ++tj) {
+    const int ibl = wn0 * C::TJ * 32 + tj * 32 + (lane & 31);
+    hB[tj] = buf_f32(rhB, ibl < rowsB, ibl);
+    eB[tj] = buf_f32(reB, ibl < rowsB, ibl);
+  }
+
+  floatx16 acc[C::TI][C::TJ];
+  const _Float16* tA = A + (int64_t)ta * C::BM * a.D;
+  const _Float16* tB = a.B + (int64_t)tb * C::BN * a.D;
+  // Called by gemm_tile once the first slabs' loads are issued and before it
+  // waits for any: the store size when the host does not know it, then the
+  // A side's row terms into LDS and each wave's largest error term among the
+  // tile's rows (the error bound uses the tile's largest), all while the
+  // slabs load.  gemm_tile ends with a barrier, so the epilogue sees them.
+  auto go_on = [&]() {
+    if (!known) {
+      rowsA = min(C::BM, a.meta->m - ta * C::BM);
+      if (rowsA <= 0) return false;
+    }
+    if ((int)threadIdx.x < C::BM) hbA[threadIdx.x] = hA;
+    const float e = wave_max_f32((int)threadIdx.x < rowsA ? eA : 0.0f);
+    if (lane == 0) emx[wave] = e;
+    return true;
+  };
+  if (!gemm_tile<C, NS, SETS>(tA, rowsLim, tB, rowsB, a.D, a.D, lds, acc, go_on)) return;
+  screen_epilogue<C, WANT_MAX>(a, MODE, ta, tb, rowsA, rowsB, acc, hB, eB, hbA, emx);
+}
+
 // 128 x 128, eight waves of 64 x 32 held to 128 registers, so that LDS (two
 // 37 KB stages) and registers both allow two workgroups (four waves per SIMD)
 // per CU: the short reductions (D = 768) are latency-bound, and this
 // occupancy took the subset stream's screen from 1.16 to 1.01 ms against
 // four waves of 64 x 64 at two waves per SIMD.
 using ScreenTile = Tile<2, 4, 2, 1, 4>;
+
+// 256 x 256, sixteen waves of 64 x 64 (64 accumulators per lane, held to 128
+// registers) at four waves per SIMD: one workgroup per CU (two 74 KB
+// stages), half the global loads per flop of the 128 x 128 tile and a third
+// fewer LDS bytes per MFMA, with one slab of loads in flight in registers.
+// Faster when a launch holds many tiles (the steady state of large stores);
+// a lone tile takes more than twice as long, so small launches keep
+// ScreenTile.  (Eight waves of 128 x 64 run as fast but need every register
+// of two waves per SIMD and spill on the rare path.)
+using ScreenTileL = Tile<4, 4, 2, 2, 4>;
+constexpr int64_t kLargeTileMinTiles = 768;   // automatic choice: large tiles from this many
 
 // ------------------------------------------------------------------ merge predicate of one pair
 // sum_d (a_d - b_d)^2 <= delta^2 for float32 rows a, b (16-byte aligned, D a
@@ -1866,7 +1913,15 @@ lam_status dedup_ingest(lam_ctx* ctx, lam_store* st, const float* x, int64_t n, 
       // against the store (rows retained before this chunk; the kernel reads
       // the exact count, the grid covers an upper bound) and inside the chunk
       const int64_t m_grid = m_before + c0;
-      const int tb_rows = ScreenTile::BN;
+      auto grid_of = [&](int rows) {
+        const int64_t nt = (nB + rows - 1) / rows;
+        return ((m_grid + rows - 1) / rows) * nt + nt * (nt + 1) / 2;
+      };
+      const bool large_ok = !want_max && (D == 768 || D == 1024);
+      const bool large = large_ok && (ctx->screen_tile == LAM_SCREEN_TILE_LARGE ||
+                                      (ctx->screen_tile == LAM_SCREEN_TILE_AUTO &&
+                                       grid_of(ScreenTileL::BN) >= kLargeTileMinTiles));
+      const int tb_rows = large ? ScreenTileL::BN : ScreenTile::BN;
       const int ntBt = (nB + tb_rows - 1) / tb_rows;
       sa.ntB = ntBt;
       sa.nb0 = ((m_grid + tb_rows - 1) / tb_rows) * ntBt;
@@ -1878,15 +1933,24 @@ lam_status dedup_ingest(lam_ctx* ctx, lam_store* st, const float* x, int64_t n, 
         hipEvent_t e0, e1;
         LAM_TRY(prof_launch_events(ctx, "dedup_screen", &e0, &e1));
         // the common dims get a fully unrolled reduction
-        const dim3 g((unsigned)grid), b(ScreenTile::kThreads);
-        if (want_max)
-          hipExtLaunchKernelGGL((k_screen<ScreenTile, true, 0>), g, b, 0, ctx->stream, e0, e1, 0, sa);
-        else if (D == 768)
-          hipExtLaunchKernelGGL((k_screen<ScreenTile, false, 12>), g, b, 0, ctx->stream, e0, e1, 0, sa);
-        else if (D == 1024)
-          hipExtLaunchKernelGGL((k_screen<ScreenTile, false, 16>), g, b, 0, ctx->stream, e0, e1, 0, sa);
-        else
-          hipExtLaunchKernelGGL((k_screen<ScreenTile, false, 0>), g, b, 0, ctx->stream, e0, e1, 0, sa);
+        const dim3 g((unsigned)grid);
+        if (large) {
+          const dim3 b(ScreenTileL::kThreads);
+          if (D == 768)
+            hipExtLaunchKernelGGL((k_screen<ScreenTileL, false, 12, 1>), g, b, 0, ctx->stream, e0, e1, 0, sa);
+          else
+            hipExtLaunchKernelGGL((k_screen<ScreenTileL, false, 16, 1>), g, b, 0, ctx->stream, e0, e1, 0, sa);
+        } else {
+          const dim3 b(ScreenTile::kThreads);
+          if (want_max)
+            hipExtLaunchKernelGGL((k_screen<ScreenTile, true, 0>), g, b, 0, ctx->stream, e0, e1, 0, sa);
+          else if (D == 768)
+            hipExtLaunchKernelGGL((k_screen<ScreenTile, false, 12>), g, b, 0, ctx->stream, e0, e1, 0, sa);
+          else if (D == 1024)
+            hipExtLaunchKernelGGL((k_screen<ScreenTile, false, 16>), g, b, 0, ctx->stream, e0, e1, 0, sa);
+          else
+            hipExtLaunchKernelGGL((k_screen<ScreenTile, false, 0>), g, b, 0, ctx->stream, e0, e1, 0, sa);
+        }
         LAM_HIP(hipGetLastError());
       }
       VerifyArgs va{pairs, status, cc, cap, xc, st->x32, D, st->d2, st->thr, firstHit, bitmap, W, hasEdge,

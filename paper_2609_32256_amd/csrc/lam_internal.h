@@ -99,6 +99,7 @@ struct lam_ctx {
   lam::DevBuf scratch[lam::kScratchSlots];
   // profiling
   uint32_t pair_cap = 1u << 20;         // ambiguous-pair list capacity (grows on overflow)
+  int screen_tile = 0;                  // LAM_SCREEN_TILE_*
   bool profiling = false;
   std::string prof_only;                // empty: every kernel
   std::vector<lam::ProfRec> prof;

@@ -141,17 +141,21 @@ __device__ __forceinline__ void slab_store_n(_Float16* __restrict__ s, const uin
 // WN.
 //
 // Pipeline: global loads run two slabs ahead of the MFMAs in two register
-// sets (three slabs ahead in three sets when NS > 0); slab s is multiplied from LDS stage s % 2 while slab s + 1 is written
-// to the other stage, so one barrier per slab suffices and the LDS writes
-// overlap the MFMAs.  Loads past the last slab are issued too (they fall
-// outside the buffer bound, read zeros and touch no memory), so that no load
-// sits behind a branch.  With NS > 0 the reduction has exactly NS slabs and the
-// loop is unrolled, which lets the compiler wait for exactly the loads each
-// LDS store needs (across a loop back edge it waits for all of them); NS = 0
-// takes kdim at run time.  go_on() runs once the first two slabs' loads are in
-// flight; if it returns false the tile is abandoned and gemm_tile returns
-// false.
-template <class C, int NS = 0, class Go>
+// sets (three slabs ahead in three sets when NS > 0 and SETS = 3; one slab
+// ahead in one set when SETS = 1, for tiles whose accumulators leave no room
+// for more: the loads of slab s + 2 are issued once slab s + 1 is in LDS, so
+// they have one slab's MFMAs to land); slab s is multiplied from LDS stage
+// s % 2 while slab s + 1 is written to the other stage, so one barrier per
+// slab suffices and the LDS writes overlap the MFMAs.  With NS > 0 the
+// reduction has exactly NS slabs (kdim = 64 NS) and the loop is unrolled,
+// which lets the compiler wait for exactly the loads each LDS store needs
+// (across a loop back edge it waits for all of them), and loads past the last
+// slab are dropped at compile time.  NS = 0 takes kdim at run time; there the
+// loads past the last slab are issued too (they fall outside the buffer
+// bound, read zeros and touch no memory), so that no load sits behind a
+// branch.  go_on() runs once the first slabs' loads are in flight; if it
+// returns false the tile is abandoned and gemm_tile returns false.
+template <class C, int NS = 0, int SETS = 3, class Go>
 __device__ __forceinline__ bool gemm_tile(const _Float16* __restrict__ A, int ra, const _Float16* __restrict__ B,
                                           int rb, int64_t ld, int kdim, _Float16* lds,
                                           floatx16 (&acc)[C::TI][C::TJ], Go&& go_on) {
@@ -181,35 +185,60 @@ __device__ __forceinline__ bool gemm_tile(const _Float16* __restrict__ A, int ra
     }
   };
   const __amdgpu_buffer_rsrc_t rsA = tile_rsrc(A, ra, ld), rsB = tile_rsrc(B, rb, ld);
+  static_assert(SETS == 3 || (SETS == 1 && NS > 0), "three register sets, or one with an unrolled reduction");
+  // (NS > 0: the caller guarantees kdim = 64 NS <= ld)
   if constexpr (NS > 0) {
-    // Fully unrolled reduction: three register sets, so each slab's loads are
-    // issued three slabs before its LDS store (set and stage indices are
-    // compile-time constants after unrolling).
-    uint4 xa[3][C::kPerA], xb[3][C::kPerB];
-#pragma unroll
-    for (int u = 0; u < 3; ++u) {
-      slab_load_n<C::kPerA>(rsA, ra, ld, u * kBK, kdim, xa[u], C::kThreads);
-      slab_load_n<C::kPerB>(rsB, rb, ld, u * kBK, kdim, xb[u], C::kThreads);
-    }
-    if (!go_on()) return false;
-    slab_store_n<C::kPerA>(sa(0), xa[0], C::kThreads);
-    slab_store_n<C::kPerB>(sb(0), xb[0], C::kThreads);
-    slab_load_n<C::kPerA>(rsA, ra, ld, 3 * kBK, kdim, xa[0], C::kThreads);
-    slab_load_n<C::kPerB>(rsB, rb, ld, 3 * kBK, kdim, xb[0], C::kThreads);
-    __syncthreads();
-#pragma unroll
-    for (int s = 0; s < NS; ++s) {
-      compute(s & 1);
-      if (s + 1 < NS) {
-        const int u = (s + 1) % 3;
-        slab_store_n<C::kPerA>(sa((s + 1) & 1), xa[u], C::kThreads);
-        slab_store_n<C::kPerB>(sb((s + 1) & 1), xb[u], C::kThreads);
-        slab_load_n<C::kPerA>(rsA, ra, ld, (s + 4) * kBK, kdim, xa[u], C::kThreads);
-        slab_load_n<C::kPerB>(rsB, rb, ld, (s + 4) * kBK, kdim, xb[u], C::kThreads);
+    // exactly NS slabs: loads past the last slab are not issued
+    auto load = [&](int slab, uint4 (&xa)[C::kPerA], uint4 (&xb)[C::kPerB]) {
+      if (slab < NS) {
+        slab_load_n<C::kPerA>(rsA, ra, ld, slab * kBK, kdim, xa, C::kThreads);
+        slab_load_n<C::kPerB>(rsB, rb, ld, slab * kBK, kdim, xb, C::kThreads);
       }
+    };
+    if constexpr (SETS == 1) {
+      uint4 xa[C::kPerA], xb[C::kPerB];
+      load(0, xa, xb);
+      if (!go_on()) return false;
+      slab_store_n<C::kPerA>(sa(0), xa, C::kThreads);
+      slab_store_n<C::kPerB>(sb(0), xb, C::kThreads);
+      load(1, xa, xb);
       __syncthreads();
+#pragma unroll
+      for (int s = 0; s < NS; ++s) {
+        compute(s & 1);
+        if (s + 1 < NS) {
+          slab_store_n<C::kPerA>(sa((s + 1) & 1), xa, C::kThreads);
+          slab_store_n<C::kPerB>(sb((s + 1) & 1), xb, C::kThreads);
+          load(s + 2, xa, xb);
+        }
+        __syncthreads();
+      }
+      return true;
+    } else {
+      // three register sets, so each slab's loads are issued three slabs
+      // before its LDS store (set and stage indices are compile-time
+      // constants after unrolling)
+      uint4 xa[3][C::kPerA], xb[3][C::kPerB];
+#pragma unroll
+      for (int u = 0; u < 3; ++u) load(u, xa[u], xb[u]);
+      if (!go_on()) return false;
+      slab_store_n<C::kPerA>(sa(0), xa[0], C::kThreads);
+      slab_store_n<C::kPerB>(sb(0), xb[0], C::kThreads);
+      load(3, xa[0], xb[0]);
+      __syncthreads();
+#pragma unroll
+      for (int s = 0; s < NS; ++s) {
+        compute(s & 1);
+        if (s + 1 < NS) {
+          const int u = (s + 1) % 3;
+          slab_store_n<C::kPerA>(sa((s + 1) & 1), xa[u], C::kThreads);
+          slab_store_n<C::kPerB>(sb((s + 1) & 1), xb[u], C::kThreads);
+          load(s + 4, xa[u], xb[u]);
+        }
+        __syncthreads();
+      }
+      return true;
     }
-    return true;
   }
   const int S = (kdim + kBK - 1) / kBK;
   uint4 a0[C::kPerA], b0[C::kPerB], a1[C::kPerA], b1[C::kPerB];
