@@ -267,13 +267,27 @@ __device__ __forceinline__ void push_pair(const ScreenArgs& a, int i, int kind, 
   }
 }
 
-// Tile (MODE, ta, tb) of workgroup slot bid of a screen launch: slots
-// [0, nb0) screen the chunk against the store (MODE 0: A = store rows, B =
-// chunk rows), slots [nb0, nb0 + nb1) the chunk against itself (MODE 1: A = B
-// = chunk rows, the lower triangle ta <= tb).
-__device__ __forceinline__ void screen_tile_of(const ScreenArgs& a, int bid, int& MODE, int& ta, int& tb) {
+// One launch screens a chunk against the store (workgroups [0, nb0), MODE 0:
+// A = store rows, B = chunk rows) and against itself (workgroups
+// [nb0, nb0 + nb1), MODE 1: A = B = chunk rows, pairs ia < ib only).  The
+// A side of the error bound is the largest per-row term among the tile's own
+// A rows.
+// NS > 0: the reduction has exactly NS slabs of 64 (D = 64 NS), fully
+// unrolled; NS = 0: any D.  Each is its own kernel, so each gets its own
+// register allocation (the unrolled ones need no scratch memory).
+template <class C, bool WANT_MAX, int NS, int SETS = 3>
+__global__ __launch_bounds__(C::kThreads, C::kMinWaves) void k_screen(ScreenArgs a) {
+  static_assert(C::BM == C::BN, "the in-chunk triangle needs square tiles");
+  static_assert(C::BM <= C::kThreads, "one thread per A row for the row terms");
+  __shared__ _Float16 lds[C::kLdsHalves];
+  __shared__ __attribute__((aligned(16))) float hbA[C::BM];
+  __shared__ float emx[C::kWaves];
+  // (no early exit on the status words: the screen writes only chunk scratch,
+  // and every kernel that writes caller outputs or the store checks them)
+  const int bid = (int)blockIdx.x;
   const int nb0 = (int)a.nb0;
-  MODE = bid < nb0 ? 0 : 1;
+  const int MODE = bid < nb0 ? 0 : 1;
+  int ta, tb;
   if (MODE == 0) {
     // Grouped order: a group is gA store tiles against every chunk tile,
     // swept store tile fastest, and one XCD takes a whole group, so the tiles
@@ -304,18 +318,58 @@ __device__ __forceinline__ void screen_tile_of(const ScreenArgs& a, int bid, int
     tb = t;
     ta = (int)(logical - (int64_t)t * (t + 1) / 2);
   }
-}
-
-// The epilogue of one tile: thresholds from the row terms (hbA: the A side's
-// ||y||^2 / 2 in LDS; emx: each wave's largest A error term; hB, eB: this
-// lane's B columns), then the rare path that records hits and ambiguous
-// pairs.  rowsA / rowsB: valid rows of the tile.
-template <class C, bool WANT_MAX>
-__device__ __forceinline__ void screen_epilogue(const ScreenArgs& a, int MODE, int ta, int tb, int rowsA, int rowsB,
-                                                floatx16 (&acc)[C::TI][C::TJ], const float (&hB)[C::TJ],
-                                                const float (&eB)[C::TJ], const float* hbA, const float* emx) {
+  const _Float16* A = MODE == 0 ? a.As : a.B;
+  const float* hnA = MODE == 0 ? a.hnS : a.hnB;
+  const float* etA = MODE == 0 ? a.etS : a.etB;
+  const int rowsB = min(C::BN, a.nB - tb * C::BN);
+  // When the host does not know the store size, loads start against the
+  // capacity bound and the size is read while they are in flight; tiles past
+  // it stop before the main loop.  Rows between size and capacity only reach
+  // accumulators the epilogue masks out.
+  const bool known = MODE == 1 || a.m_exact >= 0;
+  const int nA0 = MODE == 1 ? a.nB : (known ? a.m_exact : a.capA);
+  const int rowsLim = min(C::BM, nA0 - ta * C::BM);
+  if (rowsLim <= 0 || rowsB <= 0) return;
+  int rowsA = rowsLim;
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
+  const int wn0 = wave % C::WN;
+
+  // Row terms of both sides: loaded before the GEMM, used after it, so their
+  // latency hides behind the first slabs.
+  const __amdgpu_buffer_rsrc_t rhA = f32_rsrc(hnA + (int64_t)ta * C::BM, rowsLim);
+  const __amdgpu_buffer_rsrc_t reA = f32_rsrc(etA + (int64_t)ta * C::BM, rowsLim);
+  const __amdgpu_buffer_rsrc_t rhB = f32_rsrc(a.hnB + (int64_t)tb * C::BN, rowsB);
+  const __amdgpu_buffer_rsrc_t reB = f32_rsrc(a.etB + (int64_t)tb * C::BN, rowsB);
+  const float hA = buf_f32(rhA, (int)threadIdx.x < rowsLim, threadIdx.x);
+  float eA = buf_f32(reA, (int)threadIdx.x < rowsLim, threadIdx.x);
+  float hB[C::TJ], eB[C::TJ];
+#pragma unroll
+  for (int tj = 0; tj < C::TJ; ++tj) {
+    const int ibl = wn0 * C::TJ * 32 + tj * 32 + (lane & 31);
+    hB[tj] = buf_f32(rhB, ibl < rowsB, ibl);
+    eB[tj] = buf_f32(reB, ibl < rowsB, ibl);
+  }
+
+  floatx16 acc[C::TI][C::TJ];
+  const _Float16* tA = A + (int64_t)ta * C::BM * a.D;
+  const _Float16* tB = a.B + (int64_t)tb * C::BN * a.D;
+  // Called by gemm_tile once the first slabs' loads are issued and before it
+  // waits for any: the store size when the host does not know it, then the
+  // A side's row terms into LDS and each wave's largest error term among the
+  // tile's rows (the error bound uses the tile's largest), all while the
+  // slabs load.  gemm_tile ends with a barrier, so the epilogue sees them.
+  auto go_on = [&]() {
+    if (!known) {
+      rowsA = min(C::BM, a.meta->m - ta * C::BM);
+      if (rowsA <= 0) return false;
+    }
+    if ((int)threadIdx.x < C::BM) hbA[threadIdx.x] = hA;
+    const float e = wave_max_f32((int)threadIdx.x < rowsA ? eA : 0.0f);
+    if (lane == 0) emx[wave] = e;
+    return true;
+  };
+  if (!gemm_tile<C, NS, SETS>(tA, rowsLim, tB, rowsB, a.D, a.D, lds, acc, go_on)) return;
   const int wm = wave / C::WN, wn = wave % C::WN;
   float ebA = emx[0];
 #pragma unroll
@@ -422,81 +476,6 @@ __device__ __forceinline__ void screen_epilogue(const ScreenArgs& a, int MODE, i
       }
     }
   }
-}
-
-// One launch screens a chunk against the store (workgroups [0, nb0), MODE 0:
-// A = store rows, B = chunk rows) and against itself (workgroups
-// [nb0, nb0 + nb1), MODE 1: A = B = chunk rows, pairs ia < ib only).  The
-// A side of the error bound is the largest per-row term among the tile's own
-// A rows.
-// NS > 0: the reduction has exactly NS slabs of 64 (D = 64 NS), fully
-// unrolled; NS = 0: any D.  Each is its own kernel, so each gets its own
-// register allocation (the unrolled ones need no scratch memory).
-template <class C, bool WANT_MAX, int NS, int SETS = 3>
-__global__ __launch_bounds__(C::kThreads, C::kMinWaves) void k_screen(ScreenArgs a) {
-  static_assert(C::BM == C::BN, "the in-chunk triangle needs square tiles");
-  static_assert(C::BM <= C::kThreads, "one thread per A row for the row terms");
-  __shared__ _Float16 lds[C::kLdsHalves];
-  __shared__ __attribute__((aligned(16))) float hbA[C::BM];
-  __shared__ float emx[C::kWaves];
-  // (no early exit on the status words: the screen writes only chunk scratch,
-  // and every kernel that writes caller outputs or the store checks them)
-  const int bid = (int)blockIdx.x;
-  int MODE, ta, tb;
-  screen_tile_of(a, bid, MODE, ta, tb);
-  const _Float16* A = MODE == 0 ? a.As : a.B;
-  const float* hnA = MODE == 0 ? a.hnS : a.hnB;
-  const float* etA = MODE == 0 ? a.etS : a.etB;
-  const int rowsB = min(C::BN, a.nB - tb * C::BN);
-  // When the host does not know the store size, loads start against the
-  // capacity bound and the size is read while they are in flight; tiles past
-  // it stop before the main loop.  Rows between size and capacity only reach
-  // accumulators the epilogue masks out.
-  const bool known = MODE == 1 || a.m_exact >= 0;
-  const int nA0 = MODE == 1 ? a.nB : (known ? a.m_exact : a.capA);
-  const int rowsLim = min(C::BM, nA0 - ta * C::BM);
-  if (rowsLim <= 0 || rowsB <= 0) return;
-  int rowsA = rowsLim;
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
-  const int wn0 = wave % C::WN;
-
-  // Row terms of both sides: loaded before the GEMM, used after it, so their
-  // latency hides behind the first slabs.
-  const __amdgpu_buffer_rsrc_t rhA = f32_rsrc(hnA + (int64_t)ta * C::BM, rowsLim);
-  const __amdgpu_buffer_rsrc_t reA = f32_rsrc(etA + (int64_t)ta * C::BM, rowsLim);
-  const __amdgpu_buffer_rsrc_t rhB = f32_rsrc(a.hnB + (int64_t)tb * C::BN, rowsB);
-  const __amdgpu_buffer_rsrc_t reB = f32_rsrc(a.etB + (int64_t)tb * C::BN, rowsB);
-  const float hA = buf_f32(rhA, (int)threadIdx.x < rowsLim, threadIdx.x);
-  float eA = buf_f32(reA, (int)threadIdx.x < rowsLim, threadIdx.x);
-  float hB[C::TJ], eB[C::TJ];
-#pragma unroll
-  for (int tj = 0; tj < C::TJ; ++tj) {
-    const int ibl = wn0 * C::TJ * 32 + tj * 32 + (lane & 31);
-    hB[tj] = buf_f32(rhB, ibl < rowsB, ibl);
-    eB[tj] = buf_f32(reB, ibl < rowsB, ibl);
-  }
-
-  floatx16 acc[C::TI][C::TJ];
-  const _Float16* tA = A + (int64_t)ta * C::BM * a.D;
-  const _Float16* tB = a.B + (int64_t)tb * C::BN * a.D;
-  // Called by gemm_tile once the first slabs' loads are issued and before it
-  // waits for any: the store size when the host does not know it, then the
-  // A side's row terms into LDS and each wave's largest error term among the
-  // tile's rows (the error bound uses the tile's largest), all while the
-  // slabs load.  gemm_tile ends with a barrier, so the epilogue sees them.
-  auto go_on = [&]() {
-    if (!known) {
-      rowsA = min(C::BM, a.meta->m - ta * C::BM);
-      if (rowsA <= 0) return false;
-    }
-    if ((int)threadIdx.x < C::BM) hbA[threadIdx.x] = hA;
-    const float e = wave_max_f32((int)threadIdx.x < rowsA ? eA : 0.0f);
-    if (lane == 0) emx[wave] = e;
-    return true;
-  };
-  if (!gemm_tile<C, NS, SETS>(tA, rowsLim, tB, rowsB, a.D, a.D, lds, acc, go_on)) return;
-  screen_epilogue<C, WANT_MAX>(a, MODE, ta, tb, rowsA, rowsB, acc, hB, eB, hbA, emx);
 }
 
 // 128 x 128, eight waves of 64 x 32 held to 128 registers, so that LDS (two
