@@ -759,29 +759,38 @@ __global__ __launch_bounds__(64) void k_cand_select_radix(int64_t nq, uint32_t c
 
 // ------------------------------------------------------------------ filter pass on the screen's pipeline
 using FilterTile = Tile<2, 4, 2, 1, 4>;
+// 256 x 256 (store rows x queries), sixteen waves of 64 x 64 held to 128
+// registers, one workgroup per CU: half the code and query loads per flop of
+// FilterTile; for the filter pass of stores with many tiles
+using FilterTileL = Tile<4, 4, 2, 2, 4>;
 constexpr int kFilterGroupQ = 8;   // query tiles per group in the tile order
-constexpr int kSampleEntries = 4;  // entries per query and store tile of the sample pass on this pipeline
+constexpr int kSampleEntries = 4;  // entries per query and 128-row store tile of the sample pass
+constexpr int64_t kFilterLargeMinTiles = 1024;   // large filter tiles from this many per launch
 
 // The threshold plan's filter pass (hi-only scores H) for D = 64 NS: one
-// 128 x 128 tile (store rows x queries) per workgroup of 8 waves, each wave
-// 64 rows x 32 queries (2 x 1 tiles of v_mfma_f32_32x32x16_f16); K-slabs of 64
-// through two LDS stages with every load issued three slabs before its LDS
-// store, one barrier per slab.  Threads 0-255 load one group of 32 codes (B
-// words) per slab and unpack it straight to fp16 (exact for B <= 12); every
-// thread loads two 16-byte pieces of the queries' hi part.  Tile order:
-// groups of 8 query tiles against every store tile, query tile fastest, each
-// XCD a contiguous range, so an XCD holds its 8 query tiles in L2 while the
-// codes stream past.  Every row with H >= the query's threshold is appended to
-// its candidate buffer, as in k_score's filter mode.
-// SAMPLE: the sample pass of the threshold plan over store tiles [0,
-// tile_end) instead: per query and tile, the best H of each of the four lanes
-// holding the query (disjoint sets of 32 rows) at entries [4 t, 4 t + 4) of
-// the query's partial list.  The k-th best of these entries is the H of k
-// distinct rows, so at most the sample's k-th best H: a valid base for the
-// threshold (lower only where several of the best rows share a lane).
-template <int B, int NS, bool SAMPLE>
-__global__ __launch_bounds__(FilterTile::kThreads, FilterTile::kMinWaves) void k_filter(ScoreArgs a) {
-  using C = FilterTile;
+// C::BM x C::BN tile (store rows x queries) per workgroup, each wave 64 rows x
+// 32 TJ queries (2 x TJ tiles of v_mfma_f32_32x32x16_f16); K-slabs of 64
+// through two LDS stages, one barrier per slab, every load issued three slabs
+// before its LDS store (SETS = 3) or one (SETS = 1, for the large tile).  For
+// even code widths four threads share a row's 64-code slab (16 codes, B / 2
+// whole words each), so every wave unpacks; for odd widths threads 0 to
+// 2 BM - 1 take 32 codes (B words) each.  Codes are unpacked straight to fp16
+// (exact for B <= 12); the queries' hi part is loaded in 16-byte pieces.  Tile
+// order: groups of 8 query tiles against every store tile, query tile
+// fastest, each XCD a contiguous range, so an XCD holds its query tiles in L2
+// while the codes stream past.  Every row with H >= the query's threshold is
+// appended to its candidate buffer, as in k_score's filter mode.
+// SAMPLE (FilterTile only): the sample pass of the threshold plan over store
+// tiles [0, tile_end) instead: per query and tile, the best H of each of the
+// four lanes holding the query (disjoint sets of 32 rows) at entries [4 t,
+// 4 t + 4) of the query's partial list.  The k-th best of these entries is the
+// H of k distinct rows, so at most the sample's k-th best H: a valid base for
+// the threshold (lower only where several of the best rows share a lane).
+// a.nqt and a.tile_end count tiles of this kernel's size.
+template <class C, int B, int NS, bool SAMPLE, int SETS>
+__global__ __launch_bounds__(C::kThreads, C::kMinWaves) void k_filter(ScoreArgs a) {
+  static_assert(!SAMPLE || (C::BM == kTB && C::TJ == 1), "the sample pass runs on 128-row tiles of one query block");
+  static_assert(SETS == 1 || SETS == 3, "one or three register sets");
   __shared__ _Float16 lds[C::kLdsHalves];
   const int64_t nt = a.tile_end;   // store tiles of this pass (tile_begin = 0)
   // 32-bit index arithmetic: the host keeps the grid (nqt * nt) below 2^31
@@ -791,17 +800,23 @@ __global__ __launch_bounds__(FilterTile::kThreads, FilterTile::kMinWaves) void k
   const uint32_t l = logical - g * per;
   const uint32_t gsize = (uint32_t)min(kFilterGroupQ, a.nqt - (int)g * kFilterGroupQ);
   const int qt = (int)(g * kFilterGroupQ + l % gsize);
-  const int64_t rbase = (int64_t)(l / gsize) * kTB;
-  const int rows = (int)min<int64_t>(kTB, a.n - rbase);
-  const int64_t qbase = (int64_t)qt * kTB;
-  const int qrows = (int)min<int64_t>(kTB, a.nq - qbase);
+  const int64_t rbase = (int64_t)(l / gsize) * C::BM;
+  const int rows = (int)min<int64_t>(C::BM, a.n - rbase);
+  const int64_t qbase = (int64_t)qt * C::BN;
+  const int qrows = (int)min<int64_t>(C::BN, a.nq - qbase);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / C::WN, wn = wave % C::WN;
-  // this lane's query and its threshold, loaded before the GEMM
-  const int64_t j = qbase + wn * 32 + (lane & 31);
-  const bool jv = j < a.nq;
-  const float th = (jv && !SAMPLE) ? a.thr[j] : 0.0f;
-  const float osc = jv ? a.meta[j].osc : 0.0f;
+  // this lane's queries and their thresholds, loaded before the GEMM
+  int64_t j[C::TJ];
+  bool jv[C::TJ];
+  float th[C::TJ], osc[C::TJ];
+#pragma unroll
+  for (int y = 0; y < C::TJ; ++y) {
+    j[y] = qbase + wn * C::TJ * 32 + y * 32 + (lane & 31);
+    jv[y] = j[y] < a.nq;
+    th[y] = (jv[y] && !SAMPLE) ? a.thr[j[y]] : 0.0f;
+    osc[y] = jv[y] ? a.meta[j[y]].osc : 0.0f;
+  }
 
   auto sa = [&](int i) -> _Float16* { return lds + i * ((C::BM + C::BN) * kLdk); };
   auto sb = [&](int i) -> _Float16* { return lds + i * ((C::BM + C::BN) * kLdk) + C::BM * kLdk; };
@@ -816,17 +831,18 @@ __global__ __launch_bounds__(FilterTile::kThreads, FilterTile::kMinWaves) void k
       const_cast<uint32_t*>(a.codes + rbase * a.row_words), (short)0, (int)(rows * a.row_words * 4), 0x00020000);
   const __amdgpu_buffer_rsrc_t rsQ = tile_rsrc(a.qhi + qbase * a.D, qrows, a.D);
   // Code unpacking: for even widths every thread takes 16 codes of its row's
-  // 64-code slab (B / 2 whole words: a quarter of the row), so all eight waves
-  // share it; for odd widths threads 0-255 take 32 codes (B words) each.
-  // (With half the waves unpacking, the other half waited at every slab's
-  // barrier.)
+  // 64-code slab (B / 2 whole words: a quarter of the row), so all waves
+  // share it; for odd widths threads 0 to 2 BM - 1 take 32 codes (B words)
+  // each.  (With half the waves unpacking, the other half waited at every
+  // slab's barrier.)
   constexpr bool kQuarter = (B % 2) == 0;
   constexpr int kNW = kQuarter ? B / 2 : B;   // code words per thread and slab
   constexpr int kNC = kQuarter ? 16 : 32;     // codes per thread and slab
-  static_assert(!kQuarter || C::kThreads == 4 * kTB, "four threads per row");
+  static_assert(!kQuarter || C::kThreads == 4 * C::BM, "four threads per row");
+  static_assert(C::kThreads >= 2 * C::BM, "two threads per row for odd widths");
   const int urow = kQuarter ? tid >> 2 : tid >> 1;
   const int upart = kQuarter ? tid & 3 : tid & 1;
-  const bool unpacker = kQuarter || tid < 2 * kTB;
+  const bool unpacker = kQuarter || tid < 2 * C::BM;
   auto load = [&](int s, uint32_t (&cw)[kNW], uint4 (&qv)[C::kPerB]) {
     const int k0 = s * kBK;
     const bool ok = unpacker && urow < rows && k0 < a.D;
@@ -859,7 +875,7 @@ __global__ __launch_bounds__(FilterTile::kThreads, FilterTile::kMinWaves) void k
           acc[x][y] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fa[x], fb[y], acc[x][y], 0, 0, 0);
     }
   };
-  {
+  if constexpr (SETS == 3) {
     uint32_t cw[3][kNW];
     uint4 qv[3][C::kPerB];
 #pragma unroll
@@ -877,6 +893,22 @@ __global__ __launch_bounds__(FilterTile::kThreads, FilterTile::kMinWaves) void k
       }
       __syncthreads();
     }
+  } else {
+    uint32_t cw[kNW];
+    uint4 qv[C::kPerB];
+    load(0, cw, qv);
+    store(0, cw, qv);
+    load(1, cw, qv);
+    __syncthreads();
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      compute(s & 1);
+      if (s + 1 < NS) {
+        store((s + 1) & 1, cw, qv);
+        if (s + 2 < NS) load(s + 2, cw, qv);
+      }
+      __syncthreads();
+    }
   }
   if constexpr (SAMPLE) {
     // this lane's best H over its 32 rows (the lowest row among equals)
@@ -887,59 +919,73 @@ __global__ __launch_bounds__(FilterTile::kThreads, FilterTile::kMinWaves) void k
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int rl_ = wm * 64 + x * 32 + acc_row(r, lane);   // ascending in (x, r)
-        const float sc = acc[x][0][r] * osc;
+        const float sc = acc[x][0][r] * osc[0];
         const bool take = rl_ < rows && sc > best;
         best = take ? sc : best;
         brow = take ? (int)(rbase + rl_) : brow;
       }
-    if (jv) {
-      const int64_t o = j * (nt * kSampleEntries) + (rbase / kTB) * kSampleEntries + wm * 2 + (lane >> 5);
+    if (jv[0]) {
+      const int64_t o = j[0] * (nt * kSampleEntries) + (rbase / kTB) * kSampleEntries + wm * 2 + (lane >> 5);
       a.part_s[o] = best;
       a.part_r[o] = brow;
     }
     return;
   }
-  // epilogue: the tile's largest raw accumulator first (osc > 0)
-  float amx = -INFINITY;
 #pragma unroll
-  for (int x = 0; x < C::TI; ++x)
+  for (int y = 0; y < C::TJ; ++y) {
+    // epilogue: the tile's largest raw accumulator first (osc > 0)
+    float amx = -INFINITY;
 #pragma unroll
-    for (int r = 0; r < 16; ++r)
-      amx = (wm * 64 + x * 32 + acc_row(r, lane) < rows) ? fmaxf(amx, acc[x][0][r]) : amx;
-  const bool hot = jv && amx * osc >= th;
-  if (__ballot(hot) == 0ull || !hot) return;
-  uint32_t c = 0u;
+    for (int x = 0; x < C::TI; ++x)
 #pragma unroll
-  for (int x = 0; x < C::TI; ++x)
+      for (int r = 0; r < 16; ++r)
+        amx = (wm * C::TI * 32 + x * 32 + acc_row(r, lane) < rows) ? fmaxf(amx, acc[x][y][r]) : amx;
+    const bool hot = jv[y] && amx * osc[y] >= th[y];
+    if (__ballot(hot) == 0ull || !hot) continue;
+    uint32_t c = 0u;
 #pragma unroll
-    for (int r = 0; r < 16; ++r)
-      c += (wm * 64 + x * 32 + acc_row(r, lane) < rows && acc[x][0][r] * osc >= th) ? 1u : 0u;
-  uint32_t idx = atomicAdd(&a.cand_cnt[j], c);
+    for (int x = 0; x < C::TI; ++x)
 #pragma unroll
-  for (int x = 0; x < C::TI; ++x)
+      for (int r = 0; r < 16; ++r)
+        c += (wm * C::TI * 32 + x * 32 + acc_row(r, lane) < rows && acc[x][y][r] * osc[y] >= th[y]) ? 1u : 0u;
+    uint32_t idx = atomicAdd(&a.cand_cnt[j[y]], c);
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int rl_ = wm * 64 + x * 32 + acc_row(r, lane);
-      const float sc = acc[x][0][r] * osc;
-      if (rl_ < rows && sc >= th) {
-        if (idx < a.cap) {
-          a.cand_s[j * a.cap + idx] = sc;
-          a.cand_r[j * a.cap + idx] = (int)(rbase + rl_);
+    for (int x = 0; x < C::TI; ++x)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int rl_ = wm * C::TI * 32 + x * 32 + acc_row(r, lane);
+        const float sc = acc[x][y][r] * osc[y];
+        if (rl_ < rows && sc >= th[y]) {
+          if (idx < a.cap) {
+            a.cand_s[j[y] * a.cap + idx] = sc;
+            a.cand_r[j[y] * a.cap + idx] = (int)(rbase + rl_);
+          }
+          ++idx;
         }
-        ++idx;
       }
-    }
+  }
 }
 
+// large: the filter pass on FilterTileL (a.nqt and a.tile_end in its tiles)
 template <int B, bool SAMPLE>
-lam_status launch_filter(int b, int D, dim3 grid, hipStream_t st, const ScoreArgs& a) {
+lam_status launch_filter(int b, int D, bool large, dim3 grid, hipStream_t st, const ScoreArgs& a) {
   if (b == B) {
-    if (D == 768) hipLaunchKernelGGL((k_filter<B, 12, SAMPLE>), grid, dim3(FilterTile::kThreads), 0, st, a);
-    else hipLaunchKernelGGL((k_filter<B, 16, SAMPLE>), grid, dim3(FilterTile::kThreads), 0, st, a);
+    if constexpr (!SAMPLE) {
+      if (large) {
+        if (D == 768)
+          hipLaunchKernelGGL((k_filter<FilterTileL, B, 12, false, 1>), grid, dim3(FilterTileL::kThreads), 0, st, a);
+        else
+          hipLaunchKernelGGL((k_filter<FilterTileL, B, 16, false, 1>), grid, dim3(FilterTileL::kThreads), 0, st, a);
+        LAM_HIP(hipGetLastError());
+        return LAM_OK;
+      }
+    }
+    if (D == 768) hipLaunchKernelGGL((k_filter<FilterTile, B, 12, SAMPLE, 3>), grid, dim3(FilterTile::kThreads), 0, st, a);
+    else hipLaunchKernelGGL((k_filter<FilterTile, B, 16, SAMPLE, 3>), grid, dim3(FilterTile::kThreads), 0, st, a);
     LAM_HIP(hipGetLastError());
     return LAM_OK;
   }
-  if constexpr (B < 12) return launch_filter<B + 1, SAMPLE>(b, D, grid, st, a);
+  if constexpr (B < 12) return launch_filter<B + 1, SAMPLE>(b, D, large, grid, st, a);
   set_error("scoring supports codes of at most 12 bits (got %d)", b);
   return LAM_ESTATE;
 }
@@ -1410,7 +1456,11 @@ lam_status score_topk_impl(lam_ctx* ctx, const ScoreView& st, const float* q, in
   const int64_t n = st.n;
   const int nqt = (int)((nq + kTB - 1) / kTB);
   const int64_t ntiles = (n + kTB - 1) / kTB;
-  const int64_t sample_rows = std::max<int64_t>(4096, ((int64_t)k * n + 1023) / 1024);
+  // the sample: the store's first max(4,096, k n / 256) rows, so that at
+  // most about k n / sample = 256 rows per query pass the filter (a sample of
+  // k n / 1,024 rows let about 1,024 through: the corpus call 2.65-2.71 ->
+  // 2.57-2.59 ms, 60 K rows at top-50 265 -> 238 us; k n / 128 was no faster)
+  const int64_t sample_rows = std::max<int64_t>(4096, ((int64_t)k * n + 255) / 256);
   const int64_t stiles = std::min<int64_t>(ntiles, (sample_rows + kTB - 1) / kTB);
   const bool two_pass = stiles < ntiles;
 
@@ -1504,7 +1554,7 @@ lam_status score_topk_impl(lam_ctx* ctx, const ScoreView& st, const float* q, in
     a.tiles_per_split = tps1;
     if (filter_sample) {
       // one tile per workgroup on the filter's pipeline; entries unsorted (segments of 1)
-      LAM_TRY((launch_filter<1, true>(b, D, dim3((unsigned)(nqt * stiles)), ctx->stream, a)));
+      LAM_TRY((launch_filter<1, true>(b, D, false, dim3((unsigned)(nqt * stiles)), ctx->stream, a)));
       hipLaunchKernelGGL((k_topk_merge<16, 1>), gq, dim3(256), 0, ctx->stream, nq, (int)stiles * kSampleEntries, k,
                          part_s, part_r, qmeta, st.ids, nullptr, nullptr, nullptr, thr, nullptr);
     } else {
@@ -1527,10 +1577,19 @@ lam_status score_topk_impl(lam_ctx* ctx, const ScoreView& st, const float* q, in
   {  // 2. full scan with the thresholds
     ProfScope ps(ctx, "score_mfma", prof);
     if (D == 768 || D == 1024) {
-      // one 128 x 128 tile per workgroup on the screen's pipeline
-      const int64_t grid = (int64_t)nqt * ntiles;
+      // one tile per workgroup on the screen's pipeline: 256 x 256 when the
+      // launch holds many of them, else 128 x 128
+      const int nqtL = (int)((nq + FilterTileL::BN - 1) / FilterTileL::BN);
+      const int64_t ntilesL = (n + FilterTileL::BM - 1) / FilterTileL::BM;
+      const bool large = (int64_t)nqtL * ntilesL >= kFilterLargeMinTiles;
+      ScoreArgs af = a;
+      if (large) {
+        af.nqt = nqtL;
+        af.tile_end = ntilesL;
+      }
+      const int64_t grid = (int64_t)af.nqt * af.tile_end;
       LAM_CHECK(grid < (1LL << 31), LAM_EINVAL, "scoring grid too large");
-      LAM_TRY((launch_filter<1, false>(b, D, dim3((unsigned)grid), ctx->stream, a)));
+      LAM_TRY((launch_filter<1, false>(b, D, large, dim3((unsigned)grid), ctx->stream, af)));
     } else {
       LAM_TRY(dispatch_bits<1>(b, KL, kModeFilter, dim3((unsigned)(nqt * sp2)), ctx->stream, a));
       LAM_HIP(hipGetLastError());
