@@ -180,7 +180,7 @@ def banded_ingest(lam, torch, np, xd, rep_exh, pairs, ctx, r=BAND_R, rel=BAND_RE
     return out
 
 
-def beside_the_step(lam, torch, np, xd, qd, store, rep, pairs, ctx, raw_sets, raw_out):
+def beside_the_step(lam, torch, np, xd, qd, store, rep, pairs, ctx, raw_sets, raw_out, width_codes):
     """Measurements beside the timed step (not in it): the decision
     statistics of the stream (ambiguous pairs, exact decisions, smallest
     decided margin), the triad and matrix-unit anchors, raw Q_eps at three widths,
@@ -211,7 +211,7 @@ def beside_the_step(lam, torch, np, xd, qd, store, rep, pairs, ctx, raw_sets, ra
     return {"decisions": decisions,
             "triad": triad,
             "matmul_anchor": matmul,
-            "qeps_widths": qeps_widths(lam, torch, raw_sets, raw_out, ctx, triad["GBps"]),
+            "qeps_widths": qeps_widths(lam, torch, raw_sets, raw_out, width_codes, ctx, triad["GBps"]),
             "screen_steady_state": steady,
             "one_call": one_call_ingest(lam, torch, np, xd, rep, pairs, ctx),
             "online_store": online_store_run(lam, torch, np, ctx),
@@ -385,16 +385,19 @@ def matmul_anchor(torch, n=8192, reps=10):
             "k768_workload": "fp16 GEMM 32768 x 32768 x 768, C = A B^T (both K-major), N(0, 1) operands"}
 
 
-def qeps_widths(lam, torch, raw_sets, raw_out, ctx, triad_gbs, reps=20):
+def qeps_widths(lam, torch, raw_sets, raw_out, width_codes, ctx, triad_gbs, reps=20):
     """Raw Q_eps (2^26 values) at eps = 1e-2, 1e-3 and 1e-4 (7-, 10- and
     14-bit codes, absmax 1 declared): encode and decode GB/s from events the
     launches stamp themselves, four input sets rotating; (4 + b/8) bytes per
-    element, against the spec and the measured triad."""
+    element, against the spec and the measured triad.  The code buffers
+    (width_codes, sized for the widest codes) are allocated with the other
+    inputs at the start: buffers allocated after the other measurements had
+    freed memory landed where the 7-bit decode ran at half its rate."""
     n = raw_sets[0].numel()
     out = {}
     for eps in QEPS_WIDTH_EPS:
         p = lam.qeps_plan(eps, 1.0, "bits", n)
-        codes = [torch.empty(p.code_bytes // 4, dtype=torch.int32, device="cuda") for _ in raw_sets]
+        codes = [w[:p.code_bytes // 4] for w in width_codes]
         for k in range(len(raw_sets)):   # warm-up
             lam.quantize(raw_sets[k], eps, absmax=1.0, out=codes[k], ctx=ctx)
             lam.dequantize(codes[k], p, out=raw_out[k], ctx=ctx)
@@ -618,6 +621,9 @@ def main():
     p_raw = lam.qeps_plan(EPS, 1.0, "bits", n_raw)
     raw_codes = [torch.empty(p_raw.code_bytes // 4, dtype=torch.int32, device=dev) for _ in range(RAW_SETS)]
     raw_out = [torch.empty(n_raw, dtype=torch.float32, device=dev) for _ in range(RAW_SETS)]
+    p_wide = lam.qeps_plan(min(QEPS_WIDTH_EPS), 1.0, "bits", n_raw)   # the widest codes of the width sweep
+    width_codes = [] if args.no_extras else [torch.empty(p_wide.code_bytes // 4, dtype=torch.int32, device=dev)
+                                             for _ in range(RAW_SETS)]
 
     cfg = synth.subset_ingest()
     x = cfg["x"]
@@ -755,7 +761,7 @@ def main():
 
     extras = {}
     if not args.no_extras:
-        extras = beside_the_step(lam, torch, np, xd, qd, store, rep, pairs, ctx, raw_sets, raw_out)
+        extras = beside_the_step(lam, torch, np, xd, qd, store, rep, pairs, ctx, raw_sets, raw_out, width_codes)
         tgbs = extras["triad"]["GBps"]
         for v in qeps_timed.values():
             v["frac_of_triad"] = v["GBps"] / tgbs

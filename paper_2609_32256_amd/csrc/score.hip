@@ -26,8 +26,9 @@
 // sample and filter passes multiply the hi part alone -- half the MFMAs --
 // with thresholds lowered by twice a per-query bound on the hi part's error;
 // the few candidates near the k-th are then rescored exactly.  At D = 768 and
-// 1,024 the filter pass is k_filter: one 128 x 128 tile per workgroup on the
-// similarity screen's pipeline (two LDS stages, loads three slabs ahead).
+// 1,024 the filter pass is k_filter: one tile per workgroup on the
+// similarity screen's pipeline (two LDS stages), 128 x 128 or, for launches
+// of many tiles, 256 x 256.
 #include <cmath>
 #include <cstring>
 #include <mutex>
