@@ -985,16 +985,28 @@ struct ResolveArgs {
 
 constexpr int kResolveThreads = 1024;
 static_assert(kChunk % kResolveThreads == 0, "whole rows per thread");
-constexpr int kEdgeCap = 20480;    // in-chunk candidate entries held in LDS
+constexpr int kEdgeCap = 20480;    // in-chunk candidate entries held in LDS (list form)
+constexpr int kBitsCap = 8704;     // candidate bitmap words of active rows held in LDS (bitmap form)
 
 // LDS of the in-chunk resolve.  rrow: the decision of each row as rep_row
 // encodes it; posv: the store position of each kept row (-1 if dropped).
+// The active rows' in-chunk candidates are held in one of two forms: their
+// bitmap words as loaded (bitmap form, when they fit), or ascending lists.
 struct ResolveLds {
   uint8_t st[kChunk];        // 0 undecided, 1 kept, 2 dropped
-  uint16_t edges[kEdgeCap];
-  uint32_t eoff[kChunk];
-  uint16_t elen[kChunk];
-  uint16_t ecur[kChunk];
+  union {
+    struct {
+      uint16_t edges[kEdgeCap];
+      uint32_t eoff[kChunk];
+      uint16_t elen[kChunk];
+      uint16_t ecur[kChunk];
+    } ls;                    // list form: active row i's candidates at edges[eoff[i], eoff[i] + elen[i])
+    struct {
+      unsigned long long bits[kBitsCap];
+      uint8_t first[kChunk];
+    } bm;                    // bitmap form: active row k's words at bits[k W, k W + W); first word to look at
+  };
+  unsigned long long dropped[kChunk / 64];   // rows known to be dropped, one bit each
   uint16_t active[kChunk];
   int32_t rrow[kChunk];
   int32_t posv[kChunk];
@@ -1052,13 +1064,18 @@ __device__ void resolve_sequential(const ResolveArgs& a, ResolveLds& L, int n) {
 //     store row); rows with no in-chunk edge are kept.  Neither depends on any
 //     other row of the chunk.  The rest are "active".
 //  B. Each active row's in-chunk candidates (bits j < i of its bitmap row) are
-//     copied into LDS as an ascending list.
-//  C. Rounds: an undecided active row walks its list past dropped rows; the
-//     first non-dropped candidate decides it (kept -> the row is dropped with
-//     that representative), or makes it wait if still undecided; an exhausted
-//     list keeps the row.  A decision is taken only once every earlier
-//     candidate is decided, so it is the one the sequential walk takes, and
-//     the lowest undecided row can always decide, so the rounds end.
+//     copied into LDS: the bitmap words themselves when all active rows' words
+//     fit (bitmap form), else as ascending lists.  (Expanding dense words into
+//     lists bit by bit serialised the lanes holding them: clustered streams
+//     put dozens of candidates in one word.)
+//  C. Rounds: an undecided active row looks for its lowest candidate that is
+//     not dropped (the bitmap words masked by the dropped rows, or the list
+//     walked past them); that candidate decides it (kept -> the row is dropped
+//     with that representative), or makes it wait if still undecided; a row
+//     with no such candidate is kept.  A decision is taken only once every
+//     earlier candidate is decided, so it is the one the sequential walk
+//     takes, and the lowest undecided row can always decide, so the rounds
+//     end.
 //  D. Kept rows get consecutive store positions from m0, in arrival order;
 //     L.total is the number kept among the n rows.
 // The first phase's loads (hits and edge flags) are issued by the caller
@@ -1090,6 +1107,13 @@ __device__ void resolve_core(const ResolveArgs& a, ResolveLds& L, int n, int m0,
       L.active[atomicAdd(&L.n_active, 1u)] = (uint16_t)r;
     }
   }
+  // the rows dropped so far (store hits), one word per 64 rows
+#pragma unroll
+  for (int u = 0; u < kChunk / T; ++u) {
+    const int r = tid + u * T;   // a wave's lanes hold 64 consecutive rows
+    const uint64_t b = __ballot(r < n && hit_r[u] != kNone);
+    if (lane == 0) L.dropped[(u * T) / 64 + wave] = b;
+  }
   __syncthreads();
   const int na = (int)L.n_active;
   // B. A row's bitmap words (bits j < i) are read by G lanes, G = W rounded up
@@ -1098,76 +1122,64 @@ __device__ void resolve_core(const ResolveArgs& a, ResolveLds& L, int n, int m0,
   const int G = a.W <= 1 ? 1 : 1 << (32 - __clz(a.W - 1));
   const int sub = lane / G, wl = lane % G;
   const int rstep = (T / 64) * (64 / G);
-  for (int kb = wave * (64 / G); kb < na; kb += 4 * rstep) {
-    uint64_t e[4];
-    int ir[4];
+  if ((int64_t)na * a.W <= kBitsCap) {
+    volatile unsigned long long* dropped = L.dropped;
+    for (int kb = wave * (64 / G); kb < na; kb += 4 * rstep) {
+      uint64_t e[4];
+      int ir[4];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int k = kb + u * rstep + sub;
-      ir[u] = k < na ? (int)L.active[k] : -1;
-      const int nw = (ir[u] + 63) >> 6;
-      e[u] = (ir[u] >= 0 && wl < nw) ? a.bitmap[(int64_t)ir[u] * a.W + wl] : 0ull;
-    }
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      uint64_t eu = e[u];
-      const int c = __popcll(eu);
-      int incl = c;
-      for (int o = 1; o < G; o <<= 1) {
-        const int t = __shfl_up(incl, o, G);
-        if (wl >= o) incl += t;
+      for (int u = 0; u < 4; ++u) {
+        const int k = kb + u * rstep + sub;
+        ir[u] = k < na ? (int)L.active[k] : -1;
+        const int nw = (ir[u] + 63) >> 6;
+        e[u] = (ir[u] >= 0 && wl < nw) ? a.bitmap[(int64_t)ir[u] * a.W + wl] : 0ull;
       }
-      const int tot = __shfl(incl, sub * G + G - 1);
-      uint32_t base = 0u;
-      if (wl == 0 && ir[u] >= 0) base = atomicAdd(&L.n_edges, (uint32_t)tot);
-      base = __shfl(base, sub * G);
-      if (ir[u] >= 0) {
-        if (base + (uint32_t)tot <= (uint32_t)kEdgeCap) {
-          uint32_t p = base + (uint32_t)(incl - c);
-          while (eu) {
-            L.edges[p++] = (uint16_t)(wl * 64 + __builtin_ctzll(eu));
-            eu &= eu - 1ull;
-          }
-        }
-        if (wl == 0) {
-          L.eoff[ir[u]] = base;
-          L.elen[ir[u]] = (uint16_t)tot;
-          L.ecur[ir[u]] = 0;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int k = kb + u * rstep + sub;
+        if (ir[u] >= 0 && wl < a.W) L.bm.bits[k * a.W + wl] = e[u];
+        const uint64_t nz = __ballot(e[u] != 0ull);
+        if (wl == 0 && ir[u] >= 0) {
+          const uint64_t gm = (G == 64) ? nz : (nz >> (sub * G)) & ((1ull << G) - 1ull);
+          L.bm.first[k] = gm ? (uint8_t)__builtin_ctzll(gm) : (uint8_t)a.W;
         }
       }
     }
-  }
-  __syncthreads();
-  if (L.n_edges > (uint32_t)kEdgeCap) {
-    if (wave == 0) resolve_sequential(a, L, n);
-  } else {
+    __syncthreads();
     for (;;) {
       if (tid == 0) L.pending = 0u;
       __syncthreads();
       for (int k = tid; k < na; k += T) {
         const int i = L.active[k];
         if (st[i] != 0) continue;
-        const int len = L.elen[i];
-        const uint32_t b0 = L.eoff[i];
-        int p = L.ecur[i];
-        int dec = -1;   // -1 wait, 0 keep, 1 drop
+        const int nw = (i + 63) >> 6;
+        int dec = 0;   // 0 keep, 1 drop, -1 wait
         int j = -1;
-        for (; p < len; ++p) {
-          j = L.edges[b0 + p];
-          const uint8_t s = st[j];
-          if (s == 2) continue;
-          dec = (s == 1) ? 1 : -1;
-          break;
+        int w = L.bm.first[k];
+        for (; w < nw; ++w) {
+          uint64_t x = L.bm.bits[k * a.W + w] & ~dropped[w];
+          while (x) {
+            const int c = w * 64 + __builtin_ctzll(x);
+            const uint8_t sc = st[c];
+            if (sc == 2) {   // dropped since the word was read
+              x &= x - 1ull;
+              continue;
+            }
+            dec = (sc == 1) ? 1 : -1;
+            j = c;
+            break;
+          }
+          if (j >= 0) break;
         }
-        if (p == len) dec = 0;
-        L.ecur[i] = (uint16_t)p;
         if (dec == 1) {
           st[i] = 2;
           L.rrow[i] = -(j + 2);
+          atomicOr(&L.dropped[i >> 6], 1ull << (i & 63));
         } else if (dec == 0) {
           st[i] = 1;
           L.rrow[i] = -1;
         } else {
+          L.bm.first[k] = (uint8_t)w;   // the words before it hold only dropped candidates
           L.pending = 1u;
         }
       }
@@ -1176,9 +1188,107 @@ __device__ void resolve_core(const ResolveArgs& a, ResolveLds& L, int n, int m0,
       __syncthreads();
       if (done) break;
     }
+  } else {
+    for (int kb = wave * (64 / G); kb < na; kb += 4 * rstep) {
+      uint64_t e[4];
+      int ir[4];
+  #pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int k = kb + u * rstep + sub;
+        ir[u] = k < na ? (int)L.active[k] : -1;
+        const int nw = (ir[u] + 63) >> 6;
+        e[u] = (ir[u] >= 0 && wl < nw) ? a.bitmap[(int64_t)ir[u] * a.W + wl] : 0ull;
+      }
+  #pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        uint64_t eu = e[u];
+        const int c = __popcll(eu);
+        int incl = c;
+        for (int o = 1; o < G; o <<= 1) {
+          const int t = __shfl_up(incl, o, G);
+          if (wl >= o) incl += t;
+        }
+        const int tot = __shfl(incl, sub * G + G - 1);
+        uint32_t base = 0u;
+        if (wl == 0 && ir[u] >= 0) base = atomicAdd(&L.n_edges, (uint32_t)tot);
+        base = __shfl(base, sub * G);
+        if (ir[u] >= 0) {
+          if (base + (uint32_t)tot <= (uint32_t)kEdgeCap) {
+            uint32_t p = base + (uint32_t)(incl - c);
+            while (eu) {
+              L.ls.edges[p++] = (uint16_t)(wl * 64 + __builtin_ctzll(eu));
+              eu &= eu - 1ull;
+            }
+          }
+          if (wl == 0) {
+            L.ls.eoff[ir[u]] = base;
+            L.ls.elen[ir[u]] = (uint16_t)tot;
+            L.ls.ecur[ir[u]] = 0;
+          }
+        }
+      }
+    }
+    __syncthreads();
+    if (L.n_edges > (uint32_t)kEdgeCap) {
+      if (wave == 0) resolve_sequential(a, L, n);
+    } else {
+      for (;;) {
+        if (tid == 0) L.pending = 0u;
+        __syncthreads();
+        for (int k = tid; k < na; k += T) {
+          const int i = L.active[k];
+          if (st[i] != 0) continue;
+          const int len = L.ls.elen[i];
+          const uint32_t b0 = L.ls.eoff[i];
+          int p = L.ls.ecur[i];
+          int dec = -1;   // -1 wait, 0 keep, 1 drop
+          int j = -1;
+          for (; p < len; ++p) {
+            j = L.ls.edges[b0 + p];
+            const uint8_t s = st[j];
+            if (s == 2) continue;
+            dec = (s == 1) ? 1 : -1;
+            break;
+          }
+          if (p == len) dec = 0;
+          L.ls.ecur[i] = (uint16_t)p;
+          if (dec == 1) {
+            st[i] = 2;
+            L.rrow[i] = -(j + 2);
+          } else if (dec == 0) {
+            st[i] = 1;
+            L.rrow[i] = -1;
+          } else {
+            L.pending = 1u;
+          }
+        }
+        __syncthreads();
+        const bool done = L.pending == 0u;
+        __syncthreads();
+        if (done) break;
+      }
+    }
   }
   __syncthreads();
   // D. store positions: exclusive scan of kept flags, whole rows per thread
+  // (one row per thread: the wave's ballot gives the counts)
+  if (n <= T) {
+    const bool kp = tid < n && st[tid] == 1;
+    const uint64_t bal = __ballot(kp);
+    if (lane == 0) L.wsum[wave] = __popcll(bal);
+    __syncthreads();
+    int base = 0, total = 0;
+#pragma unroll
+    for (int w = 0; w < T / 64; ++w) {
+      const int v = L.wsum[w];
+      base += w < wave ? v : 0;
+      total += v;
+    }
+    if (tid == 0) L.total = (uint32_t)total;
+    if (tid < n) L.posv[tid] = kp ? m0 + base + __popcll(bal & ((1ull << lane) - 1ull)) : -1;
+    __syncthreads();
+    return;
+  }
   const int per = (n + T - 1) / T;
   const int r0 = tid * per, r1 = min(n, r0 + per);
   int c = 0;
