@@ -1010,7 +1010,8 @@ struct ResolveLds {
   uint16_t active[kChunk];
   int32_t rrow[kChunk];
   int32_t posv[kChunk];
-  uint32_t n_active, n_edges, pending, total;
+  uint32_t n_active, n_edges, total;
+  uint32_t pend[3];          // round r sets pend[r % 3] while a row waits
   int wsum[kResolveThreads / 64];
 };
 
@@ -1089,6 +1090,7 @@ __device__ void resolve_core(const ResolveArgs& a, ResolveLds& L, int n, int m0,
   if (tid == 0) {
     L.n_active = 0u;
     L.n_edges = 0u;
+    L.pend[0] = 0u;   // the first round's flag (later ones are cleared a round ahead)
   }
   __syncthreads();
 #pragma unroll
@@ -1146,9 +1148,10 @@ __device__ void resolve_core(const ResolveArgs& a, ResolveLds& L, int n, int m0,
       }
     }
     __syncthreads();
-    for (;;) {
-      if (tid == 0) L.pending = 0u;
-      __syncthreads();
+    // one barrier per round: round r raises pend[r % 3] and clears pend[(r + 1)
+    // % 3], which every thread last read before the previous barrier
+    for (int r = 0;; ++r) {
+      if (tid == 0) L.pend[(r + 1) % 3] = 0u;
       for (int k = tid; k < na; k += T) {
         const int i = L.active[k];
         if (st[i] != 0) continue;
@@ -1180,13 +1183,11 @@ __device__ void resolve_core(const ResolveArgs& a, ResolveLds& L, int n, int m0,
           L.rrow[i] = -1;
         } else {
           L.bm.first[k] = (uint8_t)w;   // the words before it hold only dropped candidates
-          L.pending = 1u;
+          L.pend[r % 3] = 1u;
         }
       }
       __syncthreads();
-      const bool done = L.pending == 0u;
-      __syncthreads();
-      if (done) break;
+      if (L.pend[r % 3] == 0u) break;
     }
   } else {
     for (int kb = wave * (64 / G); kb < na; kb += 4 * rstep) {
@@ -1232,9 +1233,8 @@ __device__ void resolve_core(const ResolveArgs& a, ResolveLds& L, int n, int m0,
     if (L.n_edges > (uint32_t)kEdgeCap) {
       if (wave == 0) resolve_sequential(a, L, n);
     } else {
-      for (;;) {
-        if (tid == 0) L.pending = 0u;
-        __syncthreads();
+      for (int r = 0;; ++r) {   // one barrier per round, as in the bitmap form
+        if (tid == 0) L.pend[(r + 1) % 3] = 0u;
         for (int k = tid; k < na; k += T) {
           const int i = L.active[k];
           if (st[i] != 0) continue;
@@ -1259,13 +1259,11 @@ __device__ void resolve_core(const ResolveArgs& a, ResolveLds& L, int n, int m0,
             st[i] = 1;
             L.rrow[i] = -1;
           } else {
-            L.pending = 1u;
+            L.pend[r % 3] = 1u;
           }
         }
         __syncthreads();
-        const bool done = L.pending == 0u;
-        __syncthreads();
-        if (done) break;
+        if (L.pend[r % 3] == 0u) break;
       }
     }
   }
