@@ -88,7 +88,11 @@ __global__ __launch_bounds__(256) void k_score_prep(const float* __restrict__ q,
   // tile start at zero (the buffers may hold anything from an earlier call)
   if (cand_cnt && lane == 0) {
     cand_cnt[j] = 0u;
-    if (j % kTB == 0) tflag[j / kTB] = 0u;
+    if (j % kTB == 0) {
+      const int64_t nqt = (nq + kTB - 1) / kTB;
+      tflag[j / kTB] = 0u;          // the tile's flag
+      tflag[nqt + j / kTB] = 0u;    // and its fallback workgroups' completion count
+    }
   }
   const float* p = q + j * D;
   float mx = 0.0f;
@@ -208,6 +212,14 @@ struct ScoreArgs {
   uint32_t* cand_cnt;
   uint32_t cap;
   const uint32_t* tflag;     // fallback mode: query tiles to redo
+  // fallback mode: the last workgroup of a query tile merges its flagged queries
+  const uint32_t* qflag;     // queries to redo
+  uint32_t* tdone;           // per query tile: workgroups finished
+  int k;
+  float* out_s;
+  int64_t* out_i;
+  float* out_bound;
+  const int64_t* ids;        // store row -> global id
 };
 
 __device__ __forceinline__ bool better(float a, int ra, float b, int rb) {
@@ -411,6 +423,12 @@ __device__ __forceinline__ void score_tile(const ScoreArgs& a, int64_t rbase, in
 
 enum { kModeLists = 0, kModeFilter = 1, kModeFallback = 2 };
 
+template <int KL, int SEG>
+__device__ void merge_query(int64_t j, int cands, int k, const float* __restrict__ ps,
+                            const int32_t* __restrict__ pr, const QMeta* __restrict__ meta,
+                            const int64_t* __restrict__ ids, float* __restrict__ out_s, int64_t* __restrict__ out_i,
+                            float* __restrict__ bound, float* __restrict__ kth);
+
 // MODE kModeLists / kModeFallback: each lane keeps a sorted private list of its
 // best KL (score, row) pairs; the lists go to part_s/part_r.  kModeFallback
 // only runs query tiles flagged in tflag.  MODE kModeFilter: every score at or
@@ -524,13 +542,33 @@ __global__ __launch_bounds__(kWG, 2) void k_score(ScoreArgs a) {
     }
   }
   if constexpr (MODE != kModeFilter) {
-    if (j >= a.nq) return;
-    const int slot = lane >> 5;
-    const int64_t o = ((j * a.splits + split) * 2 + slot) * (int64_t)KL;
+    if (j < a.nq) {
+      const int slot = lane >> 5;
+      const int64_t o = ((j * a.splits + split) * 2 + slot) * (int64_t)KL;
 #pragma unroll
-    for (int p = 0; p < KL; ++p) {
-      a.part_s[o + p] = ls[p];
-      a.part_r[o + p] = lr[p];
+      for (int p = 0; p < KL; ++p) {
+        a.part_s[o + p] = ls[p];
+        a.part_r[o + p] = lr[p];
+      }
+    }
+  }
+  if constexpr (MODE == kModeFallback) {
+    // The last of the tile's workgroups to finish merges the lists of the
+    // tile's flagged queries (one wave per query), so the pass needs no merge
+    // launch of its own.  Runs only for flagged tiles: the fences (release
+    // of every workgroup's lists, acquire by the last) cost nothing otherwise.
+    __shared__ bool last;
+    __threadfence();
+    __syncthreads();
+    if (threadIdx.x == 0) last = atomicAdd(&a.tdone[qt], 1u) == (uint32_t)(a.splits - 1);
+    __syncthreads();
+    if (!last) return;
+    __threadfence();
+    for (int q = wave; q < qrows; q += kWG / 64) {
+      const int64_t jq = qbase + q;
+      if (a.qflag[jq] == 0u) continue;
+      merge_query<KL, KL>(jq, a.splits * 2 * KL, a.k, a.part_s, a.part_r, a.meta, a.ids, a.out_s, a.out_i,
+                          a.out_bound, nullptr);
     }
   }
 }
@@ -589,18 +627,24 @@ __device__ __forceinline__ bool write_bad(const QMeta& m, int64_t j, int k, floa
 // entries, of which only the first k can matter), each lane folding its share
 // into a register list of KL.  With KL >= k and the shares' lists complete this
 // is the exact k best; otherwise the k picks are still k distinct entries.
-// With qflag set, only flagged queries are processed (the fallback after a
-// candidate overflow).
 template <int KL, int SEG = KL>
 __global__ __launch_bounds__(256) void k_topk_merge(int64_t nq, int cands, int k, const float* __restrict__ ps,
                                                     const int32_t* __restrict__ pr, const QMeta* __restrict__ meta,
                                                     const int64_t* __restrict__ ids, float* __restrict__ out_s,
                                                     int64_t* __restrict__ out_i, float* __restrict__ bound,
-                                                    float* __restrict__ kth, const uint32_t* __restrict__ qflag) {
-  const int lane = threadIdx.x & 63;
+                                                    float* __restrict__ kth) {
   const int64_t j = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   if (j >= nq) return;
-  if (qflag && qflag[j] == 0u) return;
+  merge_query<KL, SEG>(j, cands, k, ps, pr, meta, ids, out_s, out_i, bound, kth);
+}
+
+// One wave: the merge of query j's lists (the body of k_topk_merge).
+template <int KL, int SEG>
+__device__ void merge_query(int64_t j, int cands, int k, const float* __restrict__ ps,
+                            const int32_t* __restrict__ pr, const QMeta* __restrict__ meta,
+                            const int64_t* __restrict__ ids, float* __restrict__ out_s, int64_t* __restrict__ out_i,
+                            float* __restrict__ bound, float* __restrict__ kth) {
+  const int lane = threadIdx.x & 63;
   if (write_bad(meta[j], j, k, out_s, out_i, bound)) {
     if (kth && lane == 0) kth[j] = __builtin_nanf("");
     return;
@@ -1495,7 +1539,7 @@ lam_status score_topk_impl(lam_ctx* ctx, const ScoreView& st, const float* q, in
   LAM_TRY(w.take(ctx, S_QLO, (size_t)nq * D * 2, &qlo));
   LAM_TRY(w.take(ctx, S_QMETA, (size_t)nq * sizeof(QMeta), &qmeta));
   LAM_TRY(w.take(ctx, S_PART, (size_t)nq * cands_max * 8, &part_s));
-  if (two_pass) LAM_TRY(w.take(ctx, S_CAND, (size_t)nq * cap * 8 + (size_t)nq * 12 + (size_t)nqt * 4 + 256, &cand_s));
+  if (two_pass) LAM_TRY(w.take(ctx, S_CAND, (size_t)nq * cap * 8 + (size_t)nq * 12 + (size_t)nqt * 8 + 256, &cand_s));
   int32_t* part_r = reinterpret_cast<int32_t*>(part_s + (size_t)nq * cands_max);
   int32_t* cand_r = two_pass ? reinterpret_cast<int32_t*>(cand_s + (size_t)nq * cap) : nullptr;
   uint32_t* cand_cnt = two_pass ? reinterpret_cast<uint32_t*>(cand_r + (size_t)nq * cap) : nullptr;
@@ -1538,10 +1582,10 @@ lam_status score_topk_impl(lam_ctx* ctx, const ScoreView& st, const float* q, in
     const int nc = ntiles > 0 ? sp2 * 2 * KL : 0;
     if (KL == 16)
       hipLaunchKernelGGL((k_topk_merge<16>), gq, dim3(256), 0, ctx->stream, nq, nc, k, part_s, part_r, qmeta, st.ids,
-                         scores, ids, bound, nullptr, nullptr);
+                         scores, ids, bound, nullptr);
     else
       hipLaunchKernelGGL((k_topk_merge<64>), gq, dim3(256), 0, ctx->stream, nq, nc, k, part_s, part_r, qmeta, st.ids,
-                         scores, ids, bound, nullptr, nullptr);
+                         scores, ids, bound, nullptr);
     LAM_HIP(hipGetLastError());
     return LAM_OK;
   }
@@ -1557,11 +1601,11 @@ lam_status score_topk_impl(lam_ctx* ctx, const ScoreView& st, const float* q, in
       // one tile per workgroup on the filter's pipeline; entries unsorted (segments of 1)
       LAM_TRY((launch_filter<1, true>(b, D, false, dim3((unsigned)(nqt * stiles)), ctx->stream, a)));
       hipLaunchKernelGGL((k_topk_merge<16, 1>), gq, dim3(256), 0, ctx->stream, nq, (int)stiles * kSampleEntries, k,
-                         part_s, part_r, qmeta, st.ids, nullptr, nullptr, nullptr, thr, nullptr);
+                         part_s, part_r, qmeta, st.ids, nullptr, nullptr, nullptr, thr);
     } else {
       LAM_TRY(dispatch_bits<1>(b, kSampleKL, kModeLists, dim3((unsigned)(nqt * sp1)), ctx->stream, a));
       hipLaunchKernelGGL((k_topk_merge<16, kSampleKL>), gq, dim3(256), 0, ctx->stream, nq, sp1 * 2 * kSampleKL, k,
-                         part_s, part_r, qmeta, st.ids, nullptr, nullptr, nullptr, thr, nullptr);
+                         part_s, part_r, qmeta, st.ids, nullptr, nullptr, nullptr, thr);
     }
     LAM_HIP(hipGetLastError());
   }
@@ -1607,15 +1651,17 @@ lam_status score_topk_impl(lam_ctx* ctx, const ScoreView& st, const float* q, in
                               qmeta, st.ids, q, st.step, a.codes, a.row_words, D, scores, ids, bound, qflag, tflag));
   }
   {
+    // exact lists for the flagged query tiles, merged by each tile's last
+    // workgroup (returns at once when nothing is flagged)
     ProfScope ps(ctx, "score_fallback", prof);
+    a.qflag = qflag;
+    a.tdone = tflag + nqt;
+    a.k = k;
+    a.out_s = scores;
+    a.out_i = ids;
+    a.out_bound = bound;
+    a.ids = st.ids;
     LAM_TRY(dispatch_bits<1>(b, KL, kModeFallback, dim3((unsigned)(nqt * sp2)), ctx->stream, a));
-    const int nc = sp2 * 2 * KL;
-    if (KL == 16)
-      hipLaunchKernelGGL((k_topk_merge<16>), gq, dim3(256), 0, ctx->stream, nq, nc, k, part_s, part_r, qmeta, st.ids,
-                         scores, ids, bound, nullptr, qflag);
-    else
-      hipLaunchKernelGGL((k_topk_merge<64>), gq, dim3(256), 0, ctx->stream, nq, nc, k, part_s, part_r, qmeta, st.ids,
-                         scores, ids, bound, nullptr, qflag);
     LAM_HIP(hipGetLastError());
   }
   return LAM_OK;
