@@ -184,7 +184,9 @@ typedef struct lam_store_info {
 } lam_store_info;
 
 /* Synchronous: waits for ingest calls that did not wait (see lam_dedup_ingest)
- * and returns EINVAL, once, if any of them met invalid input. */
+ * and returns EINVAL, once, if any of them met invalid input.  The wait is for
+ * the stream of the last such call, so it also covers work queued on that
+ * stream after the call. */
 lam_status lam_store_get_info(const lam_store* store, lam_store_info* out);
 
 /* Empty the store (size, n_seen, delta_hat and codes reset; memory kept), as
@@ -241,7 +243,12 @@ lam_status lam_dedup_ingest(lam_ctx* ctx, lam_store* store, const float* x_dev, 
 
 /* Q_eps over every retained row (the store's codec, Algorithm "admit",
  * "store the compressed embedding"); rows start on word boundaries (dim is a
- * multiple of 32).  Same absmax semantics as lam_quantize.  Synchronous.
+ * multiple of 32).  Same absmax semantics as lam_quantize: a declared absmax
+ * below the store's largest |x| (kept exactly by the appends) is ERANGE,
+ * decided on the host before any code is written, and leaves the store
+ * unquantized.  Waits for ingest calls that did not wait (as
+ * lam_store_get_info), then returns with the encode queued (fills *out; the
+ * rows were checked at ingest, so the encode cannot fail on the data).
  * Rows retained later are not coded until this is called again. */
 lam_status lam_store_quantize(lam_ctx* ctx, lam_store* store, double eps, float absmax, int mode,
                               lam_qparams* out);

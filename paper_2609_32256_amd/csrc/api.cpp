@@ -145,9 +145,12 @@ lam_status read_flags(lam_ctx* ctx) {
 }
 
 // Shared body of lam_quantize and lam_store_quantize.
+// known_valid: the caller knows every |x| to be finite and at most a positive
+// absmax (a store's rows against the store's exact maximum), so no status word
+// can be set and the encode is not waited for.
 lam_status quantize_impl(lam_ctx* ctx, const float* x, int64_t n, double eps, float absmax, int mode,
                          uint32_t* codes, uint64_t cap, lam_qparams* out, DevBuf* grow_into,
-                         bool store_path = false) {
+                         bool store_path = false, bool known_valid = false) {
   lam_qparams p{};
   // argument checks that do not depend on the data
   LAM_TRY(qeps_plan_host(eps, 0.0f, mode, n, &p));
@@ -172,6 +175,11 @@ lam_status quantize_impl(lam_ctx* ctx, const float* x, int64_t n, double eps, fl
   LAM_CHECK(cap >= p.code_bytes, LAM_EINVAL, "codes capacity %llu < %llu bytes needed",
             (unsigned long long)cap, (unsigned long long)p.code_bytes);
   LAM_TRY(launch_encode(ctx, x, n, p, codes, &ctx->flags_dev->nonfinite, store_path ? "store_encode" : "qeps_encode"));
+  if (known_valid && absmax > 0.0f) {
+    ctx->flags_zero = true;   // cleared above and left untouched by valid input
+    if (out) *out = p;
+    return LAM_OK;
+  }
   LAM_TRY(read_flags(ctx));
   LAM_CHECK(ctx->flags_host->nonfinite == 0, LAM_EINVAL, "input holds NaN or Inf (%u elements)",
             ctx->flags_host->nonfinite);
@@ -446,7 +454,20 @@ lam_status lam_store_quantize(lam_ctx* ctx, lam_store* st, double eps, float abs
   st->blk_rows = -1;   // any block encoding describes the previous codes
   float a = absmax;
   if (!(absmax > 0.0f) && st->absmax_bits != 0u) memcpy(&a, &st->absmax_bits, 4);   // the exact maximum
-  lam_status s = quantize_impl(ctx, st->x32, n, eps, a, mode, nullptr, 0, &p, &holder, true);
+  if (absmax > 0.0f && std::isfinite(absmax)) {
+    // the rows were checked finite at ingest; against a declared absmax the
+    // store's exact maximum decides ERANGE before any code is written
+    uint32_t ab = 0u;
+    memcpy(&ab, &absmax, 4);
+    if (st->absmax_bits > ab) {
+      float mx = 0.0f;
+      memcpy(&mx, &st->absmax_bits, 4);
+      st->coded_rows = -1;
+      LAM_CHECK(false, LAM_ERANGE, "the store's largest |x| (%g) exceeds the declared absmax %g", (double)mx,
+                (double)absmax);
+    }
+  }
+  lam_status s = quantize_impl(ctx, st->x32, n, eps, a, mode, nullptr, 0, &p, &holder, true, true);
   st->codes = holder.as<uint32_t>();
   st->codes_cap = holder.bytes;
   if (s != LAM_OK) {

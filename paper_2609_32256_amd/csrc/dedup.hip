@@ -1688,6 +1688,7 @@ lam_status store_alloc(lam_store* st) {
   LAM_HIP(hipMalloc(&st->ids, cap * 8));
   LAM_HIP(hipMalloc(&st->stat_dev, sizeof(StoreMeta)));
   LAM_HIP(hipMemset(st->stat_dev, 0, sizeof(StoreMeta)));
+  LAM_HIP(hipHostMalloc(&st->meta_host, sizeof(StoreMeta), hipHostMallocDefault));
   if (st->lsh_r > 0) {
     const uint64_t entries = (uint64_t)cap * (uint64_t)st->lsh_nb;
     uint64_t slots = 1;
@@ -1700,10 +1701,6 @@ lam_status store_alloc(lam_store* st) {
     LAM_HIP(hipMemset(st->lsh_key, 0, slots * 8));
     LAM_HIP(hipMemset(st->lsh_head, 0xff, slots * 4));   // -1: empty list
   }
-  // Marks the end of the store's last call that did not wait.  Settling reads
-  // the device-side bookkeeping with a device copy after it, so the event
-  // needs no system-scope fence (which would flush the L2 between calls).
-  LAM_HIP(hipEventCreateWithFlags(&st->done, hipEventDisableTiming | hipEventDisableSystemFence));
   LAM_HIP(hipDeviceSynchronize());
   st->thr = exact_threshold(st->tau);
   return LAM_OK;
@@ -1739,8 +1736,8 @@ void store_free(lam_store* st) {
   st->blk_data = nullptr;
   st->blk_cap = 0;
   st->blk_rows = -1;
-  if (st->done) (void)hipEventDestroy(st->done);
-  st->done = nullptr;
+  if (st->meta_host) (void)hipHostFree(st->meta_host);
+  st->meta_host = nullptr;
   st->x32 = nullptr;
   st->x16 = nullptr;
   st->hn = st->et = st->stat_dev = nullptr;
@@ -1772,11 +1769,15 @@ constexpr uint64_t kAsyncPairLimit = 1ull << 26;
 
 }  // namespace
 
+// The device bookkeeping is copied to pinned host memory on the stream of the
+// last call that did not wait, behind that call, and read after one wait for
+// the stream (an event wait and then a synchronous copy would be two).
 lam_status store_settle(lam_store* st) {
   if (!st->pending) return LAM_OK;
-  LAM_HIP(hipEventSynchronize(st->done));
+  LAM_HIP(hipMemcpyAsync(st->meta_host, st->stat_dev, sizeof(StoreMeta), hipMemcpyDeviceToHost, st->last_stream));
+  LAM_HIP(hipStreamSynchronize(st->last_stream));
   StoreMeta m{};
-  LAM_HIP(hipMemcpy(&m, st->stat_dev, sizeof m, hipMemcpyDeviceToHost));
+  memcpy(&m, st->meta_host, sizeof m);
   st->pending = false;
   st->size = m.m;
   st->size_ub = m.m;
@@ -2088,7 +2089,7 @@ lam_status dedup_ingest(lam_ctx* ctx, lam_store* st, const float* x, int64_t n, 
     }
     ctx->flags_zero = true;   // the last append clears the status words
     if (async) {
-      LAM_HIP(hipEventRecord(st->done, ctx->stream));
+      st->last_stream = ctx->stream;
       st->pending = true;
       st->size_ub = m_before + n;
       return LAM_OK;

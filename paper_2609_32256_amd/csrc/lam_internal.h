@@ -127,7 +127,7 @@ struct lam_store {
   double delta_hat_run = 0.0; // exact when !pending
   bool pending = false;       // ingest calls ran without waiting; the device bookkeeping holds the truth
   int64_t size_ub = 0;        // upper bound of the size while pending
-  hipEvent_t done = nullptr;  // recorded after the last call that did not wait
+  hipStream_t last_stream = nullptr;  // stream of the last call that did not wait
   lam::Big6 thr{};            // floor((2 - 2 tau) * 2^298), the exact predicate's right side
   // retained rows (capacity rows each)
   float* x32 = nullptr;       // float32 rows
@@ -136,6 +136,7 @@ struct lam_store {
   float* et = nullptr;        // per-row term of the screen's error bound (float32, rounded up)
   int64_t* ids = nullptr;     // global ids
   float* stat_dev = nullptr;  // device bookkeeping block (retained-row count)
+  void* meta_host = nullptr;  // pinned host copy of that block, made when settling
   uint32_t hn_max = 0;        // max of hn over the coded rows (float bits), set with the codes
   // the device bookkeeping's maxima over the retained rows, as last read by the host
   bool maxima_known = false;  // false until read again after calls that may have changed them

@@ -402,3 +402,32 @@ def test_store_maxima_after_calls_that_wait_and_calls_that_do_not(lam):
     kept = ref["kept"]
     assert p.absmax == float(np.abs(x[kept]).max()) == np.float32(0.9)
     assert np.array_equal(rep.cpu().numpy(), ref["rep"][2000:])
+
+
+def test_store_quantize_declared_absmax_against_store_maximum(lam):
+    """With a declared absmax the store's exact maximum |x| decides ERANGE
+    before any code is written (the largest coordinate arrives in a call that
+    does not wait); the failed call leaves the store unquantized, and the exact
+    maximum itself is accepted."""
+    rng = np.random.default_rng(22)
+    x = synth.unit_rows(rng, 2000, 128).astype(np.float32)
+    x[1500, 7] = np.float32(0.75)
+    s = lam.Store(128, 0.95, x.shape[0])
+    xd = _dev(x)
+    s.ingest(xd[:1000], sync=False)
+    s.ingest(xd[1000:], sync=False)
+    ref = dedup.greedy(x, 0.95)
+    kept = ref["kept"]
+    a = np.abs(x[kept]).max()
+    assert a == np.float32(0.75)
+    below = float(np.nextafter(np.float32(0.75), np.float32(0)))
+    with pytest.raises(lam.LamError) as e:
+        s.quantize(1e-3, absmax=below)
+    assert e.value.name == "LAM_ERANGE"
+    with pytest.raises(lam.LamError) as e:
+        s.score_topk(_dev(x[:4]), 3)
+    assert e.value.name == "LAM_ESTATE"
+    p = s.quantize(1e-3, absmax=0.75)
+    assert p.absmax == np.float32(0.75)
+    assert np.array_equal(s.codes().cpu().numpy().view(np.uint32), qeps.pack(qeps.codes(x[kept], 1e-3), p.bits))
+    assert s.info().size == kept.size
