@@ -189,11 +189,17 @@ def beside_the_step(lam, torch, np, xd, qd, store, rep, pairs, ctx, raw_sets, ra
     of benchmark queries whose top-10 is certified rank-invariant, the
     per-block codec (size and speed) on the retained store, scoring at the
     corpus size, and the stream through the banded candidate index."""
+    # first, before the heavy measurements below: run after them, the 7-bit
+    # decode took 94 us per launch against 65 us in a process of its own
+    widths = qeps_widths(lam, torch, raw_sets, raw_out, width_codes, ctx, None)
     ceil = lam.removal_ceiling(xd, TAU, batch=BATCH, ctx=ctx)
     cert = store.score_topk_certified(qd, TOPK)[3]
     blk_t = block_codec_timing(lam, torch, store, ctx)
     blk = store.block_encode()
     triad = triad_anchor(lam, torch, ctx)
+    for row in widths.values():
+        for name in ("qeps_encode", "qeps_decode"):
+            row[name]["frac_of_triad"] = row[name]["GBps"] / triad["GBps"]
     matmul = matmul_anchor(torch)
     # the stream once more with calls that wait, for the decision statistics
     n = xd.shape[0]
@@ -211,7 +217,7 @@ def beside_the_step(lam, torch, np, xd, qd, store, rep, pairs, ctx, raw_sets, ra
     return {"decisions": decisions,
             "triad": triad,
             "matmul_anchor": matmul,
-            "qeps_widths": qeps_widths(lam, torch, raw_sets, raw_out, width_codes, ctx, triad["GBps"]),
+            "qeps_widths": widths,
             "screen_steady_state": steady,
             "one_call": one_call_ingest(lam, torch, np, xd, rep, pairs, ctx),
             "online_store": online_store_run(lam, torch, np, ctx),
