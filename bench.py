@@ -644,9 +644,13 @@ def main():
                 torch.empty(qd.shape[0], dtype=torch.float32, device=dev))
     reps = [torch.empty(min(BATCH, n - b0), dtype=torch.int64, device=dev) for b0 in range(0, n, BATCH)]
 
+    # the raw encode does not wait: its invalid-input counters are checked
+    # after the timed steps
+    qstatus = torch.zeros(2, dtype=torch.int32, device=dev)
+
     def step(i):
         k = i % RAW_SETS
-        _, p = lam.quantize(raw_sets[k], EPS, absmax=1.0, out=raw_codes[k], ctx=ctx)
+        _, p = lam.quantize_async(raw_sets[k], EPS, 1.0, qstatus, out=raw_codes[k], ctx=ctx)
         lam.dequantize(raw_codes[k], p, out=raw_out[k], ctx=ctx)
         store.clear()
         for bi, b0 in enumerate(range(0, n, BATCH)):
@@ -713,6 +717,9 @@ def main():
     ms = (t1 - t0) * 1e3 / args.steps
     dom_tot, dom_cnt = ctx.profile_read(dominant)
     timed_qeps = {name: ctx.profile_read(name) for name in ("qeps_encode", "qeps_decode")}
+    if qstatus.any().item():
+        print(f"raw Q_eps input reported invalid: {qstatus.tolist()}", file=sys.stderr)
+        sys.exit(1)
 
     if args.copy_calibration:
         src = torch.ones(1 << 28, dtype=torch.float32, device=dev)

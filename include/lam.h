@@ -134,6 +134,19 @@ lam_status lam_qeps_plan(double eps, float absmax, int mode, int64_t n, lam_qpar
 lam_status lam_quantize(lam_ctx* ctx, const float* x_dev, int64_t n, double eps, float absmax,
                         int mode, uint32_t* codes_dev, uint64_t codes_cap_bytes, lam_qparams* out);
 
+/* lam_quantize for pipelines that do not wait: returns once the encode is
+ * queued on the context's stream, with *out planned from the declared
+ * absmax (> 0, required; EINVAL otherwise).  Instead of a status, the encode
+ * adds, in stream order, a positive count to status_dev[0] if any element is
+ * NaN or Inf and to status_dev[1] if any |x| > absmax (Inf included): two
+ * uint32 in device memory that the caller owns and clears (the counts are of
+ * the device threads that met such elements).  The codes are valid when
+ * neither count grew.  Argument errors (EINVAL, ERANGE for a code range
+ * beyond 2^31) are returned at once, before anything is queued. */
+lam_status lam_quantize_async(lam_ctx* ctx, const float* x_dev, int64_t n, double eps, float absmax, int mode,
+                              uint32_t* codes_dev, uint64_t codes_cap_bytes, uint32_t* status_dev,
+                              lam_qparams* out);
+
 /* Decode p->n codes: x_hat = float32(float64(code * step)) (round to binary64,
  * then to binary32; the bound holds on the exact code*step).  Asynchronous. */
 lam_status lam_dequantize(lam_ctx* ctx, const uint32_t* codes_dev, const lam_qparams* p, float* xhat_dev);

@@ -108,6 +108,8 @@ _SIGS = {
     "lam_qeps_plan": ([ctypes.c_double, ctypes.c_float, ctypes.c_int, _I64, ctypes.POINTER(QParams)], ctypes.c_int),
     "lam_quantize": ([_P, _P, _I64, ctypes.c_double, ctypes.c_float, ctypes.c_int, _P, ctypes.c_uint64,
                       ctypes.POINTER(QParams)], ctypes.c_int),
+    "lam_quantize_async": ([_P, _P, _I64, ctypes.c_double, ctypes.c_float, ctypes.c_int, _P, ctypes.c_uint64, _P,
+                            ctypes.POINTER(QParams)], ctypes.c_int),
     "lam_dequantize": ([_P, _P, ctypes.POINTER(QParams), _P], ctypes.c_int),
     "lam_store_create": ([_P, ctypes.c_int32, ctypes.c_double, _I64, ctypes.POINTER(_P)], ctypes.c_int),
     "lam_store_create_banded": ([_P, ctypes.c_int32, ctypes.c_double, _I64, ctypes.c_double, ctypes.c_int32,
@@ -265,6 +267,28 @@ def quantize(x: torch.Tensor, eps: float, absmax: float | None = None, mode: str
     p = QParams()
     _check(_lib.lam_quantize(ctx.handle, _ptr(x), n, float(eps), a, _MODES[mode], _ptr(out),
                              out.numel() * 4, ctypes.byref(p)))
+    return out[: p.code_bytes // 4], p
+
+
+def quantize_async(x: torch.Tensor, eps: float, absmax: float, status: torch.Tensor, mode: str = "bits",
+                   out: torch.Tensor | None = None, ctx: Context | None = None):
+    """Q_eps that does not wait for the device (lam_quantize_async): returns
+    (codes, QParams) once the encode is queued; the encode adds a positive
+    count to status[0] if any element is NaN/Inf and to status[1] if any is
+    above absmax (status: a contiguous int32 device tensor of at least 2
+    entries that the caller clears)."""
+    ctx = ctx or default_context()
+    x = _dev_tensor(x, torch.float32, "x").reshape(-1)
+    if not isinstance(status, torch.Tensor) or not status.is_cuda or status.dtype != torch.int32 \
+            or not status.is_contiguous() or status.numel() < 2:
+        raise ValueError("status must be a contiguous int32 device tensor of at least 2 entries")
+    n = x.numel()
+    if out is None:
+        out = torch.empty(max(1, (n * qeps_plan(eps, absmax, mode, n).bits + 31) // 32), dtype=torch.int32,
+                          device=x.device)
+    p = QParams()
+    _check(_lib.lam_quantize_async(ctx.handle, _ptr(x), n, float(eps), float(absmax), _MODES[mode], _ptr(out),
+                                   out.numel() * 4, _ptr(status), ctypes.byref(p)))
     return out[: p.code_bytes // 4], p
 
 

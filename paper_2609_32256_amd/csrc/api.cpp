@@ -336,6 +336,27 @@ lam_status lam_quantize(lam_ctx* ctx, const float* x_dev, int64_t n, double eps,
   return quantize_impl(ctx, x_dev, n, eps, absmax, mode, codes_dev, codes_cap_bytes, out, nullptr);
 }
 
+lam_status lam_quantize_async(lam_ctx* ctx, const float* x_dev, int64_t n, double eps, float absmax, int mode,
+                              uint32_t* codes_dev, uint64_t codes_cap_bytes, uint32_t* status_dev,
+                              lam_qparams* out) {
+  LAM_CHECK(ctx != nullptr, LAM_EINVAL, "ctx is NULL");
+  LAM_CHECK(n >= 0, LAM_EINVAL, "n must be >= 0");
+  LAM_CHECK(x_dev != nullptr || n == 0, LAM_EINVAL, "x is NULL");
+  LAM_CHECK(status_dev != nullptr, LAM_EINVAL, "status is NULL");
+  LAM_CHECK(((uintptr_t)x_dev & 3u) == 0 && ((uintptr_t)codes_dev & 3u) == 0 && ((uintptr_t)status_dev & 3u) == 0,
+            LAM_EINVAL, "x, codes and status must be 4-byte aligned");
+  LAM_CHECK(std::isfinite(absmax) && absmax > 0.0f, LAM_EINVAL, "an asynchronous encode needs a declared absmax > 0");
+  lam_qparams p{};
+  LAM_TRY(qeps_plan_host(eps, absmax, mode, n, &p));
+  LAM_CHECK(codes_dev != nullptr || n == 0, LAM_EINVAL, "codes buffer is NULL");
+  LAM_CHECK(codes_cap_bytes >= p.code_bytes, LAM_EINVAL, "codes capacity %llu < %llu bytes needed",
+            (unsigned long long)codes_cap_bytes, (unsigned long long)p.code_bytes);
+  DeviceGuard g(ctx->device);
+  LAM_TRY(launch_encode(ctx, x_dev, n, p, codes_dev, status_dev, "qeps_encode"));
+  if (out) *out = p;
+  return LAM_OK;
+}
+
 lam_status lam_dequantize(lam_ctx* ctx, const uint32_t* codes_dev, const lam_qparams* p, float* xhat_dev) {
   LAM_CHECK(ctx != nullptr && p != nullptr, LAM_EINVAL, "ctx or params is NULL");
   LAM_CHECK(p->n >= 0 && p->bits >= 1 && p->bits <= 32, LAM_EINVAL, "bad params (n=%lld, bits=%d)",

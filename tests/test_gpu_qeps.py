@@ -87,3 +87,31 @@ def test_raw_workload_full_size(lam, eps, bits):
     q_ref, xh = _check(lam, x, eps, absmax=1.0)
     assert qeps.plan(eps, 1.0)["bits"] >= bits
     assert qeps.bound_violations(x, q_ref, eps) == 0
+
+
+def test_quantize_async_codes_and_status(lam):
+    """The asynchronous encode writes the codes of the waiting one and reports
+    invalid elements through the caller's counters instead of a status."""
+    import torch
+    x = np.linspace(-1, 1, 100003).astype(np.float32)
+    status = torch.zeros(2, dtype=torch.int32, device="cuda")
+    c1, p1 = lam.quantize(_dev(x), 1e-3, absmax=1.0)
+    c2, p2 = lam.quantize_async(_dev(x), 1e-3, 1.0, status)
+    assert (p1.bits, p1.max_code, p1.code_bytes) == (p2.bits, p2.max_code, p2.code_bytes)
+    assert torch.equal(c1, c2)
+    assert status.tolist() == [0, 0]
+    y = x.copy()
+    y[5] = np.nan
+    y[70001] = 1.5
+    lam.quantize_async(_dev(y), 1e-3, 1.0, status)
+    s = status.tolist()
+    assert s[0] > 0 and s[1] > 0
+    status.zero_()
+    y = x.copy()
+    y[123] = -1.25
+    lam.quantize_async(_dev(y), 1e-3, 1.0, status)
+    s = status.tolist()
+    assert s[0] == 0 and s[1] > 0
+    with pytest.raises(lam.LamError) as e:
+        lam.quantize_async(_dev(x), 1e-3, 0.0, status)
+    assert e.value.name == "LAM_EINVAL"
