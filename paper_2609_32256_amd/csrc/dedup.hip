@@ -256,14 +256,25 @@ struct ScreenArgs {
   DevFlags* flags;
 };
 
-__device__ __forceinline__ void push_pair(const ScreenArgs& a, int i, int kind, int y) {
-  const uint32_t idx = atomicAdd(&a.cc->npairs, 1u);
-  atomicAdd(&a.flags->n_pairs, 1u);
-  if (idx < a.pair_cap) {
-    a.pairs[idx] = make_int2(i | (kind << 31), y);
-  } else {
+// Lists the ambiguous pairs (i, row_of(e)) for the set bits e of `bits`: one
+// atomic reserves the lane's whole run of list entries (one per pair had put
+// a round trip per pair on the tile's critical path).
+template <class RowOf>
+__device__ __forceinline__ void push_pairs(const ScreenArgs& a, int i, int kind, uint64_t bits, RowOf&& row_of) {
+  const uint32_t cnt = (uint32_t)__popcll(bits);
+  if (cnt == 0u) return;
+  const uint32_t idx0 = atomicAdd(&a.cc->npairs, cnt);
+  atomicAdd(&a.flags->n_pairs, cnt);
+  uint32_t idx = idx0;
+  while (bits) {
+    const int e = __builtin_ctzll(bits);
+    bits &= bits - 1ull;
+    if (idx < a.pair_cap) a.pairs[idx] = make_int2(i | (kind << 31), row_of(e));
+    ++idx;
+  }
+  if (idx0 + cnt > a.pair_cap) {
     atomicOr(&a.flags->pair_overflow, 1u);
-    atomicMax(&a.flags->pairs_needed, idx + 1u);   // capacity that would have sufficed
+    atomicMax(&a.flags->pairs_needed, idx0 + cnt);   // capacity that would have sufficed
   }
 }
 
@@ -453,27 +464,23 @@ __global__ __launch_bounds__(C::kThreads, C::kMinWaves) void k_screen(ScreenArgs
     if (MODE == 0) {
       // lowest definite row, and the ambiguous rows below it
       const int edef = def ? __builtin_ctzll(def) : 64;
-      uint64_t amb = cand & ~def & (edef < 64 ? ((1ull << edef) - 1ull) : ~0ull);
-      while (amb) {
-        const int e = __builtin_ctzll(amb);
-        amb &= amb - 1ull;
-        push_pair(a, ib, 0, row_of(e));
-      }
+      push_pairs(a, ib, 0, cand & ~def & (edef < 64 ? ((1ull << edef) - 1ull) : ~0ull), row_of);
       if (edef < 64) atomicMin(&a.firstHit[ib], row_of(edef));
     } else {
-      uint64_t c = cand;
-      while (c) {
-        const int e = __builtin_ctzll(c);
-        c &= c - 1ull;
-        const int ia = row_of(e);
-        if ((def >> e) & 1ull) {
-          atomicOr(reinterpret_cast<unsigned long long*>(&a.bitmap[(int64_t)ib * a.W + (ia >> 6)]),
-                   1ull << (ia & 63));
-          a.hasEdge[ib] = 1u;
-        } else {
-          push_pair(a, ib, 1, ia);
+      // a lane's rows are 64 consecutive rows from a multiple of 64, so its
+      // definite edges fall in one bitmap word: one atomic for all of them
+      static_assert(C::TI * 32 == 64 && C::BM % 64 == 0, "a lane's A rows fill one bitmap word");
+      if (def) {
+        uint64_t word = 0ull, d = def;
+        while (d) {
+          const int e = __builtin_ctzll(d);
+          d &= d - 1ull;
+          word |= 1ull << (row_of(e) & 63);
         }
+        atomicOr(reinterpret_cast<unsigned long long*>(&a.bitmap[(int64_t)ib * a.W + (row_of(0) >> 6)]), word);
+        a.hasEdge[ib] = 1u;
       }
+      push_pairs(a, ib, 1, cand & ~def, row_of);
     }
   }
 }
