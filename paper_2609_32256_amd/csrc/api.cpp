@@ -505,9 +505,9 @@ lam_status lam_store_quantize(lam_ctx* ctx, lam_store* st, double eps, float abs
 lam_status lam_store_clear(lam_ctx* ctx, lam_store* st) {
   LAM_CHECK(ctx != nullptr && st != nullptr, LAM_EINVAL, "ctx or store is NULL");
   DeviceGuard g(ctx->device);
-  hipLaunchKernelGGL(k_zero_words, dim3(1), dim3(64), 0, ctx->stream, reinterpret_cast<uint32_t*>(st->stat_dev),
-                     (int)(store_meta_bytes() / 4));
-  LAM_HIP(hipGetLastError());
+  // the device bookkeeping is zeroed by the next ingest's first kernel (no
+  // launch of its own); until then nothing on the device reads it
+  st->meta_reset = true;
   LAM_TRY(lsh_reset(ctx, st, 0));
   st->pending = false;   // errors of earlier calls that did not wait are dropped with the contents
   st->blk_rows = -1;

@@ -131,6 +131,7 @@ struct ChunkState {
   ChunkCounters* cc;
   StoreMeta* meta;
   int32_t m_first;         // store size at the start of the call, or -1 to leave it
+  int32_t reset_meta;      // the store was cleared since its last ingest: zero its bookkeeping first
 };
 
 __device__ __forceinline__ void init_chunk_row(const ChunkState& c, int64_t r, int lane) {
@@ -167,6 +168,7 @@ __global__ __launch_bounds__(256) void k_prep(const float* __restrict__ x, int64
     cs.cc->n_escalate = 0u;
     cs.cc->blocks_done = 0u;
     cs.cc->kept = 0u;
+    if (cs.reset_meta) *cs.meta = StoreMeta{};       // lam_store_clear, applied by the next ingest
     if (cs.m_first >= 0) cs.meta->m = cs.m_first;   // a retried call starts from the store as it was
   }
   if (row < cs.nB) init_chunk_row(cs, row, lane);
@@ -1684,7 +1686,6 @@ __global__ __launch_bounds__(256) void k_maxcos(int nB, const uint32_t* maxcos_s
 }  // namespace
 
 // ------------------------------------------------------------------ store memory
-size_t store_meta_bytes() { return sizeof(StoreMeta); }
 
 lam_status store_alloc(lam_store* st) {
   const size_t cap = (size_t)st->capacity, D = (size_t)st->dim;
@@ -1812,6 +1813,12 @@ lam_status store_settle(lam_store* st) {
 lam_status store_maxima(lam_store* st) {
   LAM_TRY(store_settle(st));
   if (st->maxima_known) return LAM_OK;
+  if (st->meta_reset) {   // cleared, and no ingest since: nothing retained
+    st->absmax_bits = 0u;
+    st->hnmax_bits = 0u;
+    st->maxima_known = true;
+    return LAM_OK;
+  }
   StoreMeta m{};
   LAM_HIP(hipMemcpy(&m, st->stat_dev, sizeof m, hipMemcpyDeviceToHost));
   st->absmax_bits = m.absmax_bits;
@@ -1943,7 +1950,8 @@ lam_status dedup_ingest(lam_ctx* ctx, lam_store* st, const float* x, int64_t n, 
       const bool last_chunk = c0 + CH >= n;
       // a waiting call sets the store size (so a repeated attempt starts from
       // the store as it was); otherwise the kernels keep it
-      const ChunkState cs{firstHit, hasEdge, maxcos, bitmap, W, nB, cc, meta, async ? -1 : (int32_t)m_before};
+      const ChunkState cs{firstHit, hasEdge, maxcos, bitmap, W, nB, cc, meta, async ? -1 : (int32_t)m_before,
+                          st->meta_reset ? 1 : 0};
       if (c0 == 0) {
         // the status words must be zero before prep counts into them; the
         // last append of every call leaves them zero
@@ -1953,6 +1961,7 @@ lam_status dedup_ingest(lam_ctx* ctx, lam_store* st, const float* x, int64_t n, 
         hipLaunchKernelGGL(k_prep, dim3((unsigned)((n + 3) / 4)), dim3(256), 0, ctx->stream, x, n, D, x16c, hnc,
                            etc, K.K1, K.K2, K.K3h, ctx->flags_dev, cs);
         LAM_HIP(hipGetLastError());
+        st->meta_reset = false;
       } else {
         hipLaunchKernelGGL(k_chunk_init, dim3(64), dim3(256), 0, ctx->stream, cs);
         LAM_HIP(hipGetLastError());

@@ -137,6 +137,7 @@ struct lam_store {
   int64_t* ids = nullptr;     // global ids
   float* stat_dev = nullptr;  // device bookkeeping block (retained-row count)
   void* meta_host = nullptr;  // pinned host copy of that block, made when settling
+  bool meta_reset = false;    // cleared: the next ingest's first kernel zeroes the block
   uint32_t hn_max = 0;        // max of hn over the coded rows (float bits), set with the codes
   // the device bookkeeping's maxima over the retained rows, as last read by the host
   bool maxima_known = false;  // false until read again after calls that may have changed them
@@ -191,7 +192,6 @@ lam_status launch_decode(lam_ctx* ctx, const uint32_t* codes, const lam_qparams&
 lam_status dedup_ingest(lam_ctx* ctx, lam_store* st, const float* x, int64_t n, int64_t* rep,
                         float* max_cos, lam_ingest_stats* stats);
 lam_status store_alloc(lam_store* st);
-size_t store_meta_bytes();   // device bookkeeping block of a store (cleared by lam_store_clear)
 lam_status store_maxima(lam_store* st);   // settles the store and makes absmax_bits / hnmax_bits current
 void store_free(lam_store* st);
 

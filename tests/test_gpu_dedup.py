@@ -431,3 +431,27 @@ def test_store_quantize_declared_absmax_against_store_maximum(lam):
     assert p.absmax == np.float32(0.75)
     assert np.array_equal(s.codes().cpu().numpy().view(np.uint32), qeps.pack(qeps.codes(x[kept], 1e-3), p.bits))
     assert s.info().size == kept.size
+
+
+def test_clear_resets_bookkeeping_and_pending_errors(lam):
+    """lam_store_clear drops the error report of a pending invalid call and
+    resets the device bookkeeping before the next ingest uses it: the next
+    stream's ids start at 0, its delta_hat and its codec width are its own."""
+    cfg = synth.subset_ingest()
+    x, y = cfg["x"][:3000], cfg["x"][3000:7000]
+    s = lam.Store(768, 0.95, 8000)
+    s.ingest(_dev(x), sync=False)
+    bad = x[:64].copy()
+    bad[5, 3] = np.nan
+    s.ingest(_dev(bad), sync=False)
+    s.clear()
+    info = s.info()                      # no error: the pending report was dropped
+    assert (info.size, info.n_seen, info.delta_hat_run) == (0, 0, 0.0)
+    reps = [s.ingest(_dev(y[b0:b0 + 1000]), sync=False)[0] for b0 in range(0, y.shape[0], 1000)]
+    ref = dedup.greedy(y, 0.95, block=512)
+    assert np.array_equal(torch.cat(reps).cpu().numpy(), ref["rep"])
+    info = s.info()
+    assert info.size == int(ref["kept"].size) and info.n_seen == y.shape[0]
+    assert abs(info.delta_hat_run - ref["delta_hat"]) <= 1e-12
+    p = s.quantize(1e-3)
+    assert p.absmax == np.abs(y[ref["kept"]]).max()
