@@ -658,13 +658,25 @@ __device__ void merge_query(int64_t j, int cands, int k, const float* __restrict
     ls[p] = -INFINITY;
     lr[p] = kNoRow;
   }
-  for (int c = lane; c < cands; c += 64) {
-    if ((c % SEG) >= k) continue;             // below rank k of its own sorted segment
-    const int cr = r[c];
-    if (cr == kNoRow) continue;
-    const float cs = s[c];
-    if (!better(cs, cr, ls[KL - 1], lr[KL - 1])) continue;
-    list_insert<KL>(ls, lr, cs, cr);
+  // a lane's next entries loaded together before any is used (one load
+  // after another's test had put two round trips per entry on the path);
+  // four for the sample's unsorted entries, two beside 16-entry lists
+  constexpr int kU = (SEG == 1 || KL < 16) ? 4 : 2;
+  for (int c0 = lane; c0 < cands; c0 += 64 * kU) {
+    float cs[kU];
+    int cr[kU];
+#pragma unroll
+    for (int u = 0; u < kU; ++u) {
+      const int c = c0 + 64 * u;
+      const bool in = c < cands && (c % SEG) < k;   // not below rank k of its own sorted segment
+      cr[u] = in ? r[c] : kNoRow;
+      cs[u] = in ? s[c] : -INFINITY;
+    }
+#pragma unroll
+    for (int u = 0; u < kU; ++u) {
+      if (cr[u] == kNoRow || !better(cs[u], cr[u], ls[KL - 1], lr[KL - 1])) continue;
+      list_insert<KL>(ls, lr, cs[u], cr[u]);
+    }
   }
   // the sample's k-th hi-only score, lowered by 2 err: a threshold no row of
   // the final top-k falls below in hi-only terms
