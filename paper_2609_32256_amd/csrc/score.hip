@@ -1050,7 +1050,7 @@ lam_status launch_filter(int b, int D, bool large, dim3 grid, hipStream_t st, co
 // ------------------------------------------------------------------ rescoring
 constexpr int kRescoreCap = 256;     // candidates near the k-th score rescored per query
 constexpr int kRescoreThreads = 256;
-constexpr int kRescoreLanes = 16;    // lanes per rescored row
+constexpr int kRescoreLanes = 8;     // lanes per rescored row
 
 // The rescoring of m rows (in LDS) of query j from the codes and the float32
 // query, summed in binary64 and rounded once, and a bitonic sort of the keys
@@ -1122,7 +1122,7 @@ __device__ __forceinline__ void rescore_sort(int64_t j, uint32_t m, int kk, int 
 // row asc) replace the selection's output.  More than kRescoreCap such
 // candidates (many near-equal scores) flag the query for the exact fallback
 // pass.  Queries already flagged, or invalid, are left as the selection wrote
-// them.  Sixteen lanes share a row (16 rows in flight per workgroup); a lane
+// them.  Eight lanes share a row (32 rows in flight per workgroup); a lane
 // takes whole groups of 32 codes (B words), unpacked as the scoring kernel
 // unpacks them (exactly, to fp16).
 template <int B>
