@@ -1159,7 +1159,56 @@ __device__ void resolve_core(const ResolveArgs& a, ResolveLds& L, int n, int m0,
     __syncthreads();
     // one barrier per round: round r raises pend[r % 3] and clears pend[(r + 1)
     // % 3], which every thread last read before the previous barrier
-    for (int r = 0;; ++r) {
+    if (na <= T) {
+      // one active row per thread: its index, whether it is still open, its
+      // current word index and that word stay in registers across rounds
+      // (only the row's own thread changes them), so a round reads only the
+      // dropped words and the candidates' states
+      const bool mine = tid < na;
+      const int i = mine ? (int)L.active[tid] : 0;
+      const int nw = (i + 63) >> 6;
+      int w = mine ? (int)L.bm.first[tid] : 0;
+      uint64_t cur = (mine && w < nw) ? L.bm.bits[tid * a.W + w] : 0ull;
+      bool open = mine;
+      for (int r = 0;; ++r) {
+        if (tid == 0) L.pend[(r + 1) % 3] = 0u;
+        if (open) {
+          int dec = 0;   // 0 keep, 1 drop, -1 wait
+          int j = -1;
+          while (w < nw) {
+            uint64_t x = cur & ~dropped[w];
+            while (x) {
+              const int c = w * 64 + __builtin_ctzll(x);
+              const uint8_t sc = st[c];
+              if (sc == 2) {   // dropped since the word was read
+                x &= x - 1ull;
+                continue;
+              }
+              dec = (sc == 1) ? 1 : -1;
+              j = c;
+              break;
+            }
+            if (j >= 0) break;
+            ++w;   // the word holds only dropped candidates
+            cur = w < nw ? L.bm.bits[tid * a.W + w] : 0ull;
+          }
+          if (dec == 1) {
+            st[i] = 2;
+            L.rrow[i] = -(j + 2);
+            atomicOr(&L.dropped[i >> 6], 1ull << (i & 63));
+            open = false;
+          } else if (dec == 0) {
+            st[i] = 1;
+            L.rrow[i] = -1;
+            open = false;
+          } else {
+            L.pend[r % 3] = 1u;
+          }
+        }
+        __syncthreads();
+        if (L.pend[r % 3] == 0u) break;
+      }
+    } else for (int r = 0;; ++r) {
       if (tid == 0) L.pend[(r + 1) % 3] = 0u;
       for (int k = tid; k < na; k += T) {
         const int i = L.active[k];
