@@ -91,9 +91,13 @@ struct StoreMeta {
 struct ChunkCounters {
   uint32_t npairs;        // ambiguous pairs appended in this chunk
   uint32_t n_escalate;
+  // one 64-bit word, added to with one atomic per append workgroup:
   uint32_t blocks_done;   // append workgroups finished (last one exports the status words)
   uint32_t kept;          // rows of the chunk kept, summed by the workgroups of k_resolve_append
 };
+static_assert(offsetof(ChunkCounters, blocks_done) % 8 == 0 &&
+                  offsetof(ChunkCounters, kept) == offsetof(ChunkCounters, blocks_done) + 4,
+              "blocks_done and kept form one little-endian 64-bit word");
 
 __device__ __forceinline__ bool skip_all(const DevFlags* f) {
   return (f->nonfinite | f->out_of_range | f->pair_overflow) != 0u;
@@ -1544,44 +1548,60 @@ __device__ __forceinline__ void append_maxima(const AppendArgs& a, double dmax, 
       am = max(am, apart[w]);
       hm = max(hm, hpart[w]);
     }
+    // A call that waits gathers its delta_hat in the status words, read back
+    // by the host; a call that does not goes straight to the store's
+    // bookkeeping (rows are appended only by calls that go through, and skip
+    // is uniform over the call, so an invalid call leaves it as it was).
     if (m > 0.0)
-      atomicMax(reinterpret_cast<unsigned long long*>(&a.flags->dhat2_bits),
+      atomicMax(a.async_call ? &a.meta->dhat2_bits : reinterpret_cast<unsigned long long*>(&a.flags->dhat2_bits),
                 (unsigned long long)__double_as_longlong(m));
-    // the store's maxima: rows are appended only by calls that go through
-    // (skip is uniform over the call), so an invalid call leaves them as they were
     if (am > am0) atomicMax(&a.meta->absmax_bits, am);
     if (hm > hm0) atomicMax(&a.meta->hnmax_bits, hm);
-    // This workgroup is counted (append_finish) only once its maxima have been
+    // When the last workgroup reads the status words' maximum (a call that
+    // waits), this workgroup is counted only once its maxima have been
     // performed: the wait covers the atomics issued above.  Device-scope
     // atomics are performed where every XCD sees them, so the last workgroup,
     // which reads the status words with device-scope atomic loads, needs no
     // cache write-back or invalidation (fences here cost 1.7 us per call).
-    __builtin_amdgcn_s_waitcnt(0);
+    // Nothing of this launch reads the bookkeeping's maxima, so a call that
+    // does not wait does not wait here (its row stores are not waited for).
+    if (!a.async_call) __builtin_amdgcn_s_waitcnt(0);
   }
 }
 
-// The last workgroup to finish (counted in cc->blocks_done) runs `last_work`
-// (thread 0), and on the call's last chunk folds the call into the store's
-// bookkeeping (arrival count and delta_hat if the call went through, an error
-// count if its input was invalid), copies the status words to host memory
-// when asked, and clears them for the next call.  The only words of this
-// launch it reads are the status words' maxima, updated by atomics that each
-// workgroup has waited for before its count; everything else it reads was
-// written by earlier launches.  Called by every thread of every workgroup.
+// The last workgroup to finish runs `last_work(kept)` (thread 0; kept = the
+// rows kept by the launch's workgroups, each adding its own kept_here), and
+// on the call's last chunk folds the call into the store's bookkeeping
+// (arrival count, and delta_hat of a call that waits, if the call went
+// through; an error count if its input was invalid), copies the status words
+// to host memory when asked, and clears them for the next call.  A
+// workgroup's count and its kept rows go in one 64-bit atomic, so the last
+// one knows the total from the value it gets back.  The only words of this
+// launch it reads are the status words' maxima of a call that waits, updated
+// by atomics that each workgroup has waited for before its count;
+// everything else it reads was written by earlier launches.  Called by every
+// thread of every workgroup.
 template <class F>
-__device__ __forceinline__ void append_finish(const AppendArgs& a, bool count_every_chunk, F&& last_work) {
+__device__ __forceinline__ void append_finish(const AppendArgs& a, bool count_every_chunk, uint32_t kept_here,
+                                              F&& last_work) {
   if (!a.last_chunk && !count_every_chunk) return;
   __shared__ bool last;
+  __shared__ uint32_t kept_total;
+  unsigned long long* done_kept = reinterpret_cast<unsigned long long*>(&a.cc->blocks_done);
   __syncthreads();
-  if (threadIdx.x == 0) last = atomicAdd(&a.cc->blocks_done, 1u) == gridDim.x - 1;
+  if (threadIdx.x == 0) {
+    const unsigned long long prev = atomicAdd(done_kept, ((unsigned long long)kept_here << 32) | 1ull);
+    last = (uint32_t)prev == gridDim.x - 1;
+    kept_total = (uint32_t)(prev >> 32) + kept_here;
+  }
   __syncthreads();
   if (!last) return;
   if (threadIdx.x == 0) {
-    last_work();
+    last_work(kept_total);
     __builtin_amdgcn_s_waitcnt(0);   // its atomics are performed before the words are read below
   }
   if (!a.last_chunk) {
-    if (threadIdx.x == 0) a.cc->blocks_done = 0u;
+    if (threadIdx.x == 0) *done_kept = 0ull;
     return;
   }
   constexpr int kWords = (int)(sizeof(DevFlags) / 4);
@@ -1596,9 +1616,11 @@ __device__ __forceinline__ void append_finish(const AppendArgs& a, bool count_ev
       a.meta->err_bits |= bad | (overflow ? 4u : 0u);
     } else if (!overflow) {
       a.meta->n_seen += a.n_call;
-      const unsigned long long d2 =
-          __hip_atomic_load(&a.flags->dhat2_bits, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      if (d2 > a.meta->dhat2_bits) a.meta->dhat2_bits = d2;   // non-negative doubles order as their bits
+      if (!a.async_call) {   // (a call that does not wait put its maximum in the bookkeeping already)
+        const unsigned long long d2 =
+            __hip_atomic_load(&a.flags->dhat2_bits, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (d2 > a.meta->dhat2_bits) a.meta->dhat2_bits = d2;   // non-negative doubles order as their bits
+      }
     }
   }
   __syncthreads();
@@ -1608,7 +1630,7 @@ __device__ __forceinline__ void append_finish(const AppendArgs& a, bool count_ev
   }
   __syncthreads();
   if ((int)threadIdx.x < kWords) f[threadIdx.x] = 0u;
-  if (threadIdx.x == 0) a.cc->blocks_done = 0u;
+  if (threadIdx.x == 0) *done_kept = 0ull;
 }
 
 // One wave per row, four rows per workgroup, decisions from k_resolve.  Kept
@@ -1637,7 +1659,7 @@ __global__ __launch_bounds__(256) void k_append(AppendArgs a, int nB) {
   __shared__ double part[4];
   __shared__ uint32_t apart[4], hpart[4];
   append_maxima<4>(a, dmax, amax, hmax, am0, hm0, part, apart, hpart);
-  append_finish(a, false, [] {});
+  append_finish(a, false, 0u, [](uint32_t) {});
 }
 
 // The in-chunk resolve and the append in one launch.  Workgroup b appends
@@ -1704,13 +1726,11 @@ __global__ __launch_bounds__(kAppendGroupThreads) void k_resolve_append(ResolveA
     const uint64_t k = __ballot(lane < nres - first && L.st[first + lane] == 1);
     kept_here = (uint32_t)__popcll(k);
   }
-  if (tid == 0 && kept_here) atomicAdd(&a.cc->kept, kept_here);   // waited for in append_maxima
   __shared__ double part[T / 64];
   __shared__ uint32_t apart[T / 64], hpart[T / 64];
   append_maxima<T / 64>(a, dmax, amax, hmax, am0, hm0, part, apart, hpart);
-  append_finish(a, true, [&] {
+  append_finish(a, true, kept_here, [&](uint32_t total) {
     if (skip) return;
-    const uint32_t total = __hip_atomic_load(&a.cc->kept, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     a.meta->m = m0 + (int)total;
     atomicAdd(&a.flags->n_kept, total);
   });
