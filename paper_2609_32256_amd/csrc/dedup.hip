@@ -1598,7 +1598,7 @@ __device__ __forceinline__ void append_finish(const AppendArgs& a, bool count_ev
   if (!last) return;
   if (threadIdx.x == 0) {
     last_work(kept_total);
-    __builtin_amdgcn_s_waitcnt(0);   // its atomics are performed before the words are read below
+    if (a.flags_out) __builtin_amdgcn_s_waitcnt(0);   // its atomics are performed before the words are exported
   }
   if (!a.last_chunk) {
     if (threadIdx.x == 0) *done_kept = 0ull;
@@ -1624,11 +1624,13 @@ __device__ __forceinline__ void append_finish(const AppendArgs& a, bool count_ev
     }
   }
   __syncthreads();
-  if ((int)threadIdx.x < kWords) {
-    const uint32_t v = __hip_atomic_load(f + threadIdx.x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (a.flags_out) reinterpret_cast<uint32_t*>(a.flags_out)[threadIdx.x] = v;
+  if (a.flags_out) {   // (uniform) a call that waits: the words go to host memory first
+    if ((int)threadIdx.x < kWords) {
+      const uint32_t v = __hip_atomic_load(f + threadIdx.x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      reinterpret_cast<uint32_t*>(a.flags_out)[threadIdx.x] = v;
+    }
+    __syncthreads();
   }
-  __syncthreads();
   if ((int)threadIdx.x < kWords) f[threadIdx.x] = 0u;
   if (threadIdx.x == 0) *done_kept = 0ull;
 }
