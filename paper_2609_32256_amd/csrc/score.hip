@@ -988,15 +988,24 @@ __global__ __launch_bounds__(C::kThreads, C::kMinWaves) void k_filter(ScoreArgs 
     }
     return;
   }
+  // a tile whose store rows are all valid needs no per-element row test
+  const bool full = rows == C::BM;
 #pragma unroll
   for (int y = 0; y < C::TJ; ++y) {
     // epilogue: the tile's largest raw accumulator first (osc > 0)
     float amx = -INFINITY;
+    if (full) {
 #pragma unroll
-    for (int x = 0; x < C::TI; ++x)
+      for (int x = 0; x < C::TI; ++x)
 #pragma unroll
-      for (int r = 0; r < 16; ++r)
-        amx = (wm * C::TI * 32 + x * 32 + acc_row(r, lane) < rows) ? fmaxf(amx, acc[x][y][r]) : amx;
+        for (int r = 0; r < 16; ++r) amx = fmaxf(amx, acc[x][y][r]);
+    } else {
+#pragma unroll
+      for (int x = 0; x < C::TI; ++x)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          amx = (wm * C::TI * 32 + x * 32 + acc_row(r, lane) < rows) ? fmaxf(amx, acc[x][y][r]) : amx;
+    }
     const bool hot = jv[y] && amx * osc[y] >= th[y];
     if (__ballot(hot) == 0ull || !hot) continue;
     uint32_t c = 0u;
