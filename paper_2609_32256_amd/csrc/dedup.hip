@@ -404,9 +404,11 @@ __global__ __launch_bounds__(C::kThreads, C::kMinWaves) void k_screen(ScreenArgs
       thrIn = round_up_f32(base + e);
     }
     float mx = -3.0e38f, cmax = -3.0e38f;
-    // A store tile with every A row valid: no element needs a validity test
-    // (a lane past rowsB has thrAmb = 3e38, which no finite mx reaches)
-    const bool full = !WANT_MAX && MODE == 0 && rowsA == C::BM;
+    // A tile with every A row valid, against the store or below the chunk's
+    // diagonal (ta < tb: every A row precedes every B row): no element needs
+    // a validity test (a lane past rowsB has thrAmb = 3e38, which no finite
+    // mx reaches)
+    const bool full = !WANT_MAX && rowsA == C::BM && (MODE == 0 || ta < tb);
 #pragma unroll
     for (int ti = 0; ti < C::TI; ++ti) {
       // the row terms of this lane's 16 rows of the 32 x 32 tile: four
