@@ -115,3 +115,19 @@ def test_quantize_async_codes_and_status(lam):
     with pytest.raises(lam.LamError) as e:
         lam.quantize_async(_dev(x), 1e-3, 0.0, status)
     assert e.value.name == "LAM_EINVAL"
+
+
+def test_quantize_async_empty_and_counts_accumulate(lam):
+    """An empty input queues nothing and leaves the counters as they were;
+    counts from several calls add up until the caller clears them."""
+    import torch
+    status = torch.zeros(2, dtype=torch.int32, device="cuda")
+    codes, p = lam.quantize_async(torch.empty(0, dtype=torch.float32, device="cuda"), 1e-3, 1.0, status)
+    assert p.n == 0 and p.code_bytes == 0 and status.tolist() == [0, 0]
+    y = np.linspace(-1, 1, 5000).astype(np.float32)
+    y[10] = 3.0
+    lam.quantize_async(_dev(y), 1e-3, 1.0, status)
+    one = status.tolist()
+    lam.quantize_async(_dev(y), 1e-3, 1.0, status)
+    two = status.tolist()
+    assert one[0] == 0 and one[1] > 0 and two == [0, 2 * one[1]]
