@@ -317,3 +317,30 @@ def test_rescoring_cap_falls_back_exactly(lam, d):
     gi = gi.cpu().numpy()
     assert np.array_equal(gi[2], np.concatenate([[200], np.arange(300, 309)]))
     _compare(gs.cpu().numpy(), gi, c, np.arange(x.shape[0]), q, eps, 10)
+
+
+@pytest.mark.parametrize("near", [600, 2000])
+@pytest.mark.parametrize("k,d", [(1, 64), (10, 64), (16, 768)])
+def test_selection_over_many_candidates(lam, near, k, d):
+    """The store's first 4,096 rows (the threshold plan's sample) are random
+    directions; after them each query has `near` rows whose cosines with it
+    run from 0.5 to 0.99, all above the sample's k-th score, so the filter
+    pass hands the selection about `near` candidates per query (several per
+    lane of its per-lane lists), and the top-k must match the oracle."""
+    rng = np.random.default_rng(21)
+    nq = 4
+    q = synth.unit_rows(rng, nq, d)
+    parts = [synth.unit_rows(rng, 4096, d)]
+    for j in range(nq):
+        parts.append(synth.members(rng, np.repeat(q[j:j + 1], near, axis=0), np.linspace(0.5, 0.99, near)))
+    x = np.concatenate(parts).astype(np.float32)
+    n = x.shape[0]
+    s = _store_from_rows(lam, x)
+    eps = 1e-3
+    s.quantize(eps)
+    assert s.info().size == n
+    c = qeps.codes(x, eps).reshape(n, -1)
+    S = score.scores(q.astype(np.float32), c, eps)
+    assert np.all((S[:, 4096:] >= 0.49).sum(1) >= near)
+    gs, gi, _ = s.score_topk(_dev(q.astype(np.float32)), k)
+    _compare(gs.cpu().numpy(), gi.cpu().numpy(), c, np.arange(n), q.astype(np.float32), eps, k)
