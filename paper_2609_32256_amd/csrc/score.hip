@@ -1217,6 +1217,16 @@ __global__ __launch_bounds__(kRescoreThreads) void k_select_rescore(
     out_i[j * k + t] = -1;
   }
   if (kk == 0) return;
+  // every thread's first two candidates for the threshold test below, loaded
+  // while wave 0 selects
+  float fs[2];
+  int fr[2];
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    const uint32_t i = (uint32_t)(tid + u * kRescoreThreads);
+    fs[u] = i < c ? cs[j * cap + i] : 0.0f;
+    fr[u] = i < c ? cr[j * cap + i] : 0;
+  }
   if (wave == 0) {
     float ls[KL];
     int lr[KL];
@@ -1225,7 +1235,21 @@ __global__ __launch_bounds__(kRescoreThreads) void k_select_rescore(
       ls[p] = -INFINITY;
       lr[p] = kNoRow;
     }
-    for (uint32_t i = lane; i < c; i += 64) {
+    // a lane's first kPre candidates are loaded before any is inserted
+    constexpr int kPre = 8;
+    float ps[kPre];
+    int pr[kPre];
+#pragma unroll
+    for (int u = 0; u < kPre; ++u) {
+      const uint32_t i = (uint32_t)(lane + u * 64);
+      ps[u] = i < c ? cs[j * cap + i] : 0.0f;
+      pr[u] = i < c ? cr[j * cap + i] : 0;
+    }
+#pragma unroll
+    for (int u = 0; u < kPre; ++u)
+      if ((uint32_t)(lane + u * 64) < c && better(ps[u], pr[u], ls[KL - 1], lr[KL - 1]))
+        list_insert<KL>(ls, lr, ps[u], pr[u]);
+    for (uint32_t i = lane + kPre * 64; i < c; i += 64) {
       const int row = cr[j * cap + i];
       const float sc = cs[j * cap + i];
       if (!better(sc, row, ls[KL - 1], lr[KL - 1])) continue;
@@ -1255,7 +1279,14 @@ __global__ __launch_bounds__(kRescoreThreads) void k_select_rescore(
   }
   __syncthreads();
   const float thr = thr_sh;
-  for (uint32_t i = tid; i < c; i += kRescoreThreads) {
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    if ((uint32_t)(tid + u * kRescoreThreads) < c && fs[u] >= thr) {
+      const uint32_t p = atomicAdd(&m_sh, 1u);
+      if (p < (uint32_t)kRescoreCap) rows[p] = fr[u];
+    }
+  }
+  for (uint32_t i = tid + 2 * kRescoreThreads; i < c; i += kRescoreThreads) {
     if (cs[j * cap + i] >= thr) {
       const uint32_t p = atomicAdd(&m_sh, 1u);
       if (p < (uint32_t)kRescoreCap) rows[p] = cr[j * cap + i];
